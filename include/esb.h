@@ -1,0 +1,170 @@
+/*
+ * libesb — the data-parallel hot path of elastic significant bit (ESB)
+ * quantization (Gong et al., "Elastic Significant Bit Quantization and
+ * Acceleration for Deep Neural Networks", IEEE TPDS 2021) on AMD MI355X
+ * (gfx950).
+ *
+ * C ABI.  Every pointer argument documented "device" is a HIP device pointer
+ * on the current device; "host" pointers are ordinary CPU memory.  `stream` is
+ * a hipStream_t passed as void* (NULL = the null stream).  All device work is
+ * enqueued asynchronously on `stream`; functions return once it is enqueued.
+ * The caller owns every buffer; the library allocates no device memory.
+ * Functions are stateless and thread-safe.
+ *
+ * Errors: every call returns an int status.  Arguments are validated on the
+ * host before any launch; on error nothing is enqueued.  ESB_E_HIP means a HIP
+ * runtime call failed; esb_last_hip_error() returns its hipError_t (per thread).
+ *
+ * Parameters of the format (Sec. 3.2, eq. (4)-(5)):
+ *   n      total bits b, 2 <= n <= 8;
+ *   k_sig  significant bits, 1 <= k_sig <= n-1.  The paper's k (fraction bits)
+ *          is k = k_sig - 1: ESB(b, k) holds values with at most k+1
+ *          significant bits.  Examples: (n=4, k_sig=2) is the paper's ESB(4,1);
+ *          (n=3, k_sig=1) is ESB(3,0), powers of two; (n=3, k_sig=2) is
+ *          ESB(3,1), a uniform grid.
+ *
+ * Code layout (ESB float format, eq. (14)): one code per byte, bits
+ *   [n-1] sign | [n-2 .. k] exponent e | [k-1 .. 0] fraction f,
+ * value 0.f when e is all ones (the subnormal binade), else 2^e * 1.f.  Zero
+ * is always produced with sign 0; the code with sign 1 and value 0 is accepted
+ * as input.  Bits above bit n-1 of an input code are ignored.
+ */
+#ifndef ESB_H
+#define ESB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ESB_OK 0
+#define ESB_E_INVALID (-1)     /* bad n/k_sig, sizes, NULL pointer, layout, descriptor */
+#define ESB_E_OVERFLOW (-3)    /* reduction length * max|mA| * max|mB| > 2^31 - 1 */
+#define ESB_E_UNSUPPORTED (-4) /* decoded integers exceed the split int8 range (|m| > 32639) */
+#define ESB_E_HIP (-5)         /* HIP launch / runtime failure, see esb_last_hip_error() */
+#define ESB_E_WORKSPACE (-6)   /* workspace NULL or smaller than esb_dda_workspace_size() */
+
+#define ESB_B_NK 0 /* B stored N x K, row-major (K contiguous) */
+#define ESB_B_KN 1 /* B stored K x N, row-major (N contiguous) */
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int esb_version(void);
+
+/* Human-readable name of a status code (static string). */
+const char* esb_strerror(int status);
+
+/* hipError_t of the last ESB_E_HIP returned on this thread (0 if none). */
+int esb_last_hip_error(void);
+
+/*
+ * Value set, eq. (4)-(5) (Sec. 3.2).  Host only.
+ * Writes the 2^n - 1 unscaled values of Q_e(1, n, k) in ascending order
+ * (negatives, 0, positives) to vals_out[0 .. 2^n-2] (host, capacity `cap`
+ * floats) and the count to *count_out (host).  The values are exact in fp32.
+ * Returns ESB_E_INVALID for bad (n, k_sig), NULL pointers or cap < 2^n - 1.
+ */
+int esb_valueset(int n, int k_sig, float* vals_out, int cap, int* count_out);
+
+/*
+ * Projection operator Pi, eq. (6)-(8) (Sec. 3.3), emitting eq. (14) codes.
+ *   x       device, len fp32 values, any layout;
+ *   alpha   device, one fp32 scale (read on the device, so a preceding
+ *           esb_dda_align on the same stream can produce it);
+ *   codes   device, len bytes, same element order as x.
+ * For each element: v = fl32(x / alpha) (IEEE binary32 division), clipped to
+ * [-C, C] with C the largest set value, then rounded to the nearest set value
+ * with ties going to the larger magnitude, sign restored (Pi(-x) = -Pi(x)).
+ * NaN inputs give the +0 code; +-Inf give +-C.  If *alpha is not a positive
+ * finite number every code is the +0 code.  len == 0 enqueues nothing.
+ */
+int esb_project(const float* x, int64_t len, const float* alpha, int n, int k_sig,
+                uint8_t* codes, void* stream);
+
+/*
+ * Dequantization: out[i] = fl32(alpha * q(codes[i])), the values alpha * P(v)
+ * of eq. (8).  codes, alpha, out are device pointers; len elements.
+ */
+int esb_dequantize(const uint8_t* codes, int64_t len, const float* alpha, int n, int k_sig,
+                   float* out, void* stream);
+
+/*
+ * Bytes of device workspace esb_dda_align needs for these arguments (0 for
+ * invalid arguments).  Deterministic in its arguments.
+ */
+size_t esb_dda_workspace_size(int64_t len, int n, int k_sig, int G);
+
+/*
+ * Distribution difference aligner: the search for the scale alpha of eq. (13)
+ * over a candidate grid, with the objective of eq. (9) taken on the data
+ * (the empirical distribution of x in place of p, both signs):
+ *   D_j = sum_i (x_i - alpha_j * q_j(x_i))^2,   j = 0 .. G-1,
+ * where q_j(x_i) is the projection of x_i under alpha_j (as esb_project).
+ *   x          device, len fp32 values;
+ *   grid       device, G fp32 candidate scales, 1 <= G and G * (2^(n-1)-1) <= 8192;
+ *   alpha_out  device, one fp32: receives grid[j*];
+ *   D_out      device, G doubles (may be NULL): the objective per candidate;
+ *   workspace  device, at least esb_dda_workspace_size(len, n, k_sig, G) bytes.
+ * j* is the smallest index with the least D_j.  A candidate that is not a
+ * positive finite number gets D_j = NaN and ranks above every number; if any
+ * x_i is NaN every D_j is NaN, else if any is +-Inf every D_j is +Inf (so
+ * j* = 0).  D_j is accumulated in fp64 from exact per-interval partial sums;
+ * it is deterministic for a given (len, grid) and agrees with the exact sum to
+ * about 1e-12 relative.  Concurrent calls must use distinct workspaces.
+ */
+int esb_dda_align(const float* x, int64_t len, int n, int k_sig, const float* grid, int G,
+                  float* alpha_out, double* D_out, void* workspace, size_t ws_bytes,
+                  void* stream);
+
+/*
+ * Contraction over codes (Sec. 4.2, Forward(A_q, W_q); multiplication eq. (15)):
+ *   acc[i][j] = sum_k mA[i][k] * mB[k][j]     (exact, int32)
+ *   y[i][j]   = fl32(s * fl32(acc[i][j])),   s = 2^-(kA+kB) * fl32(alphaA * alphaB)
+ * where m = q * 2^k is the exact integer of a code (q its unscaled value, k
+ * the paper's fraction bits) and kA = kA_sig - 1, kB = kB_sig - 1.
+ *   A        device, M x K codes, row-major with row pitch lda >= K bytes;
+ *   B        device, N x K codes (b_layout ESB_B_NK, ldb >= K) or K x N codes
+ *            (ESB_B_KN, ldb >= N);
+ *   alphaA, alphaB  device, one fp32 each (only used for y);
+ *   acc      device, M x N int32 with row pitch ldc elements, or NULL;
+ *   y        device, M x N fp32 with row pitch ldc elements, or NULL;
+ *            at least one of acc, y must be non-NULL.
+ * ESB_E_UNSUPPORTED if an operand's largest decoded integer exceeds 32639
+ * (operands above 127 use a split high/low int8 decomposition); ESB_E_OVERFLOW
+ * if K * max|mA| * max|mB| > 2^31 - 1.  M, N or K == 0 is allowed (K == 0
+ * writes zeros).
+ */
+int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+             const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+             const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+             void* stream);
+
+/* Convolution geometry.  Output P = (H + 2*pad_h - R)/stride_h + 1, Q likewise. */
+typedef struct esb_conv_desc {
+    int N, H, W, C;          /* input batch, height, width, channels (NHWC) */
+    int K, R, S;             /* output channels, filter height, filter width */
+    int stride_h, stride_w;  /* >= 1 */
+    int pad_h, pad_w;        /* >= 0, zero padding by value 0 */
+    int groups;              /* divides C and K; groups == C == K is depthwise */
+} esb_conv_desc;
+
+/*
+ * Convolution stage of Sec. 4.2 (Fig. "computing_logic"): cross-correlation of
+ * ESB-coded activations with ESB-coded filters, as an implicit GEMM with
+ * M = N*P*Q, N = K, reduction R*S*C/groups, scaled like esb_gemm.
+ *   x      device, NHWC codes [N, H, W, C];
+ *   w      device, KRSC codes [K, R, S, C/groups];
+ *   acc    device, NHWC int32 [N, P, Q, K], or NULL;
+ *   y      device, NHWC fp32 [N, P, Q, K], or NULL (at least one non-NULL).
+ * Errors as esb_gemm, with the reduction length R*S*C/groups.
+ */
+int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+               const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+               const float* alphaW, int32_t* acc, float* y, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ESB_H */

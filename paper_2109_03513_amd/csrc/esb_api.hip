@@ -1,0 +1,203 @@
+// C ABI of libesb: argument validation, format tables, dispatch.
+#include <math.h>
+#include <string.h>
+
+#include "../../include/esb.h"
+#include "esb_internal.h"
+
+namespace esb {
+
+bool valid_fmt(int n, int k_sig) { return n >= 2 && n <= 8 && k_sig >= 1 && k_sig <= n - 1; }
+
+// ESB(b, k) as a minifloat: 1 sign bit, b-k-1 exponent bits, k fraction bits,
+// the all-ones exponent being the subnormal binade (eq. (14)).
+Fmt make_fmt(int n, int k_sig) {
+    Fmt f;
+    f.n = n;
+    f.k = k_sig - 1;
+    f.ebits = n - f.k - 1;
+    f.N = (1 << f.ebits) - 1;
+    f.zero_code = (uint32_t)f.N << f.k;
+    f.c_code = ((uint32_t)(f.N - 1) << f.k) | ((1u << f.k) - 1u);
+    f.sign_bit = 1u << (n - 1);
+    f.C = ldexpf((float)((1 << (f.k + 1)) - 1), f.N - f.k - 1);
+    uint32_t cb;
+    memcpy(&cb, &f.C, 4);
+    f.c_bits = cb;
+    const double mi = ldexp((double)((1 << (f.k + 1)) - 1), f.N - 1);
+    f.max_int = mi > 2147483647.0 ? 2147483647 : (int)mi;
+    return f;
+}
+
+double decode_value(const Fmt& f, uint32_t code) {
+    code &= (1u << f.n) - 1u;
+    const uint32_t e = (code >> f.k) & (uint32_t)f.N;
+    const uint32_t fr = code & ((1u << f.k) - 1u);
+    const double mag = (e == (uint32_t)f.N) ? ldexp((double)fr, -f.k)
+                                             : ldexp((double)((1u << f.k) | fr), (int)e - f.k);
+    return (code & f.sign_bit) ? -mag : mag;
+}
+
+int decode_int(const Fmt& f, uint32_t code) {
+    const double v = ldexp(decode_value(f, code), f.k);
+    return v > 2147483647.0 ? 2147483647 : (v < -2147483647.0 ? -2147483647 : (int)v);
+}
+
+int num_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+            v = 256;
+        cached[dev] = v;
+    }
+    return cached[dev];
+}
+
+}  // namespace esb
+
+using namespace esb;
+
+static thread_local int g_last_hip = 0;
+
+static int hip_status(hipError_t e) {
+    if (e == hipSuccess) return ESB_OK;
+    g_last_hip = (int)e;
+    return ESB_E_HIP;
+}
+
+extern "C" {
+
+int esb_version(void) { return 100; }
+
+const char* esb_strerror(int status) {
+    switch (status) {
+        case ESB_OK: return "ok";
+        case ESB_E_INVALID: return "invalid argument";
+        case ESB_E_OVERFLOW: return "int32 accumulator bound exceeded";
+        case ESB_E_UNSUPPORTED: return "decoded integers exceed the split int8 range";
+        case ESB_E_HIP: return "HIP runtime error";
+        case ESB_E_WORKSPACE: return "workspace missing or too small";
+        default: return "unknown status";
+    }
+}
+
+int esb_last_hip_error(void) { return g_last_hip; }
+
+int esb_valueset(int n, int k_sig, float* vals_out, int cap, int* count_out) {
+    if (!valid_fmt(n, k_sig) || !vals_out || !count_out) return ESB_E_INVALID;
+    const int count = (1 << n) - 1;
+    if (cap < count) return ESB_E_INVALID;
+    const Fmt f = make_fmt(n, k_sig);
+    float v[256];
+    int m = 0;
+    for (uint32_t c = 0; c < (1u << n); c++) {
+        if ((c & f.sign_bit) && ((c & ~f.sign_bit) == f.zero_code)) continue;   // -0
+        v[m++] = (float)decode_value(f, c);
+    }
+    for (int i = 1; i < m; i++)
+        for (int t = i; t > 0 && v[t] < v[t - 1]; t--) {
+            const float tmp = v[t]; v[t] = v[t - 1]; v[t - 1] = tmp;
+        }
+    memcpy(vals_out, v, sizeof(float) * (size_t)m);
+    *count_out = m;
+    return ESB_OK;
+}
+
+int esb_project(const float* x, int64_t len, const float* alpha, int n, int k_sig, uint8_t* codes,
+                void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !alpha) return ESB_E_INVALID;
+    if (len > 0 && (!x || !codes)) return ESB_E_INVALID;
+    return hip_status(launch_project(x, len, alpha, make_fmt(n, k_sig), codes, (hipStream_t)stream));
+}
+
+int esb_dequantize(const uint8_t* codes, int64_t len, const float* alpha, int n, int k_sig,
+                   float* out, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !alpha) return ESB_E_INVALID;
+    if (len > 0 && (!codes || !out)) return ESB_E_INVALID;
+    return hip_status(launch_dequantize(codes, len, alpha, make_fmt(n, k_sig), out, (hipStream_t)stream));
+}
+
+size_t esb_dda_workspace_size(int64_t len, int n, int k_sig, int G) {
+    if (!valid_fmt(n, k_sig)) return 0;
+    DdaLayout L;
+    if (!dda_layout(len, make_fmt(n, k_sig), G, &L)) return 0;
+    return L.total;
+}
+
+int esb_dda_align(const float* x, int64_t len, int n, int k_sig, const float* grid, int G,
+                  float* alpha_out, double* D_out, void* workspace, size_t ws_bytes, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !grid || !alpha_out) return ESB_E_INVALID;
+    if (len > 0 && !x) return ESB_E_INVALID;
+    const Fmt f = make_fmt(n, k_sig);
+    DdaLayout L;
+    if (!dda_layout(len, f, G, &L)) return ESB_E_INVALID;
+    if (!workspace || ws_bytes < L.total) return ESB_E_WORKSPACE;
+    return hip_status(launch_dda(x, len, f, grid, G, alpha_out, D_out, workspace, L, (hipStream_t)stream));
+}
+
+static int contraction_contract(int64_t kred, const Fmt& a, const Fmt& b) {
+    if (a.max_int > 32639 || b.max_int > 32639) return ESB_E_UNSUPPORTED;
+    if ((double)kred * (double)a.max_int * (double)b.max_int > 2147483647.0) return ESB_E_OVERFLOW;
+    return ESB_OK;
+}
+
+int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+             const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+             const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc, void* stream) {
+    if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig)) return ESB_E_INVALID;
+    if (M < 0 || N < 0 || K < 0 || (b_layout != ESB_B_NK && b_layout != ESB_B_KN)) return ESB_E_INVALID;
+    if (!acc && !y) return ESB_E_INVALID;
+    if (ldc < N || lda < K || (b_layout == ESB_B_NK ? ldb < K : ldb < N)) return ESB_E_INVALID;
+    if (y && (!alphaA || !alphaB)) return ESB_E_INVALID;
+    if ((int64_t)M * N > 0 && K > 0 && (!A || !B)) return ESB_E_INVALID;
+    const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
+    const int st = contraction_contract(K, fa, fb);
+    if (st) return st;
+    if (M == 0 || N == 0) return ESB_OK;
+    ConvGeom g;
+    g.Nb = M; g.H = 1; g.W = 1; g.C = K; g.pitch = (int)(lda > 0x7fffffff ? 0x7fffffff : lda);
+    g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
+    if (lda > 0x7fffffff) return ESB_E_INVALID;
+    return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
+                                         decode_info(fb), alphaB, acc, y, ldc, N, (hipStream_t)stream));
+}
+
+int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
+               const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
+               void* stream) {
+    if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return ESB_E_INVALID;
+    if (!acc && !y) return ESB_E_INVALID;
+    if (y && (!alphaX || !alphaW)) return ESB_E_INVALID;
+    if (d->N < 0 || d->H < 1 || d->W < 1 || d->C < 1 || d->K < 1 || d->R < 1 || d->S < 1 ||
+        d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0 || d->groups < 1 ||
+        d->C % d->groups || d->K % d->groups)
+        return ESB_E_INVALID;
+    if ((int64_t)d->H + 2 * d->pad_h < d->R || (int64_t)d->W + 2 * d->pad_w < d->S) return ESB_E_INVALID;
+    const int P = (d->H + 2 * d->pad_h - d->R) / d->stride_h + 1;
+    const int Q = (d->W + 2 * d->pad_w - d->S) / d->stride_w + 1;
+    const int64_t Mrows = (int64_t)d->N * P * Q;
+    if (Mrows > 0x7fffffff) return ESB_E_INVALID;
+    const int Cg = d->C / d->groups, Kg = d->K / d->groups;
+    const int64_t kred = (int64_t)d->R * d->S * Cg;
+    if (kred > 0x7fffffff) return ESB_E_INVALID;
+    if (Mrows > 0 && (!x || !w)) return ESB_E_INVALID;
+    const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
+    const int st = contraction_contract(kred, fx, fw);
+    if (st) return st;
+    if (Mrows == 0) return ESB_OK;
+    ConvGeom g;
+    g.Nb = d->N; g.H = d->H; g.W = d->W; g.C = d->C; g.pitch = d->C; g.Cg = Cg;
+    g.R = d->R; g.S = d->S; g.sh = d->stride_h; g.sw = d->stride_w; g.ph = d->pad_h; g.pw = d->pad_w;
+    g.P = P; g.Q = Q;
+    const hipStream_t s = (hipStream_t)stream;
+    if (Cg == 1 && Kg == 1 && (int64_t)d->C * d->R * d->S <= 16384)
+        return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
+    return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
+                                         alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
+                                         d->K, Kg, s));
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Internal declarations of libesb (gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace esb {
+
+// Native clang vectors (HIP's float4 is a struct, not usable with the
+// nontemporal builtins).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Parameters of one ESB(b, k) format, k = fraction bits (paper notation),
+// derived on the host from (n, k_sig) by make_fmt().
+struct Fmt {
+    int n;            // total bits b
+    int k;            // fraction bits, k = k_sig - 1
+    int ebits;        // exponent bits, b - k - 1
+    int N;            // 2^ebits - 1: the all-ones exponent is the subnormal binade
+    uint32_t zero_code;   // +0: exponent all ones, fraction 0, sign 0
+    uint32_t c_code;      // largest value C = 2^(N-1) * (2 - 2^-k)
+    uint32_t sign_bit;    // 1 << (b-1)
+    uint32_t c_bits;      // fp32 bit pattern of C
+    float C;
+    int max_int;          // largest |m|, m = q * 2^k the exact integer of a code
+};
+
+bool valid_fmt(int n, int k_sig);
+Fmt make_fmt(int n, int k_sig);
+int decode_int(const Fmt& f, uint32_t code);   // m = q * 2^k (host)
+double decode_value(const Fmt& f, uint32_t code);
+int num_cus();
+
+// ----------------------------------------------------------------- projection
+struct ProjParams {
+    uint32_t k, zero_code, c_code, c_bits, sign_bit, one;   // one = 2^k
+};
+ProjParams proj_params(const Fmt& f);
+
+hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,
+                          uint8_t* codes, hipStream_t s);
+hipError_t launch_dequantize(const uint8_t* codes, int64_t len, const float* alpha, const Fmt& f,
+                             float* out, hipStream_t s);
+
+// ----------------------------------------------------------------------- DDA
+constexpr int kDdaMaxThresholds = 8192;   // G * (2^(b-1) - 1)
+constexpr int kDdaMaxG = 1024;
+constexpr int kDdaBins = 4096;
+constexpr int kDdaMaxBlocks = 256;
+
+struct DdaLayout {
+    int G, M, A;            // candidates, midpoints per candidate, thresholds (G*M)
+    int nblk;               // blocks of the one-pass histogram kernel
+    size_t off_ubits, off_rank, off_bins, off_meta, off_pcnt, off_psum, off_pscal,
+        off_s0, off_s1, total;
+};
+bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L);
+hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
+                      float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
+                      hipStream_t s);
+
+// ---------------------------------------------------------------- contraction
+// Decoding of one operand's codes to exact integers.
+struct DecodeInfo {
+    uint32_t lut[8];   // int8 m for codes 0..31 (perm modes), 4 per dword
+    int mode;          // 3, 4, 5: v_perm table for n <= 3, n == 4, n == 5; 0: arithmetic
+    int n, k, emax;
+    int split;         // 1: m needs the high/low int8 split
+};
+DecodeInfo decode_info(const Fmt& f);
+
+struct ConvGeom {   // implicit-GEMM view; a dense row-major A is N=M, H=W=1, R=S=1
+    int Nb, H, W, C, pitch, Cg, R, S, sh, sw, ph, pw, P, Q;
+};
+
+hipError_t launch_contraction(int M, int N, int K, int groups, const ConvGeom& ga,
+                              const uint8_t* A, const DecodeInfo& da, const float* alphaA,
+                              const uint8_t* B, int64_t ldb, int b_layout, const DecodeInfo& db,
+                              const float* alphaB, int32_t* acc, float* y, int64_t ldc,
+                              int out_col_per_group, hipStream_t s);
+
+// Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
+hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
+                         const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,
+                         float* y, hipStream_t s);
+
+}  // namespace esb

@@ -1,0 +1,211 @@
+"""Thin ctypes binding of libesb (include/esb.h), same entry-point names.
+
+Argument marshalling only: every step of the hot path runs in the HIP kernels
+of libesb.so.  PyTorch provides device memory and streams.  If libesb.so is
+missing the import of any entry point raises; there is no fallback.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libesb.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "esb.h")
+
+ESB_OK = 0
+ESB_E_INVALID = -1
+ESB_E_OVERFLOW = -3
+ESB_E_UNSUPPORTED = -4
+ESB_E_HIP = -5
+ESB_E_WORKSPACE = -6
+ESB_B_NK = 0
+ESB_B_KN = 1
+
+_lib = None
+
+
+class EsbError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        msg = lib().esb_strerror(status).decode()
+        if status == ESB_E_HIP:
+            msg += " (hipError %d)" % lib().esb_last_hip_error()
+        super().__init__("%s: %s (%d)" % (fn, msg, status))
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in
+                ("N", "H", "W", "C", "K", "R", "S", "stride_h", "stride_w", "pad_h", "pad_w",
+                 "groups")]
+
+
+def lib():
+    """Load libesb.so (after torch, so that both share one HIP runtime)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libesb.so not built: run paper_2109_03513_amd.build.build()")
+        try:
+            import torch  # noqa: F401  (loads torch's HIP runtime first)
+        except ImportError:
+            pass
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+        sig = {
+            "esb_version": (i32, []),
+            "esb_strerror": (ctypes.c_char_p, [i32]),
+            "esb_last_hip_error": (i32, []),
+            "esb_valueset": (i32, [i32, i32, P, i32, P]),
+            "esb_project": (i32, [P, i64, P, i32, i32, P, P]),
+            "esb_dequantize": (i32, [P, i64, P, i32, i32, P, P]),
+            "esb_dda_workspace_size": (sz, [i64, i32, i32, i32]),
+            "esb_dda_align": (i32, [P, i64, i32, i32, P, i32, P, P, P, sz, P]),
+            "esb_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32, P, P,
+                               i64, P]),
+            "esb_conv2d": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
+                                 P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(fn, status):
+    if status != ESB_OK:
+        raise EsbError(fn, status)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(stream if isinstance(stream, int) else stream.cuda_stream)
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev_tensor(t, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s" % (name, dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def esb_version():
+    return lib().esb_version()
+
+
+def esb_valueset(n, k_sig):
+    """Sorted 2^n - 1 unscaled values of Q_e (host call)."""
+    out = np.zeros(256, dtype=np.float32)
+    cnt = ctypes.c_int(0)
+    _check("esb_valueset", lib().esb_valueset(n, k_sig, out.ctypes.data_as(ctypes.c_void_p), 256,
+                                              ctypes.byref(cnt)))
+    return out[:cnt.value].copy()
+
+
+def esb_project(x, alpha, n, k_sig, codes=None, stream=None):
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(alpha, torch.float32, "alpha")
+    if codes is None:
+        codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _dev_tensor(codes, torch.uint8, "codes")
+    if codes.numel() != x.numel():
+        raise ValueError("codes must have as many elements as x")
+    _check("esb_project", lib().esb_project(_ptr(x), x.numel(), _ptr(alpha), n, k_sig, _ptr(codes),
+                                            _stream(stream)))
+    return codes
+
+
+def esb_dequantize(codes, alpha, n, k_sig, out=None, stream=None):
+    import torch
+    _dev_tensor(codes, torch.uint8, "codes")
+    _dev_tensor(alpha, torch.float32, "alpha")
+    if out is None:
+        out = torch.empty(codes.shape, dtype=torch.float32, device=codes.device)
+    _dev_tensor(out, torch.float32, "out")
+    _check("esb_dequantize", lib().esb_dequantize(_ptr(codes), codes.numel(), _ptr(alpha), n, k_sig,
+                                                  _ptr(out), _stream(stream)))
+    return out
+
+
+def esb_dda_workspace_size(length, n, k_sig, G):
+    return int(lib().esb_dda_workspace_size(length, n, k_sig, G))
+
+
+def esb_dda_align(x, n, k_sig, grid, alpha_out=None, D_out=None, workspace=None, stream=None,
+                  want_D=True):
+    """Returns (alpha_out[1] fp32 tensor, D_out[G] fp64 tensor or None)."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(grid, torch.float32, "grid")
+    G = grid.numel()
+    dev = x.device
+    if alpha_out is None:
+        alpha_out = torch.empty(1, dtype=torch.float32, device=dev)
+    if D_out is None and want_D:
+        D_out = torch.empty(G, dtype=torch.float64, device=dev)
+    need = esb_dda_workspace_size(x.numel(), n, k_sig, G)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("esb_dda_align", lib().esb_dda_align(_ptr(x), x.numel(), n, k_sig, _ptr(grid), G,
+                                                _ptr(alpha_out), _ptr(D_out), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(),
+                                                _stream(stream)))
+    return alpha_out, D_out
+
+
+def esb_gemm(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, b_layout=ESB_B_NK, acc=None, y=None,
+             want_acc=True, want_y=True, stream=None):
+    """A: M x K codes; B: N x K (ESB_B_NK) or K x N (ESB_B_KN) codes.  Returns (acc, y)."""
+    import torch
+    _dev_tensor(A, torch.uint8, "A")
+    _dev_tensor(B, torch.uint8, "B")
+    M, K = A.shape
+    N = B.shape[0] if b_layout == ESB_B_NK else B.shape[1]
+    dev = A.device
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=dev)
+    if y is None and want_y:
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    _check("esb_gemm", lib().esb_gemm(M, N, K, _ptr(A), A.stride(0) if M else K, nA, kA_sig,
+                                      _ptr(alphaA), _ptr(B), B.stride(0) if B.shape[0] else 0,
+                                      nB, kB_sig, _ptr(alphaB), b_layout, _ptr(acc), _ptr(y), N,
+                                      _stream(stream)))
+    return acc, y
+
+
+def conv_out_hw(H, W, R, S, stride, pad):
+    return (H + 2 * pad[0] - R) // stride[0] + 1, (W + 2 * pad[1] - S) // stride[1] + 1
+
+
+def esb_conv2d(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, stride=(1, 1), pad=(0, 0), groups=1,
+               acc=None, y=None, want_acc=True, want_y=True, stream=None):
+    """x: [N, H, W, C] codes (NHWC); w: [K, R, S, C/groups] codes (KRSC).  Returns (acc, y) NHWC."""
+    import torch
+    _dev_tensor(x, torch.uint8, "x")
+    _dev_tensor(w, torch.uint8, "w")
+    Nb, H, W, C = x.shape
+    K, R, S, _ = w.shape
+    P, Q = conv_out_hw(H, W, R, S, stride, pad)
+    dev = x.device
+    if acc is None and want_acc:
+        acc = torch.empty((Nb, P, Q, K), dtype=torch.int32, device=dev)
+    if y is None and want_y:
+        y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
+    d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], groups)
+    _check("esb_conv2d", lib().esb_conv2d(ctypes.byref(d), _ptr(x), nX, kX_sig, _ptr(alphaX),
+                                          _ptr(w), nW, kW_sig, _ptr(alphaW), _ptr(acc), _ptr(y),
+                                          _stream(stream)))
+    return acc, y

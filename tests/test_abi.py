@@ -1,0 +1,104 @@
+"""The C ABI loads and exports every symbol include/esb.h declares; host-only
+calls and argument validation work without a GPU (no device work is enqueued
+by any call in this file)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import ALL_BK, ROOT
+
+LIB = os.path.join(ROOT, "paper_2109_03513_amd", "libesb.so")
+HEADER = os.path.join(ROOT, "include", "esb.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(LIB):
+        from paper_2109_03513_amd import build
+        build.build()
+    from paper_2109_03513_amd import esb
+    return esb.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(esb_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 10, names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_strerror(L):
+    assert L.esb_version() >= 100
+    for s in (0, -1, -3, -4, -5, -6, 12345):
+        assert isinstance(L.esb_strerror(s), bytes)
+
+
+@pytest.mark.parametrize("b,ks", ALL_BK)
+def test_valueset_matches_oracle(b, ks):
+    from paper_2109_03513_amd import esb
+    np.testing.assert_array_equal(esb.esb_valueset(b, ks), oracle.full_valueset(b, ks).astype(np.float32))
+
+
+def test_valueset_errors(L):
+    out = np.zeros(4, np.float32)
+    cnt = ctypes.c_int()
+    p = out.ctypes.data_as(ctypes.c_void_p)
+    assert L.esb_valueset(4, 2, p, 4, ctypes.byref(cnt)) == -1          # cap too small
+    assert L.esb_valueset(9, 2, p, 1000, ctypes.byref(cnt)) == -1
+    assert L.esb_valueset(4, 4, p, 1000, ctypes.byref(cnt)) == -1
+    assert L.esb_valueset(4, 2, None, 1000, ctypes.byref(cnt)) == -1
+
+
+def test_argument_validation_without_launch(L):
+    fake = ctypes.c_void_p(0x1000)     # never dereferenced: every call below fails validation
+    assert L.esb_project(fake, -1, fake, 4, 2, fake, None) == -1
+    assert L.esb_project(fake, 10, fake, 4, 0, fake, None) == -1
+    assert L.esb_project(None, 10, fake, 4, 2, fake, None) == -1
+    assert L.esb_project(fake, 10, None, 4, 2, fake, None) == -1
+    assert L.esb_dequantize(fake, 10, fake, 1, 1, fake, None) == -1
+    # DDA: grid too large, workspace missing / too small
+    assert L.esb_dda_align(fake, 100, 8, 7, fake, 65, fake, None, fake, 1 << 30, None) == -1
+    assert L.esb_dda_align(fake, 100, 4, 2, fake, 64, fake, None, None, 0, None) == -6
+    need = L.esb_dda_workspace_size(100, 4, 2, 64)
+    assert need > 0
+    assert L.esb_dda_align(fake, 100, 4, 2, fake, 64, fake, None, fake, need - 1, None) == -6
+    assert L.esb_dda_workspace_size(100, 4, 2, 0) == 0
+    assert L.esb_dda_workspace_size(100, 8, 7, 65) == 0
+    # GEMM contract: unsupported magnitudes, overflow, bad pitches, no output
+    g = L.esb_gemm
+    assert g(4, 4, 8, fake, 8, 6, 2, fake, fake, 8, 6, 2, fake, 0, fake, None, 4, None) == -4
+    assert g(4, 4, 600, fake, 600, 8, 5, fake, fake, 600, 8, 5, fake, 0, fake, None, 4, None) == -3
+    assert g(4, 4, 8, fake, 7, 4, 2, fake, fake, 8, 4, 2, fake, 0, fake, None, 4, None) == -1
+    assert g(4, 4, 8, fake, 8, 4, 2, fake, fake, 8, 4, 2, fake, 0, None, None, 4, None) == -1
+    assert g(4, 4, 8, fake, 8, 4, 2, fake, fake, 8, 4, 2, fake, 2, fake, None, 4, None) == -1
+    assert g(4, 4, 8, fake, 8, 4, 2, None, fake, 8, 4, 2, fake, 0, None, fake, 4, None) == -1
+    from paper_2109_03513_amd.esb import ConvDesc
+    d = ConvDesc(1, 8, 8, 6, 4, 3, 3, 1, 1, 1, 1, 4)       # groups does not divide C
+    assert L.esb_conv2d(ctypes.byref(d), fake, 4, 2, fake, fake, 4, 2, fake, fake, None, None) == -1
+    d = ConvDesc(1, 2, 2, 4, 4, 5, 5, 1, 1, 0, 0, 1)       # window larger than padded input
+    assert L.esb_conv2d(ctypes.byref(d), fake, 4, 2, fake, fake, 4, 2, fake, fake, None, None) == -1
+    d = ConvDesc(1, 8, 8, 600, 4, 1, 1, 1, 1, 0, 0, 1)
+    assert L.esb_conv2d(ctypes.byref(d), fake, 8, 5, fake, fake, 8, 5, fake, fake, None, None) == -3
+
+
+def test_contract_matches_oracle():
+    """Status codes of the contraction contract agree with the oracle's."""
+    from paper_2109_03513_amd import esb
+    fake = ctypes.c_void_p(0x1000)
+    for (bA, ksA), (bB, ksB), K in [((6, 2), (4, 2), 8), ((8, 5), (8, 5), 545), ((8, 5), (8, 5), 546),
+                                    ((5, 1), (3, 1), 4)]:
+        A = np.zeros((1, K), np.uint8)
+        ost = oracle.gemm(A, A, bA, ksA, 1.0, bB, ksB, 1.0)[0]
+        gst = esb.lib().esb_gemm(0, 0, K, fake, K, bA, ksA, fake, fake, K, bB, ksB, fake, 0, fake,
+                                 None, 0, None)
+        assert gst == ost, (bA, ksA, bB, ksB, K, gst, ost)

@@ -1,0 +1,173 @@
+"""GPU contraction (esb_gemm, esb_conv2d) vs the oracle: bit-exact int32
+accumulators; scaled fp32 outputs within 1e-6 relative (they are computed as
+fl32(s * fl32(acc)) on both sides, so they agree bit for bit in practice)."""
+import numpy as np
+import pytest
+
+import oracle
+from gpuutil import assert_rel, dev, host, log, scalar
+from paper_2109_03513_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+YREL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def esb():
+    from paper_2109_03513_amd import esb as e
+    e.lib()
+    return e
+
+
+def gemm_case(esb, M, N, K, fa, fb, layout=0, seed=0, aA=0.37, aB=0.021, want_acc=True, want_y=True):
+    (bA, ksA), (bB, ksB) = fa, fb
+    A = wl.random_codes(seed, (M, K), 8)           # all 8 bits set at random: upper bits ignored
+    Bnk = wl.random_codes(seed + 1, (N, K), 8)
+    B = Bnk if layout == 0 else np.ascontiguousarray(Bnk.T)
+    log("gemm M=%d N=%d K=%d A=%s B=%s layout=%d" % (M, N, K, fa, fb, layout))
+    acc, y = esb.esb_gemm(dev(A), bA, ksA, scalar(aA), dev(B), bB, ksB, scalar(aB), b_layout=layout,
+                          want_acc=want_acc, want_y=want_y)
+    st, oacc, oy = oracle.gemm(A, B, bA, ksA, aA, bB, ksB, aB, b_layout=layout)
+    assert st == 0
+    if want_acc:
+        np.testing.assert_array_equal(host(acc), oacc)
+    if want_y:
+        assert_rel(host(y), oy, YREL, "y")
+
+
+SHAPES = [(1, 1, 1), (7, 5, 33), (16, 16, 64), (64, 64, 576), (65, 63, 130), (128, 128, 128),
+          (129, 257, 200), (300, 70, 1000), (256, 512, 64)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("fmt", [((4, 2), (4, 2)), ((3, 2), (3, 1)), ((5, 3), (5, 3)),
+                                 ((2, 1), (8, 7)), ((7, 5), (6, 4))])
+def test_gemm_int8_path(esb, shape, fmt):
+    gemm_case(esb, *shape, *fmt)
+
+
+@pytest.mark.parametrize("shape", [(7, 5, 33), (64, 64, 576), (129, 65, 200)])
+@pytest.mark.parametrize("fmt", [((5, 2), (5, 2)), ((8, 5), (4, 2)), ((3, 2), (8, 6)),
+                                 ((5, 1), (3, 1)), ((6, 3), (6, 3))])
+def test_gemm_split_path(esb, shape, fmt):
+    M, N, K = shape
+    (bA, ksA), (bB, ksB) = fmt
+    MA = oracle.C(bA, ksA) * 2 ** (ksA - 1)
+    MB = oracle.C(bB, ksB) * 2 ** (ksB - 1)
+    if K * MA * MB > 2 ** 31 - 1:
+        K = int((2 ** 31 - 1) // (MA * MB))
+    gemm_case(esb, M, N, K, *fmt)
+
+
+@pytest.mark.parametrize("shape", [(7, 5, 33), (64, 64, 576), (100, 300, 17)])
+def test_gemm_kn_layout(esb, shape):
+    gemm_case(esb, *shape, (4, 2), (4, 2), layout=1)
+    gemm_case(esb, *shape, (5, 2), (4, 2), layout=1)
+
+
+def test_gemm_outputs_and_degenerate(esb):
+    gemm_case(esb, 33, 17, 64, (4, 2), (4, 2), want_y=False)
+    gemm_case(esb, 33, 17, 64, (4, 2), (4, 2), want_acc=False)
+    gemm_case(esb, 5, 6, 0, (4, 2), (4, 2))          # K = 0 writes zeros
+    gemm_case(esb, 8, 8, 64, (4, 2), (4, 2), aA=0.0)             # zero scale: y = +-0
+
+
+def test_gemm_tiny_workload(esb):
+    """Config: 64x576 weights times 576x64 activations, ESB(4,1) both, alpha by DDA."""
+    c = wl.tiny_gemm(0)
+    Wd, Ad = dev(c["W"]), dev(c["A"])
+    aW, _ = esb.esb_dda_align(Wd, 4, 2, dev(c["gridW"]))
+    aA, _ = esb.esb_dda_align(Ad, 4, 2, dev(c["gridA"]))
+    cW = esb.esb_project(Wd, aW, 4, 2)
+    cA = esb.esb_project(Ad, aA, 4, 2)
+    acc, y = esb.esb_gemm(cW, 4, 2, aW, cA, 4, 2, aA, b_layout=1)
+    jW, _ = oracle.dda(c["W"], 4, 2, c["gridW"])
+    jA, _ = oracle.dda(c["A"], 4, 2, c["gridA"])
+    oW = oracle.project(c["W"], c["gridW"][jW], 4, 2)
+    oA = oracle.project(c["A"], c["gridA"][jA], 4, 2)
+    np.testing.assert_array_equal(host(cW), oW)
+    np.testing.assert_array_equal(host(cA), oA)
+    st, oacc, oy = oracle.gemm(oW, oA, 4, 2, c["gridW"][jW], 4, 2, c["gridA"][jA], b_layout=1)
+    np.testing.assert_array_equal(host(acc), oacc)
+    assert_rel(host(y), oy, YREL, "y")
+
+
+def test_gemm_alexnet_fc_full(esb):
+    """AlexNet FC 9216->4096 at batch 128, W ESB(3,0), X ESB(3,1), full size."""
+    c = wl.alexnet_fc(0)
+    aW, aX = c["gridW"][9], c["gridX"][20]
+    cW = oracle.project(c["W"], aW, 3, 1)
+    cX = oracle.project(c["X"], aX, 3, 2)
+    log("gemm alexnet fc full")
+    acc, y = esb.esb_gemm(dev(cX), 3, 2, scalar(aX), dev(cW), 3, 1, scalar(aW))
+    st, oacc, oy = oracle.gemm(cX, cW, 3, 2, aX, 3, 1, aW)
+    np.testing.assert_array_equal(host(acc), oacc)
+    assert_rel(host(y), oy, YREL, "y")
+
+
+CONV_CASES = [
+    # N, H, W, C, K, R, stride, pad, groups
+    (1, 56, 56, 64, 64, 3, 1, 1, 1),       # ResNet18 layer1 3x3
+    (2, 9, 11, 8, 16, 3, 1, 1, 1),
+    (2, 15, 15, 3, 64, 7, 2, 3, 1),        # conv1-like, C = 3
+    (1, 14, 14, 128, 256, 3, 2, 1, 1),     # stride-2 3x3
+    (2, 14, 14, 64, 128, 1, 2, 0, 1),      # 1x1 stride-2 downsample
+    (2, 8, 8, 24, 144, 1, 1, 0, 1),        # 1x1 expand, C = 24
+    (2, 8, 8, 144, 24, 1, 1, 0, 1),        # 1x1 project
+    (2, 10, 10, 144, 144, 3, 1, 1, 144),   # depthwise
+    (1, 9, 7, 6, 6, 3, 2, 1, 6),           # depthwise, C % 4 != 0
+    (1, 8, 8, 32, 32, 3, 1, 1, 2),         # grouped, C/groups = 16
+    (1, 7, 7, 12, 8, 3, 1, 1, 4),          # grouped, C/groups = 3
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+@pytest.mark.parametrize("fmt", [((4, 2), (4, 2)), ((5, 3), (5, 3)), ((5, 2), (6, 3))])
+def test_conv_parity(esb, case, fmt):
+    Nb, H, W, C, K, R, st, pd, groups = case
+    (bX, ksX), (bW, ksW) = fmt
+    x = wl.random_codes(5, (Nb, H, W, C), 8)
+    w = wl.random_codes(6, (K, R, R, C // groups), 8)
+    log("conv %s fmt=%s" % (case, fmt))
+    acc, y = esb.esb_conv2d(dev(x), bX, ksX, scalar(0.5), dev(w), bW, ksW, scalar(0.03),
+                            stride=(st, st), pad=(pd, pd), groups=groups)
+    s, oacc, oy = oracle.conv2d(x, w, bX, ksX, 0.5, bW, ksW, 0.03, stride=(st, st), pad=(pd, pd),
+                                groups=groups)
+    assert s == 0
+    np.testing.assert_array_equal(host(acc), oacc)
+    assert_rel(host(y), oy, YREL, "y")
+
+
+def test_conv_resnet_workload(esb):
+    """ResNet18 3x3 conv 64->64 at 56x56, batch 1, ESB(4,1), DDA -> project -> conv on device."""
+    c = wl.resnet_conv3x3(0)
+    wd, xd = dev(c["w"]), dev(c["x"])
+    aW, _ = esb.esb_dda_align(wd, 4, 2, dev(c["gridW"]))
+    aX, _ = esb.esb_dda_align(xd, 4, 2, dev(c["gridX"]))
+    cw = esb.esb_project(wd, aW, 4, 2)
+    cx = esb.esb_project(xd, aX, 4, 2)
+    acc, y = esb.esb_conv2d(cx, 4, 2, aX, cw, 4, 2, aW, stride=(1, 1), pad=(1, 1))
+    jW, _ = oracle.dda(c["w"], 4, 2, c["gridW"])
+    jX, _ = oracle.dda(c["x"], 4, 2, c["gridX"])
+    ow = oracle.project(c["w"], c["gridW"][jW], 4, 2)
+    ox = oracle.project(c["x"], c["gridX"][jX], 4, 2)
+    s, oacc, oy = oracle.conv2d(ox, ow, 4, 2, c["gridX"][jX], 4, 2, c["gridW"][jW], stride=(1, 1),
+                                pad=(1, 1))
+    np.testing.assert_array_equal(host(acc), oacc)
+    assert_rel(host(y), oy, YREL, "y")
+
+
+def test_conv_mobilenet_block_full(esb):
+    """MobileNetV2 block at batch 32, 56x56: expand 1x1, depthwise 3x3, project 1x1; ESB(5,2)."""
+    m = wl.mobilenetv2_block(0)
+    aW, aX = m["gridW"][12], m["gridX"][10]
+    for L in m["layers"]:
+        cw = oracle.project(L["w"], aW, 5, 3)
+        cx = oracle.project(L["x"], aX, 5, 3)
+        log("conv mobilenet %s" % L["name"])
+        acc, y = esb.esb_conv2d(dev(cx), 5, 3, scalar(aX), dev(cw), 5, 3, scalar(aW),
+                                stride=L["stride"], pad=L["pad"], groups=L["groups"])
+        s, oacc, oy = oracle.conv2d(cx, cw, 5, 3, aX, 5, 3, aW, stride=L["stride"], pad=L["pad"],
+                                    groups=L["groups"])
+        np.testing.assert_array_equal(host(acc), oacc)
+        assert_rel(host(y), oy, YREL, "y " + L["name"])

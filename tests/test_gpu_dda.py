@@ -1,0 +1,135 @@
+"""GPU distribution difference aligner (esb_dda_align) vs the oracle:
+bit-exact chosen alpha, objective within 1e-9 relative.
+
+The tolerance: the GPU sums exact per-interval integer moments and combines
+D_j = S2 - 2 a A_j + a^2 B_j in fp64; the cancellation in that combination
+is at most S2 / D_j (about 1e4 for the finest formats) times fp64 rounding
+(1e-16) and the fixed-order reductions, so 1e-9 leaves a wide margin while a
+wrong cell boundary (one element moved) changes D by far more on these sizes."""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import ALL_BK
+from gpuutil import assert_rel, dev, host, log
+from paper_2109_03513_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+REL = 1e-9
+
+
+@pytest.fixture(scope="module")
+def esb():
+    from paper_2109_03513_amd import esb as e
+    e.lib()
+    return e
+
+
+def run(esb, x, b, ks, grid):
+    a, D = esb.esb_dda_align(dev(x), b, ks, dev(grid))
+    return host(a)[0], host(D)
+
+
+def check(esb, x, b, ks, grid, what, min_margin=1e-7):
+    log("dda %s b=%d k_sig=%d len=%d G=%d" % (what, b, ks, x.size, grid.size))
+    a, D = run(esb, x, b, ks, grid)
+    j, Do = oracle.dda(x, b, ks, grid)
+    assert_rel(D, Do, REL, what)
+    Ds = np.sort(Do[~np.isnan(Do)])
+    if Ds.size > 1 and np.isfinite(Ds[0]) and Ds[0] > 0:
+        margin = (Ds[1] - Ds[0]) / Ds[0]
+        if margin > min_margin:     # the argmin is decided by more than the tolerance
+            assert a == grid[j], (what, a, grid[j])
+    return a, D, j
+
+
+def test_dda_workload_tensors(esb):
+    c0 = wl.tiny_gemm(0)
+    check(esb, c0["W"], c0["nW"], c0["ksW"], c0["gridW"], "tiny W")
+    check(esb, c0["A"], c0["nA"], c0["ksA"], c0["gridA"], "tiny A")
+    c1 = wl.resnet_conv3x3(0)
+    check(esb, c1["w"], c1["nW"], c1["ksW"], c1["gridW"], "resnet w")
+    check(esb, c1["x"], c1["nX"], c1["ksX"], c1["gridX"], "resnet x")
+    c2 = wl.alexnet_fc(0)
+    check(esb, c2["X"], c2["nX"], c2["ksX"], c2["gridX"], "alexnet X")
+    check(esb, c2["W"], c2["nW"], c2["ksW"], c2["gridW"], "alexnet W")
+    m = wl.mobilenetv2_block(0)
+    check(esb, m["layers"][0]["x"], m["n"], m["ks"], m["gridX"], "mobilenet x_expand")
+    check(esb, m["layers"][1]["w"], m["n"], m["ks"], m["gridW"], "mobilenet w_dw")
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_dda_seeds(esb, seed):
+    c1 = wl.resnet_conv3x3(seed)
+    check(esb, c1["w"], c1["nW"], c1["ksW"], c1["gridW"], "resnet w seed %d" % seed)
+    check(esb, c1["x"], c1["nX"], c1["ksX"], c1["gridX"], "resnet x seed %d" % seed)
+
+
+@pytest.mark.parametrize("b,ks", ALL_BK)
+def test_dda_all_formats(esb, b, ks):
+    M = 2 ** (b - 1) - 1
+    G = min(64, 8192 // M)
+    x = np.random.default_rng([31, b, ks]).standard_normal(50000).astype(np.float32)
+    grid = wl.scale_grid(1.0, G)
+    check(esb, x, b, ks, grid, "normal")
+
+
+@pytest.mark.parametrize("length", [0, 1, 3, 4, 5, 1023, 16384, 16385, 300001])
+def test_dda_lengths(esb, length):
+    x = (np.random.default_rng(length).standard_normal(length) * 0.3).astype(np.float32)
+    check(esb, x, 4, 2, wl.scale_grid(0.3), "len")
+
+
+def test_dda_special_data(esb):
+    g = wl.scale_grid(1.0)
+    x = np.zeros(5000, np.float32)
+    a, D, _ = check(esb, x, 4, 2, g, "zeros")
+    assert (D == 0).all() and a == g[0]
+    x = np.random.default_rng(3).standard_normal(5000).astype(np.float32)
+    x[17] = np.inf
+    a, D, _ = check(esb, x, 4, 2, g, "inf")
+    assert np.isinf(D).all() and a == g[0]
+    x[17] = np.nan
+    a, D, _ = check(esb, x, 4, 2, g, "nan")
+    assert np.isnan(D).all() and a == g[0]
+    # subnormal data with tiny scales
+    x = (np.random.default_rng(4).standard_normal(5000) * 1e-40).astype(np.float32)
+    check(esb, x, 5, 3, (np.arange(1, 65) * 1e-41).astype(np.float32), "subnormal")
+    # heavy tails: outliers far above every threshold land in the unbounded top cell
+    x = np.random.default_rng(5).standard_normal(20000).astype(np.float32)
+    x[::97] *= 1e6
+    check(esb, x, 4, 2, g, "outliers")
+
+
+def test_dda_grid_rules(esb):
+    x = np.random.default_rng(6).standard_normal(20000).astype(np.float32)
+    grid = np.array([np.nan, 0.5, -1.0, 0.5, 0.0, np.inf, 0.49, 3e38, 1e-30], dtype=np.float32)
+    a, D, j = check(esb, x, 4, 2, grid, "grid rules")
+    assert np.isnan(D[[0, 2, 4, 5]]).all()
+    assert D[1] == D[3]
+    _, Do = oracle.dda(x, 4, 2, grid)
+    assert a == grid[int(np.nanargmin(Do))]
+    g1 = np.array([0.4871], dtype=np.float32)
+    a, D, _ = check(esb, x, 4, 2, g1, "G=1")
+    assert a == g1[0]
+    # G = 1024 candidates with ESB(2, k=0): 1024 thresholds
+    check(esb, x, 2, 1, wl.scale_grid(1.0, 1024), "G=1024")
+    # ESB(8, k=4) with 64 candidates: 8128 thresholds, the largest table
+    check(esb, x, 8, 5, wl.scale_grid(1.0, 64), "8128 thresholds")
+
+
+def test_dda_deterministic(esb):
+    c = wl.resnet_conv3x3(0)
+    a1, D1 = run(esb, c["x"], 4, 2, c["gridX"])
+    a2, D2 = run(esb, c["x"], 4, 2, c["gridX"])
+    assert a1 == a2 and np.array_equal(D1.view(np.uint64), D2.view(np.uint64))
+
+
+def test_dda_then_project_on_device(esb):
+    """alpha stays on the device: DDA output feeds the projection directly."""
+    c = wl.resnet_conv3x3(0)
+    xd = dev(c["w"])
+    alpha, _ = esb.esb_dda_align(xd, 4, 2, dev(c["gridW"]))
+    codes = host(esb.esb_project(xd, alpha, 4, 2))
+    j, _ = oracle.dda(c["w"], 4, 2, c["gridW"])
+    np.testing.assert_array_equal(codes, oracle.project(c["w"], c["gridW"][j], 4, 2))
