@@ -34,6 +34,10 @@ def parse():
                    help="approximate CPU time budget of the oracle baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (for counter calibration)")
+    p.add_argument("--sweep", action="store_true",
+                   help="time every kernel at the large layer shapes (one JSON line per case)")
+    p.add_argument("--only", default="", help="with --sweep: comma-separated case names")
+    p.add_argument("--reps", type=int, default=20)
     return p.parse_args()
 
 
@@ -59,6 +63,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.sweep:
+        sweep(args)
         return
 
     from paper_2109_03513_amd import esb, workloads
@@ -104,50 +111,79 @@ def main():
             esb.esb_conv2d(cx, n, ks, ax, cw, n, ks, aw, stride=c["stride"], pad=c["pad"], y=y,
                            want_acc=False, stream=sh)
 
+    def step():
+        for i in range(5):
+            run_stage(i)
+
     with torch.cuda.stream(stream):
-        for _ in range(args.warmup):
-            for i in range(5):
-                run_stage(i)
+        for _ in range(args.warmup):       # eager warm-up: first-call set-up happens here
+            step()
         stream.synchronize()
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+        # the whole step as one HIP graph: launch overhead out of the measurement
+        g_step = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_step, stream=stream):
+            step()
+        for _ in range(3):
+            g_step.replay()
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for s in range(args.steps):
-            ev[s][0].record(stream)
-            for i in range(5):
-                run_stage(i)
-                ev[s][i + 1].record(stream)
-        stream.synchronize()
-        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            g_step.replay()
+        e1.record(stream)
+        e1.synchronize()
         wall = time.perf_counter() - t0
-    stage_ms = [sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)) / args.steps
-                for i in range(5)]
-    step_ms = sum(ev[s][0].elapsed_time(ev[s][5]) for s in range(args.steps)) / args.steps
-    ms_per_step = max(step_ms, 1e3 * wall / args.steps)
+        ms_per_step = max(e0.elapsed_time(e1), 1e3 * wall) / args.steps
+
+        # per launch group: a graph of INNER back-to-back copies of one stage
+        INNER, REPS = 20, 5
+        stage_ms = []
+        for i in range(5):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(INNER):
+                    run_stage(i)
+            g.replay()
+            stream.synchronize()
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record(stream)
+            for _ in range(REPS):
+                g.replay()
+            a1.record(stream)
+            a1.synchronize()
+            stage_ms.append(a0.elapsed_time(a1) / (REPS * INNER))
+            del g
     value = ops / (ms_per_step * 1e-3) / 1e12
 
-    # roofline of the dominant stage
+    # roofline of the dominant launch group
     nel_w, nel_x = w.numel(), x.numel()
-    traffic_alg = {
-        "dda_w": ("hbm", 4.0 * nel_w), "dda_x": ("hbm", 4.0 * nel_x),
-        "project_w": ("hbm", 5.0 * nel_w), "project_x": ("hbm", 5.0 * nel_x),
-        # conv: codes of x and w read once, fp32 y written once
-        "conv2d": ("hbm", 1.0 * nel_x + 1.0 * nel_w + 4.0 * M * Ncol),
+    groups = {
+        "dda_w": ("esb_dda_align(w): k_dda_hist + k_dda_finalize", "hbm", 4.0 * nel_w),
+        "dda_x": ("esb_dda_align(x): k_dda_hist + k_dda_finalize", "hbm", 4.0 * nel_x),
+        "project_w": ("esb_project(w): k_project_vec", "hbm", 5.0 * nel_w),
+        "project_x": ("esb_project(x): k_project_vec", "hbm", 5.0 * nel_x),
+        # conv: codes of x and w read once, fp32 y written once (AI below the int8 ridge)
+        "conv2d": ("esb_conv2d: k_contract", "hbm", 1.0 * nel_x + 1.0 * nel_w + 4.0 * M * Ncol),
     }
     dom = int(np.argmax(stage_ms))
-    name = stages[dom]
-    bound, nbytes = traffic_alg[name]
+    kname, bound, nbytes = groups[stages[dom]]
     achieved = nbytes / (stage_ms[dom] * 1e-3) / 1e9
-    roof = {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None,
-            "algorithmic_bytes": nbytes}
+    roof = {"kernel": kname, "bound": bound, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
+            "traffic": measured_traffic(kname.split(":")[0] + "@" + c["name"]),
+            "algorithmic_bytes": nbytes, "launch_us": round(stage_ms[dom] * 1e3, 3)}
     conv_ms = stage_ms[4]
     extra = {
-        "stages_ms": {k: round(v, 5) for k, v in zip(stages, stage_ms)},
+        "stage_launch_us": {k: round(v * 1e3, 3) for k, v in zip(stages, stage_ms)},
         "conv_int_tops": round(ops / (conv_ms * 1e-3) / 1e12, 3),
         "conv_frac_int8_peak": round(ops / (conv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 6),
         "project_x_gbps": round(5.0 * nel_x / (stage_ms[3] * 1e-3) / 1e9, 2),
         "dda_x_gbps": round(4.0 * nel_x / (stage_ms[1] * 1e-3) / 1e9, 2),
+        "timing": "whole step replayed as one HIP graph; launch groups as graphs of 20 copies",
     }
 
     cpu = None
@@ -164,6 +200,128 @@ def main():
         "roofline": roof, "cpu_baseline": cpu, "detail": extra,
     }
     print(json.dumps(rec), flush=True)
+
+
+def measured_traffic(key):
+    """HBM bytes per launch of `key` from the committed counter runs, or None when the
+    kernel source changed since they were taken (sha256 recorded with the figure)."""
+    import hashlib
+    try:
+        table = json.load(open(os.path.join(ROOT, "profiles", "hbm_traffic.json")))
+        ent = table[key]
+        src = open(os.path.join(ROOT, ent["source"]), "rb").read()
+        if hashlib.sha256(src).hexdigest() != ent["sha256"]:
+            return None
+        return ent["bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def time_launches(fn, reps, stream):
+    """Average device time of one call, over `reps` back-to-back calls bracketed by events."""
+    import torch
+    with torch.cuda.stream(stream):
+        fn()
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def sweep(args):
+    """Per-kernel throughput at the large shapes of the paper's layers."""
+    import numpy as np
+    import torch
+    from paper_2109_03513_amd import esb, workloads
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()
+    sh = stream.cuda_stream
+    only = set(filter(None, args.only.split(",")))
+    dev = "cuda"
+
+    def emit(name, ms, nbytes=None, ops=None, **kw):
+        rec = {"case": name, "ms": round(ms, 5)}
+        if nbytes is not None:
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            rec.update(alg_bytes=nbytes, gbps=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4))
+        if ops is not None:
+            tops = ops / (ms * 1e-3) / 1e12
+            rec.update(ops=ops, tops=round(tops, 2), frac_int8=round(tops / INT8_PEAK_TOPS, 4))
+        rec.update(kw)
+        print(json.dumps(rec), flush=True)
+
+    def want(name):
+        return not only or name in only
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    if want("dda_small"):
+        grid = torch.from_numpy(workloads.scale_grid(1.0)).to(dev)
+        ao = torch.empty(1, device=dev)
+        Do = torch.empty(64, dtype=torch.float64, device=dev)
+        for length in [0, 4096, 200704, 1 << 22]:
+            xs = torch.randn(max(length, 1), device=dev, generator=g)[:length]
+            ws = torch.empty(esb.esb_dda_workspace_size(length, 4, 2, 64), dtype=torch.uint8, device=dev)
+            ms = time_launches(lambda: esb.esb_dda_align(xs, 4, 2, grid, alpha_out=ao, D_out=Do,
+                                                         workspace=ws, stream=sh), args.reps, stream)
+            emit("dda_small_n4_k2_G64_len%d" % length, ms, nbytes=4.0 * length)
+    big = 1 << 27
+    if want("project") or want("dda"):
+        x = torch.randn(big, device=dev, generator=g)
+        alpha = torch.tensor([0.4871], device=dev)
+        codes = torch.empty(big, dtype=torch.uint8, device=dev)
+        for (n, ks) in [(4, 2), (3, 1), (5, 3), (8, 6)]:
+            if want("project"):
+                ms = time_launches(lambda: esb.esb_project(x, alpha, n, ks, codes=codes, stream=sh),
+                                   args.reps, stream)
+                emit("project_n%d_k%d_2^27" % (n, ks), ms, nbytes=5.0 * big)
+            if want("dda"):
+                grid = torch.from_numpy(workloads.scale_grid(1.0)).to(dev)
+                ao = torch.empty(1, device=dev)
+                Do = torch.empty(64, dtype=torch.float64, device=dev)
+                ws = torch.empty(esb.esb_dda_workspace_size(big, n, ks, 64), dtype=torch.uint8, device=dev)
+                ms = time_launches(lambda: esb.esb_dda_align(x, n, ks, grid, alpha_out=ao, D_out=Do,
+                                                             workspace=ws, stream=sh), args.reps, stream)
+                emit("dda_n%d_k%d_G64_2^27" % (n, ks), ms, nbytes=4.0 * big)
+        del x, codes
+    if want("gemm"):
+        for (M, N, K, fa, fb, name) in [(128, 4096, 9216, (3, 2), (3, 1), "alexnet_fc_b128"),
+                                        (4096, 4096, 4096, (4, 2), (4, 2), "square_4096"),
+                                        (8192, 8192, 8192, (5, 3), (5, 3), "square_8192")]:
+            A = torch.randint(0, 256, (M, K), dtype=torch.uint8, device=dev)
+            B = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev)
+            a = torch.tensor([0.5], device=dev)
+            y = torch.empty((M, N), dtype=torch.float32, device=dev)
+            ms = time_launches(lambda: esb.esb_gemm(A, fa[0], fa[1], a, B, fb[0], fb[1], a, y=y,
+                                                    want_acc=False, stream=sh), args.reps, stream)
+            emit("gemm_" + name, ms, nbytes=float(M * K + N * K + 4 * M * N), ops=2.0 * M * N * K)
+    if want("conv"):
+        cases = [("resnet18_conv1_b64", 64, 224, 224, 3, 64, 7, 2, 3, 1),
+                 ("resnet18_l1_3x3_b64", 64, 56, 56, 64, 64, 3, 1, 1, 1),
+                 ("resnet18_l2_3x3_b64", 64, 28, 28, 128, 128, 3, 1, 1, 1),
+                 ("resnet18_l3_3x3_b64", 64, 14, 14, 256, 256, 3, 1, 1, 1),
+                 ("resnet18_l4_3x3_b64", 64, 7, 7, 512, 512, 3, 1, 1, 1),
+                 ("mobilenet_expand_b32", 32, 56, 56, 24, 144, 1, 1, 0, 1),
+                 ("mobilenet_dw_b32", 32, 56, 56, 144, 144, 3, 1, 1, 144),
+                 ("mobilenet_project_b32", 32, 56, 56, 144, 24, 1, 1, 0, 1)]
+        for (name, Nb, H, W, C, K, R, st, pd, groups) in cases:
+            xc = torch.randint(0, 256, (Nb, H, W, C), dtype=torch.uint8, device=dev)
+            wc = torch.randint(0, 256, (K, R, R, C // groups), dtype=torch.uint8, device=dev)
+            P, Q = esb.conv_out_hw(H, W, R, R, (st, st), (pd, pd))
+            y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
+            a = torch.tensor([0.5], device=dev)
+            ms = time_launches(lambda: esb.esb_conv2d(xc, 5, 3, a, wc, 5, 3, a, stride=(st, st),
+                                                      pad=(pd, pd), groups=groups, y=y,
+                                                      want_acc=False, stream=sh), args.reps, stream)
+            ops = 2.0 * Nb * P * Q * K * R * R * (C // groups)
+            nbytes = float(xc.numel() + wc.numel() + 4 * y.numel())
+            emit("conv_" + name, ms, nbytes=nbytes, ops=ops)
 
 
 def cpu_baseline(c, ops, budget_s):

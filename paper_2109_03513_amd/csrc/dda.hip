@@ -6,60 +6,58 @@
 // candidate j holds |x|, and the cell boundaries are exact fp32 thresholds:
 // T_{j,c} = the smallest fp32 X with fl32(X / alpha_j) >= mu_c, mu_c the
 // midpoint between set values c-1 and c (ties go up, as in the projection).
-// Sorting all G*M thresholds splits [0, inf) into "atoms"; every candidate's
-// cell is a union of consecutive atoms.  So one pass over x suffices:
-//   1. setup (1 block): thresholds by bisection over bit patterns, bitonic
-//      sort, atom ranks, and a bin table over the threshold bit range;
-//   2. histogram (<= 256 blocks): per element find its atom (bin lookup +
-//      short scan), add (count, |x| in fixed point) to an LDS histogram with
-//      integer atomics, accumulate x^2 in fp64; the unbounded top atom sums
-//      |x| in fp64; per-block partials go to the workspace;
-//   3. reduce: per atom, sum the partials over blocks (integers, exact);
-//   4. finalize (1 block): per candidate, walk the atoms with the cell index,
-//      A_j = sum Q_c S1, B_j = sum Q_c^2 S0, D_j = S2 + a (a B_j - 2 A_j),
-//      then the argmin with ties to the lowest index.
-// Fixed point: an atom [U_a, U_{a+1}) is bounded with U_{a+1} <= 3 U_a + ulps
-// (neighbouring midpoints differ by at most a factor 3), so |x| / ulp(U_a) is
-// an integer below 2^26 and a uint64 per atom holds >= 2^38 elements exactly.
-// Everything is integer or fixed-order fp64: the result is deterministic.
+// All G*M thresholds, sorted and further split at every power of two, cut
+// [0, inf) into "atoms": every candidate's cell is a union of consecutive atoms
+// and every bounded atom lies inside one binade.  One pass over x suffices:
+//
+// k_dda_hist (<= 256 blocks of 1024 threads), per block:
+//   set-up in LDS: thresholds by a local search around fl32(alpha mu); their
+//   ranks in the sorted order from branch-free binary searches in the other
+//   candidates' (already ascending) lists; power-of-two split points; a bin
+//   table over the threshold bit range whose entries name the atom directly
+//   unless a boundary falls inside the bin;
+//   pass: per element its atom, and one LDS atomic adding (significand << 20) + 1
+//   to a packed 64-bit (sum, count) cell; x^2 in fp64; the unbounded top atom in
+//   fp64.  Every 2^19 elements the packed cells are flushed to per-block totals.
+// k_dda_reduce (only for many blocks): sums the per-block totals in slices.
+// k_dda_finalize (1 block): per-atom sums, prefix sums over atoms, then per
+//   candidate A_j = sum_c Q_c (P1[end_c] - P1[start_c]), B_j likewise with P0 and
+//   Q_c^2, D_j = S2 + a (a B_j - 2 A_j); argmin with ties to the lowest index.
+// Integer sums are exact; fp64 sums run in a fixed order: the result is
+// deterministic.
 #include "esb_internal.h"
 
 namespace esb {
 
+constexpr int kHistThreads = 1024;
+constexpr int kMaxSplits = 256;          // power-of-two split points (at most 254)
+constexpr int kChunk4 = 4096;            // float4 per chunk: 16384 elements
+constexpr int kFlushChunks = 32;         // 2^19 elements between flushes
+constexpr int kReduceSlices = 16;
+
 struct DdaArgs {
     float mids[128];   // mu_c, c = 1..M (index c-1)
     float q[128];      // Q_c, c = 0..M (unscaled values, ascending)
-    int G, M, A, nblk;
+    int G, M, A, Aa, nblk, nslice;
 };
 
 struct DdaWs {   // pointers into the caller's workspace
-    uint32_t* ubits;   // [A+2]: 0, sorted threshold bits (1..A), 0xffffffff
-    int32_t* rank;     // [G*M]: atom index where cell c of candidate j starts
-    uint32_t* bins;    // [kDdaBins]: first atom of each bin
-    uint32_t* meta;    // lo, shift, nbins, A_fin, hi
-    uint32_t* pcnt;    // [nblk][A+1]
-    uint64_t* psum;    // [nblk][A+1]
+    uint32_t* ubits;   // [Aa+2]: augmented sorted bounds of the atoms
+    int32_t* rank;     // [A]: atom where cell c of candidate j starts (j*M + c-1)
+    uint32_t* meta;    // afin (top atom), Aprime (number of bounds)
+    uint64_t* pcnt;    // [nblk][Aa+1] per-block element counts
+    uint64_t* psum;    // [nblk][Aa+1] per-block significand sums
     double* pscal;     // [nblk][4]: sum x^2, top-atom sum |x|, top count, flags
-    double* s0;        // [A+1]
-    double* s1;        // [A+1]
+    uint64_t* rcnt;    // [nslice][Aa+1] sliced sums (k_dda_reduce)
+    uint64_t* rsum;    // [nslice][Aa+1]
 };
 
-static DdaWs ws_ptrs(void* ws, const DdaLayout& L) {
-    char* b = (char*)ws;
-    DdaWs w;
-    w.ubits = (uint32_t*)(b + L.off_ubits);
-    w.rank = (int32_t*)(b + L.off_rank);
-    w.bins = (uint32_t*)(b + L.off_bins);
-    w.meta = (uint32_t*)(b + L.off_meta);
-    w.pcnt = (uint32_t*)(b + L.off_pcnt);
-    w.psum = (uint64_t*)(b + L.off_psum);
-    w.pscal = (double*)(b + L.off_pscal);
-    w.s0 = (double*)(b + L.off_s0);
-    w.s1 = (double*)(b + L.off_s1);
-    return w;
-}
+__host__ __device__ static inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+static int dda_nblk(int64_t len) {
+    const int64_t chunks = (len + 4 * kChunk4 - 1) / (4 * kChunk4);
+    return (int)(chunks < 1 ? 1 : (chunks > kDdaMaxBlocks ? kDdaMaxBlocks : chunks));
+}
 
 bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L) {
     const int M = (1 << (f.n - 1)) - 1;
@@ -67,284 +65,477 @@ bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L) {
     L->G = G;
     L->M = M;
     L->A = G * M;
-    int64_t nb = (len + 16383) / 16384;
-    L->nblk = (int)(nb < 1 ? 1 : (nb > kDdaMaxBlocks ? kDdaMaxBlocks : nb));
-    const size_t A1 = (size_t)L->A + 1;
+    L->nblk = dda_nblk(len);
+    const size_t Aa1 = (size_t)L->A + kMaxSplits + 1;
+    const size_t ns = kReduceSlices;
     size_t o = 0;
-    L->off_ubits = o; o = align256(o + sizeof(uint32_t) * (A1 + 1));
+    L->off_ubits = o; o = align256(o + sizeof(uint32_t) * (Aa1 + 1));
     L->off_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)L->A);
-    L->off_bins = o;  o = align256(o + sizeof(uint32_t) * kDdaBins);
     L->off_meta = o;  o = align256(o + sizeof(uint32_t) * 8);
-    L->off_pcnt = o;  o = align256(o + sizeof(uint32_t) * A1 * L->nblk);
-    L->off_psum = o;  o = align256(o + sizeof(uint64_t) * A1 * L->nblk);
+    L->off_pcnt = o;  o = align256(o + sizeof(uint64_t) * Aa1 * L->nblk);
+    L->off_psum = o;  o = align256(o + sizeof(uint64_t) * Aa1 * L->nblk);
     L->off_pscal = o; o = align256(o + sizeof(double) * 4 * L->nblk);
-    L->off_s0 = o;    o = align256(o + sizeof(double) * A1);
-    L->off_s1 = o;    o = align256(o + sizeof(double) * A1);
+    L->off_s0 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
+    L->off_s1 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
+    L->off_bins = 0;
     L->total = o;
     return true;
 }
 
+static DdaWs ws_ptrs(void* ws, const DdaLayout& L) {
+    char* b = (char*)ws;
+    DdaWs w;
+    w.ubits = (uint32_t*)(b + L.off_ubits);
+    w.rank = (int32_t*)(b + L.off_rank);
+    w.meta = (uint32_t*)(b + L.off_meta);
+    w.pcnt = (uint64_t*)(b + L.off_pcnt);
+    w.psum = (uint64_t*)(b + L.off_psum);
+    w.pscal = (double*)(b + L.off_pscal);
+    w.rcnt = (uint64_t*)(b + L.off_s0);
+    w.rsum = (uint64_t*)(b + L.off_s1);
+    return w;
+}
+
 __device__ __forceinline__ bool alpha_ok(float a) { return a > 0.0f && a < __builtin_inff(); }
 
-// Smallest fp32 X >= 0 (as bits) with fl32(X / alpha) >= mu: bisection over the
-// monotone predicate on [0, +inf]; pred(0) is false (mu > 0), pred(inf) true.
+__device__ __forceinline__ bool reaches(uint32_t xbits, float alpha, float mu) {
+    return __uint_as_float(xbits) / alpha >= mu;   // fl32(X / alpha) >= mu, IEEE division
+}
+
+// Smallest fp32 X >= 0 (as bits) with fl32(X / alpha) >= mu.  The predicate is
+// monotone in X, false at 0 (mu > 0) and true at +inf.  Local search from
+// fl32(alpha * mu), which is within a few ulps of the answer; bisection if the
+// walk does not settle.
 __device__ uint32_t threshold_bits(float alpha, float mu) {
+    uint32_t b = __float_as_uint(alpha * mu);
+    if (b > 0x7f800000u) b = 0x7f800000u;
+    int it = 0;
+    if (reaches(b, alpha, mu)) {
+        while (b > 0u && it < 32 && reaches(b - 1u, alpha, mu)) { b--; it++; }
+    } else {
+        while (it < 32 && !reaches(b, alpha, mu)) { b++; it++; }
+    }
+    if (it < 32) return b;
     uint32_t lo = 0u, hi = 0x7f800000u;
     while (hi - lo > 1u) {
         const uint32_t mid = lo + ((hi - lo) >> 1);
-        if (__uint_as_float(mid) / alpha >= mu) hi = mid; else lo = mid;
+        if (reaches(mid, alpha, mu)) hi = mid; else lo = mid;
     }
     return hi;
 }
 
-// ------------------------------------------------------------------- setup
-__global__ __launch_bounds__(1024) void k_dda_setup(const float* __restrict__ grid, DdaArgs a,
-                                                    DdaWs w) {
-    __shared__ uint64_t keys[kDdaMaxThresholds];
-    const int A = a.A, tid = threadIdx.x;
-    int P = 1;
-    while (P < A) P <<= 1;
-    for (int i = tid; i < P; i += blockDim.x) {
-        uint64_t key = ~0ull;
-        if (i < A) {
-            const int j = i / a.M, c = i % a.M;
-            const float al = grid[j];
-            const uint32_t t = alpha_ok(al) ? threshold_bits(al, a.mids[c]) : 0x7f800000u;
-            key = ((uint64_t)t << 32) | (uint32_t)i;
-        }
-        keys[i] = key;
-    }
-    __syncthreads();
-    // bitonic sort, ascending; keys are unique (index in the low word)
-    for (int size = 2; size <= P; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = tid; i < P / 2; i += blockDim.x) {
-                const int lo = 2 * i - (i & (stride - 1));
-                const int hi = lo + stride;
-                const bool up = ((lo & size) == 0);
-                const uint64_t x = keys[lo], y = keys[hi];
-                if ((x > y) == up) { keys[lo] = y; keys[hi] = x; }
-            }
-            __syncthreads();
-        }
-    }
-    for (int p = tid; p < A; p += blockDim.x) {
-        const uint64_t key = keys[p];
-        w.ubits[p + 1] = (uint32_t)(key >> 32);
-        w.rank[(uint32_t)key] = p + 1;
-    }
-    if (tid == 0) { w.ubits[0] = 0u; w.ubits[A + 1] = 0xffffffffu; }
-    // number of finite thresholds
-    __shared__ int s_afin;
-    if (tid == 0) s_afin = 0;
-    __syncthreads();
-    for (int p = tid; p < A; p += blockDim.x) {
-        const bool fin = (uint32_t)(keys[p] >> 32) < 0x7f800000u;
-        const bool next_fin = (p + 1 < A) && ((uint32_t)(keys[p + 1] >> 32) < 0x7f800000u);
-        if (fin && !next_fin) s_afin = p + 1;
-    }
-    __syncthreads();
-    const int afin = s_afin;
-    uint32_t lo = 0x7f800000u, hi = 0x7f800000u, shift = 0, nb = 1;
-    if (afin > 0) {
-        lo = (uint32_t)(keys[0] >> 32);
-        hi = (uint32_t)(keys[afin - 1] >> 32);
-        const uint32_t range = hi - lo;
-        while ((range >> shift) >= (uint32_t)(kDdaBins - 1)) shift++;
-        nb = (range >> shift) + 1;
-    }
-    // bins[b] = #{p in 1..A : U_p <= lo + (b << shift)} (>= 1 when afin > 0)
-    for (uint32_t b = tid; b < nb; b += blockDim.x) {
-        const uint32_t v = lo + (b << shift);
-        int l = 0, r = afin;   // count of sorted finite keys with value <= v
-        while (l < r) {
-            const int mid = (l + r) >> 1;
-            if ((uint32_t)(keys[mid] >> 32) <= v) l = mid + 1; else r = mid;
-        }
-        w.bins[b] = (uint32_t)l;
-    }
-    if (tid == 0) {
-        w.meta[0] = lo; w.meta[1] = shift; w.meta[2] = nb; w.meta[3] = (uint32_t)afin;
-        w.meta[4] = hi;
-    }
+// Number of powers of two strictly between bit patterns lo < hi (both finite).
+__device__ __forceinline__ uint32_t splits_between(uint32_t lo, uint32_t hi) {
+    const uint32_t e1 = lo >> 23, e2 = hi >> 23;
+    const uint32_t last = (hi & 0x7fffffu) ? e2 : e2 - 1u;   // exponent of the last start < hi
+    const uint32_t first = e1 + 1u;                           // first binade start > lo
+    return (e2 > e1 && last >= first) ? last - first + 1u : 0u;
 }
 
-// --------------------------------------------------------------- histogram
-template <int BS>
-__device__ __forceinline__ double block_sum(double v, double* red) {
-    const int tid = threadIdx.x;
-    red[tid] = v;
-    __syncthreads();
-    for (int s = BS / 2; s > 0; s >>= 1) {
-        if (tid < s) red[tid] += red[tid + s];
-        __syncthreads();
+// Block-wide exclusive scan (1024 threads), fixed summation order.
+template <typename T>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T* total) {
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
+    T x = v;
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(x, off);
+        if (lane >= off) x += y;
     }
-    const double r = red[0];
+    if (lane == 63) sh[wid] = x;
     __syncthreads();
-    return r;
+    if (wid == 0) {
+        T s = lane < nw ? sh[lane] : (T)0;
+        for (int off = 1; off < 64; off <<= 1) {
+            const T y = __shfl_up(s, off);
+            if (lane >= off) s += y;
+        }
+        if (lane < nw) sh[lane] = s;
+    }
+    __syncthreads();
+    const T before = (wid > 0 ? sh[wid - 1] : (T)0) + x - v;
+    if (total) *total = sh[nw - 1];
+    __syncthreads();
+    return before;
 }
 
-constexpr int kHistThreads = 1024;
+template <typename T>
+__device__ __forceinline__ T block_sum(T v, T* sh) {
+    T t;
+    block_exclusive_scan<T>(v, sh, &t);
+    return t;
+}
+
+// Dynamic LDS of k_dda_hist:
+//   U     u32[Aa + 2]   sorted atom bounds: U[0] = 0, U[1..Ap] boundaries, U[Ap+1] = ~0
+//   binfo u32[nbins]    per bin: first atom (low 16 bits) | boundaries inside (high 16)
+//   TH    u32[A]        thresholds, later their atom positions (the cell starts)
+//   KH    u64[Aa + 1]   (value << 32 | id) bucket keys, later the packed histogram
+static int hist_nbins(int A) { return A <= 2048 ? 8192 : 4096; }
+static size_t hist_lds_bytes(int A) {
+    const size_t Aa = (size_t)A + kMaxSplits;
+    return align256(sizeof(uint32_t) * (Aa + 2)) + sizeof(uint32_t) * hist_nbins(A) +
+           align256(sizeof(uint32_t) * A) + sizeof(uint64_t) * (Aa + 1);
+}
 
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restrict__ x, int64_t len,
+                                                           const float* __restrict__ grid,
                                                            DdaArgs a, DdaWs w) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int A = a.A, A1 = A + 1;
-    uint64_t* hsum = (uint64_t*)smem;                       // [A+1]
-    uint32_t* ub = (uint32_t*)(hsum + A1);                  // [A+2]
-    uint32_t* hcnt = ub + (A + 2);                          // [A+1]
-    uint32_t* bins = hcnt + A1;                             // [nb]
-    __shared__ double red[kHistThreads];
-    const uint32_t lo = w.meta[0], shift = w.meta[1], nb = w.meta[2], afin = w.meta[3];
-    const uint32_t hi = w.meta[4];
-    for (int i = threadIdx.x; i < A1; i += blockDim.x) { hsum[i] = 0; hcnt[i] = 0; }
-    for (int i = threadIdx.x; i < A + 2; i += blockDim.x) ub[i] = w.ubits[i];
-    for (uint32_t i = threadIdx.x; i < nb; i += blockDim.x) bins[i] = w.bins[i];
+    const int A = a.A, M = a.M, tid = threadIdx.x;
+    const int nbins = A <= 2048 ? 8192 : 4096;
+    const size_t Aa = (size_t)A + kMaxSplits;
+    uint32_t* U = (uint32_t*)smem;
+    uint32_t* binfo = (uint32_t*)(smem + align256(sizeof(uint32_t) * (Aa + 2)));
+    uint32_t* TH = binfo + nbins;
+    uint64_t* KH = (uint64_t*)((unsigned char*)TH + align256(sizeof(uint32_t) * A));
+    uint64_t* hist = KH;
+    __shared__ float s_mids[128];
+    __shared__ uint32_t s_lo, s_hi, s_nfin, s_flags;
+    __shared__ uint32_t s_scan[16];
+    __shared__ double s_red[16];
+    __shared__ unsigned long long s_redu[16];
+
+    // ---- 1. thresholds, their finite range and count
+    if (tid < M) s_mids[tid] = a.mids[tid];
+    if (tid == 0) { s_lo = 0x7f800000u; s_hi = 0u; s_nfin = 0u; s_flags = 0u; }
+    __syncthreads();
+    for (int i = tid; i < A; i += kHistThreads) {
+        const int j = i / M, c = i - j * M;
+        const float al = grid[j];
+        const uint32_t t = alpha_ok(al) ? threshold_bits(al, s_mids[c]) : 0x7f800000u;
+        TH[i] = t;
+        if (t < 0x7f800000u) {
+            atomicMin(&s_lo, t);
+            atomicMax(&s_hi, t);
+            atomicAdd(&s_nfin, 1u);
+        }
+    }
+    __syncthreads();
+    const uint32_t nfin = s_nfin;
+    uint32_t lo = 0x7f800000u, hi = 0x7f800000u, shift = 0, base = 0, nb = 0, nsplit = 0;
+    if (nfin > 0) {
+        lo = s_lo;
+        hi = s_hi;
+        while (((hi >> shift) - (lo >> shift)) >= (uint32_t)(nbins - 1)) shift++;   // <= 19
+        base = lo >> shift;
+        nb = (hi >> shift) - base + 1;
+        if (hi > lo) {
+            const uint32_t e_lo = lo >> 23, e_hi = (hi - 1u) >> 23;   // binade starts in (lo, hi)
+            nsplit = e_hi - e_lo;
+        }
+    }
+    // ---- 2. boundaries per bin: finite thresholds and the powers of two in (lo, hi)
+    for (uint32_t b = tid; b < nb; b += kHistThreads) binfo[b] = 0u;
+    __syncthreads();
+    for (int i = tid; i < A; i += kHistThreads) {
+        const uint32_t t = TH[i];
+        if (t < 0x7f800000u) atomicAdd(&binfo[(t >> shift) - base], 1u);
+    }
+    for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
+        const uint32_t v = ((lo >> 23) + 1u + e) << 23;
+        atomicAdd(&binfo[(v >> shift) - base], 1u);
+    }
+    __syncthreads();
+    // ---- 3. first atom of every bin: exclusive scan of the counts
+    const uint32_t Ap = nfin + nsplit;
+    {
+        const int per = (int)((nb + kHistThreads - 1) / kHistThreads);
+        uint32_t mysum = 0;
+        for (int e = 0; e < per; e++) {
+            const uint32_t b = (uint32_t)(tid * per + e);
+            if (b < nb) mysum += binfo[b];
+        }
+        uint32_t run = block_exclusive_scan<uint32_t>(mysum, s_scan, nullptr);
+        for (int e = 0; e < per; e++) {
+            const uint32_t b = (uint32_t)(tid * per + e);
+            if (b < nb) {
+                const uint32_t c = binfo[b];
+                binfo[b] = run;                 // fill counter (high half) starts at 0
+                run += c;
+            }
+        }
+    }
+    __syncthreads();
+    // ---- 4. scatter the keys into their buckets; non-finite thresholds start past the top
+    for (int i = tid; i < A; i += kHistThreads) {
+        const uint32_t t = TH[i];
+        if (t < 0x7f800000u) {
+            const uint32_t old = atomicAdd(&binfo[(t >> shift) - base], 0x10000u);
+            KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)t << 32) | (uint32_t)i;
+        } else {
+            TH[i] = Ap + 1u;
+        }
+    }
+    for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
+        const uint32_t v = ((lo >> 23) + 1u + e) << 23;
+        const uint32_t old = atomicAdd(&binfo[(v >> shift) - base], 0x10000u);
+        KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)v << 32) | (uint32_t)(A + e);
+    }
+    __syncthreads();
+    // ---- 5. order inside each bucket by counting: position = first + #smaller keys
+    for (uint32_t k = tid; k < Ap; k += kHistThreads) {
+        const uint64_t key = KH[k];
+        const uint32_t v = (uint32_t)(key >> 32), id = (uint32_t)key;
+        const uint32_t bi = binfo[(v >> shift) - base];
+        const uint32_t o = bi & 0xffffu, n = bi >> 16;
+        uint32_t pos = o;
+        for (uint32_t t = o; t < o + n; t++) pos += (KH[t] < key) ? 1u : 0u;
+        U[pos + 1] = v;
+        if (id < (uint32_t)A) TH[id] = pos + 1;      // atom where this cell starts
+    }
+    if (tid == 0) { U[0] = 0u; U[Ap + 1] = 0xffffffffu; }
+    const uint32_t afin = Ap;                        // the top atom [hi, inf)
+    __syncthreads();   // the keys are dead: KH becomes the histogram
+    for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0;
     __syncthreads();
 
+    // ---- 6. the pass
     double sumsq = 0.0, top_s1 = 0.0;
     uint32_t top_cnt = 0, flags = 0;
-    auto visit = [&](float xf) {
-        const uint32_t ab = __float_as_uint(xf) & 0x7fffffffu;
-        if (ab >= 0x7f800000u) { flags |= (ab > 0x7f800000u) ? 2u : 1u; return; }
-        const double xd = (double)__uint_as_float(ab);
-        sumsq = fma(xd, xd, sumsq);
-        if (ab < lo) return;                              // atom 0: q = 0 for all candidates
-        if (ab >= hi) { top_s1 += xd; top_cnt++; return; }  // top atom, unbounded
-        uint32_t at = bins[(ab - lo) >> shift];
-        while (ub[at + 1] <= ab) at++;
-        const uint32_t eb = max(ub[at] >> 23, 1u);
-        const uint32_t ex = max(ab >> 23, 1u);
-        const uint32_t sig = (ab & 0x7fffffu) | ((ab >> 23) ? 0x800000u : 0u);
-        atomicAdd(&hsum[at], (uint64_t)sig << (ex - eb));
-        atomicAdd(&hcnt[at], 1u);
-    };
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    const int64_t tid0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (((uintptr_t)x & 15) == 0) {
-        const int64_t n4 = len >> 2;
-        const f32x4* x4 = (const f32x4*)x;
-        for (int64_t i = tid0; i < n4; i += stride) {
-            const f32x4 v = __builtin_nontemporal_load(&x4[i]);
-            visit(v.x); visit(v.y); visit(v.z); visit(v.w);
+    constexpr int E = 8;
+    auto visit = [&](const uint32_t (&xb)[E]) {
+        uint32_t ab[E], at[E];
+        bool mid[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+            ab[e] = xb[e] & 0x7fffffffu;
+            const bool fin = ab[e] < 0x7f800000u;
+            flags |= fin ? 0u : ((ab[e] > 0x7f800000u) ? 2u : 1u);
+            const double xd = fin ? (double)__uint_as_float(ab[e]) : 0.0;
+            sumsq = fma(xd, xd, sumsq);
+            const bool top = fin && ab[e] >= hi;
+            top_s1 += top ? xd : 0.0;
+            top_cnt += top ? 1u : 0u;
+            mid[e] = ab[e] >= lo && ab[e] < hi;       // atom 0 (q = 0 for all) is skipped
+            at[e] = binfo[mid[e] ? (ab[e] >> shift) - base : 0u];
         }
-        for (int64_t i = (n4 << 2) + tid0; i < len; i += stride) visit(x[i]);
-    } else {
-        for (int64_t i = tid0; i < len; i += stride) visit(x[i]);
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+            if (mid[e] && (at[e] >> 16)) {           // a boundary inside the bin: scan
+                uint32_t t = at[e] & 0xffffu;
+                while (U[t + 1] <= ab[e]) t++;
+                at[e] = t;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+            if (mid[e]) {
+                const uint32_t sig = (ab[e] & 0x7fffffu) | ((ab[e] >> 23) ? 0x800000u : 0u);
+                atomicAdd(&hist[at[e] & 0xffffu], ((uint64_t)sig << 20) | 1u);
+            }
+        }
+    };
+    const int64_t cnt_base = (int64_t)blockIdx.x * (int64_t)(Aa + 1);
+    bool first_flush = true;
+    auto flush = [&]() {
+        __syncthreads();
+        for (uint32_t i = tid; i <= Ap; i += kHistThreads) {
+            const uint64_t v = hist[i];
+            hist[i] = 0;
+            const uint64_t c = v & 0xfffffu, s = v >> 20;
+            if (first_flush) { w.pcnt[cnt_base + i] = c; w.psum[cnt_base + i] = s; }
+            else if (v) { w.pcnt[cnt_base + i] += c; w.psum[cnt_base + i] += s; }
+        }
+        first_flush = false;
+        __syncthreads();
+    };
+    const bool vec = ((uintptr_t)x & 15) == 0;
+    const int64_t n4 = vec ? (len >> 2) : (len + 3) >> 2;   // scalar path: chunks of 4 elements
+    const int64_t nchunks = (n4 + kChunk4 - 1) / kChunk4;
+    const int64_t cpb = (nchunks + gridDim.x - 1) / gridDim.x;
+    const int64_t c0 = (int64_t)blockIdx.x * cpb;
+    const int64_t c1 = min(nchunks, c0 + cpb);
+    int since = 0;
+    for (int64_t ch = c0; ch < c1; ch++) {
+        uint32_t g[16];
+        if (vec) {
+            const f32x4* x4 = (const f32x4*)x;
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int64_t i4 = ch * kChunk4 + tid + u * kHistThreads;
+                f32x4 v = {0.f, 0.f, 0.f, 0.f};
+                if (i4 < n4) v = __builtin_nontemporal_load(&x4[i4]);
+                g[4 * u + 0] = __float_as_uint(v.x); g[4 * u + 1] = __float_as_uint(v.y);
+                g[4 * u + 2] = __float_as_uint(v.z); g[4 * u + 3] = __float_as_uint(v.w);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                const int64_t i = ch * (4 * kChunk4) + tid + (int64_t)u * kHistThreads;
+                g[u] = i < len ? __float_as_uint(x[i]) : 0u;    // zeros: atom 0, add nothing
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            uint32_t gg[E];
+#pragma unroll
+            for (int e = 0; e < E; e++) gg[e] = g[E * h + e];
+            visit(gg);
+        }
+        if (++since == kFlushChunks) { flush(); since = 0; }
     }
-    if (afin > 0 && top_cnt) atomicAdd(&hcnt[afin], top_cnt);
-    const double s_sumsq = block_sum<kHistThreads>(sumsq, red);
-    const double s_top = block_sum<kHistThreads>(top_s1, red);
-    __shared__ uint32_t s_flags;
-    if (threadIdx.x == 0) s_flags = 0;
-    __syncthreads();
+    if (vec && blockIdx.x == gridDim.x - 1 && tid < (int)(len & 3)) {   // tail of the vector path
+        uint32_t gg[E];
+        gg[0] = __float_as_uint(x[(len & ~(int64_t)3) + tid]);
+#pragma unroll
+        for (int e = 1; e < E; e++) gg[e] = 0u;
+        visit(gg);
+    }
+    flush();
+
+    // ---- 7. block scalars; block 0 also publishes the tables
     if (flags) atomicOr(&s_flags, flags);
-    __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * A1;
-    for (int i = threadIdx.x; i < A1; i += blockDim.x) {
-        w.pcnt[base + i] = hcnt[i];
-        w.psum[base + i] = hsum[i];
-    }
-    if (threadIdx.x == 0) {
+    const double b_sumsq = block_sum<double>(sumsq, s_red);
+    const double b_top = block_sum<double>(top_s1, s_red);
+    const unsigned long long b_topc = block_sum<unsigned long long>(top_cnt, s_redu);
+    if (tid == 0) {
         double* ps = w.pscal + 4 * blockIdx.x;
-        ps[0] = s_sumsq; ps[1] = s_top; ps[2] = 0.0; ps[3] = (double)s_flags;
+        ps[0] = b_sumsq; ps[1] = b_top; ps[2] = (double)b_topc; ps[3] = (double)s_flags;
+    }
+    if (blockIdx.x == 0) {
+        for (uint32_t i = tid; i <= Ap + 1; i += kHistThreads) w.ubits[i] = U[i];
+        for (int i = tid; i < A; i += kHistThreads) w.rank[i] = (int32_t)TH[i];
+        if (tid == 0) { w.meta[0] = afin; w.meta[1] = Ap; }
     }
 }
 
-// ------------------------------------------------------------------ reduce
+// -------------------------------------------------------------------- reduce
+// Slice s of the blocks, per atom: sums of the per-block totals (integers).
 __global__ __launch_bounds__(256) void k_dda_reduce(DdaArgs a, DdaWs w) {
-    const int A1 = a.A + 1;
-    const int at = blockIdx.x * blockDim.x + threadIdx.x;
-    if (at >= A1) return;
-    const uint32_t afin = w.meta[3];
-    uint64_t c = 0, s = 0;
-    for (int b = 0; b < a.nblk; b++) {
-        c += w.pcnt[(int64_t)b * A1 + at];
-        s += w.psum[(int64_t)b * A1 + at];
+    const int at = blockIdx.x * 256 + threadIdx.x;
+    const int Aa1 = a.Aa + 1;
+    if (at >= Aa1) return;
+    const uint32_t Ap = w.meta[1];
+    if ((uint32_t)at > Ap) return;
+    const int s = blockIdx.y, per = (a.nblk + a.nslice - 1) / a.nslice;
+    const int b0 = s * per, b1 = min(a.nblk, b0 + per);
+    uint64_t c = 0, t = 0;
+    for (int b = b0; b < b1; b++) {
+        c += w.pcnt[(int64_t)b * Aa1 + at];
+        t += w.psum[(int64_t)b * Aa1 + at];
     }
-    double s1 = 0.0;
-    if (at >= 1 && (uint32_t)at < afin) {
-        const int eb = (int)max(w.ubits[at] >> 23, 1u);
-        s1 = ldexp((double)s, eb - 150);
-    } else if ((uint32_t)at == afin && afin > 0) {
-        for (int b = 0; b < a.nblk; b++) s1 += w.pscal[4 * b + 1];
-    }
-    w.s0[at] = (double)c;
-    w.s1[at] = (at == 0) ? 0.0 : s1;
+    w.rcnt[(int64_t)s * Aa1 + at] = c;
+    w.rsum[(int64_t)s * Aa1 + at] = t;
 }
 
-// ---------------------------------------------------------------- finalize
+// ------------------------------------------------------------------ finalize
 constexpr int kFinThreads = 1024;
 
 __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
                                                               DdaArgs a, DdaWs w,
                                                               float* __restrict__ alpha_out,
                                                               double* __restrict__ D_out) {
-    __shared__ double red[kFinThreads];
-    __shared__ double sA[kFinThreads], sB[kFinThreads];
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x, G = a.G, M = a.M;
+    const int Aa1 = a.Aa + 1;
+    double* P0 = (double*)smem;                  // [Aa+2] prefix sums of counts
+    double* P1 = P0 + (Aa1 + 1);                 // [Aa+2] prefix sums of |x|
+    __shared__ double s_red[16];
+    __shared__ double sq[128];
     __shared__ double Dv[kDdaMaxG];
-    const int tid = threadIdx.x;
-    double ss = 0.0;
-    uint32_t fl = 0;
-    for (int b = tid; b < a.nblk; b += blockDim.x) {
-        ss += w.pscal[4 * b];
-        fl |= (uint32_t)w.pscal[4 * b + 3];
-    }
-    const double sumsq = block_sum<kFinThreads>(ss, red);
     __shared__ uint32_t s_fl;
+    if (tid <= M) sq[tid] = (double)a.q[tid];
     if (tid == 0) s_fl = 0;
-    __syncthreads();
+    // block scalars
+    double ss = 0.0, ts = 0.0, tc = 0.0;
+    uint32_t fl = 0;
+    for (int b = tid; b < a.nblk; b += kFinThreads) {
+        const double* ps = w.pscal + 4 * b;
+        ss += ps[0]; ts += ps[1]; tc += ps[2]; fl |= (uint32_t)ps[3];
+    }
+    const double sumsq = block_sum<double>(ss, s_red);
+    const double top_s1 = block_sum<double>(ts, s_red);
+    const double top_c = block_sum<double>(tc, s_red);
     if (fl) atomicOr(&s_fl, fl);
-    const int G = a.G, M = a.M;
-    const int T = kFinThreads / G;            // threads per candidate (>= 1)
-    const int afin = (int)w.meta[3];
-    const int natoms = afin;                  // atoms 1..afin carry q > 0 possibly
-    const int j = tid / T, part = tid % T;
-    double Aj = 0.0, Bj = 0.0;
-    if (j < G && natoms > 0) {
-        const int per = (natoms + T - 1) / T;
-        const int a0 = 1 + part * per;
-        const int a1 = min(natoms + 1, a0 + per);
-        if (a0 < a1) {
-            const int32_t* rk = w.rank + (int64_t)j * M;   // rk[c-1]: start atom of cell c
-            int l = 0, r = M;                              // cell = #{c : rank_c <= a0}
-            while (l < r) {
-                const int mid = (l + r) >> 1;
-                if (rk[mid] <= a0) l = mid + 1; else r = mid;
+    const uint32_t afin = w.meta[0];
+    // per-atom sums S0, S1 for atoms 0..afin (atom 0 carries q = 0 for everyone),
+    // loaded coalesced into LDS, then an in-place exclusive prefix scan over atoms
+    const bool sliced = a.nslice > 0;
+    const int nsrc = sliced ? a.nslice : a.nblk;
+    const uint64_t* srcc = sliced ? w.rcnt : w.pcnt;
+    const uint64_t* srcs = sliced ? w.rsum : w.psum;
+    for (int at = tid; at <= (int)afin + 1; at += kFinThreads) {
+        double s0 = 0.0, s1 = 0.0;
+        if (at >= 1 && (uint32_t)at < afin) {
+            uint64_t c = 0, t = 0;
+            for (int b = 0; b < nsrc; b++) {
+                c += srcc[(int64_t)b * Aa1 + at];
+                t += srcs[(int64_t)b * Aa1 + at];
             }
-            int c = l;
-            for (int at = a0; at < a1; at++) {
-                while (c < M && rk[c] <= at) c++;
-                const double q = (double)a.q[c];
-                Aj = fma(q, w.s1[at], Aj);
-                Bj = fma(q * q, w.s0[at], Bj);
+            s0 = (double)c;
+            s1 = ldexp((double)t, (int)max(w.ubits[at] >> 23, 1u) - 150);
+        } else if (afin > 0 && (uint32_t)at == afin) {
+            s0 = top_c;
+            s1 = top_s1;
+        }
+        P0[at] = s0;
+        P1[at] = s1;
+    }
+    __syncthreads();
+    {
+        const int per = ((int)afin + 2 + kFinThreads - 1) / kFinThreads;
+        double m0 = 0.0, m1 = 0.0;
+        for (int e = 0; e < per; e++) {
+            const int at = tid * per + e;
+            if (at <= (int)afin + 1) { m0 += P0[at]; m1 += P1[at]; }
+        }
+        double r0 = block_exclusive_scan<double>(m0, s_red, nullptr);
+        double r1 = block_exclusive_scan<double>(m1, s_red, nullptr);
+        for (int e = 0; e < per; e++) {
+            const int at = tid * per + e;
+            if (at <= (int)afin + 1) {
+                const double v0 = P0[at], v1 = P1[at];
+                P0[at] = r0;
+                P1[at] = r1;
+                r0 += v0;
+                r1 += v1;
             }
         }
     }
-    sA[tid] = Aj;
-    sB[tid] = Bj;
     __syncthreads();
-    if (part == 0 && j < G) {
-        double ta = 0.0, tb = 0.0;
-        for (int p = 0; p < T; p++) { ta += sA[tid + p]; tb += sB[tid + p]; }
+    // per candidate: cells as atom ranges [start_c, start_{c+1}), the last one to afin+1
+    for (int j = tid; j < G; j += kFinThreads) {
+        const int32_t* rk = w.rank + (int64_t)j * M;
+        const int end = (int)afin + 1;
+        double Aj = 0.0, Bj = 0.0;
+        int start = min(rk[0], end);
+        for (int c = 1; c <= M; c++) {
+            const int next = (c < M) ? min(rk[c], end) : end;
+            const double q = sq[c];
+            Aj = fma(q, P1[next] - P1[start], Aj);
+            Bj = fma(q * q, P0[next] - P0[start], Bj);
+            start = next;
+        }
         const float al = grid[j];
         const double ad = (double)al;
-        double D = fma(ad, fma(ad, tb, -2.0 * ta), sumsq);
+        double D = fma(ad, fma(ad, Bj, -2.0 * Aj), sumsq);
         if (!alpha_ok(al) || (s_fl & 2u)) D = __builtin_nan("");
         else if (s_fl & 1u) D = __builtin_inf();
         Dv[j] = D;
     }
     __syncthreads();
-    if (tid == 0) {
-        int best = 0;
-        for (int jj = 1; jj < G; jj++) {
-            const double d = Dv[jj], db = Dv[best];
-            if (d < db || (db != db && d == d)) best = jj;
+    if (tid < 64) {
+        // argmin over (isnan(D), D, j) in lexicographic order: the smallest index
+        // with the least D, NaN ranking above every number
+        double bd = __builtin_nan("");
+        int bj = 0x7fffffff;
+        for (int jj = tid; jj < G; jj += 64) {
+            const double d = Dv[jj];
+            const bool better = (d < bd) || (bd != bd && d == d) || (bj == 0x7fffffff);
+            if (better) { bd = d; bj = jj; }
         }
-        *alpha_out = grid[best];
+        for (int off = 32; off > 0; off >>= 1) {
+            const double od = __shfl_xor(bd, off);
+            const int oj = __shfl_xor(bj, off);
+            const bool onan = od != od, mnan = bd != bd;
+            const bool better = (!onan && mnan) || (onan == mnan && (od < bd || (od == bd && oj < bj))) ||
+                                (onan && mnan && oj < bj);
+            if (better) { bd = od; bj = oj; }
+        }
+        if (tid == 0) *alpha_out = grid[bj];
     }
     if (D_out)
-        for (int jj = tid; jj < G; jj += blockDim.x) D_out[jj] = Dv[jj];
+        for (int jj = tid; jj < G; jj += kFinThreads) D_out[jj] = Dv[jj];
 }
 
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
@@ -362,25 +553,29 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
         for (int t = i; t > 0 && vals[t] < vals[t - 1]; t--) {
             const double tmp = vals[t]; vals[t] = vals[t - 1]; vals[t - 1] = tmp;
         }
-    // drop the duplicate zero only if present (it is not: the -0 code is skipped)
     for (int c = 0; c <= M; c++) a.q[c] = (float)vals[c];
     for (int c = 1; c <= M; c++) a.mids[c - 1] = (float)(0.5 * (vals[c - 1] + vals[c]));
-    a.G = G; a.M = M; a.A = L.A; a.nblk = L.nblk;
+    a.G = G; a.M = M; a.A = L.A; a.Aa = L.A + kMaxSplits; a.nblk = L.nblk;
+    a.nslice = L.nblk > 2 * kReduceSlices ? kReduceSlices : 0;
     const DdaWs w = ws_ptrs(ws, L);
-    k_dda_setup<<<1, 1024, 0, s>>>(grid, a, w);
-    const size_t smem = sizeof(uint64_t) * (L.A + 1) + sizeof(uint32_t) * ((L.A + 2) + (L.A + 1) + kDdaBins);
     static bool lds_attr_set[64] = {false};
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
-        const hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 150 * 1024);
+        hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
+        if (e != hipSuccess) return e;
+        e = hipFuncSetAttribute((const void*)k_dda_finalize,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 140 * 1024);
         if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
-    k_dda_hist<<<L.nblk, kHistThreads, smem, s>>>(x, len, a, w);
-    k_dda_reduce<<<(L.A + 1 + 255) / 256, 256, 0, s>>>(a, w);
-    k_dda_finalize<<<1, kFinThreads, 0, s>>>(grid, a, w, alpha_out, D_out);
+    k_dda_hist<<<L.nblk, kHistThreads, hist_lds_bytes(L.A), s>>>(x, len, grid, a, w);
+    if (a.nslice > 0) {
+        dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
+        k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
+    }
+    const size_t fin_lds = sizeof(double) * 2 * (size_t)(a.Aa + 2);
+    k_dda_finalize<<<1, kFinThreads, fin_lds, s>>>(grid, a, w, alpha_out, D_out);
     return hipGetLastError();
 }
 

@@ -92,3 +92,32 @@ def test_project_full_size_workloads(esb):
         log("project full mobilenet %s %s" % (L["name"], L["x"].shape))
         got = host(esb.esb_project(dev(L["x"]), scalar(m["gridX"][10]), m["n"], m["ks"]))
         np.testing.assert_array_equal(got, oracle.project(L["x"], m["gridX"][10], m["n"], m["ks"]))
+
+
+@pytest.mark.parametrize("b,ks", [(4, 2), (3, 1), (3, 2), (5, 3), (8, 6), (8, 1), (2, 1)])
+def test_project_near_scaled_midpoints(esb, b, ks):
+    """x within +-8 ulps of alpha * mu for many non-power-of-two alpha: the region where
+    x * fl32(1/alpha) and fl32(x/alpha) can round to different set values."""
+    r = np.random.default_rng([41, b, ks])
+    v = oracle.valueset(b, ks)
+    mids = ((v[1:] + v[:-1]) / 2)
+    alphas = np.concatenate([r.uniform(1e-3, 3.0, 24), [1.0 / 3, 0.1, 0.7, 1.1, 2.9]]).astype(np.float32)
+    for alpha in alphas:
+        base = (mids * np.float64(alpha)).astype(np.float32)
+        steps = np.arange(-8, 9, dtype=np.int64)
+        bits = (base.view(np.uint32).astype(np.int64)[:, None] + steps[None, :]).ravel()
+        x = bits.astype(np.uint32).view(np.float32)
+        x = np.concatenate([x, -x])
+        got = host(esb.esb_project(dev(x), scalar(float(alpha)), b, ks))
+        np.testing.assert_array_equal(got, oracle.project(x, alpha, b, ks))
+
+
+def test_project_extreme_scales(esb):
+    """Scales outside [2^-125, 2^125] use the exact division for every element."""
+    z = np.random.default_rng(9).standard_normal(4096)
+    for alpha in [1e-39, 2.0 ** -126, 2.0 ** -125, 2.0 ** 125, 3e38]:
+        for b, ks in [(4, 2), (8, 7)]:
+            with np.errstate(over="ignore"):
+                xs = (z * np.float64(alpha)).astype(np.float32)
+            got = host(esb.esb_project(dev(xs), scalar(alpha), b, ks))
+            np.testing.assert_array_equal(got, oracle.project(xs, alpha, b, ks))
