@@ -39,6 +39,7 @@ struct DdaArgs {
     float mids[128];   // mu_c, c = 1..M (index c-1)
     float q[128];      // Q_c, c = 0..M (unscaled values, ascending)
     int G, M, A, Aa, nblk, nslice;
+    int rk_lds;        // the finalize keeps the cell starts in LDS (when they fit)
 };
 
 struct DdaWs {   // pointers into the caller's workspace
@@ -158,6 +159,60 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T* total) {
     return before;
 }
 
+// Block-wide exclusive scan of N fp64 components at once (one set of barriers).
+template <int N>
+__device__ __forceinline__ void block_exclusive_scan_n(const double (&v)[N], double (*sh)[16],
+                                                       double (&before)[N], double (&total)[N]) {
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
+    double x[N];
+#pragma unroll
+    for (int c = 0; c < N; c++) x[c] = v[c];
+    for (int off = 1; off < 64; off <<= 1) {
+#pragma unroll
+        for (int c = 0; c < N; c++) {
+            const double y = __shfl_up(x[c], off);
+            if (lane >= off) x[c] += y;
+        }
+    }
+    if (lane == 63) {
+#pragma unroll
+        for (int c = 0; c < N; c++) sh[c][wid] = x[c];
+    }
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+        for (int c = 0; c < N; c++) {
+            double t = lane < nw ? sh[c][lane] : 0.0;
+            for (int off = 1; off < 64; off <<= 1) {
+                const double y = __shfl_up(t, off);
+                if (lane >= off) t += y;
+            }
+            if (lane < nw) sh[c][lane] = t;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < N; c++) {
+        before[c] = (wid > 0 ? sh[c][wid - 1] : 0.0) + x[c] - v[c];
+        total[c] = sh[c][nw - 1];
+    }
+    __syncthreads();
+}
+
+// Wave-level min / max / sum of 32-bit values (all 64 lanes take part).
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, off));
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off));
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_add(uint32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
+    return v;
+}
+
 template <typename T>
 __device__ __forceinline__ T block_sum(T v, T* sh) {
     T t;
@@ -192,22 +247,31 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     __shared__ float s_mids[128];
     __shared__ uint32_t s_lo, s_hi, s_nfin, s_flags;
     __shared__ uint32_t s_scan[16];
-    __shared__ double s_red[16];
-    __shared__ unsigned long long s_redu[16];
+    __shared__ double s_red3[3][16];
 
     // ---- 1. thresholds, their finite range and count
     if (tid < M) s_mids[tid] = a.mids[tid];
     if (tid == 0) { s_lo = 0x7f800000u; s_hi = 0u; s_nfin = 0u; s_flags = 0u; }
     __syncthreads();
-    for (int i = tid; i < A; i += kHistThreads) {
-        const int j = i / M, c = i - j * M;
-        const float al = grid[j];
-        const uint32_t t = alpha_ok(al) ? threshold_bits(al, s_mids[c]) : 0x7f800000u;
-        TH[i] = t;
-        if (t < 0x7f800000u) {
-            atomicMin(&s_lo, t);
-            atomicMax(&s_hi, t);
-            atomicAdd(&s_nfin, 1u);
+    {
+        uint32_t wlo = 0x7f800000u, whi = 0u, wn = 0u;
+        for (int i0 = 0; i0 < A; i0 += kHistThreads) {      // uniform trip count
+            const int i = i0 + tid;
+            if (i < A) {
+                const int j = i / M, c = i - j * M;
+                const float al = grid[j];
+                const uint32_t t = alpha_ok(al) ? threshold_bits(al, s_mids[c]) : 0x7f800000u;
+                TH[i] = t;
+                if (t < 0x7f800000u) { wlo = min(wlo, t); whi = max(whi, t); wn++; }
+            }
+        }
+        wlo = wave_min(wlo);
+        whi = wave_max(whi);
+        wn = wave_add(wn);
+        if ((tid & 63) == 0 && wn) {
+            atomicMin(&s_lo, wlo);
+            atomicMax(&s_hi, whi);
+            atomicAdd(&s_nfin, wn);
         }
     }
     __syncthreads();
@@ -385,12 +449,14 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
 
     // ---- 7. block scalars; block 0 also publishes the tables
     if (flags) atomicOr(&s_flags, flags);
-    const double b_sumsq = block_sum<double>(sumsq, s_red);
-    const double b_top = block_sum<double>(top_s1, s_red);
-    const unsigned long long b_topc = block_sum<unsigned long long>(top_cnt, s_redu);
-    if (tid == 0) {
-        double* ps = w.pscal + 4 * blockIdx.x;
-        ps[0] = b_sumsq; ps[1] = b_top; ps[2] = (double)b_topc; ps[3] = (double)s_flags;
+    {
+        const double v3[3] = {sumsq, top_s1, (double)top_cnt};   // counts exact in fp64
+        double bef[3], tot[3];
+        block_exclusive_scan_n<3>(v3, s_red3, bef, tot);
+        if (tid == 0) {
+            double* ps = w.pscal + 4 * blockIdx.x;
+            ps[0] = tot[0]; ps[1] = tot[1]; ps[2] = tot[2]; ps[3] = (double)s_flags;
+        }
     }
     if (blockIdx.x == 0) {
         for (uint32_t i = tid; i <= Ap + 1; i += kHistThreads) w.ubits[i] = U[i];
@@ -430,22 +496,26 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
     const int Aa1 = a.Aa + 1;
     double* P0 = (double*)smem;                  // [Aa+2] prefix sums of counts
     double* P1 = P0 + (Aa1 + 1);                 // [Aa+2] prefix sums of |x|
-    __shared__ double s_red[16];
+    int32_t* rk = (int32_t*)(P1 + (Aa1 + 1));   // [A] first atom of every cell
+    __shared__ double s_red3[3][16];
     __shared__ double sq[128];
     __shared__ double Dv[kDdaMaxG];
     __shared__ uint32_t s_fl;
     if (tid <= M) sq[tid] = (double)a.q[tid];
     if (tid == 0) s_fl = 0;
+    if (a.rk_lds)
+        for (int i = tid; i < a.A; i += kFinThreads) rk[i] = w.rank[i];
+    const int32_t* rks = a.rk_lds ? rk : w.rank;
     // block scalars
-    double ss = 0.0, ts = 0.0, tc = 0.0;
+    double v3[3] = {0.0, 0.0, 0.0};
     uint32_t fl = 0;
     for (int b = tid; b < a.nblk; b += kFinThreads) {
         const double* ps = w.pscal + 4 * b;
-        ss += ps[0]; ts += ps[1]; tc += ps[2]; fl |= (uint32_t)ps[3];
+        v3[0] += ps[0]; v3[1] += ps[1]; v3[2] += ps[2]; fl |= (uint32_t)ps[3];
     }
-    const double sumsq = block_sum<double>(ss, s_red);
-    const double top_s1 = block_sum<double>(ts, s_red);
-    const double top_c = block_sum<double>(tc, s_red);
+    double bef3[3], tot3[3];
+    block_exclusive_scan_n<3>(v3, s_red3, bef3, tot3);
+    const double sumsq = tot3[0], top_s1 = tot3[1], top_c = tot3[2];
     if (fl) atomicOr(&s_fl, fl);
     const uint32_t afin = w.meta[0];
     // per-atom sums S0, S1 for atoms 0..afin (atom 0 carries q = 0 for everyone),
@@ -479,8 +549,10 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
             const int at = tid * per + e;
             if (at <= (int)afin + 1) { m0 += P0[at]; m1 += P1[at]; }
         }
-        double r0 = block_exclusive_scan<double>(m0, s_red, nullptr);
-        double r1 = block_exclusive_scan<double>(m1, s_red, nullptr);
+        const double m2[2] = {m0, m1};
+        double bef[2], tot[2];
+        block_exclusive_scan_n<2>(m2, s_red3, bef, tot);
+        double r0 = bef[0], r1 = bef[1];
         for (int e = 0; e < per; e++) {
             const int at = tid * per + e;
             if (at <= (int)afin + 1) {
@@ -495,12 +567,12 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
     __syncthreads();
     // per candidate: cells as atom ranges [start_c, start_{c+1}), the last one to afin+1
     for (int j = tid; j < G; j += kFinThreads) {
-        const int32_t* rk = w.rank + (int64_t)j * M;
+        const int32_t* rkj = rks + (int64_t)j * M;
         const int end = (int)afin + 1;
         double Aj = 0.0, Bj = 0.0;
-        int start = min(rk[0], end);
+        int start = min(rkj[0], end);
         for (int c = 1; c <= M; c++) {
-            const int next = (c < M) ? min(rk[c], end) : end;
+            const int next = (c < M) ? min(rkj[c], end) : end;
             const double q = sq[c];
             Aj = fma(q, P1[next] - P1[start], Aj);
             Bj = fma(q * q, P0[next] - P0[start], Bj);
@@ -557,6 +629,7 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
     for (int c = 1; c <= M; c++) a.mids[c - 1] = (float)(0.5 * (vals[c - 1] + vals[c]));
     a.G = G; a.M = M; a.A = L.A; a.Aa = L.A + kMaxSplits; a.nblk = L.nblk;
     a.nslice = L.nblk > 2 * kReduceSlices ? kReduceSlices : 0;
+    a.rk_lds = 0;
     const DdaWs w = ws_ptrs(ws, L);
     static bool lds_attr_set[64] = {false};
     int dev = 0;
@@ -565,7 +638,7 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
         if (e != hipSuccess) return e;
         e = hipFuncSetAttribute((const void*)k_dda_finalize,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 140 * 1024);
+                                hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
         if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
@@ -574,7 +647,9 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
         dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
         k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
     }
-    const size_t fin_lds = sizeof(double) * 2 * (size_t)(a.Aa + 2);
+    size_t fin_lds = sizeof(double) * 2 * (size_t)(a.Aa + 2);
+    a.rk_lds = fin_lds + sizeof(int32_t) * (size_t)a.A <= 140 * 1024;
+    if (a.rk_lds) fin_lds += sizeof(int32_t) * (size_t)a.A;
     k_dda_finalize<<<1, kFinThreads, fin_lds, s>>>(grid, a, w, alpha_out, D_out);
     return hipGetLastError();
 }
