@@ -161,6 +161,10 @@ int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_
     g.Nb = M; g.H = 1; g.W = 1; g.C = K; g.pitch = (int)(lda > 0x7fffffff ? 0x7fffffff : lda);
     g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
     if (lda > 0x7fffffff) return ESB_E_INVALID;
+    const int op = mma_choose(fa, fb, K);
+    if (op >= 0 && mma_fits(g, A, K, 1, B, ldb, b_layout))
+        return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
+                                     ldc, (hipStream_t)stream));
     return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
                                          decode_info(fb), alphaB, acc, y, ldc, N, (hipStream_t)stream));
 }
@@ -195,6 +199,10 @@ int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, con
     const hipStream_t s = (hipStream_t)stream;
     if (Cg == 1 && Kg == 1 && (int64_t)d->C * d->R * d->S <= 16384)
         return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
+    const int op = mma_choose(fx, fw, kred);
+    if (op >= 0 && mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK))
+        return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
+                                     kred, fw, alphaW, acc, y, d->K, s));
     return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
                                          alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
                                          d->K, Kg, s));

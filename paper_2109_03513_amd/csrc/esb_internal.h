@@ -79,6 +79,25 @@ hipError_t launch_contraction(int M, int N, int K, int groups, const ConvGeom& g
                               const float* alphaB, int32_t* acc, float* y, int64_t ldc,
                               int out_col_per_group, hipStream_t s);
 
+// Large-tile path on the 32x32 MFMA shapes.  op 1: codes decoded to E4M3,
+// fp32 accumulation; op 0: codes of n <= 3 bits decoded to int8 by one
+// v_perm_b32 lookup, int32 accumulation.
+struct MmaDecode {
+    uint32_t lm, inc, lmf, sel, t0, t1;   // four-byte masks / tables
+    int shf, shs;                         // fraction and sign shifts
+};
+MmaDecode mma_decode(const Fmt& f, int op);
+// 1 (E4M3), 0 (int8 table) or -1 (not eligible) for this pair of formats and
+// reduction length.
+int mma_choose(const Fmt& fa, const Fmt& fb, int64_t K);
+// Layout conditions of the path: 16-byte chunks of codes on both operands.
+bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const uint8_t* B,
+              int64_t ldb, int b_layout);
+hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
+                      const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
+                      int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
+                      int64_t ldc, hipStream_t s);
+
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,

@@ -1,0 +1,387 @@
+// Large-tile contraction over ESB codes on the 32x32 MFMA shapes of gfx950.
+//
+// The product of two ESB values is a short fraction product shifted by the
+// two exponents (eq. (15)), so a contraction over codes is an exact integer
+// dot product over m = q * 2^k.  This kernel decodes each code once per
+// workgroup while its tile moves from HBM to LDS, into one of two exact
+// machine formats:
+//
+//  * F8: OCP E4M3.  ESB(b, k) is a minifloat with ebits = b-k-1 exponent bits
+//    whose all-ones exponent is the subnormal binade; adding 1 to the exponent
+//    field modulo 2^ebits turns it into the E4M3 layout, with value
+//    q * 2^-6 exactly (the all-ones binade lands on the E4M3 subnormals).
+//    Five VALU operations per four codes.  The 32x32x64 f8f6f4 MFMA
+//    accumulates in fp32.  Measured on gfx950: within one instruction,
+//    products more than 2^13 below the largest product of that instruction are
+//    dropped, and the accumulator input is added exactly.  The dispatcher only
+//    takes this path when every product m_A * m_B is at most 2^12 and
+//    K * max|m_A| * max|m_B| < 2^24, where every partial sum is an integer
+//    multiple of 2^-(kA+kB+12) that fp32 holds exactly.
+//  * I8: int8 m through one v_perm_b32 table lookup (codes of n <= 3 bits, 8
+//    entries), then v_mfma_i32_32x32x32_i8 with int32 accumulation.
+//
+// Tiles: BM x BN per workgroup, WGM x WGN waves of (BM/WGM) x (BN/WGN), BK =
+// 128 reduction bytes per stage, LDS double buffer, global loads of stage t+1
+// in flight while stage t is multiplied.  LDS rows are 128 bytes of eight
+// 16-byte chunks, XOR-swizzled by (row >> 1) & 7 so that 16 consecutive rows
+// read at one logical chunk touch distinct banks.  Workgroups are numbered so
+// that each XCD (every eighth workgroup id) gets a contiguous run of tiles.
+#include <type_traits>
+
+#include "esb_internal.h"
+
+namespace esb {
+
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int BK = 128;
+constexpr int CPR = BK / 16;   // 16-byte chunks per tile row
+
+struct FastParams {
+    int M, N, K;
+    int tiles_m, tiles_n, ntiles;
+    ConvGeom ga;
+    const uint8_t* A;
+    const uint8_t* B;
+    int64_t ldb;
+    MmaDecode da, db;
+    const float* alphaA;
+    const float* alphaB;
+    int32_t* acc;
+    float* y;
+    int64_t ldc;
+    int out_shift;          // F8: acc_int = acc_f32 * 2^out_shift
+    int kA, kB;
+    int zrowA, zrowB;       // rows of kZeroRows holding each operand's +0 code
+};
+
+__device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
+    const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;   // exponent + 1 (mod 2^ebits)
+    return ((c << d.shs) & 0x80808080u) | t;                       // sign to bit 7
+}
+
+__device__ __forceinline__ uint32_t dec_i8(uint32_t c, const MmaDecode& d) {
+    return __builtin_amdgcn_perm(d.t1, d.t0, c & d.sel);
+}
+
+template <int OP>
+__device__ __forceinline__ uint4 dec16(uint4 v, const MmaDecode& d) {
+    if (OP == 1) return make_uint4(dec_f8(v.x, d), dec_f8(v.y, d), dec_f8(v.z, d), dec_f8(v.w, d));
+    return make_uint4(dec_i8(v.x, d), dec_i8(v.y, d), dec_i8(v.z, d), dec_i8(v.w, d));
+}
+
+// 16 bytes of the +0 code of every ESB(n, k) (index (n - 2) * 8 + k): the
+// source of every chunk that lies outside the operand (padding, ragged edges,
+// the reduction tail), so that loads need no branches.
+struct ZeroRows {
+    uint8_t b[7 * 8][16];
+};
+constexpr ZeroRows make_zero_rows() {
+    ZeroRows z{};
+    for (int n = 2; n <= 8; n++)
+        for (int k = 0; k < 8; k++)
+            for (int i = 0; i < 16; i++)
+                z.b[(n - 2) * 8 + k][i] =
+                    (k <= n - 2) ? (uint8_t)(((1u << (n - k - 1)) - 1u) << k) : (uint8_t)0;
+    return z;
+}
+__device__ ZeroRows kZeroRows = make_zero_rows();   // read only; global, not constant, memory
+
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+    return row * BK + ((chunk ^ ((row >> 1) & 7)) << 4);
+}
+
+// Tile id -> (tm, tn): contiguous runs per XCD, then groups of 8 tile rows.
+__device__ __forceinline__ void tile_of(const FastParams& g, int& tm, int& tn) {
+    const int b = blockIdx.x, T = g.ntiles;
+    const int per = T >> 3, rem = T & 7, x = b & 7, j = b >> 3;
+    const int t = x * per + min(x, rem) + j;
+    constexpr int GM = 8;
+    const int span = GM * g.tiles_n;
+    const int grp = t / span, first = grp * GM;
+    const int gm = min(g.tiles_m - first, GM);
+    const int r = t - grp * span;
+    tm = first + r % gm;
+    tn = r / gm;
+}
+
+template <int BM, int BN, int WGM, int WGN, int OP, int CONV>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int TI = WM / 32, TJ = WN / 32;
+    constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
+    static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "whole chunks per thread");
+    static_assert(NT % CPR == 0, "a thread keeps one chunk column");
+    constexpr int RSTEP = NT / CPR;   // tile rows between a thread's chunks
+    __shared__ __align__(16) uint8_t sA[2][BM * BK];
+    __shared__ __align__(16) uint8_t sB[2][BN * BK];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int tm, tn;
+    tile_of(g, tm, tn);
+    const int grp = blockIdx.z;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int wr = (wave / WGN) * WM, wc = (wave % WGN) * WN;
+    const ConvGeom& cg = g.ga;
+    const int goffA = grp * cg.Cg;
+    const int64_t brow0 = (int64_t)grp * g.N;
+    const int ch = tid % CPR;        // chunk column of every load of this thread
+    const int row0 = tid / CPR;
+
+    // A rows of this thread.  Convolution: output pixels, whose (r, s, c)
+    // reduction position is the same for every chunk of the thread; a row
+    // outside M gets an input row far out of range so that every load of it
+    // takes the +0 code.
+    int64_t a_off[CA];
+    int a_ih[CA], a_iw[CA];
+    int kr = 0, ks = 0, kc = 16 * ch;
+    if (CONV) {
+#pragma unroll
+        for (int i = 0; i < CA; i++) {
+            const int m = m0 + row0 + i * RSTEP;
+            const bool ok = m < g.M;
+            const int mm = ok ? m : 0;
+            const int pq = cg.P * cg.Q;
+            const int img = mm / pq, rem = mm - img * pq;
+            const int p = rem / cg.Q, q = rem - p * cg.Q;
+            a_ih[i] = ok ? p * cg.sh - cg.ph : -0x40000000;
+            a_iw[i] = q * cg.sw - cg.pw;
+            a_off[i] = (((int64_t)img * cg.H + a_ih[i]) * cg.W + a_iw[i]) * cg.pitch + goffA;
+        }
+        const int rs = kc / cg.Cg;
+        kc -= rs * cg.Cg;
+        kr = rs / cg.S;
+        ks = rs - kr * cg.S;
+    }
+    const uint8_t* aptr = g.A + (int64_t)(m0 + row0) * cg.pitch + 16 * ch;
+    const int64_t astep = (int64_t)RSTEP * cg.pitch;
+    const int mrem = g.M - m0 - row0;   // dense: chunk i of A is inside M iff i * RSTEP < mrem
+    const uint8_t* bptr = g.B + (brow0 + n0 + row0) * g.ldb + 16 * ch;
+    const int64_t bstep = (int64_t)RSTEP * g.ldb;
+    const int nrem = g.N - n0 - row0;   // chunk i of B is inside N iff i * RSTEP < nrem
+
+    const uint8_t* zA = kZeroRows.b[g.zrowA];
+    const uint8_t* zB = kZeroRows.b[g.zrowB];
+    uint4 ra[CA], rb[CB];
+    auto load_stage = [&](int k0) {
+        const bool kin = k0 + 16 * ch < g.K;
+        if (CONV) {
+            const int64_t koff = ((int64_t)kr * cg.W + ks) * cg.pitch + kc;
+#pragma unroll
+            for (int i = 0; i < CA; i++) {
+                const int ih = a_ih[i] + kr, iw = a_iw[i] + ks;
+                const bool ok = kin && (unsigned)ih < (unsigned)cg.H && (unsigned)iw < (unsigned)cg.W;
+                ra[i] = *(const uint4*)(ok ? g.A + a_off[i] + koff : zA);
+            }
+            kc += BK;
+            while (kc >= cg.Cg) {
+                kc -= cg.Cg;
+                if (++ks == cg.S) { ks = 0; ++kr; }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < CA; i++)
+                ra[i] = *(const uint4*)((kin && i * RSTEP < mrem) ? aptr + i * astep + k0 : zA);
+        }
+#pragma unroll
+        for (int i = 0; i < CB; i++)
+            rb[i] = *(const uint4*)((kin && i * RSTEP < nrem) ? bptr + i * bstep + k0 : zB);
+    };
+    auto store_stage = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < CA; i++)
+            *(uint4*)&sA[buf][lds_off(row0 + i * RSTEP, ch)] = dec16<OP>(ra[i], g.da);
+#pragma unroll
+        for (int i = 0; i < CB; i++)
+            *(uint4*)&sB[buf][lds_off(row0 + i * RSTEP, ch)] = dec16<OP>(rb[i], g.db);
+    };
+
+    typedef typename std::conditional<OP == 1, v16f, v16i>::type acc_t;
+    acc_t acc[TI][TJ];
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[i][j][r] = 0;
+
+    const int KT = (g.K + BK - 1) / BK;
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+    const int lr = lane & 31, lg = lane >> 5;
+    for (int kt = 0; kt < KT; kt++) {
+        const int buf = kt & 1;
+        // The stage after the last one reads only +0 rows; loading and storing
+        // it unconditionally keeps the loop body one basic block.
+        load_stage((kt + 1) * BK);
+        __builtin_amdgcn_sched_barrier(0);   // global loads first: they have the MFMAs to land
+        const uint8_t* tA = sA[buf];
+        const uint8_t* tB = sB[buf];
+        if (OP == 1) {
+#pragma unroll
+            for (int kb = 0; kb < BK / 64; kb++) {
+                v8i fb[TJ];
+                const int c0 = 4 * kb + 2 * lg;
+#pragma unroll
+                for (int j = 0; j < TJ; j++) {
+                    const int row = wc + 32 * j + lr;
+                    const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
+                    const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
+                    fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+#pragma unroll
+                for (int i = 0; i < TI; i++) {
+                    const int row = wr + 32 * i + lr;
+                    const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
+                    const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
+                    const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+                    for (int j = 0; j < TJ; j++)
+                        acc[i][j] = (acc_t)__builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            fa, fb[j], (v16f)acc[i][j], 0, 0, 0, 127, 0, 127);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < BK / 32; kb++) {
+                v4i fa[TI], fb[TJ];
+                const int c0 = 2 * kb + lg;
+#pragma unroll
+                for (int i = 0; i < TI; i++) fa[i] = *(const v4i*)&tA[lds_off(wr + 32 * i + lr, c0)];
+#pragma unroll
+                for (int j = 0; j < TJ; j++) fb[j] = *(const v4i*)&tB[lds_off(wc + 32 * j + lr, c0)];
+#pragma unroll
+                for (int i = 0; i < TI; i++)
+#pragma unroll
+                    for (int j = 0; j < TJ; j++)
+                        acc[i][j] = (acc_t)__builtin_amdgcn_mfma_i32_32x32x32_i8(
+                            fa[i], fb[j], (v16i)acc[i][j], 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);   // decode and LDS stores after the MFMAs
+        store_stage(buf ^ 1);
+        __syncthreads();
+    }
+
+    // epilogue: register r of a 32x32 block holds row 8*(r/4) + 4*(lane/32) + r%4,
+    // column lane % 32.
+    float s = 0.0f;
+    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int row = m0 + wr + 32 * i + 8 * (r >> 2) + 4 * lg + (r & 3);
+                const int col = n0 + wc + 32 * j + lr;
+                if (row < g.M && col < g.N) {
+                    float fv;
+                    int32_t iv;
+                    if (OP == 1) {
+                        fv = ldexpf((float)acc[i][j][r], g.out_shift);
+                        iv = (int32_t)fv;
+                    } else {
+                        iv = (int32_t)acc[i][j][r];
+                        fv = (float)iv;
+                    }
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    if (g.acc) g.acc[o] = iv;
+                    if (g.y) g.y[o] = s * fv;
+                }
+            }
+}
+
+template <int BM, int BN, int WGM, int WGN, int OP>
+hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
+    const bool conv = !(g.ga.H == 1 && g.ga.W == 1 && g.ga.R == 1 && g.ga.S == 1 && g.ga.ph == 0 &&
+                        g.ga.pw == 0 && g.ga.Cg == g.K && groups == 1);
+    g.tiles_m = (g.M + BM - 1) / BM;
+    g.tiles_n = (g.N + BN - 1) / BN;
+    g.ntiles = g.tiles_m * g.tiles_n;
+    dim3 grid(g.ntiles, 1, groups);
+    if (conv) k_mma<BM, BN, WGM, WGN, OP, 1><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    else k_mma<BM, BN, WGM, WGN, OP, 0><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    return hipGetLastError();
+}
+
+template <int OP>
+hipError_t launch_op(const FastParams& g, int groups, hipStream_t s) {
+    const int64_t cus = num_cus();
+    auto tiles = [&](int bm, int bn) {
+        return (int64_t)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * groups;
+    };
+    if (g.N > 128 && tiles(256, 256) >= cus) return launch_t<256, 256, 2, 2, OP>(g, groups, s);
+    if (tiles(128, 128) >= cus) return launch_t<128, 128, 2, 2, OP>(g, groups, s);
+    return launch_t<64, 64, 2, 2, OP>(g, groups, s);
+}
+
+}  // namespace
+
+MmaDecode mma_decode(const Fmt& f, int op) {
+    MmaDecode d;
+    const uint32_t rep = 0x01010101u;
+    d.lm = ((1u << (f.n - 1)) - 1u) * rep;
+    d.inc = ((1u << f.k) << (3 - f.k)) * rep;   // + 1 in the exponent field, after the shift
+    d.shf = 3 - f.k;
+    d.lmf = (((1u << (f.n - 1)) - 1u) << d.shf) * rep;
+    d.shs = 8 - f.n;
+    d.sel = (op == 1) ? 0u : ((1u << f.n) - 1u) * rep;
+    uint32_t t[2] = {0, 0};
+    if (op == 0) {
+        for (uint32_t c = 0; c < 8; c++) {
+            const uint32_t m = (uint32_t)decode_int(f, c & ((1u << f.n) - 1u)) & 0xffu;
+            t[c >> 2] |= m << (8 * (c & 3));
+        }
+    }
+    d.t0 = t[0];
+    d.t1 = t[1];
+    return d;
+}
+
+int mma_choose(const Fmt& fa, const Fmt& fb, int64_t K) {
+    if (fa.n <= 3 && fb.n <= 3) return 0;
+    auto f8ok = [](const Fmt& f) {
+        return f.ebits <= 4 && f.k <= 3 && !(f.ebits == 4 && f.k == 3);
+    };
+    if (!f8ok(fa) || !f8ok(fb)) return -1;
+    const double p = (double)fa.max_int * (double)fb.max_int;
+    if (p > 4096.0 || (double)K * p >= 16777216.0) return -1;
+    return 1;
+}
+
+bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const uint8_t* B,
+              int64_t ldb, int b_layout) {
+    return b_layout == 0 && K > 0 && ga.Cg >= 16 && ga.Cg % 16 == 0 && ga.pitch % 16 == 0 &&
+           (uintptr_t)A % 16 == 0 && (int64_t)groups * ga.Cg <= ga.pitch && K % 16 == 0 &&
+           ldb % 16 == 0 && (uintptr_t)B % 16 == 0 &&
+           (int64_t)ga.Nb * ga.H * ga.W <= 0x7fffffff;
+}
+
+hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
+                      const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
+                      int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
+                      int64_t ldc, hipStream_t s) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    FastParams g;
+    g.M = M; g.N = N; g.K = K; g.ga = ga;
+    g.A = A; g.B = B; g.ldb = ldb;
+    g.da = mma_decode(fa, op);
+    g.db = mma_decode(fb, op);
+    g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.kA = fa.k; g.kB = fb.k;
+    g.out_shift = fa.k + fb.k + 12;
+    g.zrowA = (fa.n - 2) * 8 + fa.k;
+    g.zrowB = (fb.n - 2) * 8 + fb.k;
+    g.tiles_m = g.tiles_n = g.ntiles = 0;
+    return op == 1 ? launch_op<1>(g, groups, s) : launch_op<0>(g, groups, s);
+}
+
+}  // namespace esb

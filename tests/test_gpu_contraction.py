@@ -171,3 +171,74 @@ def test_conv_mobilenet_block_full(esb):
                                     groups=L["groups"])
         np.testing.assert_array_equal(host(acc), oacc)
         assert_rel(host(y), oy, YREL, "y " + L["name"])
+
+
+def sampled_rows(M, tile):
+    """Rows spread over every tile row of the output, plus the ragged tail."""
+    r = sorted(set(list(range(0, min(M, 40))) + list(range(max(0, M - 40), M)) +
+                   list(range(tile // 2, M, tile))))
+    return np.array(r, dtype=np.int64)
+
+
+@pytest.mark.parametrize("M,N,K,fa,fb", [
+    (4097, 4100, 208, (4, 2), (4, 2)),     # 256 x 256 tiles, E4M3 path, ragged M, N and K
+    (4097, 4100, 208, (3, 2), (3, 1)),     # 256 x 256 tiles, int8 table path
+    (2049, 2050, 400, (5, 3), (5, 3)),     # 128 x 128 tiles
+    (2049, 2050, 400, (3, 1), (3, 2)),
+    (4096, 4096, 1152, (5, 3), (4, 2)),    # mixed formats, nine stages
+])
+def test_gemm_large_tiles_sampled(esb, M, N, K, fa, fb):
+    """Full-size launch; the oracle recomputes a sample of rows that covers every tile row."""
+    (bA, ksA), (bB, ksB) = fa, fb
+    A = wl.random_codes(11, (M, K), 8)
+    B = wl.random_codes(12, (N, K), 8)
+    log("gemm large M=%d N=%d K=%d A=%s B=%s" % (M, N, K, fa, fb))
+    acc, y = esb.esb_gemm(dev(A), bA, ksA, scalar(0.37), dev(B), bB, ksB, scalar(0.021))
+    rows = sampled_rows(M, 128)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, bA, ksA, 0.37, bB, ksB, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1))])
+def test_conv_large_batch_sampled(esb, fmt):
+    """3x3 conv 64->512 at 56x56, batch 32 (256 x 256 tiles); oracle on the first and last image."""
+    (bX, ksX), (bW, ksW) = fmt
+    x = wl.random_codes(13, (32, 56, 56, 64), 8)
+    w = wl.random_codes(14, (512, 3, 3, 64), 8)
+    log("conv large batch fmt=%s" % (fmt,))
+    acc, y = esb.esb_conv2d(dev(x), bX, ksX, scalar(0.5), dev(w), bW, ksW, scalar(0.03),
+                            stride=(1, 1), pad=(1, 1))
+    acc, y = host(acc), host(y)
+    for img in (0, 31):
+        s, oacc, oy = oracle.conv2d(np.ascontiguousarray(x[img:img + 1]), w, bX, ksX, 0.5, bW, ksW,
+                                    0.03, stride=(1, 1), pad=(1, 1))
+        np.testing.assert_array_equal(acc[img:img + 1], oacc)
+        assert_rel(y[img:img + 1], oy, YREL, "y")
+
+
+def extreme_codes(b, ks, shape, seed):
+    """Codes whose decoded integers are mostly the largest magnitude with a sprinkle of the
+    smallest nonzero one, both signs: the widest spread of products within one dot product."""
+    v = oracle.valueset(b, ks)
+    top = oracle.encode(float(v[-1]), b, ks)
+    small = oracle.encode(float(v[v > 0][0]), b, ks)
+    r = np.random.default_rng(seed)
+    c = np.where(r.random(shape) < 0.8, top, small).astype(np.uint8)
+    neg = r.random(shape) < 0.3
+    return np.where(neg, c | (1 << (b - 1)), c).astype(np.uint8)
+
+
+@pytest.mark.parametrize("K", [21392, 21408, 4096])
+def test_gemm_product_spread_and_accumulator_bound(esb, K):
+    """ESB(5,2): products m_A*m_B from 1 to 784 in one reduction; K * 784 is just below 2^24
+    (21392), just above it (21408, where the E4M3 path may not be used), and moderate."""
+    A = extreme_codes(5, 3, (64, K), 1)
+    B = extreme_codes(5, 3, (96, K), 2)
+    log("gemm spread K=%d" % K)
+    acc, y = esb.esb_gemm(dev(A), 5, 3, scalar(0.37), dev(B), 5, 3, scalar(0.021))
+    st, oacc, oy = oracle.gemm(A, B, 5, 3, 0.37, 5, 3, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc), oacc)
+    assert_rel(host(y), oy, YREL, "y")
