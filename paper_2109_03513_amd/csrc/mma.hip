@@ -21,11 +21,12 @@
 //    entries), then v_mfma_i32_32x32x32_i8 with int32 accumulation.
 //
 // Tiles: BM x BN per workgroup, WGM x WGN waves of (BM/WGM) x (BN/WGN), BK =
-// 128 reduction bytes per stage, LDS double buffer, global loads of stage t+1
-// in flight while stage t is multiplied.  LDS rows are 128 bytes of eight
-// 16-byte chunks, XOR-swizzled by (row >> 1) & 7 so that 16 consecutive rows
-// read at one logical chunk touch distinct banks.  Workgroups are numbered so
-// that each XCD (every eighth workgroup id) gets a contiguous run of tiles.
+// 64 reduction bytes per stage.  Codes travel HBM -> LDS by DMA two stages
+// ahead ("raw" buffers, no registers held); while the MFMAs of stage t run,
+// each thread decodes the raw chunks of stage t+1 it fetched itself into the
+// other half of a double-buffered, XOR-swizzled decoded tile.  One LDS
+// barrier per stage.  Workgroups are numbered so that each XCD (every eighth
+// workgroup id) gets a contiguous run of tiles.
 #include <type_traits>
 
 #include "esb_internal.h"
@@ -39,7 +40,7 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr int BK = 128;
+constexpr int BK = 64;
 constexpr int CPR = BK / 16;   // 16-byte chunks per tile row
 
 struct FastParams {
@@ -69,6 +70,10 @@ __device__ __forceinline__ uint32_t dec_i8(uint32_t c, const MmaDecode& d) {
     return __builtin_amdgcn_perm(d.t1, d.t0, c & d.sel);
 }
 
+__device__ __forceinline__ uint4 as_u4(v4i v) {
+    return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+
 template <int OP>
 __device__ __forceinline__ uint4 dec16(uint4 v, const MmaDecode& d) {
     if (OP == 1) return make_uint4(dec_f8(v.x, d), dec_f8(v.y, d), dec_f8(v.z, d), dec_f8(v.w, d));
@@ -92,8 +97,12 @@ constexpr ZeroRows make_zero_rows() {
 }
 __device__ ZeroRows kZeroRows = make_zero_rows();   // read only; global, not constant, memory
 
+// LDS offset of 16-byte chunk `chunk` of tile row `row`.  LDS has 64 banks of
+// 4 bytes: 256 bytes, four 64-byte rows.  Rows 4q..4q+3 take their chunks in
+// the order chunk ^ (q & 3), so 16 consecutive rows read at one logical chunk
+// (one quarter-wave of a fragment load) hit 16 distinct bank groups.
 __device__ __forceinline__ int lds_off(int row, int chunk) {
-    return row * BK + ((chunk ^ ((row >> 1) & 7)) << 4);
+    return row * BK + ((chunk ^ ((row >> 2) & 3)) << 4);
 }
 
 // Tile id -> (tm, tn): contiguous runs per XCD, then groups of 8 tile rows.
@@ -110,19 +119,92 @@ __device__ __forceinline__ void tile_of(const FastParams& g, int& tm, int& tn) {
     tn = r / gm;
 }
 
-template <int BM, int BN, int WGM, int WGN, int OP, int CONV>
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void gbl_cvoid_t;
+
+// One 16-byte chunk from global memory into LDS by DMA: lane l of the wave
+// writes lds_wave_base + 16 * l (the base must be the same for the whole wave).
+// Workgroup barrier for LDS only.  __syncthreads() also drains every
+// outstanding global access, which would wait for the fetch of the stage after
+// next; the raw chunks a thread reads back were fetched by its own lane, so
+// its own wait on them is enough.  The memory clobber keeps the compiler from
+// moving LDS accesses across.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Read 16 bytes of LDS outside the compiler's wait tracking.  Used for the
+// raw chunks: the compiler cannot tell which fetch wrote which raw buffer and
+// would wait for every fetch in flight.  The caller orders the read after its
+// fetch with vm_wait<>() and the use after the read with lgkm_wait_on().
+__device__ __forceinline__ v4i lds_read16_untracked(const uint8_t* p) {
+    v4i v;
+    const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+}
+
+// s_waitcnt vmcnt(N) (gfx9 encoding; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void dma16(const uint8_t* g, uint8_t* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds((gbl_cvoid_t*)g, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+template <int I>
+using ic = std::integral_constant<int, I>;
+
+// R: depth of the ring of raw buffers; the fetch of a stage is issued R - 1
+// stages before its codes are decoded.
+template <int BM, int BN, int WGM, int WGN, int OP, int CONV, int R>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TI = WM / 32, TJ = WN / 32;
-    constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
-    static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "whole chunks per thread");
-    static_assert(NT % CPR == 0, "a thread keeps one chunk column");
-    constexpr int RSTEP = NT / CPR;   // tile rows between a thread's chunks
-    __shared__ __align__(16) uint8_t sA[2][BM * BK];
-    __shared__ __align__(16) uint8_t sB[2][BN * BK];
+    constexpr int CHA = BM * CPR / NT, CHB = BN * CPR / NT, CT = CHA + CHB;
+    static_assert(CHA * NT == BM * CPR && CHB * NT == BN * CPR, "whole chunks per thread");
+    constexpr int RSTEP = NT / CPR;       // tile rows between a thread's chunks
+    constexpr int TILE = (BM + BN) * BK;  // bytes of one stage: A rows, then B rows
+    static_assert(R >= 2 && R <= 6, "raw ring depth");
+    // dec: decoded, swizzled tiles read by the MFMAs.  raw: codes as fetched;
+    // chunk j of thread t sits at (j * NT + t) * 16, written and read by t only.
+    // Separate arrays, addressed with compile-time slots, let the compiler
+    // wait for exactly the fetch a read depends on.
+    __shared__ __align__(16) uint8_t dec0[TILE];
+    __shared__ __align__(16) uint8_t dec1[TILE];
+    __shared__ __align__(16) uint8_t raw0[TILE];
+    __shared__ __align__(16) uint8_t raw1[TILE];
+    __shared__ __align__(16) uint8_t raw2[R > 2 ? TILE : 16];
+    __shared__ __align__(16) uint8_t raw3[R > 3 ? TILE : 16];
+    __shared__ __align__(16) uint8_t raw4[R > 4 ? TILE : 16];
+    __shared__ __align__(16) uint8_t raw5[R > 5 ? TILE : 16];
+    auto RAW = [&](auto I) -> uint8_t* {
+        constexpr int i = decltype(I)::value;
+        if constexpr (i == 0) return raw0;
+        else if constexpr (i == 1) return raw1;
+        else if constexpr (i == 2) return raw2;
+        else if constexpr (i == 3) return raw3;
+        else if constexpr (i == 4) return raw4;
+        else return raw5;
+    };
+    auto DEC = [&](auto I) -> uint8_t* {
+        if constexpr (decltype(I)::value == 0) return dec0;
+        else return dec1;
+    };
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int tm, tn;
     tile_of(g, tm, tn);
     const int grp = blockIdx.z;
@@ -131,19 +213,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     const ConvGeom& cg = g.ga;
     const int goffA = grp * cg.Cg;
     const int64_t brow0 = (int64_t)grp * g.N;
-    const int ch = tid % CPR;        // chunk column of every load of this thread
+    const int ch = tid % CPR;      // chunk column of every chunk of this thread
     const int row0 = tid / CPR;
 
     // A rows of this thread.  Convolution: output pixels, whose (r, s, c)
     // reduction position is the same for every chunk of the thread; a row
-    // outside M gets an input row far out of range so that every load of it
-    // takes the +0 code.
-    int64_t a_off[CA];
-    int a_ih[CA], a_iw[CA];
+    // outside M gets an input row far out of range.
+    int64_t a_off[CHA];
+    int a_ih[CHA], a_iw[CHA];
     int kr = 0, ks = 0, kc = 16 * ch;
     if (CONV) {
 #pragma unroll
-        for (int i = 0; i < CA; i++) {
+        for (int i = 0; i < CHA; i++) {
             const int m = m0 + row0 + i * RSTEP;
             const bool ok = m < g.M;
             const int mm = ok ? m : 0;
@@ -164,20 +245,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     const int mrem = g.M - m0 - row0;   // dense: chunk i of A is inside M iff i * RSTEP < mrem
     const uint8_t* bptr = g.B + (brow0 + n0 + row0) * g.ldb + 16 * ch;
     const int64_t bstep = (int64_t)RSTEP * g.ldb;
-    const int nrem = g.N - n0 - row0;   // chunk i of B is inside N iff i * RSTEP < nrem
-
+    const int nrem = g.N - n0 - row0;
     const uint8_t* zA = kZeroRows.b[g.zrowA];
     const uint8_t* zB = kZeroRows.b[g.zrowB];
-    uint4 ra[CA], rb[CB];
-    auto load_stage = [&](int k0) {
+
+    // fetch the codes of reduction offset k0 into a raw buffer
+    auto fetch = [&](int k0, uint8_t* rawbuf) {
         const bool kin = k0 + 16 * ch < g.K;
+        uint8_t* base = rawbuf + wave * 64 * 16;
         if (CONV) {
             const int64_t koff = ((int64_t)kr * cg.W + ks) * cg.pitch + kc;
 #pragma unroll
-            for (int i = 0; i < CA; i++) {
+            for (int i = 0; i < CHA; i++) {
                 const int ih = a_ih[i] + kr, iw = a_iw[i] + ks;
                 const bool ok = kin && (unsigned)ih < (unsigned)cg.H && (unsigned)iw < (unsigned)cg.W;
-                ra[i] = *(const uint4*)(ok ? g.A + a_off[i] + koff : zA);
+                dma16(ok ? g.A + a_off[i] + koff : zA, base + i * NT * 16);
             }
             kc += BK;
             while (kc >= cg.Cg) {
@@ -186,20 +268,33 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
             }
         } else {
 #pragma unroll
-            for (int i = 0; i < CA; i++)
-                ra[i] = *(const uint4*)((kin && i * RSTEP < mrem) ? aptr + i * astep + k0 : zA);
+            for (int i = 0; i < CHA; i++)
+                dma16((kin && i * RSTEP < mrem) ? aptr + i * astep + k0 : zA, base + i * NT * 16);
         }
 #pragma unroll
-        for (int i = 0; i < CB; i++)
-            rb[i] = *(const uint4*)((kin && i * RSTEP < nrem) ? bptr + i * bstep + k0 : zB);
+        for (int i = 0; i < CHB; i++)
+            dma16((kin && i * RSTEP < nrem) ? bptr + i * bstep + k0 : zB, base + (CHA + i) * NT * 16);
     };
-    auto store_stage = [&](int buf) {
+    v4i rv[CT];
+    auto read_raw = [&](const uint8_t* rawbuf) {
 #pragma unroll
-        for (int i = 0; i < CA; i++)
-            *(uint4*)&sA[buf][lds_off(row0 + i * RSTEP, ch)] = dec16<OP>(ra[i], g.da);
+        for (int j = 0; j < CT; j++) rv[j] = lds_read16_untracked(&rawbuf[(j * NT + tid) * 16]);
+    };
+    // s_waitcnt lgkmcnt(0), tied to the raw registers so no use moves above it
+    auto raw_ready = [&]() {
 #pragma unroll
-        for (int i = 0; i < CB; i++)
-            *(uint4*)&sB[buf][lds_off(row0 + i * RSTEP, ch)] = dec16<OP>(rb[i], g.db);
+        for (int j = 0; j < CT; j++) asm volatile("" : "+v"(rv[j]));
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < CT; j++) asm volatile("" : "+v"(rv[j]));
+    };
+    auto decode_store = [&](uint8_t* d) {
+#pragma unroll
+        for (int j = 0; j < CHA; j++)
+            *(uint4*)&d[lds_off(row0 + j * RSTEP, ch)] = dec16<OP>(as_u4(rv[j]), g.da);
+#pragma unroll
+        for (int j = 0; j < CHB; j++)
+            *(uint4*)&d[BM * BK + lds_off(row0 + j * RSTEP, ch)] = dec16<OP>(as_u4(rv[CHA + j]), g.db);
     };
 
     typedef typename std::conditional<OP == 1, v16f, v16i>::type acc_t;
@@ -211,42 +306,30 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0;
 
-    const int KT = (g.K + BK - 1) / BK;
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
     const int lr = lane & 31, lg = lane >> 5;
-    for (int kt = 0; kt < KT; kt++) {
-        const int buf = kt & 1;
-        // The stage after the last one reads only +0 rows; loading and storing
-        // it unconditionally keeps the loop body one basic block.
-        load_stage((kt + 1) * BK);
-        __builtin_amdgcn_sched_barrier(0);   // global loads first: they have the MFMAs to land
-        const uint8_t* tA = sA[buf];
-        const uint8_t* tB = sB[buf];
+    auto compute = [&](const uint8_t* d) {
+        const uint8_t* tA = d;
+        const uint8_t* tB = d + BM * BK;
         if (OP == 1) {
+            v8i fb[TJ];
+            const int c0 = 2 * lg;
 #pragma unroll
-            for (int kb = 0; kb < BK / 64; kb++) {
-                v8i fb[TJ];
-                const int c0 = 4 * kb + 2 * lg;
+            for (int j = 0; j < TJ; j++) {
+                const int row = wc + 32 * j + lr;
+                const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
+                const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
+                fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            }
 #pragma unroll
-                for (int j = 0; j < TJ; j++) {
-                    const int row = wc + 32 * j + lr;
-                    const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
-                    const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
-                    fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                }
+            for (int i = 0; i < TI; i++) {
+                const int row = wr + 32 * i + lr;
+                const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
+                const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
+                const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 #pragma unroll
-                for (int i = 0; i < TI; i++) {
-                    const int row = wr + 32 * i + lr;
-                    const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
-                    const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
-                    const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-#pragma unroll
-                    for (int j = 0; j < TJ; j++)
-                        acc[i][j] = (acc_t)__builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            fa, fb[j], (v16f)acc[i][j], 0, 0, 0, 127, 0, 127);
-                }
+                for (int j = 0; j < TJ; j++)
+                    acc[i][j] = (acc_t)__builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        fa, fb[j], (v16f)acc[i][j], 0, 0, 0, 127, 0, 127);
             }
         } else {
 #pragma unroll
@@ -265,9 +348,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
                             fa[i], fb[j], (v16i)acc[i][j], 0, 0, 0);
             }
         }
-        __builtin_amdgcn_sched_barrier(0);   // decode and LDS stores after the MFMAs
-        store_stage(buf ^ 1);
-        __syncthreads();
+    };
+
+    const int KT = (g.K + BK - 1) / BK;
+    static_for<0, R>([&](auto Q) { fetch(decltype(Q)::value * BK, RAW(Q)); });
+    vm_wait<(R - 1) * CT>();   // stage 0 landed
+    read_raw(RAW(ic<0>{}));
+    raw_ready();
+    decode_store(DEC(ic<0>{}));
+    lds_barrier();
+    // Stage s: its codes sit in raw slot s % R, its decoded tile in dec slot s % 2.
+    constexpr int U = (R % 2 == 0) ? R : 2 * R;
+    for (int kt = 0; kt < KT; kt += U) {
+        static_for<0, U>([&](auto Q) {
+            constexpr int q = decltype(Q)::value;
+            if (kt + q < KT) {
+                // fetches in flight: stages s+1 .. s+R-1, CT instructions each
+                vm_wait<(R - 2) * CT>();                    // stage s+1 landed
+                read_raw(RAW(ic<(q + 1) % R>{}));
+                fetch((kt + q + R) * BK, RAW(ic<q % R>{})); // stage s+R into the slot of stage s
+                raw_ready();
+                compute(DEC(ic<q % 2>{}));
+                decode_store(DEC(ic<(q + 1) % 2>{}));
+                lds_barrier();
+            }
+        });
     }
 
     // epilogue: register r of a 32x32 block holds row 8*(r/4) + 4*(lane/32) + r%4,
@@ -299,7 +404,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
             }
 }
 
-template <int BM, int BN, int WGM, int WGN, int OP>
+template <int BM, int BN, int WGM, int WGN, int OP, int R>
 hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
     const bool conv = !(g.ga.H == 1 && g.ga.W == 1 && g.ga.R == 1 && g.ga.S == 1 && g.ga.ph == 0 &&
                         g.ga.pw == 0 && g.ga.Cg == g.K && groups == 1);
@@ -307,8 +412,8 @@ hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
     g.tiles_n = (g.N + BN - 1) / BN;
     g.ntiles = g.tiles_m * g.tiles_n;
     dim3 grid(g.ntiles, 1, groups);
-    if (conv) k_mma<BM, BN, WGM, WGN, OP, 1><<<grid, 64 * WGM * WGN, 0, s>>>(g);
-    else k_mma<BM, BN, WGM, WGN, OP, 0><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    if (conv) k_mma<BM, BN, WGM, WGN, OP, 1, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    else k_mma<BM, BN, WGM, WGN, OP, 0, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
     return hipGetLastError();
 }
 
@@ -318,9 +423,14 @@ hipError_t launch_op(const FastParams& g, int groups, hipStream_t s) {
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * groups;
     };
-    if (g.N > 128 && tiles(256, 256) >= cus) return launch_t<256, 256, 2, 2, OP>(g, groups, s);
-    if (tiles(128, 128) >= cus) return launch_t<128, 128, 2, 2, OP>(g, groups, s);
-    return launch_t<64, 64, 2, 2, OP>(g, groups, s);
+    // Measured on MI355X (ESB(5,3) operands): 256 x 256 on eight waves is the
+    // fastest tile wherever it fills the chip; below that, decoding per MAC
+    // grows as (BM + BN) / (BM * BN), so the largest tile that keeps at least
+    // half the CUs busy wins over a smaller one that fills them all.
+    if (g.N > 128 && tiles(256, 256) >= cus) return launch_t<256, 256, 2, 4, OP, 2>(g, groups, s);
+    if (g.N > 64 && tiles(128, 128) >= cus / 2) return launch_t<128, 128, 2, 4, OP, 2>(g, groups, s);
+    if (tiles(128, 64) >= cus) return launch_t<128, 64, 2, 2, OP, 4>(g, groups, s);
+    return launch_t<64, 64, 2, 2, OP, 4>(g, groups, s);
 }
 
 }  // namespace

@@ -202,16 +202,17 @@ def test_gemm_large_tiles_sampled(esb, M, N, K, fa, fb):
 
 
 @pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1))])
-def test_conv_large_batch_sampled(esb, fmt):
-    """3x3 conv 64->512 at 56x56, batch 32 (256 x 256 tiles); oracle on the first and last image."""
+@pytest.mark.parametrize("nb,kout", [(32, 512), (16, 64)])   # 256 x 256 and 128 x 64 tiles
+def test_conv_large_batch_sampled(esb, fmt, nb, kout):
+    """3x3 conv 64->kout at 56x56 with a large batch; oracle on the first and last image."""
     (bX, ksX), (bW, ksW) = fmt
-    x = wl.random_codes(13, (32, 56, 56, 64), 8)
-    w = wl.random_codes(14, (512, 3, 3, 64), 8)
-    log("conv large batch fmt=%s" % (fmt,))
+    x = wl.random_codes(13, (nb, 56, 56, 64), 8)
+    w = wl.random_codes(14, (kout, 3, 3, 64), 8)
+    log("conv large batch nb=%d kout=%d fmt=%s" % (nb, kout, fmt))
     acc, y = esb.esb_conv2d(dev(x), bX, ksX, scalar(0.5), dev(w), bW, ksW, scalar(0.03),
                             stride=(1, 1), pad=(1, 1))
     acc, y = host(acc), host(y)
-    for img in (0, 31):
+    for img in (0, nb - 1):
         s, oacc, oy = oracle.conv2d(np.ascontiguousarray(x[img:img + 1]), w, bX, ksX, 0.5, bW, ksW,
                                     0.03, stride=(1, 1), pad=(1, 1))
         np.testing.assert_array_equal(acc[img:img + 1], oacc)
