@@ -25,6 +25,8 @@
 //   Q_c^2, D_j = S2 + a (a B_j - 2 A_j); argmin with ties to the lowest index.
 // Integer sums are exact; fp64 sums run in a fixed order: the result is
 // deterministic.
+#include <type_traits>
+
 #include "esb_internal.h"
 
 namespace esb {
@@ -199,6 +201,29 @@ __device__ __forceinline__ void block_exclusive_scan_n(const double (&v)[N], dou
     __syncthreads();
 }
 
+// Block-wide sums of N fp64 components in a fixed order (deterministic): a
+// butterfly inside each wave, then the wave totals added in wave order.  All
+// threads receive the totals.  One barrier pair.
+template <int N>
+__device__ __forceinline__ void block_sum_n(double (&v)[N], double (*sh)[16]) {
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int c = 0; c < N; c++)
+        for (int off = 32; off > 0; off >>= 1) v[c] += __shfl_xor(v[c], off);
+    if (lane == 0) {
+#pragma unroll
+        for (int c = 0; c < N; c++) sh[c][wid] = v[c];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < N; c++) {
+        double t = 0.0;
+        for (int w = 0; w < nw; w++) t += sh[c][w];
+        v[c] = t;
+    }
+    __syncthreads();
+}
+
 // Wave-level min / max / sum of 32-bit values (all 64 lanes take part).
 __device__ __forceinline__ uint32_t wave_min(uint32_t v) {
     for (int off = 32; off > 0; off >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, off));
@@ -248,6 +273,45 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     __shared__ uint32_t s_lo, s_hi, s_nfin, s_flags;
     __shared__ uint32_t s_scan[16];
     __shared__ double s_red3[3][16];
+
+    // ---- 0. this block's chunks of x; the first one is requested now, so its
+    //         loads overlap the set-up.  Loads are unconditional (clamped
+    //         address, value zeroed outside the range), so the compiler can
+    //         leave a chunk in flight across the binning of the previous one.
+    const bool vec = ((uintptr_t)x & 15) == 0;
+    const int64_t n4 = vec ? (len >> 2) : (len + 3) >> 2;   // scalar path: chunks of 4 elements
+    const int64_t nchunks = (n4 + kChunk4 - 1) / kChunk4;
+    const int64_t cpb = (nchunks + gridDim.x - 1) / gridDim.x;
+    const int64_t c0 = (int64_t)blockIdx.x * cpb;
+    const int64_t c1 = min(nchunks, c0 + cpb);
+    auto load_chunk_t = [&](auto VEC, int64_t ch, uint32_t (&g)[16]) {
+        if constexpr (decltype(VEC)::value) {
+            const f32x4* x4 = (const f32x4*)x;
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int64_t i4 = ch * kChunk4 + tid + u * kHistThreads;
+                const bool in = ch < c1 && i4 < n4;
+                const f32x4 v = __builtin_nontemporal_load(&x4[in ? i4 : 0]);
+                g[4 * u + 0] = in ? __float_as_uint(v.x) : 0u;
+                g[4 * u + 1] = in ? __float_as_uint(v.y) : 0u;
+                g[4 * u + 2] = in ? __float_as_uint(v.z) : 0u;
+                g[4 * u + 3] = in ? __float_as_uint(v.w) : 0u;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 16; u++) {
+                const int64_t i = ch * (4 * kChunk4) + tid + (int64_t)u * kHistThreads;
+                const bool in = ch < c1 && i < len;
+                const uint32_t v = __float_as_uint(x[in ? i : 0]);
+                g[u] = in ? v : 0u;   // zeros: atom 0, add nothing
+            }
+        }
+    };
+    uint32_t gn[16];
+    if (c0 < c1) {   // (a block with no chunk touches no element: x may be empty)
+        if (vec) load_chunk_t(std::integral_constant<bool, true>{}, c0, gn);
+        else load_chunk_t(std::integral_constant<bool, false>{}, c0, gn);
+    }
 
     // ---- 1. thresholds, their finite range and count
     if (tid < M) s_mids[tid] = a.mids[tid];
@@ -357,35 +421,53 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     double sumsq = 0.0, top_s1 = 0.0;
     uint32_t top_cnt = 0, flags = 0;
     constexpr int E = 8;
+    // Per element: x^2 into the fp64 sum; |x| in [lo, hi) to its atom (bin
+    // table, then one comparison against the next bound; a loop only where a
+    // bin holds two or more bounds) and one LDS atomic adding
+    // (mantissa << 20) + 1.  Every atom lies inside one binade, so the sum of
+    // the 23-bit mantissas and the count give the exact sum of |x| over the
+    // atom.  |x| >= hi (the top atom) and non-finite x are rare: a branch.
+    const uint32_t span = hi - lo;
     auto visit = [&](const uint32_t (&xb)[E]) {
         uint32_t ab[E], at[E];
         bool mid[E];
+        bool rare = false;
 #pragma unroll
         for (int e = 0; e < E; e++) {
             ab[e] = xb[e] & 0x7fffffffu;
-            const bool fin = ab[e] < 0x7f800000u;
-            flags |= fin ? 0u : ((ab[e] > 0x7f800000u) ? 2u : 1u);
-            const double xd = fin ? (double)__uint_as_float(ab[e]) : 0.0;
+            const double xd = (double)__uint_as_float(ab[e]);
             sumsq = fma(xd, xd, sumsq);
-            const bool top = fin && ab[e] >= hi;
-            top_s1 += top ? xd : 0.0;
-            top_cnt += top ? 1u : 0u;
-            mid[e] = ab[e] >= lo && ab[e] < hi;       // atom 0 (q = 0 for all) is skipped
+            rare |= ab[e] >= hi;
+            mid[e] = ab[e] - lo < span;                // atom 0 (q = 0 for all) is skipped
             at[e] = binfo[mid[e] ? (ab[e] >> shift) - base : 0u];
         }
+        if (rare) {
 #pragma unroll
-        for (int e = 0; e < E; e++) {
-            if (mid[e] && (at[e] >> 16)) {           // a boundary inside the bin: scan
-                uint32_t t = at[e] & 0xffffu;
-                while (U[t + 1] <= ab[e]) t++;
-                at[e] = t;
+            for (int e = 0; e < E; e++) {
+                if (ab[e] >= hi) {
+                    if (ab[e] < 0x7f800000u) {
+                        top_s1 += (double)__uint_as_float(ab[e]);
+                        top_cnt += 1u;
+                    } else {
+                        flags |= (ab[e] > 0x7f800000u) ? 2u : 1u;
+                    }
+                }
             }
         }
 #pragma unroll
         for (int e = 0; e < E; e++) {
+            uint32_t t = at[e] & 0xffffu;
+            t += (ab[e] >= U[t + 1]) ? 1u : 0u;       // at most one bound inside the bin
+            if (mid[e] && at[e] >= 0x20000u) {        // two or more: walk
+                while (U[t + 1] <= ab[e]) t++;
+            }
+            at[e] = t;
+        }
+#pragma unroll
+        for (int e = 0; e < E; e++) {
             if (mid[e]) {
-                const uint32_t sig = (ab[e] & 0x7fffffu) | ((ab[e] >> 23) ? 0x800000u : 0u);
-                atomicAdd(&hist[at[e] & 0xffffu], ((uint64_t)sig << 20) | 1u);
+                const uint32_t mant = ab[e] & 0x7fffffu;
+                atomicAdd(&hist[at[e]], ((uint64_t)mant << 20) | 1u);
             }
         }
     };
@@ -403,40 +485,29 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         first_flush = false;
         __syncthreads();
     };
-    const bool vec = ((uintptr_t)x & 15) == 0;
-    const int64_t n4 = vec ? (len >> 2) : (len + 3) >> 2;   // scalar path: chunks of 4 elements
-    const int64_t nchunks = (n4 + kChunk4 - 1) / kChunk4;
-    const int64_t cpb = (nchunks + gridDim.x - 1) / gridDim.x;
-    const int64_t c0 = (int64_t)blockIdx.x * cpb;
-    const int64_t c1 = min(nchunks, c0 + cpb);
-    int since = 0;
-    for (int64_t ch = c0; ch < c1; ch++) {
-        uint32_t g[16];
-        if (vec) {
-            const f32x4* x4 = (const f32x4*)x;
+    // The pass, one chunk of loads ahead of the chunk being binned (the first
+    // chunk was requested before the set-up).
+    auto pass = [&](auto VEC) {
+        auto load_chunk = [&](int64_t ch, uint32_t (&g)[16]) { load_chunk_t(VEC, ch, g); };
+        int since = 0;
+        for (int64_t ch = c0; ch < c1; ch++) {
+            uint32_t g[16];
 #pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const int64_t i4 = ch * kChunk4 + tid + u * kHistThreads;
-                f32x4 v = {0.f, 0.f, 0.f, 0.f};
-                if (i4 < n4) v = __builtin_nontemporal_load(&x4[i4]);
-                g[4 * u + 0] = __float_as_uint(v.x); g[4 * u + 1] = __float_as_uint(v.y);
-                g[4 * u + 2] = __float_as_uint(v.z); g[4 * u + 3] = __float_as_uint(v.w);
+            for (int u = 0; u < 16; u++) g[u] = gn[u];
+            load_chunk(ch + 1, gn);
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                uint32_t gg[E];
+#pragma unroll
+                for (int e = 0; e < E; e++) gg[e] = g[E * h + e];
+                visit(gg);
             }
-        } else {
-#pragma unroll
-            for (int u = 0; u < 16; u++) {
-                const int64_t i = ch * (4 * kChunk4) + tid + (int64_t)u * kHistThreads;
-                g[u] = i < len ? __float_as_uint(x[i]) : 0u;    // zeros: atom 0, add nothing
-            }
+            if (++since == kFlushChunks) { flush(); since = 0; }
         }
-#pragma unroll
-        for (int h = 0; h < 2; h++) {
-            uint32_t gg[E];
-#pragma unroll
-            for (int e = 0; e < E; e++) gg[e] = g[E * h + e];
-            visit(gg);
-        }
-        if (++since == kFlushChunks) { flush(); since = 0; }
+    };
+    if (c0 < c1) {
+        if (vec) pass(std::integral_constant<bool, true>{});
+        else pass(std::integral_constant<bool, false>{});
     }
     if (vec && blockIdx.x == gridDim.x - 1 && tid < (int)(len & 3)) {   // tail of the vector path
         uint32_t gg[E];
@@ -450,12 +521,11 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     // ---- 7. block scalars; block 0 also publishes the tables
     if (flags) atomicOr(&s_flags, flags);
     {
-        const double v3[3] = {sumsq, top_s1, (double)top_cnt};   // counts exact in fp64
-        double bef[3], tot[3];
-        block_exclusive_scan_n<3>(v3, s_red3, bef, tot);
+        double v3[3] = {sumsq, top_s1, (double)top_cnt};   // counts exact in fp64
+        block_sum_n<3>(v3, s_red3);
         if (tid == 0) {
             double* ps = w.pscal + 4 * blockIdx.x;
-            ps[0] = tot[0]; ps[1] = tot[1]; ps[2] = tot[2]; ps[3] = (double)s_flags;
+            ps[0] = v3[0]; ps[1] = v3[1]; ps[2] = v3[2]; ps[3] = (double)s_flags;
         }
     }
     if (blockIdx.x == 0) {
@@ -513,9 +583,8 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
         const double* ps = w.pscal + 4 * b;
         v3[0] += ps[0]; v3[1] += ps[1]; v3[2] += ps[2]; fl |= (uint32_t)ps[3];
     }
-    double bef3[3], tot3[3];
-    block_exclusive_scan_n<3>(v3, s_red3, bef3, tot3);
-    const double sumsq = tot3[0], top_s1 = tot3[1], top_c = tot3[2];
+    block_sum_n<3>(v3, s_red3);
+    const double sumsq = v3[0], top_s1 = v3[1], top_c = v3[2];
     if (fl) atomicOr(&s_fl, fl);
     const uint32_t afin = w.meta[0];
     // per-atom sums S0, S1 for atoms 0..afin (atom 0 carries q = 0 for everyone),
@@ -528,12 +597,16 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
         double s0 = 0.0, s1 = 0.0;
         if (at >= 1 && (uint32_t)at < afin) {
             uint64_t c = 0, t = 0;
+#pragma unroll 8
             for (int b = 0; b < nsrc; b++) {
                 c += srcc[(int64_t)b * Aa1 + at];
                 t += srcs[(int64_t)b * Aa1 + at];
             }
+            // mantissa sums: add the implicit bit of a normal binade per element
+            const uint32_t ex = w.ubits[at] >> 23;
+            if (ex) t += c << 23;
             s0 = (double)c;
-            s1 = ldexp((double)t, (int)max(w.ubits[at] >> 23, 1u) - 150);
+            s1 = ldexp((double)t, (int)max(ex, 1u) - 150);
         } else if (afin > 0 && (uint32_t)at == afin) {
             s0 = top_c;
             s1 = top_s1;
