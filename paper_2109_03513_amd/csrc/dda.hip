@@ -247,14 +247,20 @@ __device__ __forceinline__ T block_sum(T v, T* sh) {
 
 // Dynamic LDS of k_dda_hist:
 //   U     u32[Aa + 2]   sorted atom bounds: U[0] = 0, U[1..Ap] boundaries, U[Ap+1] = ~0
-//   binfo u32[nbins]    per bin: first atom (low 16 bits) | boundaries inside (high 16)
+//   binfo u32[nbins]    per bin: first atom (low 16 bits) | boundaries inside (high 16);
+//                       for the pass it becomes u32[2 * nbins]: the pair
+//                       {first atom | bounds inside << 16, the first bound after it}
 //   TH    u32[A]        thresholds, later their atom positions (the cell starts)
-//   KH    u64[Aa + 1]   (value << 32 | id) bucket keys, later the packed histogram
-static int hist_nbins(int A) { return A <= 2048 ? 8192 : 4096; }
+//   KH    u64[Aa + 65]  (value << 32 | id) bucket keys, later the packed histogram;
+//                       the last 64 cells take the zero adds of lanes outside
+//                       [lo, hi), one per lane, so that they never collide
+__host__ __device__ static inline int hist_nbins(int A) {
+    return A <= 2048 ? 8192 : (A <= 4096 ? 4096 : 2048);
+}
 static size_t hist_lds_bytes(int A) {
     const size_t Aa = (size_t)A + kMaxSplits;
-    return align256(sizeof(uint32_t) * (Aa + 2)) + sizeof(uint32_t) * hist_nbins(A) +
-           align256(sizeof(uint32_t) * A) + sizeof(uint64_t) * (Aa + 1);
+    return align256(sizeof(uint32_t) * (Aa + 2)) + sizeof(uint32_t) * 2 * hist_nbins(A) +
+           align256(sizeof(uint32_t) * A) + sizeof(uint64_t) * (Aa + 1 + 64);
 }
 
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restrict__ x, int64_t len,
@@ -262,11 +268,11 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
                                                            DdaArgs a, DdaWs w) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x;
-    const int nbins = A <= 2048 ? 8192 : 4096;
+    const int nbins = hist_nbins(A);
     const size_t Aa = (size_t)A + kMaxSplits;
     uint32_t* U = (uint32_t*)smem;
     uint32_t* binfo = (uint32_t*)(smem + align256(sizeof(uint32_t) * (Aa + 2)));
-    uint32_t* TH = binfo + nbins;
+    uint32_t* TH = binfo + 2 * nbins;
     uint64_t* KH = (uint64_t*)((unsigned char*)TH + align256(sizeof(uint32_t) * A));
     uint64_t* hist = KH;
     __shared__ float s_mids[128];
@@ -414,7 +420,27 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     if (tid == 0) { U[0] = 0u; U[Ap + 1] = 0xffffffffu; }
     const uint32_t afin = Ap;                        // the top atom [hi, inf)
     __syncthreads();   // the keys are dead: KH becomes the histogram
-    for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0;
+    // ---- 5b. bin pairs {first atom | bounds inside << 16, next bound}: with at
+    //          most one bound inside, the atom of a value is first + (v >= next)
+    {
+        constexpr int kPer = 8192 / kHistThreads;
+        uint32_t bv[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; k++) {
+            const uint32_t b = (uint32_t)(tid + k * kHistThreads);
+            bv[k] = b < nb ? binfo[b] : 0u;
+        }
+        for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kPer; k++) {
+            const uint32_t b = (uint32_t)(tid + k * kHistThreads);
+            if (b < nb || (b == 0 && nb == 0)) {
+                binfo[2 * b] = bv[k];
+                binfo[2 * b + 1] = U[(bv[k] & 0xffffu) + 1];
+            }
+        }
+    }
     __syncthreads();
 
     // ---- 6. the pass
@@ -428,20 +454,37 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     // the 23-bit mantissas and the count give the exact sum of |x| over the
     // atom.  |x| >= hi (the top atom) and non-finite x are rare: a branch.
     const uint32_t span = hi - lo;
+    const uint32_t bmax = base + (nb > 0 ? nb - 1u : 0u);
+    const uint2* bins = (const uint2*)binfo;
+    const uint32_t spare = (uint32_t)Aa + 1u + (uint32_t)(tid & 63);
     auto visit = [&](const uint32_t (&xb)[E]) {
-        uint32_t ab[E], at[E];
+        uint32_t ab[E], t[E];
+        uint2 bi[E];
         bool mid[E];
-        bool rare = false;
+        uint32_t mx = 0;
 #pragma unroll
         for (int e = 0; e < E; e++) {
             ab[e] = xb[e] & 0x7fffffffu;
             const double xd = (double)__uint_as_float(ab[e]);
             sumsq = fma(xd, xd, sumsq);
-            rare |= ab[e] >= hi;
-            mid[e] = ab[e] - lo < span;                // atom 0 (q = 0 for all) is skipped
-            at[e] = binfo[mid[e] ? (ab[e] >> shift) - base : 0u];
+            mx = max(mx, ab[e]);
+            mid[e] = ab[e] - lo < span;                // atom 0 (q = 0 for all) adds nothing
+            const uint32_t b = min(max(ab[e] >> shift, base), bmax) - base;
+            bi[e] = bins[b];
         }
-        if (rare) {
+        bool walk = false;
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+            t[e] = (bi[e].x & 0xffffu) + ((ab[e] >= bi[e].y) ? 1u : 0u);
+            walk |= mid[e] && bi[e].x >= 0x20000u;
+        }
+        if (walk) {                                    // a bin with two or more bounds
+#pragma unroll
+            for (int e = 0; e < E; e++)
+                if (mid[e] && bi[e].x >= 0x20000u)
+                    while (U[t[e] + 1] <= ab[e]) t[e]++;
+        }
+        if (mx >= hi) {                                // the top atom, non-finite x
 #pragma unroll
             for (int e = 0; e < E; e++) {
                 if (ab[e] >= hi) {
@@ -455,20 +498,10 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
             }
         }
 #pragma unroll
-        for (int e = 0; e < E; e++) {
-            uint32_t t = at[e] & 0xffffu;
-            t += (ab[e] >= U[t + 1]) ? 1u : 0u;       // at most one bound inside the bin
-            if (mid[e] && at[e] >= 0x20000u) {        // two or more: walk
-                while (U[t + 1] <= ab[e]) t++;
-            }
-            at[e] = t;
-        }
-#pragma unroll
-        for (int e = 0; e < E; e++) {
-            if (mid[e]) {
-                const uint32_t mant = ab[e] & 0x7fffffu;
-                atomicAdd(&hist[at[e]], ((uint64_t)mant << 20) | 1u);
-            }
+        for (int e = 0; e < E; e++) {   // outside [lo, hi): zero into the lane's own spare cell
+            const uint32_t mant = ab[e] & 0x7fffffu;
+            const uint64_t v = mid[e] ? (((uint64_t)mant << 20) | 1u) : 0u;
+            atomicAdd(&hist[mid[e] ? t[e] : spare], v);
         }
     };
     const int64_t cnt_base = (int64_t)blockIdx.x * (int64_t)(Aa + 1);
