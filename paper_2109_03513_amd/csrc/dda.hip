@@ -590,42 +590,35 @@ __global__ __launch_bounds__(256) void k_dda_reduce(DdaArgs a, DdaWs w) {
 // ------------------------------------------------------------------ finalize
 constexpr int kFinThreads = 1024;
 
-__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
-                                                              DdaArgs a, DdaWs w,
-                                                              float* __restrict__ alpha_out,
-                                                              double* __restrict__ D_out) {
-    extern __shared__ __align__(16) unsigned char smem[];
+// The reduction over blocks and the per-candidate objective, for a block of
+// kFinThreads threads.  P0, P1: LDS of (afin + 2) doubles each; Dv: LDS of G
+// doubles.  ubits: the
+// sorted atom bounds; rks: the atom where each cell starts (LDS or global).
+// nsrc rows of per-atom partial sums in srcc / srcs, nblk rows of block scalars.
+__device__ void finalize_core(const float* __restrict__ grid, const DdaArgs& a, const DdaWs& w,
+                              float* __restrict__ alpha_out, double* __restrict__ D_out,
+                              double* P0, double* P1, const uint32_t* ubits, const int32_t* rks,
+                              uint32_t afin, int nsrc, const uint64_t* srcc, const uint64_t* srcs,
+                              int nblk, double* Dv) {
     const int tid = threadIdx.x, G = a.G, M = a.M;
     const int Aa1 = a.Aa + 1;
-    double* P0 = (double*)smem;                  // [Aa+2] prefix sums of counts
-    double* P1 = P0 + (Aa1 + 1);                 // [Aa+2] prefix sums of |x|
-    int32_t* rk = (int32_t*)(P1 + (Aa1 + 1));   // [A] first atom of every cell
     __shared__ double s_red3[3][16];
     __shared__ double sq[128];
-    __shared__ double Dv[kDdaMaxG];
     __shared__ uint32_t s_fl;
     if (tid <= M) sq[tid] = (double)a.q[tid];
     if (tid == 0) s_fl = 0;
-    if (a.rk_lds)
-        for (int i = tid; i < a.A; i += kFinThreads) rk[i] = w.rank[i];
-    const int32_t* rks = a.rk_lds ? rk : w.rank;
     // block scalars
     double v3[3] = {0.0, 0.0, 0.0};
     uint32_t fl = 0;
-    for (int b = tid; b < a.nblk; b += kFinThreads) {
+    for (int b = tid; b < nblk; b += kFinThreads) {
         const double* ps = w.pscal + 4 * b;
         v3[0] += ps[0]; v3[1] += ps[1]; v3[2] += ps[2]; fl |= (uint32_t)ps[3];
     }
     block_sum_n<3>(v3, s_red3);
     const double sumsq = v3[0], top_s1 = v3[1], top_c = v3[2];
     if (fl) atomicOr(&s_fl, fl);
-    const uint32_t afin = w.meta[0];
     // per-atom sums S0, S1 for atoms 0..afin (atom 0 carries q = 0 for everyone),
     // loaded coalesced into LDS, then an in-place exclusive prefix scan over atoms
-    const bool sliced = a.nslice > 0;
-    const int nsrc = sliced ? a.nslice : a.nblk;
-    const uint64_t* srcc = sliced ? w.rcnt : w.pcnt;
-    const uint64_t* srcs = sliced ? w.rsum : w.psum;
     for (int at = tid; at <= (int)afin + 1; at += kFinThreads) {
         double s0 = 0.0, s1 = 0.0;
         if (at >= 1 && (uint32_t)at < afin) {
@@ -636,7 +629,7 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
                 t += srcs[(int64_t)b * Aa1 + at];
             }
             // mantissa sums: add the implicit bit of a normal binade per element
-            const uint32_t ex = w.ubits[at] >> 23;
+            const uint32_t ex = ubits[at] >> 23;
             if (ex) t += c << 23;
             s0 = (double)c;
             s1 = ldexp((double)t, (int)max(ex, 1u) - 150);
@@ -716,6 +709,25 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
         for (int jj = tid; jj < G; jj += kFinThreads) D_out[jj] = Dv[jj];
 }
 
+__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
+                                                              DdaArgs a, DdaWs w,
+                                                              float* __restrict__ alpha_out,
+                                                              double* __restrict__ D_out) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x;
+    const int Aa1 = a.Aa + 1;
+    double* P0 = (double*)smem;                  // [Aa+2] prefix sums of counts
+    double* P1 = P0 + (Aa1 + 1);                 // [Aa+2] prefix sums of |x|
+    double* Dv = P1 + (Aa1 + 1);                 // [G] objective per candidate
+    int32_t* rk = (int32_t*)(Dv + a.G);         // [A] first atom of every cell
+    if (a.rk_lds)
+        for (int i = tid; i < a.A; i += kFinThreads) rk[i] = w.rank[i];
+    const bool sliced = a.nslice > 0;
+    finalize_core(grid, a, w, alpha_out, D_out, P0, P1, w.ubits, a.rk_lds ? rk : w.rank, w.meta[0],
+                  sliced ? a.nslice : a.nblk, sliced ? w.rcnt : w.pcnt, sliced ? w.rsum : w.psum,
+                  a.nblk, Dv);
+}
+
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
                       float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
                       hipStream_t s) {
@@ -753,7 +765,7 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
         dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
         k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
     }
-    size_t fin_lds = sizeof(double) * 2 * (size_t)(a.Aa + 2);
+    size_t fin_lds = sizeof(double) * (2 * (size_t)(a.Aa + 2) + (size_t)G);
     a.rk_lds = fin_lds + sizeof(int32_t) * (size_t)a.A <= 140 * 1024;
     if (a.rk_lds) fin_lds += sizeof(int32_t) * (size_t)a.A;
     k_dda_finalize<<<1, kFinThreads, fin_lds, s>>>(grid, a, w, alpha_out, D_out);

@@ -133,3 +133,21 @@ def test_dda_then_project_on_device(esb):
     codes = host(esb.esb_project(xd, alpha, 4, 2))
     j, _ = oracle.dda(c["w"], 4, 2, c["gridW"])
     np.testing.assert_array_equal(codes, oracle.project(c["w"], c["gridW"][j], 4, 2))
+
+
+def test_dda_reused_workspace(esb):
+    """One caller-owned workspace, reused across calls whose block counts differ (with and
+    without the sliced reduction kernel): nothing of a previous call may leak into the next."""
+    torch = pytest.importorskip("torch")
+    lengths = [200704, 36864, 1 << 20, 4096, 0, 200704]
+    need = max(esb.esb_dda_workspace_size(n, 4, 2, 64) for n in lengths)
+    ws = torch.full((need,), 0xA5, dtype=torch.uint8, device="cuda")   # not zeroed
+    grid = wl.scale_grid(1.0)
+    for i, n in enumerate(lengths):
+        x = np.random.default_rng([77, i]).standard_normal(n).astype(np.float32)
+        log("dda reused workspace call %d len=%d" % (i, n))
+        a, D = esb.esb_dda_align(dev(x), 4, 2, dev(grid), workspace=ws)
+        j, Do = oracle.dda(x, 4, 2, grid)
+        assert_rel(host(D), Do, REL, "reuse %d" % i)
+        if n > 0:
+            assert host(a)[0] == grid[j]
