@@ -21,12 +21,12 @@
 //    entries), then v_mfma_i32_32x32x32_i8 with int32 accumulation.
 //
 // Tiles: BM x BN per workgroup, WGM x WGN waves of (BM/WGM) x (BN/WGN), BK =
-// 64 reduction bytes per stage.  Codes travel HBM -> LDS by DMA two stages
-// ahead ("raw" buffers, no registers held); while the MFMAs of stage t run,
-// each thread decodes the raw chunks of stage t+1 it fetched itself into the
-// other half of a double-buffered, XOR-swizzled decoded tile.  One LDS
-// barrier per stage.  Workgroups are numbered so that each XCD (every eighth
-// workgroup id) gets a contiguous run of tiles.
+// 64 reduction bytes per stage.  Codes travel HBM -> LDS by DMA into a ring of
+// R "raw" buffers, R - 1 stages ahead (no registers held); while the MFMAs of
+// stage t run, each thread decodes the raw chunks of stage t+1 it fetched
+// itself into the other half of a double-buffered, XOR-swizzled decoded tile.
+// One LDS barrier per stage.  Workgroups are numbered so that each XCD (every
+// eighth workgroup id) gets a contiguous run of tiles.
 #include <type_traits>
 
 #include "esb_internal.h"
