@@ -162,11 +162,16 @@ __device__ __forceinline__ uint4 a_load16(const ASlot& sl, const GemmParams& g, 
     return v;
 }
 
-// Byte path for any geometry.
+// Byte path for any geometry.  With a table (kt != nullptr) the reduction index
+// kk maps to {address offset from the pixel at (ih0, iw0), r << 16 | s}, built
+// once per workgroup; without it (long reductions) the division chain is used.
+constexpr int kKtabMax = 2048;
+
 __device__ __forceinline__ uint4 a_load1(const ASlot& sl, const GemmParams& g, int k_start,
-                                         int goff) {
+                                         int goff, const int2* kt) {
     const ConvGeom& c = g.ga;
     uint32_t w[4];
+    const int64_t pix = (((int64_t)sl.nimg * c.H + sl.ih0) * c.W + sl.iw0) * c.pitch + goff;
 #pragma unroll
     for (int q4 = 0; q4 < 4; q4++) {
         uint32_t acc = 0;
@@ -175,12 +180,22 @@ __device__ __forceinline__ uint4 a_load1(const ASlot& sl, const GemmParams& g, i
             const int kk = k_start + 4 * q4 + b;
             uint32_t code = g.zeroA;
             if (sl.valid && kk < g.K) {
-                const int rs = kk / c.Cg;
-                const int ch = kk - rs * c.Cg;
-                const int r = rs / c.S, s = rs - (rs / c.S) * c.S;
+                int r, s;
+                int64_t off;
+                if (kt) {
+                    const int2 e = kt[kk];
+                    off = e.x;
+                    r = e.y >> 16;
+                    s = e.y & 0xffff;
+                } else {
+                    const int rs = kk / c.Cg;
+                    const int ch = kk - rs * c.Cg;
+                    r = rs / c.S;
+                    s = rs - r * c.S;
+                    off = ((int64_t)r * c.W + s) * c.pitch + ch;
+                }
                 const int ih = sl.ih0 + r, iw = sl.iw0 + s;
-                if (ih >= 0 && ih < c.H && iw >= 0 && iw < c.W)
-                    code = g.A[(((int64_t)sl.nimg * c.H + ih) * c.W + iw) * c.pitch + goff + ch];
+                if ((unsigned)ih < (unsigned)c.H && (unsigned)iw < (unsigned)c.W) code = g.A[pix + off];
             }
             acc |= code << (8 * b);
         }
@@ -233,6 +248,21 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
     const int goffA = grp * g.ga.Cg;
     const int64_t brow0 = (int64_t)grp * g.N;
 
+    // byte path: the reduction-index table (short reductions)
+    __shared__ int2 s_ktab[AV == 1 ? kKtabMax : 1];
+    const int2* ktab = nullptr;
+    if (AV == 1 && g.K <= kKtabMax &&
+        (int64_t)g.ga.R * g.ga.W * g.ga.pitch + g.ga.pitch < 0x7fffffff) {
+        for (int kk = threadIdx.x; kk < g.K; kk += NT) {
+            const int cg = max(g.ga.Cg, 1);
+            const int rs = kk / cg;
+            const int ch = kk - rs * cg;
+            const int r = rs / g.ga.S, s = rs - r * g.ga.S;
+            s_ktab[kk] = make_int2((r * g.ga.W + s) * g.ga.pitch + ch, (r << 16) | s);
+        }
+        __syncthreads();
+        ktab = s_ktab;
+    }
     ASlot as[CA];
 #pragma unroll
     for (int i = 0; i < CA; i++) {
@@ -255,7 +285,7 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
         for (int i = 0; i < CA; i++) {
             const int c = tid + i * NT;
             const int kst = k0 + 16 * (c % 4);
-            ra[i] = (AV == 16) ? a_load16(as[i], g, kst, goffA) : a_load1(as[i], g, kst, goffA);
+            ra[i] = (AV == 16) ? a_load16(as[i], g, kst, goffA) : a_load1(as[i], g, kst, goffA, ktab);
         }
 #pragma unroll
         for (int i = 0; i < CB; i++) {
@@ -413,7 +443,7 @@ hipError_t launch_contraction(int M, int N, int K, int groups, const ConvGeom& g
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn) * groups;
     };
-    if (tiles(128, 128) >= cus) launch_fast<128, 128, 64, 64>(g, groups, av, bv, s);
+    if (N > 64 && tiles(128, 128) >= cus) launch_fast<128, 128, 64, 64>(g, groups, av, bv, s);
     else if (tiles(64, 64) >= cus) launch_fast<64, 64, 32, 32>(g, groups, av, bv, s);
     else launch_fast<64, 32, 32, 16>(g, groups, av, bv, s);
     return hipGetLastError();
