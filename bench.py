@@ -37,6 +37,10 @@ def parse():
     p.add_argument("--sweep", action="store_true",
                    help="time every kernel at the large layer shapes (one JSON line per case)")
     p.add_argument("--only", default="", help="with --sweep: comma-separated case names")
+    p.add_argument("--resnet18", action="store_true",
+                   help="ResNet18 forward at batch 64 (ESB(5,2) everywhere): images/s and per-layer "
+                        "times (one JSON line per layer, then a summary line)")
+    p.add_argument("--batch", type=int, default=64)
     p.add_argument("--reps", type=int, default=20)
     return p.parse_args()
 
@@ -66,6 +70,9 @@ def main():
         return
     if args.sweep:
         sweep(args)
+        return
+    if args.resnet18:
+        resnet18_bench(args)
         return
 
     from paper_2109_03513_amd import esb, workloads
@@ -336,6 +343,105 @@ def sweep(args):
             ops = 2.0 * Nb * P * Q * K * R * R * (C // groups)
             nbytes = float(xc.numel() + wc.numel() + 4 * y.numel())
             emit("conv_" + name, ms, nbytes=nbytes, ops=ops)
+
+
+def resnet18_bench(args):
+    """ResNet18 stack, every layer quantized to ESB(5,2) with its DDA on the device."""
+    import numpy as np
+    import torch
+    from paper_2109_03513_amd import esb, resnet18, workloads
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()      # default priority
+    B = args.batch
+    weights = workloads.resnet18_weights(0)
+    x = torch.from_numpy(workloads.resnet18_input(0, B)).cuda()
+    with torch.cuda.stream(stream):
+        model = resnet18.ResNet18ESB(weights, B, stream=stream)
+        for _ in range(2):
+            ref = model.forward(x)
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        steps = max(args.steps // 10, 3)
+        e0.record(stream)
+        for _ in range(steps):
+            model.forward(x)
+        e1.record(stream)
+        e1.synchronize()
+        eager_ms = e0.elapsed_time(e1) / steps
+        # the whole forward as one HIP graph; used only if every replay equals the eager logits
+        graph_ms, graph_ok = None, False
+        try:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                out = model.forward(x)
+            graph_ok = True
+            for _ in range(3):
+                g.replay()
+                stream.synchronize()
+                graph_ok = graph_ok and torch.equal(out, ref)
+            if graph_ok:
+                e0.record(stream)
+                for _ in range(steps):
+                    g.replay()
+                e1.record(stream)
+                e1.synchronize()
+                graph_ms = e0.elapsed_time(e1) / steps
+            del g
+        except RuntimeError:
+            graph_ok = False
+        # per layer: inputs recorded by one forward, then each stage timed alone
+        rec = resnet18.ResNet18ESB(weights, B, stream=stream, record=True)
+        rec.forward(x)
+        stream.synchronize()
+        total_ops = 0.0
+        layer_rows = []
+        for t in rec.trace:
+            name = t["name"]
+            xin = t["x"]
+            ws = rec.ws[name]
+            q_ms = time_launches(lambda: rec._quantize(xin, ws), args.reps, stream)
+            if name == "fc":
+                M, K = t["codes"].shape
+                Nn = rec.fc_codes.shape[0]
+                yb = torch.empty((M, Nn), dtype=torch.float32, device="cuda")
+                c_ms = time_launches(lambda: esb.esb_gemm(t["codes"], 5, 3, t["alpha"], rec.fc_codes, 5, 3,
+                                                          rec.fc_alpha, y=yb, want_acc=False,
+                                                          stream=stream), args.reps, stream)
+                ops = 2.0 * M * Nn * K
+                nbytes = float(M * K + Nn * K + 4 * M * Nn)
+            else:
+                L = rec.layers[name]
+                Nb, H, W, C = t["codes"].shape
+                P, Q = esb.conv_out_hw(H, W, L["k"], L["k"], (L["stride"],) * 2, (L["pad"],) * 2)
+                yb = torch.empty((Nb, P, Q, L["cout"]), dtype=torch.float32, device="cuda")
+                c_ms = time_launches(lambda: esb.esb_conv2d(t["codes"], 5, 3, t["alpha"], L["codes"], 5, 3,
+                                                            L["alpha"], stride=(L["stride"],) * 2,
+                                                            pad=(L["pad"],) * 2, y=yb, want_acc=False,
+                                                            stream=stream), args.reps, stream)
+                ops = 2.0 * Nb * P * Q * L["cout"] * L["k"] * L["k"] * C
+                nbytes = float(t["codes"].numel() + L["codes"].numel() + 4 * yb.numel())
+            total_ops += ops
+            tops = ops / (c_ms * 1e-3) / 1e12
+            attain = min(1.0, (ops / nbytes) / (INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9)))
+            row = {"layer": name, "contraction_ms": round(c_ms, 5), "tops": round(tops, 2),
+                   "frac_int8": round(tops / INT8_PEAK_TOPS, 4), "ai_ops_per_byte": round(ops / nbytes, 1),
+                   "attainable_frac": round(attain, 4),
+                   "frac_of_attainable": round(tops / INT8_PEAK_TOPS / attain, 4),
+                   "quantize_ms": round(q_ms, 5), "input_elems": int(xin.numel()),
+                   "quantize_gbps": round(9.0 * xin.numel() / (q_ms * 1e-3) / 1e9, 1)}
+            layer_rows.append(row)
+            print(json.dumps(row), flush=True)
+    fwd_ms = graph_ms if graph_ok and graph_ms is not None else eager_ms
+    print(json.dumps({"metric": "ResNet18 forward, every layer ESB(5,2) with on-device DDA",
+                      "batch": B, "images_per_s": round(B / (fwd_ms * 1e-3), 1),
+                      "ms_per_forward": round(fwd_ms, 4), "eager_ms": round(eager_ms, 4),
+                      "graph_ms": None if graph_ms is None else round(graph_ms, 4),
+                      "graph_replays_match_eager": graph_ok,
+                      "contraction_ms_sum": round(sum(r["contraction_ms"] for r in layer_rows), 4),
+                      "quantize_ms_sum": round(sum(r["quantize_ms"] for r in layer_rows), 4),
+                      "gop_per_forward": round(total_ops / 1e9, 2), "data": "synthetic"}), flush=True)
 
 
 def cpu_baseline(c, ops, budget_s):

@@ -1,0 +1,118 @@
+"""ResNet18 (BasicBlock) forward pass over ESB codes on one GPU.
+
+Every convolution and the classifier are quantized layers of Sec. 5 (the paper
+quantizes all layers of ResNet18, including the first and the last): the
+layer input is scaled by DDA (eq. (13)) over the candidate grid
+alpha_j = fl32(max|x| * c_j), c_j = fl32((j+1) / (64 C)), j = 0..63 (C the
+largest set value, so the grid spans (0, max|x| / C]), projected to ESB codes
+(eq. (8)) and contracted with the pre-quantized weights (eq. (15)) into fp32
+outputs.  Weights are quantized once, the same way, when the model is built.
+
+Only the library's calls touch the ESB arithmetic.  The glue between layers
+(ReLU, the 3x3 / stride-2 max pool after conv1, residual additions, the global
+average pool) is plain tensor work done with torch on the same stream: the
+average is a float64 sum of the 7x7 window divided by 49 and rounded to fp32
+once.  No batch normalization (the weights are He-initialized).
+
+Activations are NHWC fp32; codes NHWC uint8; weights KRSC.
+"""
+import numpy as np
+
+from . import esb, workloads
+
+N_BITS, K_SIG = 5, 3      # ESB(5, 2) for every layer
+GRID_POINTS = 64
+
+
+def value_max(n, k_sig):
+    return float(np.max(esb.esb_valueset(n, k_sig)))
+
+
+def input_side(name):
+    """Height (= width) of a layer's input for 224 x 224 images."""
+    if name == "conv1":
+        return 224
+    stage, blk, conv = name.split(".")
+    first = {"l1": 56, "l2": 56, "l3": 28, "l4": 14}[stage]   # the stage's input
+    inner = {"l1": 56, "l2": 28, "l3": 14, "l4": 7}[stage]    # after its first conv
+    return first if (blk == "0" and conv in ("c1", "ds")) else inner
+
+
+class ResNet18ESB:
+    """Pre-quantized ResNet18; forward(x) returns the fp32 logits [batch, 1000]."""
+
+    def __init__(self, weights, batch, n=N_BITS, k_sig=K_SIG, stream=None, record=False):
+        import torch
+        self.torch = torch
+        self.n, self.ks = n, k_sig
+        self.batch = batch
+        self.stream = stream
+        self.sh = stream.cuda_stream if stream is not None else None
+        self.record = record
+        self.trace = []
+        dev = "cuda"
+        self.cmax = value_max(n, k_sig)
+        self.cgrid = torch.from_numpy(workloads.maxabs_grid_factors(self.cmax, GRID_POINTS)).to(dev)
+        self.layers = {}
+        sizes = {}
+        for name, cin, cout, k, st, pd in workloads.RESNET18_CONVS:
+            self.layers[name] = dict(cin=cin, cout=cout, k=k, stride=st, pad=pd)
+            sizes[name] = batch * input_side(name) ** 2 * cin
+        sizes["fc"] = batch * 512
+        self.ws = {k: torch.empty(max(esb.esb_dda_workspace_size(v, n, k_sig, GRID_POINTS), 1),
+                                  dtype=torch.uint8, device=dev) for k, v in sizes.items()}
+        # weights, quantized once
+        for name, L in self.layers.items():
+            w = torch.from_numpy(np.ascontiguousarray(weights[name])).to(dev)
+            L["alpha"], L["codes"] = self._quantize(w, self._ws_for(w))
+        wfc = torch.from_numpy(np.ascontiguousarray(weights["fc"])).to(dev)
+        self.fc_alpha, self.fc_codes = self._quantize(wfc, self._ws_for(wfc))
+        torch.cuda.synchronize()
+
+    def _ws_for(self, t):
+        need = esb.esb_dda_workspace_size(t.numel(), self.n, self.ks, GRID_POINTS)
+        return self.torch.empty(max(need, 1), dtype=self.torch.uint8, device=t.device)
+
+    def grid(self, x):
+        """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product)."""
+        return x.abs().amax().reshape(1) * self.cgrid
+
+    def _quantize(self, x, ws):
+        torch = self.torch
+        g = self.grid(x)
+        alpha = torch.empty(1, dtype=torch.float32, device=x.device)
+        esb.esb_dda_align(x, self.n, self.ks, g, alpha_out=alpha, D_out=None, workspace=ws,
+                          stream=self.sh, want_D=False)
+        codes = esb.esb_project(x, alpha, self.n, self.ks, stream=self.sh)
+        return alpha, codes
+
+    def conv(self, name, x):
+        L = self.layers[name]
+        ax, cx = self._quantize(x, self.ws[name])
+        acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"],
+                                stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
+                                want_acc=self.record, stream=self.sh)
+        if self.record:
+            self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
+        return y
+
+    def forward(self, x):
+        torch = self.torch
+        F = torch.nn.functional
+        a = torch.relu(self.conv("conv1", x))
+        # 3x3 max pool, stride 2, pad 1 (padding never wins: -inf)
+        a = F.max_pool2d(a.permute(0, 3, 1, 2), 3, 2, 1).permute(0, 2, 3, 1).contiguous()
+        for stage in (1, 2, 3, 4):
+            for blk in (0, 1):
+                p = "l%d.%d." % (stage, blk)
+                out = torch.relu(self.conv(p + "c1", a))
+                out = self.conv(p + "c2", out)
+                sc = self.conv(p + "ds", a) if (p + "ds") in self.layers else a
+                a = torch.relu(out + sc)
+        feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
+        af, cf = self._quantize(feat, self.ws["fc"])
+        acc, logits = esb.esb_gemm(cf, self.n, self.ks, af, self.fc_codes, self.n, self.ks,
+                                   self.fc_alpha, want_acc=self.record, stream=self.sh)
+        if self.record:
+            self.trace.append(dict(name="fc", x=feat, alpha=af, codes=cf, acc=acc, y=logits))
+        return logits

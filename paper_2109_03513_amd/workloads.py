@@ -47,6 +47,15 @@ def scale_grid(s, points=GRID_POINTS):
     return (np.float64(s) * (3.0 * j / points)).astype(np.float32)
 
 
+def maxabs_grid_factors(cmax, points=GRID_POINTS):
+    """Factors c_j = fl32((j+1) / (points * cmax)), j = 0..points-1, for the data-driven grid
+    alpha_j = fl32(max|x| * c_j) of the ResNet18 stack (cmax: the largest set value, so the
+    grid spans (0, max|x| / cmax]).  One fp32 product per candidate: it is computed the same
+    way on any device."""
+    j = np.arange(1, points + 1, dtype=np.float64)
+    return (j / (points * float(cmax))).astype(np.float32)
+
+
 def tiny_gemm(seed=0):
     """64x576 weights N(0, 0.05) times 576x64 activations ReLU(N(0,1)); ESB n=4, k_sig=2."""
     r = rng(0, seed)

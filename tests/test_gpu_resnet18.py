@@ -1,0 +1,97 @@
+"""The ResNet18 stack (every convolution and the classifier quantized to ESB(5,2),
+per-layer DDA on the device) against the same stack computed by the oracle from
+the same input images.
+
+The oracle quantizes every weight tensor and every layer input itself (DDA over
+the grid fl32(max|x| * c_j), projection) and runs the direct
+convolutions; the glue between layers (ReLU, max pool, residual sums, the
+float64 average pool) is written again here in NumPy.  Each layer must agree
+exactly: the chosen alpha, every code, every int32 accumulator; the fp32
+outputs are fl32(s * fl32(acc)) on both sides.  Because each layer's output is
+bit-identical, the two stacks stay in lockstep to the logits."""
+import numpy as np
+import pytest
+
+import oracle
+from gpuutil import assert_rel, host, log
+from paper_2109_03513_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+N, KS = 5, 3
+
+
+def grid_np(x, cmax):
+    return (np.float32(np.max(np.abs(x))) * wl.maxabs_grid_factors(cmax)).astype(np.float32)
+
+
+def quantize_np(x, cmax):
+    g = grid_np(x, cmax)
+    j, _ = oracle.dda(x, N, KS, g)
+    return g[j], oracle.project(x, g[j], N, KS)
+
+
+def maxpool_np(a):   # 3x3, stride 2, pad 1, NHWC
+    B, H, W, C = a.shape
+    P = (H + 2 - 3) // 2 + 1
+    pad = np.full((B, H + 2, W + 2, C), -np.inf, dtype=np.float32)
+    pad[:, 1:-1, 1:-1, :] = a
+    out = np.full((B, P, P, C), -np.inf, dtype=np.float32)
+    for r in range(3):
+        for s in range(3):
+            out = np.maximum(out, pad[:, r:r + 2 * P:2, s:s + 2 * P:2, :])
+    return out
+
+
+@pytest.mark.parametrize("batch", [2])
+def test_resnet18_stack_matches_oracle(batch):
+    import torch
+    from paper_2109_03513_amd import resnet18
+    weights = wl.resnet18_weights(0)
+    x = wl.resnet18_input(0, batch)
+    log("resnet18 stack batch=%d: GPU forward" % batch)
+    model = resnet18.ResNet18ESB(weights, batch, record=True)
+    logits = host(model.forward(torch.from_numpy(x).cuda()))
+    cmax = resnet18.value_max(N, KS)
+    gpu = {t["name"]: t for t in model.trace}
+
+    def layer(name, a, w, stride, pad, wq):
+        log("  oracle layer %s input %s" % (name, a.shape))
+        alpha, codes = quantize_np(a, cmax)
+        t = gpu[name]
+        assert host(t["alpha"])[0] == alpha, name
+        np.testing.assert_array_equal(host(t["codes"]), codes, err_msg=name)
+        if name == "fc":
+            st, acc, y = oracle.gemm(codes, wq[1], N, KS, alpha, N, KS, wq[0])
+        else:
+            st, acc, y = oracle.conv2d(codes, wq[1], N, KS, alpha, N, KS, wq[0],
+                                       stride=(stride, stride), pad=(pad, pad))
+        assert st == 0
+        np.testing.assert_array_equal(host(t["acc"]), acc, err_msg=name)
+        assert_rel(host(t["y"]), y, 1e-6, name)
+        return y
+
+    wq = {}
+    for name, cin, cout, k, st, pd in wl.RESNET18_CONVS:
+        wq[name] = quantize_np(weights[name], cmax)
+        L = model.layers[name]
+        assert host(L["alpha"])[0] == wq[name][0], name
+        np.testing.assert_array_equal(host(L["codes"]), wq[name][1], err_msg=name)
+    wq["fc"] = quantize_np(weights["fc"], cmax)
+    geo = {name: (st, pd) for name, _, _, _, st, pd in wl.RESNET18_CONVS}
+
+    def conv(name, a):
+        return layer(name, a, None, geo[name][0], geo[name][1], wq[name])
+
+    a = np.maximum(conv("conv1", x), 0.0).astype(np.float32)
+    a = maxpool_np(a)
+    for stage in (1, 2, 3, 4):
+        for blk in (0, 1):
+            p = "l%d.%d." % (stage, blk)
+            out = np.maximum(conv(p + "c1", a), 0.0).astype(np.float32)
+            out = conv(p + "c2", out)
+            sc = conv(p + "ds", a) if (p + "ds") in geo else a
+            a = np.maximum(out + sc, 0.0).astype(np.float32)
+    feat = (a.astype(np.float64).sum(axis=(1, 2)) / float(a.shape[1] * a.shape[2])).astype(np.float32)
+    y = layer("fc", feat, None, 1, 0, wq["fc"])
+    assert_rel(logits, y, 1e-6, "logits")
+    assert np.all(np.isfinite(logits))
