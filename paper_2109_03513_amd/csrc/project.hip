@@ -102,6 +102,12 @@ __device__ __forceinline__ uint32_t code4(const f32x4 v, float alpha, float r, b
            (esb_code(v.z, alpha, p) << 16) | (esb_code(v.w, alpha, p) << 24);
 }
 
+// One contiguous tile of kTile4 = 4 x 256 float4 (16 KB in, 4 KB out) per
+// workgroup, the four loads of a thread in flight together.  Measured on MI355X
+// with the same access pattern and trivial arithmetic: contiguous tiles stream
+// at ~6.1 TB/s where a grid-stride loop stays at ~5.1.
+constexpr int kTile4 = 4 * 256;
+
 __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x4, int64_t n4,
                                                      const float* __restrict__ alpha_p,
                                                      ProjParams p, uint32_t* __restrict__ out4) {
@@ -110,21 +116,21 @@ __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x
     const bool fast = fast_scale(alpha);
     const float r = 1.0f / alpha;
     const uint32_t z4 = p.zero_code * 0x01010101u;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (!ok) {
-        for (; i < n4; i += stride) out4[i] = z4;
-        return;
-    }
-    for (; i + 3 * stride < n4; i += 4 * stride) {
+    const int64_t i0 = (int64_t)blockIdx.x * kTile4 + threadIdx.x;
+    if (i0 + 3 * 256 < n4) {
         f32x4 v[4];
 #pragma unroll
-        for (int u = 0; u < 4; u++) v[u] = __builtin_nontemporal_load(&x4[i + u * stride]);
+        for (int u = 0; u < 4; u++) v[u] = __builtin_nontemporal_load(&x4[i0 + u * 256]);
 #pragma unroll
         for (int u = 0; u < 4; u++)
-            __builtin_nontemporal_store(code4(v[u], alpha, r, fast, p), &out4[i + u * stride]);
+            __builtin_nontemporal_store(ok ? code4(v[u], alpha, r, fast, p) : z4, &out4[i0 + u * 256]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int64_t i = i0 + u * 256;
+            if (i < n4) out4[i] = ok ? code4(x4[i], alpha, r, fast, p) : z4;
+        }
     }
-    for (; i < n4; i += stride) out4[i] = code4(x4[i], alpha, r, fast, p);
 }
 
 // Scalar path: unaligned pointers and the tail of the vector path.
@@ -153,8 +159,10 @@ hipError_t launch_project(const float* x, int64_t len, const float* alpha, const
     int64_t head = 0;
     if (aligned && len >= 4) {
         const int64_t n4 = len / 4;
-        k_project_vec<<<grid_for(n4, 256), 256, 0, s>>>((const f32x4*)x, n4, alpha, p,
-                                                        (uint32_t*)codes);
+        const int64_t tiles = (n4 + kTile4 - 1) / kTile4;
+        if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+        k_project_vec<<<(unsigned)tiles, 256, 0, s>>>((const f32x4*)x, n4, alpha, p,
+                                                      (uint32_t*)codes);
         head = n4 * 4;
     }
     if (head < len)

@@ -75,7 +75,8 @@ class ResNet18ESB:
 
     def grid(self, x):
         """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product)."""
-        return x.abs().amax().reshape(1) * self.cgrid
+        m = self.torch.linalg.vector_norm(x, float("inf"))   # max |x|, one reduction
+        return m.reshape(1) * self.cgrid
 
     def _quantize(self, x, ws):
         torch = self.torch
