@@ -8,75 +8,98 @@
 // midpoint between set values c-1 and c (ties go up, as in the projection).
 // All G*M thresholds, sorted and further split at every power of two, cut
 // [0, inf) into "atoms": every candidate's cell is a union of consecutive atoms
-// and every bounded atom lies inside one binade.  One pass over x suffices:
+// and every bounded atom lies inside one binade.  One pass over x suffices.
 //
-// k_dda_hist (<= 256 blocks of 1024 threads), per block:
-//   set-up in LDS: thresholds by a local search around fl32(alpha mu); their
-//   ranks in the sorted order from branch-free binary searches in the other
-//   candidates' (already ascending) lists; power-of-two split points; a bin
-//   table over the threshold bit range whose entries name the atom directly
-//   unless a boundary falls inside the bin;
-//   pass: per element its atom, and one LDS atomic adding (significand << 20) + 1
-//   to a packed 64-bit (sum, count) cell; x^2 in fp64; the unbounded top atom in
-//   fp64.  Every 2^19 elements the packed cells are flushed to per-block totals.
-// k_dda_reduce (only for many blocks): sums the per-block totals in slices.
+// k_dda_hist (blocks of 1024 threads, each over at most 2^19 elements):
+//   set-up in LDS: thresholds by a local search around fl32(alpha mu); bucket
+//   placement by bin of the bit pattern (counts, scan, scatter, order inside a
+//   bucket by counting), which gives the sorted bounds and each cell's first
+//   atom; then a table of 16-byte bin entries {first atom | flags, the next
+//   three bounds}, so that the atom of a value is first + (number of those
+//   three bounds <= value) unless a bin holds four or more (a flagged walk).
+//   The pass: per element one entry read and one LDS atomic adding
+//   {significand, 1} to a packed 64-bit (count << 44 | sum) cell; x^2 in fp64.
+//   Values below the smallest threshold fall in atom 0, where q = 0 for every
+//   candidate: they add nothing (ReLU zeros never touch one LDS address).
+//   Values at or above the largest threshold (the unbounded top atom) and
+//   non-finite values land in the flagged last bin and are summed in fp64.
+//   At the end the block writes its packed cells as one row.
+// k_dda_reduce (only for many blocks): sums the rows in slices.
 // k_dda_finalize (1 block): per-atom sums, prefix sums over atoms, then per
 //   candidate A_j = sum_c Q_c (P1[end_c] - P1[start_c]), B_j likewise with P0 and
 //   Q_c^2, D_j = S2 + a (a B_j - 2 A_j); argmin with ties to the lowest index.
 // Integer sums are exact; fp64 sums run in a fixed order: the result is
-// deterministic.
-#include <type_traits>
-
+// deterministic.  Wave-level scans and reductions use DPP lane moves.
 #include "esb_internal.h"
 
 namespace esb {
 
 constexpr int kHistThreads = 1024;
-constexpr int kMaxSplits = 256;          // power-of-two split points (at most 254)
-constexpr int kChunk4 = 4096;            // float4 per chunk: 16384 elements
-constexpr int kFlushChunks = 32;         // 2^19 elements between flushes
+constexpr int kFinThreads = 1024;
+constexpr int kMaxSplits = 256;            // powers of two between thresholds (at most 254)
+constexpr int kRowElems = 4 * kHistThreads; // one float4 per thread
+constexpr int kMaxRowsPerBlock = 128;      // 2^19 elements: a packed cell cannot overflow
+constexpr int kPackedMaxBlocks = 32;       // above: k_dda_reduce sums the rows in slices
 constexpr int kReduceSlices = 16;
+constexpr uint32_t kFlagWalk = 1u << 31;   // bin holds four or more bounds
+constexpr uint32_t kFlagTop = 1u << 30;    // last bin: values >= the largest threshold
+constexpr uint32_t kAtomMask = (1u << 29) - 1u;
+constexpr uint64_t kSumMask = (1ull << 44) - 1ull;
 
 struct DdaArgs {
-    float mids[128];   // mu_c, c = 1..M (index c-1)
-    float q[128];      // Q_c, c = 0..M (unscaled values, ascending)
-    int G, M, A, Aa, nblk, nslice;
-    int rk_lds;        // the finalize keeps the cell starts in LDS (when they fit)
+    int G, M, A, Aa;        // candidates, midpoints, thresholds G*M, A + kMaxSplits
+    int n, k;               // format (k fraction bits)
+    int lbins;              // log2 of the bin count of the pass
+    int nblk, rows_pb;      // blocks of k_dda_hist, rows of kRowElems per block
+    int nslice;             // slices of k_dda_reduce (0: the finalize reads the packed rows)
+    int rk_lds;             // the finalize keeps the cell starts in LDS
 };
 
 struct DdaWs {   // pointers into the caller's workspace
-    uint32_t* ubits;   // [Aa+2]: augmented sorted bounds of the atoms
+    uint32_t* ubits;   // [Aa+4]: sorted atom bounds U[0] = 0, U[1..Ap], then ~0
     int32_t* rank;     // [A]: atom where cell c of candidate j starts (j*M + c-1)
-    uint32_t* meta;    // afin (top atom), Aprime (number of bounds)
-    uint64_t* pcnt;    // [nblk][Aa+1] per-block element counts
-    uint64_t* psum;    // [nblk][Aa+1] per-block significand sums
+    uint32_t* meta;    // afin = Ap (the top atom), Ap (number of bounds)
+    uint64_t* rows;    // [nblk][Aa+1] per block: count << 44 | significand sum
     double* pscal;     // [nblk][4]: sum x^2, top-atom sum |x|, top count, flags
     uint64_t* rcnt;    // [nslice][Aa+1] sliced sums (k_dda_reduce)
     uint64_t* rsum;    // [nslice][Aa+1]
 };
 
 __host__ __device__ static inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+__host__ __device__ static inline size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
 
-static int dda_nblk(int64_t len) {
-    const int64_t chunks = (len + 4 * kChunk4 - 1) / (4 * kChunk4);
-    return (int)(chunks < 1 ? 1 : (chunks > kDdaMaxBlocks ? kDdaMaxBlocks : chunks));
+// Block geometry: rows of 4096 elements; two rows per block for small inputs
+// (short passes on many CUs), at most 128 per block.
+static void dda_blocks(int64_t len, int* nblk, int* rows_pb) {
+    const int64_t rows = (len + kRowElems - 1) / kRowElems;
+    int64_t rpb = 2;
+    if (rows > 2 * 256) {
+        rpb = (rows + 255) / 256;
+        rpb = (rpb + 1) & ~(int64_t)1;
+        if (rpb > kMaxRowsPerBlock) rpb = kMaxRowsPerBlock;
+    }
+    int64_t nb = (rows + rpb - 1) / rpb;
+    *nblk = (int)(nb < 1 ? 1 : nb);
+    *rows_pb = (int)rpb;
 }
 
 bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L) {
     const int M = (1 << (f.n - 1)) - 1;
     if (G < 1 || G > kDdaMaxG || (int64_t)G * M > kDdaMaxThresholds || len < 0) return false;
+    if (len > ((int64_t)1 << 46)) return false;
     L->G = G;
     L->M = M;
     L->A = G * M;
-    L->nblk = dda_nblk(len);
+    int rpb = 0;
+    dda_blocks(len, &L->nblk, &rpb);
     const size_t Aa1 = (size_t)L->A + kMaxSplits + 1;
-    const size_t ns = kReduceSlices;
+    const size_t ns = L->nblk > kPackedMaxBlocks ? kReduceSlices : 0;
     size_t o = 0;
-    L->off_ubits = o; o = align256(o + sizeof(uint32_t) * (Aa1 + 1));
+    L->off_ubits = o; o = align256(o + sizeof(uint32_t) * (Aa1 + 3));
     L->off_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)L->A);
     L->off_meta = o;  o = align256(o + sizeof(uint32_t) * 8);
     L->off_pcnt = o;  o = align256(o + sizeof(uint64_t) * Aa1 * L->nblk);
-    L->off_psum = o;  o = align256(o + sizeof(uint64_t) * Aa1 * L->nblk);
+    L->off_psum = o;
     L->off_pscal = o; o = align256(o + sizeof(double) * 4 * L->nblk);
     L->off_s0 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
     L->off_s1 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
@@ -91,12 +114,106 @@ static DdaWs ws_ptrs(void* ws, const DdaLayout& L) {
     w.ubits = (uint32_t*)(b + L.off_ubits);
     w.rank = (int32_t*)(b + L.off_rank);
     w.meta = (uint32_t*)(b + L.off_meta);
-    w.pcnt = (uint64_t*)(b + L.off_pcnt);
-    w.psum = (uint64_t*)(b + L.off_psum);
+    w.rows = (uint64_t*)(b + L.off_pcnt);
     w.pscal = (double*)(b + L.off_pscal);
     w.rcnt = (uint64_t*)(b + L.off_s0);
     w.rsum = (uint64_t*)(b + L.off_s1);
     return w;
+}
+
+// ------------------------------------------------------------ wave primitives
+// DPP lane moves (gfx9): row_shr:n = 0x110 + n, row_bcast:15 = 0x142 (lane 15
+// of each row to the next row), row_bcast:31 = 0x143 (lane 31 to rows 2, 3).
+// A lane whose source is outside its row, or whose row is masked off, keeps
+// `old` (the identity of the operation).
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint32_t dpp(uint32_t old, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWMASK, 0xf, false);
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = dpp<CTRL, ROWMASK>(0u, (uint32_t)b);
+    const uint32_t hi = dpp<CTRL, ROWMASK>(0u, (uint32_t)(b >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Inclusive scans over the 64 lanes of a wave (Hillis-Steele inside rows of 16,
+// then the row totals carried across rows).  Fixed order: deterministic.
+__device__ __forceinline__ uint32_t wave_scan_add(uint32_t v) {
+    v += dpp<0x111, 0xf>(0u, v);
+    v += dpp<0x112, 0xf>(0u, v);
+    v += dpp<0x114, 0xf>(0u, v);
+    v += dpp<0x118, 0xf>(0u, v);
+    v += dpp<0x142, 0xa>(0u, v);
+    v += dpp<0x143, 0xc>(0u, v);
+    return v;
+}
+__device__ __forceinline__ double wave_scan_add(double v) {
+    v += dpp_f64<0x111, 0xf>(v);
+    v += dpp_f64<0x112, 0xf>(v);
+    v += dpp_f64<0x114, 0xf>(v);
+    v += dpp_f64<0x118, 0xf>(v);
+    v += dpp_f64<0x142, 0xa>(v);
+    v += dpp_f64<0x143, 0xc>(v);
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_scan_min(uint32_t v) {
+    v = min(v, dpp<0x111, 0xf>(~0u, v));
+    v = min(v, dpp<0x112, 0xf>(~0u, v));
+    v = min(v, dpp<0x114, 0xf>(~0u, v));
+    v = min(v, dpp<0x118, 0xf>(~0u, v));
+    v = min(v, dpp<0x142, 0xa>(~0u, v));
+    v = min(v, dpp<0x143, 0xc>(~0u, v));
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_scan_max(uint32_t v) {
+    v = max(v, dpp<0x111, 0xf>(0u, v));
+    v = max(v, dpp<0x112, 0xf>(0u, v));
+    v = max(v, dpp<0x114, 0xf>(0u, v));
+    v = max(v, dpp<0x118, 0xf>(0u, v));
+    v = max(v, dpp<0x142, 0xa>(0u, v));
+    v = max(v, dpp<0x143, 0xc>(0u, v));
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_scan_or(uint32_t v) {
+    v |= dpp<0x111, 0xf>(0u, v);
+    v |= dpp<0x112, 0xf>(0u, v);
+    v |= dpp<0x114, 0xf>(0u, v);
+    v |= dpp<0x118, 0xf>(0u, v);
+    v |= dpp<0x142, 0xa>(0u, v);
+    v |= dpp<0x143, 0xc>(0u, v);
+    return v;
+}
+__device__ __forceinline__ uint32_t lane63(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+__device__ __forceinline__ double lane63(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), 63);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Workgroup barrier for LDS only.  __syncthreads() also waits for every global
+// load in flight (here: the prefetched chunk of x, which the set-up is meant
+// to overlap); all communication between threads in these kernels is through
+// LDS.  The memory clobber keeps the compiler from moving LDS accesses across.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// ---------------------------------------------------------------- format math
+// Non-negative set value number c (ascending, c = 0 .. 2^(n-1)-1) of ESB(n, k):
+// binade j = c >> k, fraction f; j = 0 is the subnormal binade f * 2^-k, else
+// 2^(j-1) * (1 + f 2^-k).  Exact in fp32.
+__host__ __device__ inline float set_value(int c, int k) {
+    const int j = c >> k, f = c & ((1 << k) - 1);
+    return j == 0 ? ldexpf((float)f, -k) : ldexpf((float)((1 << k) + f), j - 1 - k);
+}
+// Midpoint between values c-1 and c (k+2 significant bits: exact in fp32).
+__host__ __device__ inline float set_mid(int c, int k) {
+    return 0.5f * (set_value(c - 1, k) + set_value(c, k));
 }
 
 __device__ __forceinline__ bool alpha_ok(float a) { return a > 0.0f && a < __builtin_inff(); }
@@ -127,177 +244,69 @@ __device__ uint32_t threshold_bits(float alpha, float mu) {
     return hi;
 }
 
-// Number of powers of two strictly between bit patterns lo < hi (both finite).
-__device__ __forceinline__ uint32_t splits_between(uint32_t lo, uint32_t hi) {
-    const uint32_t e1 = lo >> 23, e2 = hi >> 23;
-    const uint32_t last = (hi & 0x7fffffu) ? e2 : e2 - 1u;   // exponent of the last start < hi
-    const uint32_t first = e1 + 1u;                           // first binade start > lo
-    return (e2 > e1 && last >= first) ? last - first + 1u : 0u;
+__host__ __device__ static inline int hist_lbins(int A) {
+    return A <= 960 ? 13 : (A <= 4096 ? 12 : 10);
 }
-
-// Block-wide exclusive scan (1024 threads), fixed summation order.
-template <typename T>
-__device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T* total) {
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
-    T x = v;
-    for (int off = 1; off < 64; off <<= 1) {
-        const T y = __shfl_up(x, off);
-        if (lane >= off) x += y;
-    }
-    if (lane == 63) sh[wid] = x;
-    __syncthreads();
-    if (wid == 0) {
-        T s = lane < nw ? sh[lane] : (T)0;
-        for (int off = 1; off < 64; off <<= 1) {
-            const T y = __shfl_up(s, off);
-            if (lane >= off) s += y;
-        }
-        if (lane < nw) sh[lane] = s;
-    }
-    __syncthreads();
-    const T before = (wid > 0 ? sh[wid - 1] : (T)0) + x - v;
-    if (total) *total = sh[nw - 1];
-    __syncthreads();
-    return before;
-}
-
-// Block-wide exclusive scan of N fp64 components at once (one set of barriers).
-template <int N>
-__device__ __forceinline__ void block_exclusive_scan_n(const double (&v)[N], double (*sh)[16],
-                                                       double (&before)[N], double (&total)[N]) {
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
-    double x[N];
-#pragma unroll
-    for (int c = 0; c < N; c++) x[c] = v[c];
-    for (int off = 1; off < 64; off <<= 1) {
-#pragma unroll
-        for (int c = 0; c < N; c++) {
-            const double y = __shfl_up(x[c], off);
-            if (lane >= off) x[c] += y;
-        }
-    }
-    if (lane == 63) {
-#pragma unroll
-        for (int c = 0; c < N; c++) sh[c][wid] = x[c];
-    }
-    __syncthreads();
-    if (wid == 0) {
-#pragma unroll
-        for (int c = 0; c < N; c++) {
-            double t = lane < nw ? sh[c][lane] : 0.0;
-            for (int off = 1; off < 64; off <<= 1) {
-                const double y = __shfl_up(t, off);
-                if (lane >= off) t += y;
-            }
-            if (lane < nw) sh[c][lane] = t;
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int c = 0; c < N; c++) {
-        before[c] = (wid > 0 ? sh[c][wid - 1] : 0.0) + x[c] - v[c];
-        total[c] = sh[c][nw - 1];
-    }
-    __syncthreads();
-}
-
-// Block-wide sums of N fp64 components in a fixed order (deterministic): a
-// butterfly inside each wave, then the wave totals added in wave order.  All
-// threads receive the totals.  One barrier pair.
-template <int N>
-__device__ __forceinline__ void block_sum_n(double (&v)[N], double (*sh)[16]) {
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, nw = blockDim.x >> 6;
-#pragma unroll
-    for (int c = 0; c < N; c++)
-        for (int off = 32; off > 0; off >>= 1) v[c] += __shfl_xor(v[c], off);
-    if (lane == 0) {
-#pragma unroll
-        for (int c = 0; c < N; c++) sh[c][wid] = v[c];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int c = 0; c < N; c++) {
-        double t = 0.0;
-        for (int w = 0; w < nw; w++) t += sh[c][w];
-        v[c] = t;
-    }
-    __syncthreads();
-}
-
-// Wave-level min / max / sum of 32-bit values (all 64 lanes take part).
-__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
-    for (int off = 32; off > 0; off >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, off));
-    return v;
-}
-__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-    for (int off = 32; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off));
-    return v;
-}
-__device__ __forceinline__ uint32_t wave_add(uint32_t v) {
-    for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
-    return v;
-}
-
-template <typename T>
-__device__ __forceinline__ T block_sum(T v, T* sh) {
-    T t;
-    block_exclusive_scan<T>(v, sh, &t);
-    return t;
-}
-
 // Dynamic LDS of k_dda_hist:
-//   U     u32[Aa + 2]   sorted atom bounds: U[0] = 0, U[1..Ap] boundaries, U[Ap+1] = ~0
-//   binfo u32[nbins]    per bin: first atom (low 16 bits) | boundaries inside (high 16);
-//                       for the pass it becomes u32[2 * nbins]: the pair
-//                       {first atom | bounds inside << 16, the first bound after it}
-//   TH    u32[A]        thresholds, later their atom positions (the cell starts)
-//   KH    u64[Aa + 65]  (value << 32 | id) bucket keys, later the packed histogram;
-//                       the last 64 cells take the zero adds of lanes outside
-//                       [lo, hi), one per lane, so that they never collide
-__host__ __device__ static inline int hist_nbins(int A) {
-    return A <= 2048 ? 8192 : (A <= 4096 ? 4096 : 2048);
-}
-static size_t hist_lds_bytes(int A) {
+//   ENT  uint4[nbins]  bin entries; during the set-up its start holds the bin
+//                      counts u32[nbins] (first atom | count << 16)
+//   U    u32[Aa + 4]   sorted atom bounds, padded with ~0
+//   TH   u32[A]        thresholds, then the atom where each cell starts
+//   KH   u64[Aa + 65]  (bound << 32 | id) bucket keys, then the packed histogram
+//                      (atoms 0 .. Ap, then one spare cell per lane)
+struct HistLds {
+    size_t u, th, kh, total;
+};
+__host__ __device__ static inline HistLds hist_lds(int A) {
+    HistLds h;
     const size_t Aa = (size_t)A + kMaxSplits;
-    return align256(sizeof(uint32_t) * (Aa + 2)) + sizeof(uint32_t) * 2 * hist_nbins(A) +
-           align256(sizeof(uint32_t) * A) + sizeof(uint64_t) * (Aa + 1 + 64);
+    h.u = (size_t)16 << hist_lbins(A);
+    h.th = h.u + align16(sizeof(uint32_t) * (Aa + 4));
+    h.kh = h.th + align16(sizeof(uint32_t) * (size_t)A);
+    h.total = h.kh + sizeof(uint64_t) * (Aa + 1 + 64);   // + one spare cell per lane
+    return h;
 }
 
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restrict__ x, int64_t len,
                                                            const float* __restrict__ grid,
                                                            DdaArgs a, DdaWs w) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int A = a.A, M = a.M, tid = threadIdx.x;
-    const int nbins = hist_nbins(A);
-    const size_t Aa = (size_t)A + kMaxSplits;
-    uint32_t* U = (uint32_t*)smem;
-    uint32_t* binfo = (uint32_t*)(smem + align256(sizeof(uint32_t) * (Aa + 2)));
-    uint32_t* TH = binfo + 2 * nbins;
-    uint64_t* KH = (uint64_t*)((unsigned char*)TH + align256(sizeof(uint32_t) * A));
+    const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int nbins = 1 << a.lbins;
+    const HistLds hl = hist_lds(A);
+    uint4* ENT = (uint4*)smem;
+    uint32_t* binc = (uint32_t*)smem;
+    uint32_t* U = (uint32_t*)(smem + hl.u);
+    uint32_t* TH = (uint32_t*)(smem + hl.th);
+    uint64_t* KH = (uint64_t*)(smem + hl.kh);
     uint64_t* hist = KH;
-    __shared__ float s_mids[128];
-    __shared__ uint32_t s_lo, s_hi, s_nfin, s_flags;
-    __shared__ uint32_t s_scan[16];
-    __shared__ double s_red3[3][16];
+    __shared__ float s_mid[128];
+    __shared__ uint32_t s_u[4][16];
+    __shared__ double s_d[2][16];
 
-    // ---- 0. this block's chunks of x; the first one is requested now, so its
-    //         loads overlap the set-up.  Loads are unconditional (clamped
-    //         address, value zeroed outside the range), so the compiler can
-    //         leave a chunk in flight across the binning of the previous one.
+    // ---- 0. requests first: this thread's candidate scales and the first chunk
+    //         of x, so that both latencies overlap the clearing of the bins.
+    constexpr int kMaxTpt = kDdaMaxThresholds / kHistThreads;   // thresholds per thread
+    float al[kMaxTpt];
+#pragma unroll
+    for (int r = 0; r < kMaxTpt; r++) {
+        const int i = tid + r * kHistThreads;
+        al[r] = (i < A) ? grid[i / M] : 1.0f;
+    }
     const bool vec = ((uintptr_t)x & 15) == 0;
-    const int64_t n4 = vec ? (len >> 2) : (len + 3) >> 2;   // scalar path: chunks of 4 elements
-    const int64_t nchunks = (n4 + kChunk4 - 1) / kChunk4;
-    const int64_t cpb = (nchunks + gridDim.x - 1) / gridDim.x;
-    const int64_t c0 = (int64_t)blockIdx.x * cpb;
-    const int64_t c1 = min(nchunks, c0 + cpb);
-    auto load_chunk_t = [&](auto VEC, int64_t ch, uint32_t (&g)[16]) {
-        if constexpr (decltype(VEC)::value) {
+    const int64_t e0 = (int64_t)blockIdx.x * a.rows_pb * kRowElems;
+    const int64_t e1 = min(len, e0 + (int64_t)a.rows_pb * kRowElems);
+    // element range of the vector path: whole float4 only; the last block takes
+    // the len % 4 tail separately
+    const int64_t v1 = vec ? (e1 & ~(int64_t)3) : e1;
+    auto load_chunk = [&](int64_t c, uint32_t (&g)[16]) {   // c: first element of the chunk
+        if (vec) {
             const f32x4* x4 = (const f32x4*)x;
 #pragma unroll
             for (int u = 0; u < 4; u++) {
-                const int64_t i4 = ch * kChunk4 + tid + u * kHistThreads;
-                const bool in = ch < c1 && i4 < n4;
-                const f32x4 v = __builtin_nontemporal_load(&x4[in ? i4 : 0]);
+                const int64_t e = c + 4 * ((int64_t)u * kHistThreads + tid);
+                const bool in = e < v1;
+                const f32x4 v = __builtin_nontemporal_load(&x4[in ? (e >> 2) : 0]);
                 g[4 * u + 0] = in ? __float_as_uint(v.x) : 0u;
                 g[4 * u + 1] = in ? __float_as_uint(v.y) : 0u;
                 g[4 * u + 2] = in ? __float_as_uint(v.z) : 0u;
@@ -306,95 +315,125 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         } else {
 #pragma unroll
             for (int u = 0; u < 16; u++) {
-                const int64_t i = ch * (4 * kChunk4) + tid + (int64_t)u * kHistThreads;
-                const bool in = ch < c1 && i < len;
-                const uint32_t v = __float_as_uint(x[in ? i : 0]);
-                g[u] = in ? v : 0u;   // zeros: atom 0, add nothing
+                const int64_t e = c + 4 * ((int64_t)(u >> 2) * kHistThreads + tid) + (u & 3);
+                const bool in = e < v1;
+                g[u] = in ? __float_as_uint(x[in ? e : 0]) : 0u;
             }
         }
     };
+    auto load_full = [&](int64_t c, uint32_t (&g)[16]) {    // a whole chunk inside [e0, v1)
+        if (vec) {
+            const f32x4* x4 = (const f32x4*)x + (c >> 2) + tid;
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const f32x4 v = __builtin_nontemporal_load(&x4[u * kHistThreads]);
+                g[4 * u + 0] = __float_as_uint(v.x);
+                g[4 * u + 1] = __float_as_uint(v.y);
+                g[4 * u + 2] = __float_as_uint(v.z);
+                g[4 * u + 3] = __float_as_uint(v.w);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 16; u++)
+                g[u] = __float_as_uint(x[c + 4 * ((int64_t)(u >> 2) * kHistThreads + tid) + (u & 3)]);
+        }
+    };
     uint32_t gn[16];
-    if (c0 < c1) {   // (a block with no chunk touches no element: x may be empty)
-        if (vec) load_chunk_t(std::integral_constant<bool, true>{}, c0, gn);
-        else load_chunk_t(std::integral_constant<bool, false>{}, c0, gn);
-    }
+    constexpr int64_t kChunkElems = 4 * 4 * kHistThreads;
+    if (e0 + kChunkElems <= v1) load_full(e0, gn);
+    else if (e0 < v1) load_chunk(e0, gn);   // (x may be NULL when len == 0)
+    if (tid < M) s_mid[tid] = set_mid(tid + 1, a.k);
+    for (int b = tid; b < nbins; b += kHistThreads) binc[b] = 0u;
+    lds_barrier();
 
     // ---- 1. thresholds, their finite range and count
-    if (tid < M) s_mids[tid] = a.mids[tid];
-    if (tid == 0) { s_lo = 0x7f800000u; s_hi = 0u; s_nfin = 0u; s_flags = 0u; }
-    __syncthreads();
     {
         uint32_t wlo = 0x7f800000u, whi = 0u, wn = 0u;
-        for (int i0 = 0; i0 < A; i0 += kHistThreads) {      // uniform trip count
-            const int i = i0 + tid;
-            if (i < A) {
-                const int j = i / M, c = i - j * M;
-                const float al = grid[j];
-                const uint32_t t = alpha_ok(al) ? threshold_bits(al, s_mids[c]) : 0x7f800000u;
+#pragma unroll
+        for (int r = 0; r < kMaxTpt; r++) {
+            const int i = tid + r * kHistThreads;
+            if (r * kHistThreads < A && i < A) {
+                const int c = i - (i / M) * M;
+                const uint32_t t = alpha_ok(al[r]) ? threshold_bits(al[r], s_mid[c]) : 0x7f800000u;
                 TH[i] = t;
                 if (t < 0x7f800000u) { wlo = min(wlo, t); whi = max(whi, t); wn++; }
             }
         }
-        wlo = wave_min(wlo);
-        whi = wave_max(whi);
-        wn = wave_add(wn);
-        if ((tid & 63) == 0 && wn) {
-            atomicMin(&s_lo, wlo);
-            atomicMax(&s_hi, whi);
-            atomicAdd(&s_nfin, wn);
-        }
+        wlo = wave_scan_min(wlo);
+        whi = wave_scan_max(whi);
+        wn = wave_scan_add(wn);
+        if (lane == 63) { s_u[0][wid] = wlo; s_u[1][wid] = whi; s_u[2][wid] = wn; }
     }
-    __syncthreads();
-    const uint32_t nfin = s_nfin;
-    uint32_t lo = 0x7f800000u, hi = 0x7f800000u, shift = 0, base = 0, nb = 0, nsplit = 0;
-    if (nfin > 0) {
-        lo = s_lo;
-        hi = s_hi;
-        while (((hi >> shift) - (lo >> shift)) >= (uint32_t)(nbins - 1)) shift++;   // <= 19
-        base = lo >> shift;
-        nb = (hi >> shift) - base + 1;
-        if (hi > lo) {
-            const uint32_t e_lo = lo >> 23, e_hi = (hi - 1u) >> 23;   // binade starts in (lo, hi)
-            nsplit = e_hi - e_lo;
-        }
+    lds_barrier();
+    uint32_t lo = 0x7f800000u, hi = 0u, nfin = 0u;
+#pragma unroll
+    for (int v = 0; v < kHistThreads / 64; v++) {
+        lo = min(lo, s_u[0][v]);
+        hi = max(hi, s_u[1][v]);
+        nfin += s_u[2][v];
     }
-    // ---- 2. boundaries per bin: finite thresholds and the powers of two in (lo, hi)
-    for (uint32_t b = tid; b < nb; b += kHistThreads) binfo[b] = 0u;
-    __syncthreads();
+    if (nfin == 0) { lo = 0x7f800000u; hi = 0x7f800000u; }
+    uint32_t shift = 0;
+    while (((hi >> shift) - (lo >> shift)) >= (uint32_t)(nbins - 1)) shift++;   // <= 21
+    const uint32_t base = lo >> shift;
+    const uint32_t nb = (hi >> shift) - base + 1u;
+    // binade starts strictly inside (lo, hi)
+    const uint32_t nsplit = (hi > lo) ? ((hi - 1u) >> 23) - (lo >> 23) : 0u;
+    const uint32_t Ap = nfin + nsplit;
+
+    // ---- 2. bounds per bin: finite thresholds and the powers of two in (lo, hi)
     for (int i = tid; i < A; i += kHistThreads) {
         const uint32_t t = TH[i];
-        if (t < 0x7f800000u) atomicAdd(&binfo[(t >> shift) - base], 1u);
+        if (t < 0x7f800000u) atomicAdd(&binc[(t >> shift) - base], 1u);
     }
-    for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
-        const uint32_t v = ((lo >> 23) + 1u + e) << 23;
-        atomicAdd(&binfo[(v >> shift) - base], 1u);
-    }
-    __syncthreads();
-    // ---- 3. first atom of every bin: exclusive scan of the counts
-    const uint32_t Ap = nfin + nsplit;
+    for (uint32_t e = tid; e < nsplit; e += kHistThreads)
+        atomicAdd(&binc[((((lo >> 23) + 1u + e) << 23) >> shift) - base], 1u);
+    lds_barrier();
+
+    // ---- 3. first atom of every bin: exclusive scan of the counts, P bins per thread
+    const int P = nbins / kHistThreads;   // 8, 4 or 1
     {
-        const int per = (int)((nb + kHistThreads - 1) / kHistThreads);
-        uint32_t mysum = 0;
-        for (int e = 0; e < per; e++) {
-            const uint32_t b = (uint32_t)(tid * per + e);
-            if (b < nb) mysum += binfo[b];
+        uint32_t cnt[8];
+        uint4* b4 = (uint4*)binc;
+        if (P == 8) {
+            const uint4 u0 = b4[2 * tid], u1 = b4[2 * tid + 1];
+            cnt[0] = u0.x; cnt[1] = u0.y; cnt[2] = u0.z; cnt[3] = u0.w;
+            cnt[4] = u1.x; cnt[5] = u1.y; cnt[6] = u1.z; cnt[7] = u1.w;
+        } else if (P == 4) {
+            const uint4 u0 = b4[tid];
+            cnt[0] = u0.x; cnt[1] = u0.y; cnt[2] = u0.z; cnt[3] = u0.w;
+            cnt[4] = cnt[5] = cnt[6] = cnt[7] = 0u;
+        } else {
+            cnt[0] = binc[tid];
+            cnt[1] = cnt[2] = cnt[3] = cnt[4] = cnt[5] = cnt[6] = cnt[7] = 0u;
         }
-        uint32_t run = block_exclusive_scan<uint32_t>(mysum, s_scan, nullptr);
-        for (int e = 0; e < per; e++) {
-            const uint32_t b = (uint32_t)(tid * per + e);
-            if (b < nb) {
-                const uint32_t c = binfo[b];
-                binfo[b] = run;                 // fill counter (high half) starts at 0
-                run += c;
-            }
+        uint32_t mine = 0;
+#pragma unroll
+        for (int e = 0; e < 8; e++) mine += cnt[e];
+        const uint32_t incl = wave_scan_add(mine);
+        if (lane == 63) s_u[3][wid] = incl;
+        lds_barrier();
+        uint32_t run = incl - mine;
+        for (int v = 0; v < wid; v++) run += s_u[3][v];
+        uint32_t st[8];                         // fill counter (high half) starts at 0
+#pragma unroll
+        for (int e = 0; e < 8; e++) { st[e] = run; run += cnt[e]; }
+        if (P == 8) {
+            b4[2 * tid] = make_uint4(st[0], st[1], st[2], st[3]);
+            b4[2 * tid + 1] = make_uint4(st[4], st[5], st[6], st[7]);
+        } else if (P == 4) {
+            b4[tid] = make_uint4(st[0], st[1], st[2], st[3]);
+        } else {
+            binc[tid] = st[0];
         }
     }
-    __syncthreads();
+    lds_barrier();
+
     // ---- 4. scatter the keys into their buckets; non-finite thresholds start past the top
     for (int i = tid; i < A; i += kHistThreads) {
         const uint32_t t = TH[i];
         if (t < 0x7f800000u) {
-            const uint32_t old = atomicAdd(&binfo[(t >> shift) - base], 0x10000u);
+            const uint32_t old = atomicAdd(&binc[(t >> shift) - base], 0x10000u);
             KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)t << 32) | (uint32_t)i;
         } else {
             TH[i] = Ap + 1u;
@@ -402,92 +441,90 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     }
     for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
         const uint32_t v = ((lo >> 23) + 1u + e) << 23;
-        const uint32_t old = atomicAdd(&binfo[(v >> shift) - base], 0x10000u);
+        const uint32_t old = atomicAdd(&binc[(v >> shift) - base], 0x10000u);
         KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)v << 32) | (uint32_t)(A + e);
     }
-    __syncthreads();
+    lds_barrier();
+
     // ---- 5. order inside each bucket by counting: position = first + #smaller keys
     for (uint32_t k = tid; k < Ap; k += kHistThreads) {
         const uint64_t key = KH[k];
         const uint32_t v = (uint32_t)(key >> 32), id = (uint32_t)key;
-        const uint32_t bi = binfo[(v >> shift) - base];
+        const uint32_t bi = binc[(v >> shift) - base];
         const uint32_t o = bi & 0xffffu, n = bi >> 16;
         uint32_t pos = o;
         for (uint32_t t = o; t < o + n; t++) pos += (KH[t] < key) ? 1u : 0u;
         U[pos + 1] = v;
         if (id < (uint32_t)A) TH[id] = pos + 1;      // atom where this cell starts
     }
-    if (tid == 0) { U[0] = 0u; U[Ap + 1] = 0xffffffffu; }
-    const uint32_t afin = Ap;                        // the top atom [hi, inf)
-    __syncthreads();   // the keys are dead: KH becomes the histogram
-    // ---- 5b. bin pairs {first atom | bounds inside << 16, next bound}: with at
-    //          most one bound inside, the atom of a value is first + (v >= next)
+    if (tid < 4) U[tid == 0 ? 0 : Ap + (uint32_t)tid] = tid == 0 ? 0u : 0xffffffffu;
+    lds_barrier();
+
+    // ---- 6. bin entries {first | flags, next three bounds}; the keys are dead:
+    //         KH becomes the histogram
     {
-        constexpr int kPer = 8192 / kHistThreads;
-        uint32_t bv[kPer];
+        uint32_t bv[8];
 #pragma unroll
-        for (int k = 0; k < kPer; k++) {
-            const uint32_t b = (uint32_t)(tid + k * kHistThreads);
-            bv[k] = b < nb ? binfo[b] : 0u;
-        }
-        for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0;
-        __syncthreads();
+        for (int e = 0; e < 8; e++) bv[e] = (e < P) ? binc[tid + e * kHistThreads] : 0u;
+        for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0ull;
+        lds_barrier();   // the counts alias the entries
 #pragma unroll
-        for (int k = 0; k < kPer; k++) {
-            const uint32_t b = (uint32_t)(tid + k * kHistThreads);
-            if (b < nb || (b == 0 && nb == 0)) {
-                binfo[2 * b] = bv[k];
-                binfo[2 * b + 1] = U[(bv[k] & 0xffffu) + 1];
+        for (int e = 0; e < 8; e++) {
+            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
+            if (e < P && b < nb) {
+                const uint32_t f = bv[e] & 0xffffu, n = bv[e] >> 16;
+                const uint32_t fl = (n >= 4u ? kFlagWalk : 0u) | (b == nb - 1u ? kFlagTop : 0u);
+                ENT[b] = make_uint4(f | fl, U[f + 1], U[f + 2], U[f + 3]);
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 
-    // ---- 6. the pass
-    double sumsq = 0.0, top_s1 = 0.0;
+    // ---- 7. the pass
+    double ss0 = 0.0, ss1 = 0.0, top_s1 = 0.0;
     uint32_t top_cnt = 0, flags = 0;
     constexpr int E = 8;
-    // Per element: x^2 into the fp64 sum; |x| in [lo, hi) to its atom (bin
-    // table, then one comparison against the next bound; a loop only where a
-    // bin holds two or more bounds) and one LDS atomic adding
-    // (mantissa << 20) + 1.  Every atom lies inside one binade, so the sum of
-    // the 23-bit mantissas and the count give the exact sum of |x| over the
-    // atom.  |x| >= hi (the top atom) and non-finite x are rare: a branch.
-    const uint32_t span = hi - lo;
-    const uint32_t bmax = base + (nb > 0 ? nb - 1u : 0u);
-    const uint2* bins = (const uint2*)binfo;
-    const uint32_t spare = (uint32_t)Aa + 1u + (uint32_t)(tid & 63);
-    auto visit = [&](const uint32_t (&xb)[E]) {
-        uint32_t ab[E], t[E];
-        uint2 bi[E];
-        bool mid[E];
-        uint32_t mx = 0;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    typedef const __attribute__((address_space(3))) u32x4 lds_u32x4;
+    // LDS byte address of the entry of bin (v >> shift) is (v >> shift) * 16 + ent_b
+    // (unsigned wrap-around), with the bin clamped to [base, base + nb - 1]
+    const uint32_t ent_b = (uint32_t)(uintptr_t)(lds_u32x4*)(u32x4*)ENT - (base << 4);
+    const uint32_t bhi = base + nb - 1u;
+    // lanes whose value lies in atom 0 (q = 0 for every candidate) add into a
+    // cell of their own, so that ReLU zeros never pile up on one LDS address
+    const uint32_t spare = (uint32_t)a.Aa + 1u + (uint32_t)lane;
+    auto visit = [&](const uint32_t* xb) {
+        uint32_t ab[E], t[E], fx[E];
+        u32x4 en[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) ab[e] = xb[e] & 0x7fffffffu;
+        // every entry read in flight before the first is used
 #pragma unroll
         for (int e = 0; e < E; e++) {
-            ab[e] = xb[e] & 0x7fffffffu;
+            const uint32_t bi = min(max(ab[e] >> shift, base), bhi);
+            en[e] = *(lds_u32x4*)(uintptr_t)((bi << 4) + ent_b);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < E; e++) {
             const double xd = (double)__uint_as_float(ab[e]);
-            sumsq = fma(xd, xd, sumsq);
-            mx = max(mx, ab[e]);
-            mid[e] = ab[e] - lo < span;                // atom 0 (q = 0 for all) adds nothing
-            const uint32_t b = min(max(ab[e] >> shift, base), bmax) - base;
-            bi[e] = bins[b];
+            if (e & 1) ss1 = fma(xd, xd, ss1); else ss0 = fma(xd, xd, ss0);
         }
-        bool walk = false;
+        uint32_t any = 0;
 #pragma unroll
         for (int e = 0; e < E; e++) {
-            t[e] = (bi[e].x & 0xffffu) + ((ab[e] >= bi[e].y) ? 1u : 0u);
-            walk |= mid[e] && bi[e].x >= 0x20000u;
+            t[e] = en[e].x + (ab[e] >= en[e].y ? 1u : 0u) + (ab[e] >= en[e].z ? 1u : 0u) +
+                   (ab[e] >= en[e].w ? 1u : 0u);
+            fx[e] = en[e].x;
+            any |= en[e].x;
         }
-        if (walk) {                                    // a bin with two or more bounds
-#pragma unroll
-            for (int e = 0; e < E; e++)
-                if (mid[e] && bi[e].x >= 0x20000u)
-                    while (U[t[e] + 1] <= ab[e]) t[e]++;
-        }
-        if (mx >= hi) {                                // the top atom, non-finite x
+        if (any & (kFlagWalk | kFlagTop)) {            // rare: crowded bins, the top bin
 #pragma unroll
             for (int e = 0; e < E; e++) {
-                if (ab[e] >= hi) {
+                t[e] &= kAtomMask;
+                if (fx[e] & kFlagWalk)
+                    while (U[t[e] + 1] <= ab[e]) t[e]++;
+                if ((fx[e] & kFlagTop) && ab[e] >= hi) {
                     if (ab[e] < 0x7f800000u) {
                         top_s1 += (double)__uint_as_float(ab[e]);
                         top_cnt += 1u;
@@ -498,173 +535,205 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
             }
         }
 #pragma unroll
-        for (int e = 0; e < E; e++) {   // outside [lo, hi): zero into the lane's own spare cell
-            const uint32_t mant = ab[e] & 0x7fffffu;
-            const uint64_t v = mid[e] ? (((uint64_t)mant << 20) | 1u) : 0u;
-            atomicAdd(&hist[mid[e] ? t[e] : spare], v);
+        for (int e = 0; e < E; e++) {
+            const uint32_t at = t[e] != 0u ? t[e] : spare;
+            atomicAdd(&hist[at], (1ull << 44) | (uint64_t)(ab[e] & 0x7fffffu));
         }
     };
-    const int64_t cnt_base = (int64_t)blockIdx.x * (int64_t)(Aa + 1);
-    bool first_flush = true;
-    auto flush = [&]() {
-        __syncthreads();
-        for (uint32_t i = tid; i <= Ap; i += kHistThreads) {
-            const uint64_t v = hist[i];
-            hist[i] = 0;
-            const uint64_t c = v & 0xfffffu, s = v >> 20;
-            if (first_flush) { w.pcnt[cnt_base + i] = c; w.psum[cnt_base + i] = s; }
-            else if (v) { w.pcnt[cnt_base + i] += c; w.psum[cnt_base + i] += s; }
-        }
-        first_flush = false;
-        __syncthreads();
-    };
-    // The pass, one chunk of loads ahead of the chunk being binned (the first
-    // chunk was requested before the set-up).
-    auto pass = [&](auto VEC) {
-        auto load_chunk = [&](int64_t ch, uint32_t (&g)[16]) { load_chunk_t(VEC, ch, g); };
-        int since = 0;
-        for (int64_t ch = c0; ch < c1; ch++) {
-            uint32_t g[16];
+    const int64_t cstep = 4 * kHistThreads * 4;   // elements per chunk
+    for (int64_t c = e0; c < v1; c += cstep) {
+        uint32_t g[16];
 #pragma unroll
-            for (int u = 0; u < 16; u++) g[u] = gn[u];
-            load_chunk(ch + 1, gn);
-#pragma unroll
-            for (int h = 0; h < 2; h++) {
-                uint32_t gg[E];
-#pragma unroll
-                for (int e = 0; e < E; e++) gg[e] = g[E * h + e];
-                visit(gg);
-            }
-            if (++since == kFlushChunks) { flush(); since = 0; }
-        }
-    };
-    if (c0 < c1) {
-        if (vec) pass(std::integral_constant<bool, true>{});
-        else pass(std::integral_constant<bool, false>{});
+        for (int u = 0; u < 16; u++) g[u] = gn[u];
+        const int64_t cn = c + cstep;
+        if (cn + cstep <= v1) load_full(cn, gn);
+        else if (cn < v1) load_chunk(cn, gn);
+        visit(g);
+        if (c + 2 * 4 * kHistThreads < v1) visit(g + 8);   // rows 2, 3 of the chunk
     }
     if (vec && blockIdx.x == gridDim.x - 1 && tid < (int)(len & 3)) {   // tail of the vector path
-        uint32_t gg[E];
-        gg[0] = __float_as_uint(x[(len & ~(int64_t)3) + tid]);
+        uint32_t g[E];
+        g[0] = __float_as_uint(x[(len & ~(int64_t)3) + tid]);
 #pragma unroll
-        for (int e = 1; e < E; e++) gg[e] = 0u;
-        visit(gg);
+        for (int e = 1; e < E; e++) g[e] = 0u;
+        visit(g);
     }
-    flush();
+    lds_barrier();
 
-    // ---- 7. block scalars; block 0 also publishes the tables
-    if (flags) atomicOr(&s_flags, flags);
+    // ---- 8. the block's row, its scalars; block 0 also publishes the tables
+    uint64_t* row = w.rows + (int64_t)blockIdx.x * (a.Aa + 1);
+    for (uint32_t i = tid; i <= Ap; i += kHistThreads) row[i] = hist[i];
     {
-        double v3[3] = {sumsq, top_s1, (double)top_cnt};   // counts exact in fp64
-        block_sum_n<3>(v3, s_red3);
-        if (tid == 0) {
-            double* ps = w.pscal + 4 * blockIdx.x;
-            ps[0] = v3[0]; ps[1] = v3[1]; ps[2] = v3[2]; ps[3] = (double)s_flags;
-        }
+        const double ss = wave_scan_add(ss0 + ss1), t1 = wave_scan_add(top_s1);
+        const uint32_t tc = wave_scan_add(top_cnt), fl = wave_scan_or(flags);
+        if (lane == 63) { s_d[0][wid] = ss; s_d[1][wid] = t1; s_u[0][wid] = tc; s_u[1][wid] = fl; }
     }
     if (blockIdx.x == 0) {
-        for (uint32_t i = tid; i <= Ap + 1; i += kHistThreads) w.ubits[i] = U[i];
+        for (uint32_t i = tid; i <= Ap + 3u; i += kHistThreads) w.ubits[i] = U[i];
         for (int i = tid; i < A; i += kHistThreads) w.rank[i] = (int32_t)TH[i];
-        if (tid == 0) { w.meta[0] = afin; w.meta[1] = Ap; }
+        if (tid == 0) { w.meta[0] = Ap; w.meta[1] = Ap; }
+    }
+    lds_barrier();
+    if (tid == 0) {
+        double ss = 0.0, t1 = 0.0;
+        uint32_t tc = 0, fl = 0;
+        for (int v = 0; v < kHistThreads / 64; v++) {
+            ss += s_d[0][v]; t1 += s_d[1][v]; tc += s_u[0][v]; fl |= s_u[1][v];
+        }
+        double* ps = w.pscal + 4 * (int64_t)blockIdx.x;
+        ps[0] = ss; ps[1] = t1; ps[2] = (double)tc; ps[3] = (double)fl;
     }
 }
 
 // -------------------------------------------------------------------- reduce
-// Slice s of the blocks, per atom: sums of the per-block totals (integers).
+// Slice s of the block rows, per atom: integer sums of counts and significand
+// sums (entries past the last bound are summed too and never read).
 __global__ __launch_bounds__(256) void k_dda_reduce(DdaArgs a, DdaWs w) {
     const int at = blockIdx.x * 256 + threadIdx.x;
     const int Aa1 = a.Aa + 1;
     if (at >= Aa1) return;
-    const uint32_t Ap = w.meta[1];
-    if ((uint32_t)at > Ap) return;
     const int s = blockIdx.y, per = (a.nblk + a.nslice - 1) / a.nslice;
     const int b0 = s * per, b1 = min(a.nblk, b0 + per);
     uint64_t c = 0, t = 0;
+#pragma unroll 4
     for (int b = b0; b < b1; b++) {
-        c += w.pcnt[(int64_t)b * Aa1 + at];
-        t += w.psum[(int64_t)b * Aa1 + at];
+        const uint64_t v = w.rows[(int64_t)b * Aa1 + at];
+        c += v >> 44;
+        t += v & kSumMask;
     }
     w.rcnt[(int64_t)s * Aa1 + at] = c;
     w.rsum[(int64_t)s * Aa1 + at] = t;
 }
 
 // ------------------------------------------------------------------ finalize
-constexpr int kFinThreads = 1024;
+// Dynamic LDS: C0 u64[Aa+2] (counts, then prefix sums of counts as fp64),
+// C1 u64[Aa+2] (significand sums, then prefix sums of |x|), Dv double[G],
+// rk i32[A] (cell starts, when they fit).
+__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
+                                                              DdaArgs a, DdaWs w,
+                                                              float* __restrict__ alpha_out,
+                                                              double* __restrict__ D_out) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int G = a.G, M = a.M, A = a.A;
+    const int S = a.Aa + 1;                 // row stride; atoms 0 .. Ap <= Aa
+    const int NA = a.Aa + 2;                // prefix entries 0 .. Aa+1
+    uint64_t* C0 = (uint64_t*)smem;
+    uint64_t* C1 = C0 + NA;
+    double* P0 = (double*)C0;
+    double* P1 = (double*)C1;
+    double* Dv = (double*)(C1 + NA);
+    int32_t* rk = (int32_t*)(Dv + G);
+    __shared__ double s_d[3][16];
+    __shared__ uint32_t s_u[16];
+    __shared__ float s_q[128];
+    __shared__ float s_grid[kDdaMaxG];
 
-// The reduction over blocks and the per-candidate objective, for a block of
-// kFinThreads threads.  P0, P1: LDS of (afin + 2) doubles each; Dv: LDS of G
-// doubles.  ubits: the
-// sorted atom bounds; rks: the atom where each cell starts (LDS or global).
-// nsrc rows of per-atom partial sums in srcc / srcs, nblk rows of block scalars.
-__device__ void finalize_core(const float* __restrict__ grid, const DdaArgs& a, const DdaWs& w,
-                              float* __restrict__ alpha_out, double* __restrict__ D_out,
-                              double* P0, double* P1, const uint32_t* ubits, const int32_t* rks,
-                              uint32_t afin, int nsrc, const uint64_t* srcc, const uint64_t* srcs,
-                              int nblk, double* Dv) {
-    const int tid = threadIdx.x, G = a.G, M = a.M;
-    const int Aa1 = a.Aa + 1;
-    __shared__ double s_red3[3][16];
-    __shared__ double sq[128];
-    __shared__ uint32_t s_fl;
-    if (tid <= M) sq[tid] = (double)a.q[tid];
-    if (tid == 0) s_fl = 0;
-    // block scalars
-    double v3[3] = {0.0, 0.0, 0.0};
+    // ---- 1. every global read is requested before any is used: the candidate
+    //         scales, the block scalars, the bounds of this thread's atoms (the
+    //         contiguous range of step 3), the cell starts
+    const uint32_t afin = w.meta[0];
+    for (int j = tid; j < G; j += kFinThreads) s_grid[j] = grid[j];
+    constexpr int kPerMax = 9;                       // atoms per thread, (Aa+2)/1024 <= 9
+    const int per = (NA + kFinThreads - 1) / kFinThreads;
+    uint32_t ub[kPerMax];
+#pragma unroll
+    for (int e = 0; e < kPerMax; e++) {
+        const int at = tid * per + e;
+        ub[e] = (e < per && at < NA) ? w.ubits[at] : 0u;
+    }
+    double sc[3] = {0.0, 0.0, 0.0};
     uint32_t fl = 0;
-    for (int b = tid; b < nblk; b += kFinThreads) {
-        const double* ps = w.pscal + 4 * b;
-        v3[0] += ps[0]; v3[1] += ps[1]; v3[2] += ps[2]; fl |= (uint32_t)ps[3];
+    for (int b = tid; b < a.nblk; b += kFinThreads) {
+        const double* ps = w.pscal + 4 * (int64_t)b;
+        sc[0] += ps[0]; sc[1] += ps[1]; sc[2] += ps[2]; fl |= (uint32_t)ps[3];
     }
-    block_sum_n<3>(v3, s_red3);
-    const double sumsq = v3[0], top_s1 = v3[1], top_c = v3[2];
-    if (fl) atomicOr(&s_fl, fl);
-    // per-atom sums S0, S1 for atoms 0..afin (atom 0 carries q = 0 for everyone),
-    // loaded coalesced into LDS, then an in-place exclusive prefix scan over atoms
-    for (int at = tid; at <= (int)afin + 1; at += kFinThreads) {
-        double s0 = 0.0, s1 = 0.0;
-        if (at >= 1 && (uint32_t)at < afin) {
-            uint64_t c = 0, t = 0;
+    if (a.rk_lds)
+        for (int i = tid; i < A; i += kFinThreads) rk[i] = w.rank[i];
+    if (tid <= M) s_q[tid] = set_value(tid, a.k);
+
+    // ---- 2. per-atom integer sums over the packed rows or the slices, one
+    //         thread per atom (coalesced across threads)
+    for (int at = tid; at < S; at += kFinThreads) {
+        uint64_t c = 0, t = 0;
+        if (a.nslice > 0) {
 #pragma unroll 8
-            for (int b = 0; b < nsrc; b++) {
-                c += srcc[(int64_t)b * Aa1 + at];
-                t += srcs[(int64_t)b * Aa1 + at];
+            for (int r = 0; r < a.nslice; r++) {
+                c += w.rcnt[(int64_t)r * S + at];
+                t += w.rsum[(int64_t)r * S + at];
             }
-            // mantissa sums: add the implicit bit of a normal binade per element
-            const uint32_t ex = ubits[at] >> 23;
-            if (ex) t += c << 23;
-            s0 = (double)c;
-            s1 = ldexp((double)t, (int)max(ex, 1u) - 150);
-        } else if (afin > 0 && (uint32_t)at == afin) {
-            s0 = top_c;
-            s1 = top_s1;
+        } else {
+#pragma unroll 8
+            for (int r = 0; r < a.nblk; r++) {
+                const uint64_t v = w.rows[(int64_t)r * S + at];
+                c += v >> 44;
+                t += v & kSumMask;
+            }
         }
-        P0[at] = s0;
-        P1[at] = s1;
+        C0[at] = c;
+        C1[at] = t;
     }
-    __syncthreads();
+    // block scalars: fixed-order reduction
     {
-        const int per = ((int)afin + 2 + kFinThreads - 1) / kFinThreads;
-        double m0 = 0.0, m1 = 0.0;
-        for (int e = 0; e < per; e++) {
-            const int at = tid * per + e;
-            if (at <= (int)afin + 1) { m0 += P0[at]; m1 += P1[at]; }
+        const double r0 = wave_scan_add(sc[0]), r1 = wave_scan_add(sc[1]), r2 = wave_scan_add(sc[2]);
+        const uint32_t rf = wave_scan_or(fl);
+        if (lane == 63) { s_d[0][wid] = r0; s_d[1][wid] = r1; s_d[2][wid] = r2; s_u[wid] = rf; }
+    }
+    lds_barrier();
+    double sumsq = 0.0, top_s1 = 0.0, top_c = 0.0;
+    uint32_t flags = 0;
+#pragma unroll
+    for (int v = 0; v < kFinThreads / 64; v++) {
+        sumsq += s_d[0][v]; top_s1 += s_d[1][v]; top_c += s_d[2][v]; flags |= s_u[v];
+    }
+
+    // ---- 3. per-atom S0, S1 (atom 0 carries q = 0 for everyone; the top atom
+    //         its fp64 sums) and exclusive prefix sums over atoms 0 .. afin+1
+    double s0[kPerMax], s1[kPerMax];
+    double m0 = 0.0, m1 = 0.0;
+#pragma unroll
+    for (int e = 0; e < kPerMax; e++) {
+        const int at = tid * per + e;
+        s0[e] = 0.0;
+        s1[e] = 0.0;
+        if (e < per && at < NA) {
+            if (at >= 1 && (uint32_t)at < afin) {
+                const uint64_t c = C0[at];
+                uint64_t t = C1[at];
+                const uint32_t ex = ub[e] >> 23;
+                if (ex) t += c << 23;                // the implicit bit of a normal binade
+                s0[e] = (double)c;
+                s1[e] = ldexp((double)t, (int)max(ex, 1u) - 150);
+            } else if (afin > 0 && (uint32_t)at == afin) {
+                s0[e] = top_c;
+                s1[e] = top_s1;
+            }
+            m0 += s0[e];
+            m1 += s1[e];
         }
-        const double m2[2] = {m0, m1};
-        double bef[2], tot[2];
-        block_exclusive_scan_n<2>(m2, s_red3, bef, tot);
-        double r0 = bef[0], r1 = bef[1];
-        for (int e = 0; e < per; e++) {
+    }
+    {
+        const double i0 = wave_scan_add(m0), i1 = wave_scan_add(m1);
+        lds_barrier();   // s_d reused; C0/C1 reads above are done
+        if (lane == 63) { s_d[0][wid] = i0; s_d[1][wid] = i1; }
+        lds_barrier();
+        double r0 = i0 - m0, r1 = i1 - m1;
+        for (int v = 0; v < wid; v++) { r0 += s_d[0][v]; r1 += s_d[1][v]; }
+#pragma unroll
+        for (int e = 0; e < kPerMax; e++) {
             const int at = tid * per + e;
-            if (at <= (int)afin + 1) {
-                const double v0 = P0[at], v1 = P1[at];
+            if (e < per && at < NA) {
                 P0[at] = r0;
                 P1[at] = r1;
-                r0 += v0;
-                r1 += v1;
+                r0 += s0[e];
+                r1 += s1[e];
             }
         }
     }
-    __syncthreads();
-    // per candidate: cells as atom ranges [start_c, start_{c+1}), the last one to afin+1
+    lds_barrier();
+
+    // ---- 4. per candidate: cells as atom ranges [start_c, start_{c+1}), the last to afin+1
+    const int32_t* rks = a.rk_lds ? rk : w.rank;
     for (int j = tid; j < G; j += kFinThreads) {
         const int32_t* rkj = rks + (int64_t)j * M;
         const int end = (int)afin + 1;
@@ -672,19 +741,20 @@ __device__ void finalize_core(const float* __restrict__ grid, const DdaArgs& a, 
         int start = min(rkj[0], end);
         for (int c = 1; c <= M; c++) {
             const int next = (c < M) ? min(rkj[c], end) : end;
-            const double q = sq[c];
+            const double q = (double)s_q[c];
             Aj = fma(q, P1[next] - P1[start], Aj);
             Bj = fma(q * q, P0[next] - P0[start], Bj);
             start = next;
         }
-        const float al = grid[j];
+        const float al = s_grid[j];
         const double ad = (double)al;
         double D = fma(ad, fma(ad, Bj, -2.0 * Aj), sumsq);
-        if (!alpha_ok(al) || (s_fl & 2u)) D = __builtin_nan("");
-        else if (s_fl & 1u) D = __builtin_inf();
+        if (!alpha_ok(al) || (flags & 2u)) D = __builtin_nan("");
+        else if (flags & 1u) D = __builtin_inf();
         Dv[j] = D;
+        if (D_out) D_out[j] = D;
     }
-    __syncthreads();
+    lds_barrier();
     if (tid < 64) {
         // argmin over (isnan(D), D, j) in lexicographic order: the smallest index
         // with the least D, NaN ranking above every number
@@ -703,70 +773,39 @@ __device__ void finalize_core(const float* __restrict__ grid, const DdaArgs& a, 
                                 (onan && mnan && oj < bj);
             if (better) { bd = od; bj = oj; }
         }
-        if (tid == 0) *alpha_out = grid[bj];
+        if (tid == 0) *alpha_out = s_grid[bj];
     }
-    if (D_out)
-        for (int jj = tid; jj < G; jj += kFinThreads) D_out[jj] = Dv[jj];
-}
-
-__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
-                                                              DdaArgs a, DdaWs w,
-                                                              float* __restrict__ alpha_out,
-                                                              double* __restrict__ D_out) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int tid = threadIdx.x;
-    const int Aa1 = a.Aa + 1;
-    double* P0 = (double*)smem;                  // [Aa+2] prefix sums of counts
-    double* P1 = P0 + (Aa1 + 1);                 // [Aa+2] prefix sums of |x|
-    double* Dv = P1 + (Aa1 + 1);                 // [G] objective per candidate
-    int32_t* rk = (int32_t*)(Dv + a.G);         // [A] first atom of every cell
-    if (a.rk_lds)
-        for (int i = tid; i < a.A; i += kFinThreads) rk[i] = w.rank[i];
-    const bool sliced = a.nslice > 0;
-    finalize_core(grid, a, w, alpha_out, D_out, P0, P1, w.ubits, a.rk_lds ? rk : w.rank, w.meta[0],
-                  sliced ? a.nslice : a.nblk, sliced ? w.rcnt : w.pcnt, sliced ? w.rsum : w.psum,
-                  a.nblk, Dv);
 }
 
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
                       float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
                       hipStream_t s) {
     DdaArgs a;
-    const int M = L.M;
-    double vals[128];
-    int nv = 0;
-    for (uint32_t c = 0; c < (1u << f.n); c++) {   // non-negative values, ascending
-        if (c & f.sign_bit) continue;
-        vals[nv++] = decode_value(f, c);
-    }
-    for (int i = 1; i < nv; i++)
-        for (int t = i; t > 0 && vals[t] < vals[t - 1]; t--) {
-            const double tmp = vals[t]; vals[t] = vals[t - 1]; vals[t - 1] = tmp;
-        }
-    for (int c = 0; c <= M; c++) a.q[c] = (float)vals[c];
-    for (int c = 1; c <= M; c++) a.mids[c - 1] = (float)(0.5 * (vals[c - 1] + vals[c]));
-    a.G = G; a.M = M; a.A = L.A; a.Aa = L.A + kMaxSplits; a.nblk = L.nblk;
-    a.nslice = L.nblk > 2 * kReduceSlices ? kReduceSlices : 0;
+    a.G = G; a.M = L.M; a.A = L.A; a.Aa = L.A + kMaxSplits;
+    a.n = f.n; a.k = f.k;
+    a.lbins = hist_lbins(L.A);
+    dda_blocks(len, &a.nblk, &a.rows_pb);
+    a.nslice = a.nblk > kPackedMaxBlocks ? kReduceSlices : 0;
     a.rk_lds = 0;
     const DdaWs w = ws_ptrs(ws, L);
     static bool lds_attr_set[64] = {false};
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
         hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 156 * 1024);
         if (e != hipSuccess) return e;
         e = hipFuncSetAttribute((const void*)k_dda_finalize,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
         if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
-    k_dda_hist<<<L.nblk, kHistThreads, hist_lds_bytes(L.A), s>>>(x, len, grid, a, w);
+    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A).total, s>>>(x, len, grid, a, w);
     if (a.nslice > 0) {
         dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
         k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
     }
-    size_t fin_lds = sizeof(double) * (2 * (size_t)(a.Aa + 2) + (size_t)G);
-    a.rk_lds = fin_lds + sizeof(int32_t) * (size_t)a.A <= 140 * 1024;
+    size_t fin_lds = sizeof(uint64_t) * 2 * (size_t)(a.Aa + 2) + sizeof(double) * (size_t)G;
+    a.rk_lds = fin_lds + sizeof(int32_t) * (size_t)a.A <= 150 * 1024;
     if (a.rk_lds) fin_lds += sizeof(int32_t) * (size_t)a.A;
     k_dda_finalize<<<1, kFinThreads, fin_lds, s>>>(grid, a, w, alpha_out, D_out);
     return hipGetLastError();
