@@ -6,17 +6,21 @@
 // candidate j holds |x|, and the cell boundaries are exact fp32 thresholds:
 // T_{j,c} = the smallest fp32 X with fl32(X / alpha_j) >= mu_c, mu_c the
 // midpoint between set values c-1 and c (ties go up, as in the projection).
-// All G*M thresholds, sorted and further split at every power of two, cut
-// [0, inf) into "atoms": every candidate's cell is a union of consecutive atoms
-// and every bounded atom lies inside one binade.  One pass over x suffices.
+// The distinct values among all G*M thresholds and the powers of two between
+// them cut [0, inf) into "atoms": every candidate's cell is a union of
+// consecutive atoms and every bounded atom lies inside one binade.  (Grids of
+// scales such as fl32(s (j+1)/64) make many thresholds coincide: merging them
+// leaves few bins holding two bounds.)  One pass over x suffices.
 //
 // k_dda_hist (blocks of 1024 threads, each over at most 2^19 elements):
 //   set-up in LDS: thresholds by a local search around fl32(alpha mu); bucket
 //   placement by bin of the bit pattern (counts, scan, scatter, order inside a
-//   bucket by counting), which gives the sorted bounds and each cell's first
-//   atom; then a table of 16-byte bin entries {first atom | flags, the next
-//   three bounds}, so that the atom of a value is first + (number of those
-//   three bounds <= value) unless a bin holds four or more (a flagged walk).
+//   bucket by counting), a scan that merges equal bounds, which gives the
+//   distinct sorted bounds and each cell's first atom; then a table of 8-byte
+//   bin entries {first atom | flags, the next
+//   bound}, so that the atom of a value is first + (value >= that bound)
+//   unless the bin holds two or more bounds (a flagged walk over the sorted
+//   bounds; large inputs use 16384 bins, where such bins are rare).
 //   The pass: per element one entry read and one LDS atomic adding
 //   {significand, 1} to a packed 64-bit (count << 44 | sum) cell; x^2 in fp64.
 //   Values below the smallest threshold fall in atom 0, where q = 0 for every
@@ -41,7 +45,7 @@ constexpr int kRowElems = 4 * kHistThreads; // one float4 per thread
 constexpr int kMaxRowsPerBlock = 128;      // 2^19 elements: a packed cell cannot overflow
 constexpr int kPackedMaxBlocks = 32;       // above: k_dda_reduce sums the rows in slices
 constexpr int kReduceSlices = 16;
-constexpr uint32_t kFlagWalk = 1u << 31;   // bin holds four or more bounds
+constexpr uint32_t kFlagWalk = 1u << 31;   // bin holds two or more bounds
 constexpr uint32_t kFlagTop = 1u << 30;    // last bin: values >= the largest threshold
 constexpr uint32_t kAtomMask = (1u << 29) - 1u;
 constexpr uint64_t kSumMask = (1ull << 44) - 1ull;
@@ -56,9 +60,9 @@ struct DdaArgs {
 };
 
 struct DdaWs {   // pointers into the caller's workspace
-    uint32_t* ubits;   // [Aa+4]: sorted atom bounds U[0] = 0, U[1..Ap], then ~0
+    uint32_t* ubits;   // [Aa+4]: distinct sorted bounds U[0] = 0, U[1..Dp], then ~0
     int32_t* rank;     // [A]: atom where cell c of candidate j starts (j*M + c-1)
-    uint32_t* meta;    // afin = Ap (the top atom), Ap (number of bounds)
+    uint32_t* meta;    // the top atom Dp (number of distinct bounds), twice
     uint64_t* rows;    // [nblk][Aa+1] per block: count << 44 | significand sum
     double* pscal;     // [nblk][4]: sum x^2, top-atom sum |x|, top count, flags
     uint64_t* rcnt;    // [nslice][Aa+1] sliced sums (k_dda_reduce)
@@ -216,6 +220,13 @@ __host__ __device__ inline float set_mid(int c, int k) {
     return 0.5f * (set_value(c - 1, k) + set_value(c, k));
 }
 
+// Median of three (v_med3_u32): x clamped to [lo, hi] when lo <= hi.
+__device__ __forceinline__ uint32_t med3_u32(uint32_t x, uint32_t lo, uint32_t hi) {
+    uint32_t r;
+    asm("v_med3_u32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "v"(hi));
+    return r;
+}
+
 __device__ __forceinline__ bool alpha_ok(float a) { return a > 0.0f && a < __builtin_inff(); }
 
 __device__ __forceinline__ bool reaches(uint32_t xbits, float alpha, float mu) {
@@ -244,23 +255,27 @@ __device__ uint32_t threshold_bits(float alpha, float mu) {
     return hi;
 }
 
-__host__ __device__ static inline int hist_lbins(int A) {
-    return A <= 960 ? 13 : (A <= 4096 ? 12 : 10);
+// Bins of the pass: more bins make crowded bins (two or more bounds, a walk)
+// rarer but cost set-up time, which dominates for small inputs.
+static inline int hist_lbins(int A, bool large) {
+    if (A <= 960) return large ? 13 : 12;
+    if (A <= 4096) return large ? 13 : 12;
+    return 11;
 }
 // Dynamic LDS of k_dda_hist:
-//   ENT  uint4[nbins]  bin entries; during the set-up its start holds the bin
+//   ENT  uint2[nbins]  bin entries; during the set-up its start holds the bin
 //                      counts u32[nbins] (first atom | count << 16)
 //   U    u32[Aa + 4]   sorted atom bounds, padded with ~0
 //   TH   u32[A]        thresholds, then the atom where each cell starts
 //   KH   u64[Aa + 65]  (bound << 32 | id) bucket keys, then the packed histogram
-//                      (atoms 0 .. Ap, then one spare cell per lane)
+//                      (atoms 0 .. Dp, then one spare cell per lane)
 struct HistLds {
     size_t u, th, kh, total;
 };
-__host__ __device__ static inline HistLds hist_lds(int A) {
+__host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
     HistLds h;
     const size_t Aa = (size_t)A + kMaxSplits;
-    h.u = (size_t)16 << hist_lbins(A);
+    h.u = (size_t)8 << lbins;
     h.th = h.u + align16(sizeof(uint32_t) * (Aa + 4));
     h.kh = h.th + align16(sizeof(uint32_t) * (size_t)A);
     h.total = h.kh + sizeof(uint64_t) * (Aa + 1 + 64);   // + one spare cell per lane
@@ -273,8 +288,8 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int nbins = 1 << a.lbins;
-    const HistLds hl = hist_lds(A);
-    uint4* ENT = (uint4*)smem;
+    const HistLds hl = hist_lds(A, a.lbins);
+    uint2* ENT = (uint2*)smem;
     uint32_t* binc = (uint32_t*)smem;
     uint32_t* U = (uint32_t*)(smem + hl.u);
     uint32_t* TH = (uint32_t*)(smem + hl.th);
@@ -391,41 +406,39 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     lds_barrier();
 
     // ---- 3. first atom of every bin: exclusive scan of the counts, P bins per thread
-    const int P = nbins / kHistThreads;   // 8, 4 or 1
+    const int P = nbins / kHistThreads;   // 16, 8, 4 or 2 bins per thread
     {
-        uint32_t cnt[8];
+        uint32_t cnt[16];
         uint4* b4 = (uint4*)binc;
-        if (P == 8) {
-            const uint4 u0 = b4[2 * tid], u1 = b4[2 * tid + 1];
-            cnt[0] = u0.x; cnt[1] = u0.y; cnt[2] = u0.z; cnt[3] = u0.w;
-            cnt[4] = u1.x; cnt[5] = u1.y; cnt[6] = u1.z; cnt[7] = u1.w;
-        } else if (P == 4) {
-            const uint4 u0 = b4[tid];
-            cnt[0] = u0.x; cnt[1] = u0.y; cnt[2] = u0.z; cnt[3] = u0.w;
-            cnt[4] = cnt[5] = cnt[6] = cnt[7] = 0u;
-        } else {
-            cnt[0] = binc[tid];
-            cnt[1] = cnt[2] = cnt[3] = cnt[4] = cnt[5] = cnt[6] = cnt[7] = 0u;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            if (4 * q < P && P >= 4) {
+                const uint4 u = b4[tid * (P / 4) + q];
+                cnt[4 * q] = u.x; cnt[4 * q + 1] = u.y; cnt[4 * q + 2] = u.z; cnt[4 * q + 3] = u.w;
+            } else {
+                cnt[4 * q] = cnt[4 * q + 1] = cnt[4 * q + 2] = cnt[4 * q + 3] = 0u;
+            }
+        }
+        if (P == 2) {
+            const uint2 u = ((const uint2*)binc)[tid];
+            cnt[0] = u.x; cnt[1] = u.y;
         }
         uint32_t mine = 0;
 #pragma unroll
-        for (int e = 0; e < 8; e++) mine += cnt[e];
+        for (int e = 0; e < 16; e++) mine += cnt[e];
         const uint32_t incl = wave_scan_add(mine);
         if (lane == 63) s_u[3][wid] = incl;
         lds_barrier();
         uint32_t run = incl - mine;
         for (int v = 0; v < wid; v++) run += s_u[3][v];
-        uint32_t st[8];                         // fill counter (high half) starts at 0
+        uint32_t st[16];                        // fill counter (high half) starts at 0
 #pragma unroll
-        for (int e = 0; e < 8; e++) { st[e] = run; run += cnt[e]; }
-        if (P == 8) {
-            b4[2 * tid] = make_uint4(st[0], st[1], st[2], st[3]);
-            b4[2 * tid + 1] = make_uint4(st[4], st[5], st[6], st[7]);
-        } else if (P == 4) {
-            b4[tid] = make_uint4(st[0], st[1], st[2], st[3]);
-        } else {
-            binc[tid] = st[0];
-        }
+        for (int e = 0; e < 16; e++) { st[e] = run; run += cnt[e]; }
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            if (4 * q < P && P >= 4)
+                b4[tid * (P / 4) + q] = make_uint4(st[4 * q], st[4 * q + 1], st[4 * q + 2], st[4 * q + 3]);
+        if (P == 2) ((uint2*)binc)[tid] = make_uint2(st[0], st[1]);
     }
     lds_barrier();
 
@@ -457,26 +470,81 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         U[pos + 1] = v;
         if (id < (uint32_t)A) TH[id] = pos + 1;      // atom where this cell starts
     }
-    if (tid < 4) U[tid == 0 ? 0 : Ap + (uint32_t)tid] = tid == 0 ? 0u : 0xffffffffu;
+    if (tid == 0) U[0] = 0u;
     lds_barrier();
 
-    // ---- 6. bin entries {first | flags, next three bounds}; the keys are dead:
-    //         KH becomes the histogram
+    // ---- 5b. merge equal bounds: R[i] = number of distinct values among
+    //          U[1..i] (the atom whose lower bound is U[i]); the distinct values
+    //          move to U[1..Dp] in place.  R lives where the keys were.
+    uint32_t* R = (uint32_t*)KH;                     // [Ap + 1]
+    uint32_t Dp = 0;
     {
-        uint32_t bv[8];
+        constexpr int kPerMax = (kDdaMaxThresholds + kMaxSplits + kHistThreads - 1) / kHistThreads;
+        const int per = (int)((Ap + kHistThreads - 1) / kHistThreads);
+        uint32_t uv[kPerMax], nf[kPerMax];
+        uint32_t mine = 0;
 #pragma unroll
-        for (int e = 0; e < 8; e++) bv[e] = (e < P) ? binc[tid + e * kHistThreads] : 0u;
-        for (uint32_t i = tid; i <= Ap; i += kHistThreads) hist[i] = 0ull;
-        lds_barrier();   // the counts alias the entries
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
-            if (e < P && b < nb) {
-                const uint32_t f = bv[e] & 0xffffu, n = bv[e] >> 16;
-                const uint32_t fl = (n >= 4u ? kFlagWalk : 0u) | (b == nb - 1u ? kFlagTop : 0u);
-                ENT[b] = make_uint4(f | fl, U[f + 1], U[f + 2], U[f + 3]);
+        for (int e = 0; e < kPerMax; e++) {
+            const uint32_t i = 1u + (uint32_t)(tid * per + e);
+            uv[e] = 0u;
+            nf[e] = 0u;
+            if (e < per && i <= Ap) {
+                uv[e] = U[i];
+                nf[e] = uv[e] != U[i - 1] ? 1u : 0u;
+                mine += nf[e];
             }
         }
+        const uint32_t incl = wave_scan_add(mine);
+        if (lane == 63) s_u[3][wid] = incl;
+        lds_barrier();                               // every read of U above is done
+        uint32_t run = incl - mine;
+#pragma unroll
+        for (int v = 0; v < kHistThreads / 64; v++) {
+            if (v < wid) run += s_u[3][v];
+            Dp += s_u[3][v];
+        }
+#pragma unroll
+        for (int e = 0; e < kPerMax; e++) {
+            const uint32_t i = 1u + (uint32_t)(tid * per + e);
+            if (e < per && i <= Ap) {
+                run += nf[e];
+                R[i] = run;
+                if (nf[e]) U[run] = uv[e];
+            }
+        }
+        if (tid == 0) R[0] = 0u;
+        if (tid < 3) U[Dp + 1u + (uint32_t)tid] = 0xffffffffu;
+    }
+    lds_barrier();
+
+    // ---- 6. cell starts in distinct atoms; bin entries {first | flags, next
+    //         bound}; then KH becomes the histogram
+    for (int i = tid; i < A; i += kHistThreads) {
+        const uint32_t p = TH[i];
+        TH[i] = p <= Ap ? R[p] : Dp + 1u;
+    }
+    {
+        uint32_t ef[16], ey[16];
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            ef[e] = 0u;
+            ey[e] = 0u;
+            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
+            if (e < P && b < nb) {
+                const uint32_t bv = binc[b];
+                const uint32_t o = bv & 0xffffu, n = bv >> 16;
+                const uint32_t f = R[o], nd = R[o + n] - f;   // distinct bounds inside
+                ef[e] = f | (nd >= 2u ? kFlagWalk : 0u) | (b == nb - 1u ? kFlagTop : 0u);
+                ey[e] = U[f + 1];
+            }
+        }
+        lds_barrier();   // the counts alias the entries; R aliases the histogram
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
+            if (e < P && b < nb) ENT[b] = make_uint2(ef[e], ey[e]);
+        }
+        for (uint32_t i = tid; i <= Dp; i += kHistThreads) hist[i] = 0ull;
     }
     lds_barrier();
 
@@ -484,25 +552,25 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     double ss0 = 0.0, ss1 = 0.0, top_s1 = 0.0;
     uint32_t top_cnt = 0, flags = 0;
     constexpr int E = 8;
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    typedef const __attribute__((address_space(3))) u32x4 lds_u32x4;
-    // LDS byte address of the entry of bin (v >> shift) is (v >> shift) * 16 + ent_b
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    typedef const __attribute__((address_space(3))) u32x2 lds_u32x2;
+    // LDS byte address of the entry of bin (v >> shift) is (v >> shift) * 8 + ent_b
     // (unsigned wrap-around), with the bin clamped to [base, base + nb - 1]
-    const uint32_t ent_b = (uint32_t)(uintptr_t)(lds_u32x4*)(u32x4*)ENT - (base << 4);
+    const uint32_t ent_b = (uint32_t)(uintptr_t)(lds_u32x2*)(u32x2*)ENT - (base << 3);
     const uint32_t bhi = base + nb - 1u;
     // lanes whose value lies in atom 0 (q = 0 for every candidate) add into a
     // cell of their own, so that ReLU zeros never pile up on one LDS address
     const uint32_t spare = (uint32_t)a.Aa + 1u + (uint32_t)lane;
     auto visit = [&](const uint32_t* xb) {
         uint32_t ab[E], t[E], fx[E];
-        u32x4 en[E];
+        u32x2 en[E];
 #pragma unroll
         for (int e = 0; e < E; e++) ab[e] = xb[e] & 0x7fffffffu;
         // every entry read in flight before the first is used
 #pragma unroll
         for (int e = 0; e < E; e++) {
-            const uint32_t bi = min(max(ab[e] >> shift, base), bhi);
-            en[e] = *(lds_u32x4*)(uintptr_t)((bi << 4) + ent_b);
+            const uint32_t bi = med3_u32(ab[e] >> shift, base, bhi);
+            en[e] = *(lds_u32x2*)(uintptr_t)((bi << 3) + ent_b);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -513,8 +581,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         uint32_t any = 0;
 #pragma unroll
         for (int e = 0; e < E; e++) {
-            t[e] = en[e].x + (ab[e] >= en[e].y ? 1u : 0u) + (ab[e] >= en[e].z ? 1u : 0u) +
-                   (ab[e] >= en[e].w ? 1u : 0u);
+            t[e] = en[e].x + (ab[e] >= en[e].y ? 1u : 0u);
             fx[e] = en[e].x;
             any |= en[e].x;
         }
@@ -562,16 +629,16 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
 
     // ---- 8. the block's row, its scalars; block 0 also publishes the tables
     uint64_t* row = w.rows + (int64_t)blockIdx.x * (a.Aa + 1);
-    for (uint32_t i = tid; i <= Ap; i += kHistThreads) row[i] = hist[i];
+    for (uint32_t i = tid; i <= Dp; i += kHistThreads) row[i] = hist[i];
     {
         const double ss = wave_scan_add(ss0 + ss1), t1 = wave_scan_add(top_s1);
         const uint32_t tc = wave_scan_add(top_cnt), fl = wave_scan_or(flags);
         if (lane == 63) { s_d[0][wid] = ss; s_d[1][wid] = t1; s_u[0][wid] = tc; s_u[1][wid] = fl; }
     }
     if (blockIdx.x == 0) {
-        for (uint32_t i = tid; i <= Ap + 3u; i += kHistThreads) w.ubits[i] = U[i];
+        for (uint32_t i = tid; i <= Dp + 3u; i += kHistThreads) w.ubits[i] = U[i];
         for (int i = tid; i < A; i += kHistThreads) w.rank[i] = (int32_t)TH[i];
-        if (tid == 0) { w.meta[0] = Ap; w.meta[1] = Ap; }
+        if (tid == 0) { w.meta[0] = Dp; w.meta[1] = Dp; }
     }
     lds_barrier();
     if (tid == 0) {
@@ -783,8 +850,8 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
     DdaArgs a;
     a.G = G; a.M = L.M; a.A = L.A; a.Aa = L.A + kMaxSplits;
     a.n = f.n; a.k = f.k;
-    a.lbins = hist_lbins(L.A);
     dda_blocks(len, &a.nblk, &a.rows_pb);
+    a.lbins = hist_lbins(L.A, a.rows_pb >= 8);
     a.nslice = a.nblk > kPackedMaxBlocks ? kReduceSlices : 0;
     a.rk_lds = 0;
     const DdaWs w = ws_ptrs(ws, L);
@@ -799,7 +866,7 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
         if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
-    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A).total, s>>>(x, len, grid, a, w);
+    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A, a.lbins).total, s>>>(x, len, grid, a, w);
     if (a.nslice > 0) {
         dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
         k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
