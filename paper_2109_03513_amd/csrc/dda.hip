@@ -696,10 +696,27 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
     __shared__ float s_q[128];
     __shared__ float s_grid[kDdaMaxG];
 
-    // ---- 1. every global read is requested before any is used: the candidate
-    //         scales, the block scalars, the bounds of this thread's atoms (the
-    //         contiguous range of step 3), the cell starts
+    // ---- 1. every global read is requested before any is used: the row
+    //         entries of this thread's first atom, the candidate scales, the
+    //         block scalars, the bounds of this thread's atoms (the contiguous
+    //         range of step 3), the cell starts
     const uint32_t afin = w.meta[0];
+    const bool sliced = a.nslice > 0;
+    static_assert(2 * kReduceSlices <= kPackedMaxBlocks, "slice counts and sums share rv");
+    uint64_t rv[kPackedMaxBlocks];     // packed rows, or the slice counts then sums
+    if (tid < S) {
+        if (sliced) {
+#pragma unroll
+            for (int r = 0; r < kReduceSlices; r++) {
+                rv[r] = w.rcnt[(int64_t)r * S + tid];
+                rv[kReduceSlices + r] = w.rsum[(int64_t)r * S + tid];
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < kPackedMaxBlocks; r++)
+                rv[r] = r < a.nblk ? w.rows[(int64_t)r * S + tid] : 0ull;
+        }
+    }
     for (int j = tid; j < G; j += kFinThreads) s_grid[j] = grid[j];
     constexpr int kPerMax = 9;                       // atoms per thread, (Aa+2)/1024 <= 9
     const int per = (NA + kFinThreads - 1) / kFinThreads;
@@ -721,9 +738,21 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
 
     // ---- 2. per-atom integer sums over the packed rows or the slices, one
     //         thread per atom (coalesced across threads)
-    for (int at = tid; at < S; at += kFinThreads) {
+    if (tid < S) {
         uint64_t c = 0, t = 0;
-        if (a.nslice > 0) {
+        if (sliced) {
+#pragma unroll
+            for (int r = 0; r < kReduceSlices; r++) { c += rv[r]; t += rv[kReduceSlices + r]; }
+        } else {
+#pragma unroll
+            for (int r = 0; r < kPackedMaxBlocks; r++) { c += rv[r] >> 44; t += rv[r] & kSumMask; }
+        }
+        C0[tid] = c;
+        C1[tid] = t;
+    }
+    for (int at = tid + kFinThreads; at < S; at += kFinThreads) {
+        uint64_t c = 0, t = 0;
+        if (sliced) {
 #pragma unroll 8
             for (int r = 0; r < a.nslice; r++) {
                 c += w.rcnt[(int64_t)r * S + at];
