@@ -267,18 +267,21 @@ static inline int hist_lbins(int A, bool large) {
 //                      counts u32[nbins] (first atom | count << 16)
 //   U    u32[Aa + 4]   sorted atom bounds, padded with ~0
 //   TH   u32[A]        thresholds, then the atom where each cell starts
-//   KH   u64[Aa + 65]  (bound << 32 | id) bucket keys, then the packed histogram
-//                      (atoms 0 .. Dp, then one spare cell per lane)
+//   KH   u64[C(Aa+1)+64] (bound << 32 | id) bucket keys, then the packed
+//                      histogram: C interleaved copies (cell C*atom + lane % C,
+//                      so that lanes on one dense atom add into different
+//                      banks), then one spare cell per lane
 struct HistLds {
     size_t u, th, kh, total;
 };
+__host__ __device__ static inline int hist_lcopies(int A) { return A <= 960 ? 2 : 0; }
 __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
     HistLds h;
     const size_t Aa = (size_t)A + kMaxSplits;
     h.u = (size_t)8 << lbins;
     h.th = h.u + align16(sizeof(uint32_t) * (Aa + 4));
     h.kh = h.th + align16(sizeof(uint32_t) * (size_t)A);
-    h.total = h.kh + sizeof(uint64_t) * (Aa + 1 + 64);   // + one spare cell per lane
+    h.total = h.kh + sizeof(uint64_t) * (((Aa + 1) << hist_lcopies(A)) + 64);
     return h;
 }
 
@@ -288,6 +291,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int nbins = 1 << a.lbins;
+    const uint32_t lcop = (uint32_t)hist_lcopies(A);   // log2 of the histogram copies
     const HistLds hl = hist_lds(A, a.lbins);
     uint2* ENT = (uint2*)smem;
     uint32_t* binc = (uint32_t*)smem;
@@ -544,7 +548,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
             const uint32_t b = (uint32_t)(tid + e * kHistThreads);
             if (e < P && b < nb) ENT[b] = make_uint2(ef[e], ey[e]);
         }
-        for (uint32_t i = tid; i <= Dp; i += kHistThreads) hist[i] = 0ull;
+        for (uint32_t i = tid; i < ((Dp + 1u) << lcop); i += kHistThreads) hist[i] = 0ull;
     }
     lds_barrier();
 
@@ -560,7 +564,8 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     const uint32_t bhi = base + nb - 1u;
     // lanes whose value lies in atom 0 (q = 0 for every candidate) add into a
     // cell of their own, so that ReLU zeros never pile up on one LDS address
-    const uint32_t spare = (uint32_t)a.Aa + 1u + (uint32_t)lane;
+    const uint32_t spare = (((uint32_t)a.Aa + 1u) << lcop) + (uint32_t)lane;
+    const uint32_t copy = (uint32_t)lane & ((1u << lcop) - 1u);
     auto visit = [&](const uint32_t* xb) {
         uint32_t ab[E], t[E], fx[E];
         u32x2 en[E];
@@ -603,7 +608,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         }
 #pragma unroll
         for (int e = 0; e < E; e++) {
-            const uint32_t at = t[e] != 0u ? t[e] : spare;
+            const uint32_t at = t[e] != 0u ? (t[e] << lcop) + copy : spare;
             atomicAdd(&hist[at], (1ull << 44) | (uint64_t)(ab[e] & 0x7fffffu));
         }
     };
@@ -629,7 +634,11 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
 
     // ---- 8. the block's row, its scalars; block 0 also publishes the tables
     uint64_t* row = w.rows + (int64_t)blockIdx.x * (a.Aa + 1);
-    for (uint32_t i = tid; i <= Dp; i += kHistThreads) row[i] = hist[i];
+    for (uint32_t i = tid; i <= Dp; i += kHistThreads) {
+        uint64_t v = 0;
+        for (uint32_t c = 0; c < (1u << lcop); c++) v += hist[(i << lcop) + c];   // fields stay apart
+        row[i] = v;
+    }
     {
         const double ss = wave_scan_add(ss0 + ss1), t1 = wave_scan_add(top_s1);
         const uint32_t tc = wave_scan_add(top_cnt), fl = wave_scan_or(flags);
