@@ -91,7 +91,6 @@ def main():
     ops = 2.0 * M * Ncol * Kred
 
     stream = torch.cuda.Stream()      # default priority
-    side = torch.cuda.Stream()        # default priority: second branch of the step
     sh = stream.cuda_stream
     dev = "cuda"
     aw = torch.empty(1, dtype=torch.float32, device=dev)
@@ -119,21 +118,12 @@ def main():
             esb.esb_conv2d(cx, n, ks, ax, cw, n, ks, aw, stride=c["stride"], pad=c["pad"], y=y,
                            want_acc=False, stream=st)
 
-    # The weight branch (DDA, projection) and the activation branch are
-    # independent: they run on two streams, joined before the convolution.
-    fork = torch.cuda.Event()
-    join = torch.cuda.Event()
-
+    # One chain on one stream: a HIP graph with the weight and activation
+    # branches on two streams ran them one after the other anyway and paid for
+    # the fork and join (measured 70.3 us per step against 58.7 us chained).
     def step():
-        fork.record(stream)
-        side.wait_event(fork)
-        run_stage(0)
-        run_stage(2)
-        run_stage(1, side.cuda_stream)
-        run_stage(3, side.cuda_stream)
-        join.record(side)
-        stream.wait_event(join)
-        run_stage(4)
+        for i in (0, 2, 1, 3, 4):
+            run_stage(i)
 
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):       # eager warm-up: first-call set-up happens here
@@ -203,8 +193,8 @@ def main():
         "conv_frac_int8_peak": round(ops / (conv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 6),
         "project_x_gbps": round(5.0 * nel_x / (stage_ms[3] * 1e-3) / 1e9, 2),
         "dda_x_gbps": round(4.0 * nel_x / (stage_ms[1] * 1e-3) / 1e9, 2),
-        "timing": "whole step replayed as one HIP graph (weight and activation branches on two "
-                  "streams, joined before the conv); launch groups as graphs of 20 copies",
+        "timing": "whole step replayed as one HIP graph (one stream: DDA(w), project(w), DDA(x), "
+                  "project(x), conv2d); launch groups as graphs of 20 copies",
     }
 
     cpu = None
@@ -217,7 +207,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
         "config": {"workload": c["name"] + "_esb4k2_dda64",
-                   "note": "[DDA(w), project(w)] || [DDA(x), project(x)] -> conv2d per step"},
+                   "note": "DDA(w), project(w), DDA(x), project(x), conv2d per step"},
         "roofline": roof, "cpu_baseline": cpu, "detail": extra,
     }
     print(json.dumps(rec), flush=True)
