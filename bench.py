@@ -309,9 +309,15 @@ def sweep(args):
             B = torch.randint(0, 256, (N, K), dtype=torch.uint8, device=dev)
             a = torch.tensor([0.5], device=dev)
             y = torch.empty((M, N), dtype=torch.float32, device=dev)
+            ws = torch.empty(max(esb.esb_gemm_workspace_size(M, N, K, fa[0], fa[1], fb[0], fb[1]), 1),
+                             dtype=torch.uint8, device=dev)
+            ms0 = time_launches(lambda: esb.esb_gemm(A, fa[0], fa[1], a, B, fb[0], fb[1], a, y=y,
+                                                     want_acc=False, stream=sh), args.reps, stream)
             ms = time_launches(lambda: esb.esb_gemm(A, fa[0], fa[1], a, B, fb[0], fb[1], a, y=y,
-                                                    want_acc=False, stream=sh), args.reps, stream)
-            emit("gemm_" + name, ms, nbytes=float(M * K + N * K + 4 * M * N), ops=2.0 * M * N * K)
+                                                    want_acc=False, stream=sh, workspace=ws),
+                               args.reps, stream)
+            emit("gemm_" + name, ms, nbytes=float(M * K + N * K + 4 * M * N), ops=2.0 * M * N * K,
+                 ms_without_workspace=round(ms0, 5))
     if want("conv"):
         cases = [("resnet18_conv1_b64", 64, 224, 224, 3, 64, 7, 2, 3, 1),
                  ("resnet18_l1_3x3_b64", 64, 56, 56, 64, 64, 3, 1, 1, 1),
@@ -327,12 +333,20 @@ def sweep(args):
             P, Q = esb.conv_out_hw(H, W, R, R, (st, st), (pd, pd))
             y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
             a = torch.tensor([0.5], device=dev)
+            ws = torch.empty(max(esb.esb_conv2d_workspace_size(xc.shape, wc.shape, 5, 3, 5, 3,
+                                                                stride=(st, st), pad=(pd, pd),
+                                                                groups=groups), 1),
+                             dtype=torch.uint8, device=dev)
+            ms0 = time_launches(lambda: esb.esb_conv2d(xc, 5, 3, a, wc, 5, 3, a, stride=(st, st),
+                                                       pad=(pd, pd), groups=groups, y=y,
+                                                       want_acc=False, stream=sh), args.reps, stream)
             ms = time_launches(lambda: esb.esb_conv2d(xc, 5, 3, a, wc, 5, 3, a, stride=(st, st),
                                                       pad=(pd, pd), groups=groups, y=y,
-                                                      want_acc=False, stream=sh), args.reps, stream)
+                                                      want_acc=False, stream=sh, workspace=ws),
+                               args.reps, stream)
             ops = 2.0 * Nb * P * Q * K * R * R * (C // groups)
             nbytes = float(xc.numel() + wc.numel() + 4 * y.numel())
-            emit("conv_" + name, ms, nbytes=nbytes, ops=ops)
+            emit("conv_" + name, ms, nbytes=nbytes, ops=ops, ms_without_workspace=round(ms0, 5))
 
 
 def resnet18_bench(args):

@@ -140,6 +140,29 @@ int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_
              const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
              void* stream);
 
+/*
+ * Bytes of device workspace that esb_gemm_ws may use to decode both operands
+ * once ahead of the contraction (0 when the formats do not take that path: it
+ * applies to pairs of formats whose values are exact in OCP E4M3 and whose
+ * products and partial sums over K stay exact in the fp32 accumulation of the
+ * fp8 matrix cores).  Deterministic in its arguments.
+ */
+size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig);
+
+/*
+ * esb_gemm with a caller workspace (device, at least esb_gemm_workspace_size()
+ * bytes, or NULL).  Results are bit-identical to esb_gemm.  For shapes with
+ * enough work per operand byte the codes of A and B are first decoded to E4M3
+ * into the workspace (one extra pass, 1 byte read and written per code) and the
+ * contraction reads the decoded bytes; otherwise the workspace is unused.
+ * ESB_E_WORKSPACE if workspace is non-NULL and ws_bytes is too small.  The
+ * workspace carries nothing between calls; concurrent calls need distinct ones.
+ */
+int esb_gemm_ws(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+                const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+                void* workspace, size_t ws_bytes, void* stream);
+
 /* Convolution geometry.  Output P = (H + 2*pad_h - R)/stride_h + 1, Q likewise. */
 typedef struct esb_conv_desc {
     int N, H, W, C;          /* input batch, height, width, channels (NHWC) */
@@ -162,6 +185,19 @@ typedef struct esb_conv_desc {
 int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
                const float* alphaX, const uint8_t* w, int nW, int kW_sig,
                const float* alphaW, int32_t* acc, float* y, void* stream);
+
+/*
+ * Workspace bytes for esb_conv2d_ws (0 when unused: depthwise convolutions and
+ * formats outside the E4M3 path).  The decoded activations keep the NHWC
+ * layout and the decoded filters the KRSC layout.
+ */
+size_t esb_conv2d_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int nW, int kW_sig);
+
+/* esb_conv2d with a caller workspace; same contract as esb_gemm_ws. */
+int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+                  const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+                  const float* alphaW, int32_t* acc, float* y, void* workspace,
+                  size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -144,9 +144,18 @@ static int contraction_contract(int64_t kred, const Fmt& a, const Fmt& b) {
     return ESB_OK;
 }
 
-int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
-             const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
-             const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc, void* stream) {
+// Decoding both operands once ahead of the contraction pays when the work per
+// decoded byte is high: then the decode pass (1 byte read and written per code)
+// is small next to a contraction that no longer decodes in its inner loop.
+static bool pre_worth(int64_t M, int64_t N, int64_t K, int64_t a_elems, int64_t b_elems) {
+    const double ops = 2.0 * (double)M * (double)N * (double)K;
+    return ops >= 1500.0 * (double)(a_elems + b_elems);
+}
+
+static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                     const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+                     const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+                     void* ws, size_t ws_bytes, void* stream) {
     if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig)) return ESB_E_INVALID;
     if (M < 0 || N < 0 || K < 0 || (b_layout != ESB_B_NK && b_layout != ESB_B_KN)) return ESB_E_INVALID;
     if (!acc && !y) return ESB_E_INVALID;
@@ -156,25 +165,49 @@ int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_
     const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
     const int st = contraction_contract(K, fa, fb);
     if (st) return st;
+    if (ws && ws_bytes < esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig)) return ESB_E_WORKSPACE;
     if (M == 0 || N == 0) return ESB_OK;
     ConvGeom g;
     g.Nb = M; g.H = 1; g.W = 1; g.C = K; g.pitch = (int)(lda > 0x7fffffff ? 0x7fffffff : lda);
     g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
     if (lda > 0x7fffffff) return ESB_E_INVALID;
     const int op = mma_choose(fa, fb, K);
-    if (op >= 0 && mma_fits(g, A, K, 1, B, ldb, b_layout))
+    const hipStream_t s = (hipStream_t)stream;
+    if (op >= 0 && mma_fits(g, A, K, 1, B, ldb, b_layout)) {
+        if (ws && op == 1 && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
+            return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb,
+                                             alphaB, acc, y, ldc, ws, s));
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
-                                     ldc, (hipStream_t)stream));
+                                     ldc, s));
+    }
     return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
-                                         decode_info(fb), alphaB, acc, y, ldc, N, (hipStream_t)stream));
+                                         decode_info(fb), alphaB, acc, y, ldc, N, s));
 }
 
-int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
-               const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
-               void* stream) {
-    if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return ESB_E_INVALID;
-    if (!acc && !y) return ESB_E_INVALID;
-    if (y && (!alphaX || !alphaW)) return ESB_E_INVALID;
+size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig) {
+    if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig) || M < 0 || N < 0 || K < 0) return 0;
+    if (mma_choose(make_fmt(nA, kA_sig), make_fmt(nB, kB_sig), K) != 1) return 0;
+    return mma_pre_workspace(M, K, N, K);
+}
+
+int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+             const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+             const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc, void* stream) {
+    return gemm_impl(M, N, K, A, lda, nA, kA_sig, alphaA, B, ldb, nB, kB_sig, alphaB, b_layout, acc, y,
+                     ldc, nullptr, 0, stream);
+}
+
+int esb_gemm_ws(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+                const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+                void* workspace, size_t ws_bytes, void* stream) {
+    return gemm_impl(M, N, K, A, lda, nA, kA_sig, alphaA, B, ldb, nB, kB_sig, alphaB, b_layout, acc, y,
+                     ldc, workspace, ws_bytes, stream);
+}
+
+// Checked geometry of a convolution descriptor (ESB_OK or ESB_E_INVALID).
+static int conv_geom(const esb_conv_desc* d, ConvGeom* g, int64_t* Mrows, int64_t* kred) {
+    if (!d) return ESB_E_INVALID;
     if (d->N < 0 || d->H < 1 || d->W < 1 || d->C < 1 || d->K < 1 || d->R < 1 || d->S < 1 ||
         d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0 || d->groups < 1 ||
         d->C % d->groups || d->K % d->groups)
@@ -182,30 +215,75 @@ int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, con
     if ((int64_t)d->H + 2 * d->pad_h < d->R || (int64_t)d->W + 2 * d->pad_w < d->S) return ESB_E_INVALID;
     const int P = (d->H + 2 * d->pad_h - d->R) / d->stride_h + 1;
     const int Q = (d->W + 2 * d->pad_w - d->S) / d->stride_w + 1;
-    const int64_t Mrows = (int64_t)d->N * P * Q;
-    if (Mrows > 0x7fffffff) return ESB_E_INVALID;
-    const int Cg = d->C / d->groups, Kg = d->K / d->groups;
-    const int64_t kred = (int64_t)d->R * d->S * Cg;
-    if (kred > 0x7fffffff) return ESB_E_INVALID;
+    *Mrows = (int64_t)d->N * P * Q;
+    if (*Mrows > 0x7fffffff) return ESB_E_INVALID;
+    const int Cg = d->C / d->groups;
+    *kred = (int64_t)d->R * d->S * Cg;
+    if (*kred > 0x7fffffff) return ESB_E_INVALID;
+    g->Nb = d->N; g->H = d->H; g->W = d->W; g->C = d->C; g->pitch = d->C; g->Cg = Cg;
+    g->R = d->R; g->S = d->S; g->sh = d->stride_h; g->sw = d->stride_w; g->ph = d->pad_h; g->pw = d->pad_w;
+    g->P = P; g->Q = Q;
+    return ESB_OK;
+}
+
+static bool conv_is_depthwise(const esb_conv_desc* d) {
+    return d->C / d->groups == 1 && d->K / d->groups == 1 && (int64_t)d->C * d->R * d->S <= 16384;
+}
+
+static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
+                     const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
+                     void* ws, size_t ws_bytes, void* stream) {
+    if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return ESB_E_INVALID;
+    if (!acc && !y) return ESB_E_INVALID;
+    if (y && (!alphaX || !alphaW)) return ESB_E_INVALID;
+    ConvGeom g;
+    int64_t Mrows = 0, kred = 0;
+    if (conv_geom(d, &g, &Mrows, &kred) != ESB_OK) return ESB_E_INVALID;
+    const int Kg = d->K / d->groups;
     if (Mrows > 0 && (!x || !w)) return ESB_E_INVALID;
     const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
     const int st = contraction_contract(kred, fx, fw);
     if (st) return st;
+    if (ws && ws_bytes < esb_conv2d_workspace_size(d, nX, kX_sig, nW, kW_sig)) return ESB_E_WORKSPACE;
     if (Mrows == 0) return ESB_OK;
-    ConvGeom g;
-    g.Nb = d->N; g.H = d->H; g.W = d->W; g.C = d->C; g.pitch = d->C; g.Cg = Cg;
-    g.R = d->R; g.S = d->S; g.sh = d->stride_h; g.sw = d->stride_w; g.ph = d->pad_h; g.pw = d->pad_w;
-    g.P = P; g.Q = Q;
     const hipStream_t s = (hipStream_t)stream;
-    if (Cg == 1 && Kg == 1 && (int64_t)d->C * d->R * d->S <= 16384)
+    if (conv_is_depthwise(d))
         return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
     const int op = mma_choose(fx, fw, kred);
-    if (op >= 0 && mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK))
+    if (op >= 0 && mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK)) {
+        const int64_t xel = (int64_t)d->N * d->H * d->W * d->C, wel = (int64_t)d->K * kred;
+        if (ws && op == 1 && pre_worth(Mrows, d->K, kred, xel, wel))
+            return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
+                                             (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w,
+                                             d->K, kred, fw, alphaW, acc, y, d->K, ws, s));
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
                                      kred, fw, alphaW, acc, y, d->K, s));
+    }
     return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
                                          alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
                                          d->K, Kg, s));
+}
+
+size_t esb_conv2d_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int nW, int kW_sig) {
+    if (!valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return 0;
+    ConvGeom g;
+    int64_t Mrows = 0, kred = 0;
+    if (conv_geom(d, &g, &Mrows, &kred) != ESB_OK || conv_is_depthwise(d)) return 0;
+    if (mma_choose(make_fmt(nX, kX_sig), make_fmt(nW, kW_sig), kred) != 1) return 0;
+    return mma_pre_workspace((int64_t)d->N * d->H * d->W, d->C, d->K, kred);
+}
+
+int esb_conv2d(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
+               const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
+               void* stream) {
+    return conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, acc, y, nullptr, 0, stream);
+}
+
+int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
+                  const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
+                  void* workspace, size_t ws_bytes, void* stream) {
+    return conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, acc, y, workspace, ws_bytes,
+                     stream);
 }
 
 }  // extern "C"

@@ -98,6 +98,17 @@ hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& g
                       int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
                       int64_t ldc, hipStream_t s);
 
+// The same contraction (op 1 formats) with both operands first decoded once to
+// E4M3 into a workspace of mma_pre_workspace() bytes; A is a_rows rows of a_cols
+// codes with pitch a_pitch (GEMM: M x K; convolution: the N*H*W pixels of C
+// channels), B is b_rows rows of K codes with pitch ldb.
+size_t mma_pre_workspace(int64_t a_rows, int64_t a_cols, int64_t b_rows, int64_t K);
+hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, const uint8_t* A,
+                          int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
+                          const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
+                          const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
+                          void* ws, hipStream_t s);
+
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,

@@ -60,6 +60,7 @@ struct FastParams {
     int kA, kB;
     int zrowA, zrowB;       // rows of kZeroRows holding each operand's +0 code
 };
+constexpr int kZeroRowE4M3 = 7 * 8;
 
 __device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
     const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;   // exponent + 1 (mod 2^ebits)
@@ -84,7 +85,7 @@ __device__ __forceinline__ uint4 dec16(uint4 v, const MmaDecode& d) {
 // source of every chunk that lies outside the operand (padding, ragged edges,
 // the reduction tail), so that loads need no branches.
 struct ZeroRows {
-    uint8_t b[7 * 8][16];
+    uint8_t b[7 * 8 + 1][16];   // the last row: 0x00 bytes, +0 of OCP E4M3
 };
 constexpr ZeroRows make_zero_rows() {
     ZeroRows z{};
@@ -404,6 +405,209 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
             }
 }
 
+// ------------------------------------------------------ pre-decoded operands
+// For contractions with enough work per operand byte, both operands are
+// first decoded once to OCP E4M3 (the elementwise map of dec_f8) into the
+// caller's workspace; k_mma_pre then moves E4M3 bytes by DMA straight into the
+// swizzled tile that the MFMAs read, with no decode and no second pass
+// through LDS in the loop.
+struct DecodeJob {
+    const uint8_t* src;
+    int64_t rows, cols16, pitch;   // rows of cols16 16-byte chunks, row pitch in bytes
+    MmaDecode d;
+    uint8_t* dst;                  // dense rows of 16 * cols16 bytes
+};
+// Both operands in one launch: the first n0 chunks belong to job 0.
+__global__ __launch_bounds__(256) void k_decode_e4m3(DecodeJob j0, DecodeJob j1) {
+    const int64_t n0 = j0.rows * j0.cols16, n = n0 + j1.rows * j1.cols16;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
+        const bool second = t >= n0;
+        const DecodeJob& j = second ? j1 : j0;
+        const int64_t u = second ? t - n0 : t;
+        const int64_t r = u / j.cols16, c = u - r * j.cols16;
+        const uint4 v = *(const uint4*)(j.src + r * j.pitch + 16 * c);
+        *(uint4*)(j.dst + 16 * u) = make_uint4(dec_f8(v.x, j.d), dec_f8(v.y, j.d), dec_f8(v.z, j.d),
+                                               dec_f8(v.w, j.d));
+    }
+}
+
+// DMA layout: one global_load_lds of a wave writes 1 KB = 16 tile rows of 64
+// bytes; lane l lands at row 16 q + l / 4, physical chunk l % 4, which under
+// the swizzle of lds_off holds logical chunk (l % 4) ^ ((l / 16) % 4) — the same
+// for every DMA of the lane, so each lane fetches one fixed 16-byte column of
+// the reduction in every row it serves.
+template <int BM, int BN, int WGM, int WGN, int CONV, int R>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
+    constexpr int NW = WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int TI = WM / 32, TJ = WN / 32;
+    constexpr int CHA = BM / (16 * NW), CHB = BN / (16 * NW), CT = CHA + CHB;
+    static_assert(CHA * 16 * NW == BM && CHB * 16 * NW == BN, "whole DMA rows per wave");
+    constexpr int TILE = (BM + BN) * BK;
+    static_assert(R >= 2 && R <= 4, "ring depth");
+    __shared__ __align__(16) uint8_t ring[R * TILE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int tm, tn;
+    tile_of(g, tm, tn);
+    const int grp = blockIdx.z;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int wr = (wave / WGN) * WM, wc = (wave % WGN) * WN;
+    const ConvGeom& cg = g.ga;
+    const int goffA = grp * cg.Cg;
+    const int64_t brow0 = (int64_t)grp * g.N;
+    const int rsub = lane >> 2;
+    const int lc = (lane & 3) ^ ((lane >> 4) & 3);   // logical 16-byte chunk of this lane
+
+    int64_t a_off[CHA];
+    int a_ih[CHA], a_iw[CHA];
+    int arow_ok[CHA];
+    int kr = 0, ks = 0, kc = 16 * lc;
+#pragma unroll
+    for (int i = 0; i < CHA; i++) {
+        const int m = m0 + 16 * (wave + i * NW) + rsub;
+        const bool ok = m < g.M;
+        arow_ok[i] = ok;
+        if (CONV) {
+            const int mm = ok ? m : 0;
+            const int pq = cg.P * cg.Q;
+            const int img = mm / pq, rem = mm - img * pq;
+            const int p = rem / cg.Q, q = rem - p * cg.Q;
+            a_ih[i] = ok ? p * cg.sh - cg.ph : -0x40000000;
+            a_iw[i] = q * cg.sw - cg.pw;
+            a_off[i] = (((int64_t)img * cg.H + a_ih[i]) * cg.W + a_iw[i]) * cg.pitch + goffA;
+        } else {
+            a_off[i] = (int64_t)(ok ? m : 0) * cg.pitch + 16 * lc;
+        }
+    }
+    if (CONV) {
+        const int rs = kc / cg.Cg;
+        kc -= rs * cg.Cg;
+        kr = rs / cg.S;
+        ks = rs - kr * cg.S;
+    }
+    int64_t b_off[CHB];
+    int brow_ok[CHB];
+#pragma unroll
+    for (int i = 0; i < CHB; i++) {
+        const int nn = n0 + 16 * (wave + i * NW) + rsub;
+        brow_ok[i] = nn < g.N;
+        b_off[i] = (brow0 + (brow_ok[i] ? nn : 0)) * g.ldb + 16 * lc;
+    }
+    const uint8_t* z = kZeroRows.b[kZeroRowE4M3];
+
+    // the E4M3 bytes of reduction offset k0 into a ring slot (stages in order)
+    auto fetch = [&](int k0, uint8_t* slot) {
+        const bool kin = k0 + 16 * lc < g.K;
+        if (CONV) {
+            const int64_t koff = ((int64_t)kr * cg.W + ks) * cg.pitch + kc;
+#pragma unroll
+            for (int i = 0; i < CHA; i++) {
+                const int ih = a_ih[i] + kr, iw = a_iw[i] + ks;
+                const bool ok = kin && (unsigned)ih < (unsigned)cg.H && (unsigned)iw < (unsigned)cg.W;
+                dma16(ok ? g.A + a_off[i] + koff : z, slot + 1024 * (wave + i * NW));
+            }
+            kc += BK;
+            while (kc >= cg.Cg) {
+                kc -= cg.Cg;
+                if (++ks == cg.S) { ks = 0; ++kr; }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < CHA; i++)
+                dma16((kin && arow_ok[i]) ? g.A + a_off[i] + k0 : z, slot + 1024 * (wave + i * NW));
+        }
+#pragma unroll
+        for (int i = 0; i < CHB; i++)
+            dma16((kin && brow_ok[i]) ? g.B + b_off[i] + k0 : z,
+                  slot + BM * BK + 1024 * (wave + i * NW));
+    };
+
+    v16f acc[TI][TJ];
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[i][j][r] = 0.0f;
+
+    const int lr = lane & 31, lg = lane >> 5;
+    auto compute = [&](const uint8_t* d) {
+        const uint8_t* tA = d;
+        const uint8_t* tB = d + BM * BK;
+        v8i fb[TJ];
+        const int c0 = 2 * lg;
+#pragma unroll
+        for (int j = 0; j < TJ; j++) {
+            const int row = wc + 32 * j + lr;
+            const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
+            const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
+            fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
+#pragma unroll
+        for (int i = 0; i < TI; i++) {
+            const int row = wr + 32 * i + lr;
+            const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
+            const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
+            const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+            for (int j = 0; j < TJ; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[i][j], 0, 0,
+                                                                             0, 127, 0, 127);
+        }
+    };
+
+    const int KT = (g.K + BK - 1) / BK;
+    static_for<0, R - 1>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        fetch(q * BK, ring + q * TILE);
+    });
+    // stage s sits in slot s % R; at the top of stage s the fetches of stages
+    // s .. s+R-2 are in flight (CT instructions each)
+    for (int kt = 0; kt < KT; kt += R) {
+        static_for<0, R>([&](auto Q) {
+            constexpr int q = decltype(Q)::value;
+            if (kt + q < KT) {
+                vm_wait<(R - 2) * CT>();       // this thread's part of stage s landed
+                lds_barrier();                 // everyone's part landed; slot (s-1) % R is free
+                fetch((kt + q + R - 1) * BK, ring + ((q + R - 1) % R) * TILE);
+                compute(ring + q * TILE);
+            }
+        });
+    }
+
+    float s = 0.0f;
+    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int row = m0 + wr + 32 * i + 8 * (r >> 2) + 4 * lg + (r & 3);
+                const int col = n0 + wc + 32 * j + lr;
+                if (row < g.M && col < g.N) {
+                    const float fv = ldexpf(acc[i][j][r], g.out_shift);
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    if (g.acc) g.acc[o] = (int32_t)fv;
+                    if (g.y) g.y[o] = s * fv;
+                }
+            }
+}
+
+template <int BM, int BN, int WGM, int WGN, int R>
+hipError_t launch_pre_t(FastParams g, int groups, bool conv, hipStream_t s) {
+    g.tiles_m = (g.M + BM - 1) / BM;
+    g.tiles_n = (g.N + BN - 1) / BN;
+    g.ntiles = g.tiles_m * g.tiles_n;
+    dim3 grid(g.ntiles, 1, groups);
+    if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    else k_mma_pre<BM, BN, WGM, WGN, 0, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int WGM, int WGN, int OP, int R>
 hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
     const bool conv = !(g.ga.H == 1 && g.ga.W == 1 && g.ga.R == 1 && g.ga.S == 1 && g.ga.ph == 0 &&
@@ -473,6 +677,50 @@ bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const
            (uintptr_t)A % 16 == 0 && (int64_t)groups * ga.Cg <= ga.pitch && K % 16 == 0 &&
            ldb % 16 == 0 && (uintptr_t)B % 16 == 0 &&
            (int64_t)ga.Nb * ga.H * ga.W <= 0x7fffffff;
+}
+
+size_t mma_pre_workspace(int64_t a_rows, int64_t a_cols, int64_t b_rows, int64_t K) {
+    const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    return al((size_t)a_rows * (size_t)a_cols) + al((size_t)b_rows * (size_t)K);
+}
+
+hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, const uint8_t* A,
+                          int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
+                          const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
+                          const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
+                          void* ws, hipStream_t s) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    uint8_t* dA = (uint8_t*)ws;
+    uint8_t* dB = dA + (((size_t)a_rows * (size_t)a_cols + 255) & ~(size_t)255);
+    DecodeJob j0{A, a_rows, a_cols / 16, a_pitch, mma_decode(fa, 1), dA};
+    DecodeJob j1{B, b_rows, K / 16, ldb, mma_decode(fb, 1), dB};
+    const int64_t chunks = j0.rows * j0.cols16 + j1.rows * j1.cols16;
+    int64_t blocks = (chunks + 255) / 256;
+    const int64_t cap = (int64_t)num_cus() * 16;
+    if (blocks > cap) blocks = cap;
+    k_decode_e4m3<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
+    FastParams g;
+    g.M = M; g.N = N; g.K = K; g.ga = ga;
+    g.ga.pitch = (int)a_cols;
+    g.A = dA; g.B = dB; g.ldb = K;
+    g.da = mma_decode(fa, 1);
+    g.db = mma_decode(fb, 1);
+    g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.kA = fa.k; g.kB = fb.k;
+    g.out_shift = fa.k + fb.k + 12;
+    g.zrowA = g.zrowB = kZeroRowE4M3;
+    g.tiles_m = g.tiles_n = g.ntiles = 0;
+    const bool conv = !(ga.H == 1 && ga.W == 1 && ga.R == 1 && ga.S == 1 && ga.ph == 0 && ga.pw == 0 &&
+                        ga.Cg == K && groups == 1);
+    const int64_t cus = num_cus();
+    auto tiles = [&](int bm, int bn) {
+        return (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn) * groups;
+    };
+    if (N > 128 && tiles(256, 256) >= cus) return launch_pre_t<256, 256, 2, 4, 4>(g, groups, conv, s);
+    if (N > 64 && tiles(256, 128) >= cus) return launch_pre_t<256, 128, 4, 2, 4>(g, groups, conv, s);
+    if (N > 64 && tiles(128, 128) >= cus / 2) return launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, s);
+    if (tiles(128, 64) >= cus) return launch_pre_t<128, 64, 2, 2, 4>(g, groups, conv, s);
+    return launch_pre_t<64, 64, 2, 2, 4>(g, groups, conv, s);
 }
 
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,

@@ -65,6 +65,12 @@ def lib():
                                i64, P]),
             "esb_conv2d": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
                                  P]),
+            "esb_gemm_workspace_size": (sz, [i32, i32, i32, i32, i32, i32, i32]),
+            "esb_gemm_ws": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32, P,
+                                  P, i64, P, sz, P]),
+            "esb_conv2d_workspace_size": (sz, [ctypes.POINTER(ConvDesc), i32, i32, i32, i32]),
+            "esb_conv2d_ws": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
+                                    P, sz, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -166,9 +172,29 @@ def esb_dda_align(x, n, k_sig, grid, alpha_out=None, D_out=None, workspace=None,
     return alpha_out, D_out
 
 
+def esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig):
+    return int(lib().esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig))
+
+
+def esb_conv2d_workspace_size(x_shape, w_shape, nX, kX_sig, nW, kW_sig, stride=(1, 1), pad=(0, 0),
+                              groups=1):
+    Nb, H, W, C = x_shape
+    K, R, S, _ = w_shape
+    d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], groups)
+    return int(lib().esb_conv2d_workspace_size(ctypes.byref(d), nX, kX_sig, nW, kW_sig))
+
+
+def _ws(workspace):
+    """(pointer, bytes) of an optional workspace tensor."""
+    if workspace is None:
+        return None, 0
+    return _ptr(workspace), workspace.numel() * workspace.element_size()
+
+
 def esb_gemm(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, b_layout=ESB_B_NK, acc=None, y=None,
-             want_acc=True, want_y=True, stream=None):
-    """A: M x K codes; B: N x K (ESB_B_NK) or K x N (ESB_B_KN) codes.  Returns (acc, y)."""
+             want_acc=True, want_y=True, stream=None, workspace=None):
+    """A: M x K codes; B: N x K (ESB_B_NK) or K x N (ESB_B_KN) codes.  Returns (acc, y).
+    With a workspace tensor (esb_gemm_workspace_size bytes) the call goes to esb_gemm_ws."""
     import torch
     _dev_tensor(A, torch.uint8, "A")
     _dev_tensor(B, torch.uint8, "B")
@@ -179,10 +205,17 @@ def esb_gemm(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, b_layout=ESB_B_NK, ac
         acc = torch.empty((M, N), dtype=torch.int32, device=dev)
     if y is None and want_y:
         y = torch.empty((M, N), dtype=torch.float32, device=dev)
-    _check("esb_gemm", lib().esb_gemm(M, N, K, _ptr(A), A.stride(0) if M else K, nA, kA_sig,
-                                      _ptr(alphaA), _ptr(B), B.stride(0) if B.shape[0] else 0,
-                                      nB, kB_sig, _ptr(alphaB), b_layout, _ptr(acc), _ptr(y), N,
-                                      _stream(stream)))
+    lda = A.stride(0) if M else K
+    ldb = B.stride(0) if B.shape[0] else 0
+    if workspace is None:
+        _check("esb_gemm", lib().esb_gemm(M, N, K, _ptr(A), lda, nA, kA_sig, _ptr(alphaA), _ptr(B),
+                                          ldb, nB, kB_sig, _ptr(alphaB), b_layout, _ptr(acc), _ptr(y),
+                                          N, _stream(stream)))
+    else:
+        wp, wb = _ws(workspace)
+        _check("esb_gemm_ws", lib().esb_gemm_ws(M, N, K, _ptr(A), lda, nA, kA_sig, _ptr(alphaA),
+                                                _ptr(B), ldb, nB, kB_sig, _ptr(alphaB), b_layout,
+                                                _ptr(acc), _ptr(y), N, wp, wb, _stream(stream)))
     return acc, y
 
 
@@ -191,8 +224,9 @@ def conv_out_hw(H, W, R, S, stride, pad):
 
 
 def esb_conv2d(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, stride=(1, 1), pad=(0, 0), groups=1,
-               acc=None, y=None, want_acc=True, want_y=True, stream=None):
-    """x: [N, H, W, C] codes (NHWC); w: [K, R, S, C/groups] codes (KRSC).  Returns (acc, y) NHWC."""
+               acc=None, y=None, want_acc=True, want_y=True, stream=None, workspace=None):
+    """x: [N, H, W, C] codes (NHWC); w: [K, R, S, C/groups] codes (KRSC).  Returns (acc, y) NHWC.
+    With a workspace tensor (esb_conv2d_workspace_size bytes) the call goes to esb_conv2d_ws."""
     import torch
     _dev_tensor(x, torch.uint8, "x")
     _dev_tensor(w, torch.uint8, "w")
@@ -205,7 +239,13 @@ def esb_conv2d(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, stride=(1, 1), pad=
     if y is None and want_y:
         y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
     d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], groups)
-    _check("esb_conv2d", lib().esb_conv2d(ctypes.byref(d), _ptr(x), nX, kX_sig, _ptr(alphaX),
-                                          _ptr(w), nW, kW_sig, _ptr(alphaW), _ptr(acc), _ptr(y),
-                                          _stream(stream)))
+    if workspace is None:
+        _check("esb_conv2d", lib().esb_conv2d(ctypes.byref(d), _ptr(x), nX, kX_sig, _ptr(alphaX),
+                                              _ptr(w), nW, kW_sig, _ptr(alphaW), _ptr(acc), _ptr(y),
+                                              _stream(stream)))
+    else:
+        wp, wb = _ws(workspace)
+        _check("esb_conv2d_ws", lib().esb_conv2d_ws(ctypes.byref(d), _ptr(x), nX, kX_sig,
+                                                    _ptr(alphaX), _ptr(w), nW, kW_sig, _ptr(alphaW),
+                                                    _ptr(acc), _ptr(y), wp, wb, _stream(stream)))
     return acc, y

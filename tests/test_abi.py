@@ -102,3 +102,31 @@ def test_contract_matches_oracle():
         gst = esb.lib().esb_gemm(0, 0, K, fake, K, bA, ksA, fake, fake, K, bB, ksB, fake, 0, fake,
                                  None, 0, None)
         assert gst == ost, (bA, ksA, bB, ksB, K, gst, ost)
+
+
+def test_contraction_workspace_sizes_and_errors(L):
+    """Workspace sizes of the decode-once path: nonzero exactly for pairs of formats the E4M3
+    path takes, at least both operands' bytes; a too small workspace is refused before any
+    launch (ESB_E_WORKSPACE), a NULL one falls back to the plain call."""
+    from paper_2109_03513_amd import esb
+    fake = ctypes.c_void_p(0x1000)
+    M, N, K = 300, 200, 576
+    need = L.esb_gemm_workspace_size(M, N, K, 5, 3, 5, 3)
+    assert need >= M * K + N * K
+    assert L.esb_gemm_workspace_size(M, N, K, 3, 2, 3, 1) == 0       # int8 table path
+    assert L.esb_gemm_workspace_size(M, N, K, 8, 5, 8, 5) == 0       # outside the E4M3 window
+    assert L.esb_gemm_workspace_size(M, N, K, 9, 2, 5, 3) == 0       # invalid format
+    g = L.esb_gemm_ws
+    assert g(M, N, K, fake, K, 5, 3, fake, fake, K, 5, 3, fake, 0, fake, None, N, fake, need - 1,
+             None) == -6
+    assert g(M, N, K, fake, K - 1, 5, 3, fake, fake, K, 5, 3, fake, 0, fake, None, N, fake, need,
+             None) == -1
+    d = esb.ConvDesc(64, 14, 14, 256, 256, 3, 3, 1, 1, 1, 1, 1)
+    cneed = L.esb_conv2d_workspace_size(ctypes.byref(d), 5, 3, 5, 3)
+    assert cneed >= 64 * 14 * 14 * 256 + 256 * 9 * 256
+    assert L.esb_conv2d_ws(ctypes.byref(d), fake, 5, 3, fake, fake, 5, 3, fake, fake, None, fake,
+                           cneed - 1, None) == -6
+    dw = esb.ConvDesc(32, 56, 56, 144, 144, 3, 3, 1, 1, 1, 1, 144)  # depthwise: no workspace
+    assert L.esb_conv2d_workspace_size(ctypes.byref(dw), 5, 3, 5, 3) == 0
+    assert esb.esb_conv2d_workspace_size((64, 14, 14, 256), (256, 3, 3, 256), 5, 3, 5, 3,
+                                         pad=(1, 1)) == cneed

@@ -1,0 +1,122 @@
+"""GPU contraction with a caller workspace (esb_gemm_ws, esb_conv2d_ws), where
+shapes with enough work per operand byte decode both operands once to E4M3
+ahead of the contraction: bit-exact int32 accumulators and fp32 outputs within
+1e-6 relative against the oracle, like the plain calls."""
+import numpy as np
+import pytest
+
+import oracle
+from gpuutil import assert_rel, dev, host, log, scalar, torch_cuda
+from paper_2109_03513_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+YREL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def esb():
+    from paper_2109_03513_amd import esb as e
+    e.lib()
+    return e
+
+
+def workspace(nbytes, fill=0xA5):
+    torch = torch_cuda()
+    return torch.full((max(nbytes, 1),), fill, dtype=torch.uint8, device="cuda")   # not zeroed
+
+
+def sampled_rows(M, tile):
+    r = sorted(set(list(range(0, min(M, 24))) + list(range(max(0, M - 24), M)) +
+                   list(range(tile // 2, M, tile))))
+    return np.array(r, dtype=np.int64)
+
+
+@pytest.mark.parametrize("M,N,K,fa,fb", [
+    (2049, 2050, 400, (5, 3), (5, 3)),     # decode-once path, ragged M and N
+    (4097, 4100, 208, (4, 2), (4, 2)),     # 256 x 256 tiles, ragged K within a stage
+    (1600, 1537, 1152, (5, 3), (4, 2)),    # mixed formats, 18 stages
+    (64, 64, 576, (4, 2), (4, 2)),         # too little work: the workspace is not used
+    (300, 257, 200, (3, 2), (3, 1)),       # int8 table formats: no workspace path
+])
+def test_gemm_ws_sampled(esb, M, N, K, fa, fb):
+    (bA, ksA), (bB, ksB) = fa, fb
+    A = wl.random_codes(21, (M, K), 8)
+    B = wl.random_codes(22, (N, K), 8)
+    need = esb.esb_gemm_workspace_size(M, N, K, bA, ksA, bB, ksB)
+    log("gemm_ws M=%d N=%d K=%d A=%s B=%s ws=%d" % (M, N, K, fa, fb, need))
+    ws = workspace(need)
+    acc, y = esb.esb_gemm(dev(A), bA, ksA, scalar(0.37), dev(B), bB, ksB, scalar(0.021), workspace=ws)
+    rows = sampled_rows(M, 128)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, bA, ksA, 0.37, bB, ksB, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+def test_gemm_ws_equals_plain_and_reuse(esb):
+    """Two calls through one unzeroed workspace, the second smaller, equal the plain call."""
+    for (M, N, K, seed) in [(2048, 2048, 1024, 1), (1536, 1664, 512, 2)]:
+        A = dev(wl.random_codes(seed, (M, K), 8))
+        B = dev(wl.random_codes(seed + 10, (N, K), 8))
+        need = esb.esb_gemm_workspace_size(2048, 2048, 1024, 5, 3, 5, 3)
+        ws = workspace(need) if seed == 1 else ws
+        log("gemm_ws reuse M=%d N=%d K=%d" % (M, N, K))
+        acc1, y1 = esb.esb_gemm(A, 5, 3, scalar(0.5), B, 5, 3, scalar(0.25), workspace=ws)
+        acc0, y0 = esb.esb_gemm(A, 5, 3, scalar(0.5), B, 5, 3, scalar(0.25))
+        np.testing.assert_array_equal(host(acc1), host(acc0))
+        np.testing.assert_array_equal(host(y1).view(np.uint32), host(y0).view(np.uint32))
+
+
+@pytest.mark.parametrize("case", [
+    # N, H, W, C, K, R, stride, pad
+    (8, 14, 14, 256, 256, 3, 1, 1),        # ResNet18 layer3 3x3 at batch 8
+    (4, 15, 13, 128, 320, 3, 2, 1),        # stride 2, odd sizes, ragged N tile
+    (2, 7, 7, 512, 512, 3, 1, 1),          # layer4 3x3
+])
+@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2))])
+def test_conv_ws_parity(esb, case, fmt):
+    Nb, H, W, C, K, R, st, pd = case
+    (bX, ksX), (bW, ksW) = fmt
+    x = wl.random_codes(31, (Nb, H, W, C), 8)
+    w = wl.random_codes(32, (K, R, R, C), 8)
+    need = esb.esb_conv2d_workspace_size(x.shape, w.shape, bX, ksX, bW, ksW, stride=(st, st),
+                                         pad=(pd, pd))
+    log("conv_ws %s fmt=%s ws=%d" % (case, fmt, need))
+    ws = workspace(need)
+    acc, y = esb.esb_conv2d(dev(x), bX, ksX, scalar(0.5), dev(w), bW, ksW, scalar(0.03),
+                            stride=(st, st), pad=(pd, pd), workspace=ws)
+    acc, y = host(acc), host(y)
+    for img in sorted({0, Nb - 1}):
+        s, oacc, oy = oracle.conv2d(np.ascontiguousarray(x[img:img + 1]), w, bX, ksX, 0.5, bW, ksW,
+                                    0.03, stride=(st, st), pad=(pd, pd))
+        assert s == 0
+        np.testing.assert_array_equal(acc[img:img + 1], oacc)
+        assert_rel(y[img:img + 1], oy, YREL, "y")
+
+
+def extreme_codes(b, ks, shape, seed):
+    v = oracle.valueset(b, ks)
+    top = oracle.encode(float(v[-1]), b, ks)
+    small = oracle.encode(float(v[v > 0][0]), b, ks)
+    r = np.random.default_rng(seed)
+    c = np.where(r.random(shape) < 0.8, top, small).astype(np.uint8)
+    neg = r.random(shape) < 0.3
+    return np.where(neg, c | (1 << (b - 1)), c).astype(np.uint8)
+
+
+def test_gemm_ws_product_spread_at_accumulator_bound(esb):
+    """ESB(5,2) on the decode-once path: products from 1 to 784 in one reduction and
+    K * 784 just below 2^24, where every partial sum is still exact in fp32."""
+    M, N, K = 1536, 1536, 21392
+    A = extreme_codes(5, 3, (M, K), 3)
+    B = extreme_codes(5, 3, (N, K), 4)
+    need = esb.esb_gemm_workspace_size(M, N, K, 5, 3, 5, 3)
+    assert need > 0
+    log("gemm_ws spread M=%d N=%d K=%d" % (M, N, K))
+    acc, y = esb.esb_gemm(dev(A), 5, 3, scalar(0.37), dev(B), 5, 3, scalar(0.021),
+                          workspace=workspace(need))
+    rows = np.array([0, 1, 777, M - 1], dtype=np.int64)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 5, 3, 0.37, 5, 3, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
