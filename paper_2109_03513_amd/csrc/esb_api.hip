@@ -172,22 +172,24 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
     if (lda > 0x7fffffff) return ESB_E_INVALID;
     const int op = mma_choose(fa, fb, K);
+    const bool f4 = mma_f4ok(fa, fb, K) && K % 32 == 0;
     const hipStream_t s = (hipStream_t)stream;
-    if (op >= 0 && mma_fits(g, A, K, 1, B, ldb, b_layout)) {
-        if (ws && op == 1 && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
-            return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb,
-                                             alphaB, acc, y, ldc, ws, s));
+    const bool fits = mma_fits(g, A, K, 1, B, ldb, b_layout);
+    if (ws && fits && (f4 || op == 1) && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
+        return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb, alphaB,
+                                         acc, y, ldc, f4, ws, s));
+    if (op >= 0 && fits)
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
                                      ldc, s));
-    }
     return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
                                          decode_info(fb), alphaB, acc, y, ldc, N, s));
 }
 
 size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig) {
     if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig) || M < 0 || N < 0 || K < 0) return 0;
-    if (mma_choose(make_fmt(nA, kA_sig), make_fmt(nB, kB_sig), K) != 1) return 0;
-    return mma_pre_workspace(M, K, N, K);
+    const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
+    if (mma_choose(fa, fb, K) != 1 && !(mma_f4ok(fa, fb, K) && K % 32 == 0)) return 0;
+    return mma_pre_workspace(M, K, N, K);   // E4M3 size; packed E2M1 needs half
 }
 
 int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
@@ -250,15 +252,16 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
     if (conv_is_depthwise(d))
         return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
     const int op = mma_choose(fx, fw, kred);
-    if (op >= 0 && mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK)) {
-        const int64_t xel = (int64_t)d->N * d->H * d->W * d->C, wel = (int64_t)d->K * kred;
-        if (ws && op == 1 && pre_worth(Mrows, d->K, kred, xel, wel))
-            return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
-                                             (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w,
-                                             d->K, kred, fw, alphaW, acc, y, d->K, ws, s));
+    const bool f4 = mma_f4ok(fx, fw, kred) && g.Cg % 32 == 0;
+    const bool fits = mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK);
+    const int64_t xel = (int64_t)d->N * d->H * d->W * d->C, wel = (int64_t)d->K * kred;
+    if (ws && fits && (f4 || op == 1) && pre_worth(Mrows, d->K, kred, xel, wel))
+        return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
+                                         (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w, d->K,
+                                         kred, fw, alphaW, acc, y, d->K, f4, ws, s));
+    if (op >= 0 && fits)
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
                                      kred, fw, alphaW, acc, y, d->K, s));
-    }
     return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
                                          alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
                                          d->K, Kg, s));
@@ -269,7 +272,8 @@ size_t esb_conv2d_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int
     ConvGeom g;
     int64_t Mrows = 0, kred = 0;
     if (conv_geom(d, &g, &Mrows, &kred) != ESB_OK || conv_is_depthwise(d)) return 0;
-    if (mma_choose(make_fmt(nX, kX_sig), make_fmt(nW, kW_sig), kred) != 1) return 0;
+    const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
+    if (mma_choose(fx, fw, kred) != 1 && !(mma_f4ok(fx, fw, kred) && g.Cg % 32 == 0)) return 0;
     return mma_pre_workspace((int64_t)d->N * d->H * d->W, d->C, d->K, kred);
 }
 

@@ -67,6 +67,13 @@ __device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
     return ((c << d.shs) & 0x80808080u) | t;                       // sign to bit 7
 }
 
+// Four codes to four OCP E2M1 nibbles (low half of each byte), value q
+// exactly: the same exponent-field increment as dec_f8 on a 1-bit fraction.
+__device__ __forceinline__ uint32_t dec_f4(uint32_t c, const MmaDecode& d) {
+    const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;
+    return ((c << d.shs) & 0x08080808u) | t;
+}
+
 __device__ __forceinline__ uint32_t dec_i8(uint32_t c, const MmaDecode& d) {
     return __builtin_amdgcn_perm(d.t1, d.t0, c & d.sel);
 }
@@ -432,12 +439,35 @@ __global__ __launch_bounds__(256) void k_decode_e4m3(DecodeJob j0, DecodeJob j1)
     }
 }
 
+// Rows of 32-code groups to packed E2M1: 16 bytes per group, byte i of dword j
+// holding codes 8j+i (low nibble) and 8j+4+i (high nibble) -- a permutation of
+// the reduction order applied to both operands alike.  Here cols16 counts
+// groups of 32 codes.
+__global__ __launch_bounds__(256) void k_decode_fp4(DecodeJob j0, DecodeJob j1) {
+    const int64_t n0 = j0.rows * j0.cols16, n = n0 + j1.rows * j1.cols16;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
+        const bool second = t >= n0;
+        const DecodeJob& j = second ? j1 : j0;
+        const int64_t u = second ? t - n0 : t;
+        const int64_t r = u / j.cols16, c = u - r * j.cols16;
+        const uint8_t* p = j.src + r * j.pitch + 32 * c;
+        const uint4 a = *(const uint4*)p, b = *(const uint4*)(p + 16);
+        *(uint4*)(j.dst + 16 * u) =
+            make_uint4(dec_f4(a.x, j.d) | (dec_f4(a.y, j.d) << 4), dec_f4(a.z, j.d) | (dec_f4(a.w, j.d) << 4),
+                       dec_f4(b.x, j.d) | (dec_f4(b.y, j.d) << 4), dec_f4(b.z, j.d) | (dec_f4(b.w, j.d) << 4));
+    }
+}
+
 // DMA layout: one global_load_lds of a wave writes 1 KB = 16 tile rows of 64
 // bytes; lane l lands at row 16 q + l / 4, physical chunk l % 4, which under
 // the swizzle of lds_off holds logical chunk (l % 4) ^ ((l / 16) % 4) — the same
 // for every DMA of the lane, so each lane fetches one fixed 16-byte column of
 // the reduction in every row it serves.
-template <int BM, int BN, int WGM, int WGN, int CONV, int R>
+// F4: the operands hold packed E2M1 (a 64-byte row is 128 reduction values,
+// two 32x32x64 fp4 MFMAs per stage); otherwise E4M3 (64 values, one MFMA).
+// Reduction lengths, pitches and offsets are in bytes of the decoded rows.
+template <int BM, int BN, int WGM, int WGN, int CONV, int R, int F4>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
@@ -537,25 +567,47 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     auto compute = [&](const uint8_t* d) {
         const uint8_t* tA = d;
         const uint8_t* tB = d + BM * BK;
-        v8i fb[TJ];
-        const int c0 = 2 * lg;
+        if (F4) {
 #pragma unroll
-        for (int j = 0; j < TJ; j++) {
-            const int row = wc + 32 * j + lr;
-            const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
-            const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
-            fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        }
+            for (int h = 0; h < 2; h++) {
+                const int c0 = 2 * h + lg;   // 16 bytes = 32 values per lane
+                v8i fb[TJ];
 #pragma unroll
-        for (int i = 0; i < TI; i++) {
-            const int row = wr + 32 * i + lr;
-            const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
-            const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
-            const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                for (int j = 0; j < TJ; j++) {
+                    const v4i v = *(const v4i*)&tB[lds_off(wc + 32 * j + lr, c0)];
+                    fb[j] = v8i{v[0], v[1], v[2], v[3], 0, 0, 0, 0};
+                }
 #pragma unroll
-            for (int j = 0; j < TJ; j++)
-                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[i][j], 0, 0,
-                                                                             0, 127, 0, 127);
+                for (int i = 0; i < TI; i++) {
+                    const v4i v = *(const v4i*)&tA[lds_off(wr + 32 * i + lr, c0)];
+                    const v8i fa = v8i{v[0], v[1], v[2], v[3], 0, 0, 0, 0};
+#pragma unroll
+                    for (int j = 0; j < TJ; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            fa, fb[j], acc[i][j], 4, 4, 0, 127, 0, 127);
+                }
+            }
+        } else {
+            v8i fb[TJ];
+            const int c0 = 2 * lg;
+#pragma unroll
+            for (int j = 0; j < TJ; j++) {
+                const int row = wc + 32 * j + lr;
+                const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
+                const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
+                fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            }
+#pragma unroll
+            for (int i = 0; i < TI; i++) {
+                const int row = wr + 32 * i + lr;
+                const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
+                const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
+                const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+                for (int j = 0; j < TJ; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[i][j], 0,
+                                                                                 0, 0, 127, 0, 127);
+            }
         }
     };
 
@@ -598,13 +650,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
 }
 
 template <int BM, int BN, int WGM, int WGN, int R>
-hipError_t launch_pre_t(FastParams g, int groups, bool conv, hipStream_t s) {
+hipError_t launch_pre_t(FastParams g, int groups, bool conv, bool f4, hipStream_t s) {
     g.tiles_m = (g.M + BM - 1) / BM;
     g.tiles_n = (g.N + BN - 1) / BN;
     g.ntiles = g.tiles_m * g.tiles_n;
     dim3 grid(g.ntiles, 1, groups);
-    if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
-    else k_mma_pre<BM, BN, WGM, WGN, 0, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    const int nt = 64 * WGM * WGN;
+    if (f4) {
+        if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R, 1><<<grid, nt, 0, s>>>(g);
+        else k_mma_pre<BM, BN, WGM, WGN, 0, R, 1><<<grid, nt, 0, s>>>(g);
+    } else {
+        if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R, 0><<<grid, nt, 0, s>>>(g);
+        else k_mma_pre<BM, BN, WGM, WGN, 0, R, 0><<<grid, nt, 0, s>>>(g);
+    }
     return hipGetLastError();
 }
 
@@ -671,6 +729,23 @@ int mma_choose(const Fmt& fa, const Fmt& fb, int64_t K) {
     return 1;
 }
 
+MmaDecode mma_decode_f4(const Fmt& f) {
+    MmaDecode d{};
+    const uint32_t rep = 0x01010101u;
+    d.shf = 1 - f.k;                                     // fraction to E2M1's one bit
+    d.lm = ((1u << (f.n - 1)) - 1u) * rep;
+    d.inc = 0x02u * rep;                                 // + 1 in the exponent field
+    d.lmf = (((1u << (f.n - 1)) - 1u) << d.shf) * rep;
+    d.shs = 4 - f.n;                                     // sign to bit 3
+    return d;
+}
+
+bool mma_f4ok(const Fmt& fa, const Fmt& fb, int64_t K) {
+    auto in_e2m1 = [](const Fmt& f) { return f.ebits <= 2 && f.k <= 1; };
+    if (!in_e2m1(fa) || !in_e2m1(fb)) return false;
+    return (double)K * (double)fa.max_int * (double)fb.max_int < 16777216.0;
+}
+
 bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const uint8_t* B,
               int64_t ldb, int b_layout) {
     return b_layout == 0 && K > 0 && ga.Cg >= 16 && ga.Cg % 16 == 0 && ga.pitch % 16 == 0 &&
@@ -688,39 +763,46 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          void* ws, hipStream_t s) {
+                          bool f4, void* ws, hipStream_t s) {
     if (M <= 0 || N <= 0) return hipSuccess;
-    uint8_t* dA = (uint8_t*)ws;
-    uint8_t* dB = dA + (((size_t)a_rows * (size_t)a_cols + 255) & ~(size_t)255);
-    DecodeJob j0{A, a_rows, a_cols / 16, a_pitch, mma_decode(fa, 1), dA};
-    DecodeJob j1{B, b_rows, K / 16, ldb, mma_decode(fb, 1), dB};
-    const int64_t chunks = j0.rows * j0.cols16 + j1.rows * j1.cols16;
-    int64_t blocks = (chunks + 255) / 256;
-    const int64_t cap = (int64_t)num_cus() * 16;
-    if (blocks > cap) blocks = cap;
-    k_decode_e4m3<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
-    FastParams g;
-    g.M = M; g.N = N; g.K = K; g.ga = ga;
-    g.ga.pitch = (int)a_cols;
-    g.A = dA; g.B = dB; g.ldb = K;
-    g.da = mma_decode(fa, 1);
-    g.db = mma_decode(fb, 1);
-    g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
-    g.kA = fa.k; g.kB = fb.k;
-    g.out_shift = fa.k + fb.k + 12;
-    g.zrowA = g.zrowB = kZeroRowE4M3;
-    g.tiles_m = g.tiles_n = g.ntiles = 0;
     const bool conv = !(ga.H == 1 && ga.W == 1 && ga.R == 1 && ga.S == 1 && ga.ph == 0 && ga.pw == 0 &&
                         ga.Cg == K && groups == 1);
+    // decoded bytes per code: 1 (E4M3) or 1/2 (E2M1); lengths below are in bytes
+    const int sh = f4 ? 1 : 0;
+    const int64_t a_bytes = a_cols >> sh, kbytes = (int64_t)K >> sh;
+    uint8_t* dA = (uint8_t*)ws;
+    uint8_t* dB = dA + (((size_t)a_rows * (size_t)a_bytes + 255) & ~(size_t)255);
+    const int grp = f4 ? 32 : 16;    // codes per decode item
+    DecodeJob j0{A, a_rows, a_cols / grp, a_pitch, f4 ? mma_decode_f4(fa) : mma_decode(fa, 1), dA};
+    DecodeJob j1{B, b_rows, (int64_t)K / grp, ldb, f4 ? mma_decode_f4(fb) : mma_decode(fb, 1), dB};
+    const int64_t items = j0.rows * j0.cols16 + j1.rows * j1.cols16;
+    int64_t blocks = (items + 255) / 256;
+    const int64_t cap = (int64_t)num_cus() * 16;
+    if (blocks > cap) blocks = cap;
+    if (f4) k_decode_fp4<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
+    else k_decode_e4m3<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
+    FastParams g;
+    g.M = M; g.N = N; g.K = (int)kbytes; g.ga = ga;
+    g.ga.pitch = (int)a_bytes;
+    g.ga.Cg = ga.Cg >> sh;
+    g.A = dA; g.B = dB; g.ldb = kbytes;
+    g.da = j0.d;
+    g.db = j1.d;
+    g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.kA = fa.k; g.kB = fb.k;
+    // E4M3 holds q * 2^-6 per operand; E2M1 holds q itself
+    g.out_shift = fa.k + fb.k + (f4 ? 0 : 12);
+    g.zrowA = g.zrowB = kZeroRowE4M3;
+    g.tiles_m = g.tiles_n = g.ntiles = 0;
     const int64_t cus = num_cus();
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn) * groups;
     };
-    if (N > 128 && tiles(256, 256) >= cus) return launch_pre_t<256, 256, 2, 4, 4>(g, groups, conv, s);
-    if (N > 64 && tiles(256, 128) >= cus) return launch_pre_t<256, 128, 4, 2, 4>(g, groups, conv, s);
-    if (N > 64 && tiles(128, 128) >= cus / 2) return launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, s);
-    if (tiles(128, 64) >= cus) return launch_pre_t<128, 64, 2, 2, 4>(g, groups, conv, s);
-    return launch_pre_t<64, 64, 2, 2, 4>(g, groups, conv, s);
+    if (N > 128 && tiles(256, 256) >= cus) return launch_pre_t<256, 256, 2, 4, 4>(g, groups, conv, f4, s);
+    if (N > 64 && tiles(256, 128) >= cus) return launch_pre_t<256, 128, 4, 2, 4>(g, groups, conv, f4, s);
+    if (N > 64 && tiles(128, 128) >= cus / 2) return launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, f4, s);
+    if (tiles(128, 64) >= cus) return launch_pre_t<128, 64, 2, 2, 4>(g, groups, conv, f4, s);
+    return launch_pre_t<64, 64, 2, 2, 4>(g, groups, conv, f4, s);
 }
 
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,

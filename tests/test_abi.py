@@ -106,14 +106,15 @@ def test_contract_matches_oracle():
 
 def test_contraction_workspace_sizes_and_errors(L):
     """Workspace sizes of the decode-once path: nonzero exactly for pairs of formats the E4M3
-    path takes, at least both operands' bytes; a too small workspace is refused before any
-    launch (ESB_E_WORKSPACE), a NULL one falls back to the plain call."""
+    or the E2M1 path takes, at least both operands' decoded bytes; a too small workspace is
+    refused before any launch (ESB_E_WORKSPACE)."""
     from paper_2109_03513_amd import esb
     fake = ctypes.c_void_p(0x1000)
     M, N, K = 300, 200, 576
     need = L.esb_gemm_workspace_size(M, N, K, 5, 3, 5, 3)
     assert need >= M * K + N * K
-    assert L.esb_gemm_workspace_size(M, N, K, 3, 2, 3, 1) == 0       # int8 table path
+    assert L.esb_gemm_workspace_size(M, N, K, 3, 2, 3, 1) >= M * K // 2 + N * K // 2   # E2M1 path
+    assert L.esb_gemm_workspace_size(M, N, 48, 3, 2, 3, 1) == 0      # K % 32: int8 table path only
     assert L.esb_gemm_workspace_size(M, N, K, 8, 5, 8, 5) == 0       # outside the E4M3 window
     assert L.esb_gemm_workspace_size(M, N, K, 9, 2, 5, 3) == 0       # invalid format
     g = L.esb_gemm_ws

@@ -36,7 +36,10 @@ def sampled_rows(M, tile):
     (4097, 4100, 208, (4, 2), (4, 2)),     # 256 x 256 tiles, ragged K within a stage
     (1600, 1537, 1152, (5, 3), (4, 2)),    # mixed formats, 18 stages
     (64, 64, 576, (4, 2), (4, 2)),         # too little work: the workspace is not used
-    (300, 257, 200, (3, 2), (3, 1)),       # int8 table formats: no workspace path
+    (300, 257, 200, (3, 2), (3, 1)),       # K % 32 != 0: no E2M1 path, int8 table
+    (2049, 2050, 416, (4, 2), (4, 2)),     # E2M1 (fp4) path: ESB(4,1) is exactly E2M1
+    (2048, 2080, 576, (3, 2), (3, 1)),     # E2M1 path for the 3-bit formats
+    (1537, 1600, 1024, (2, 1), (4, 2)),    # E2M1 path, mixed formats
 ])
 def test_gemm_ws_sampled(esb, M, N, K, fa, fb):
     (bA, ksA), (bB, ksB) = fa, fb
@@ -73,7 +76,7 @@ def test_gemm_ws_equals_plain_and_reuse(esb):
     (4, 15, 13, 128, 320, 3, 2, 1),        # stride 2, odd sizes, ragged N tile
     (2, 7, 7, 512, 512, 3, 1, 1),          # layer4 3x3
 ])
-@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2))])
+@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1))])
 def test_conv_ws_parity(esb, case, fmt):
     Nb, H, W, C, K, R, st, pd = case
     (bX, ksX), (bW, ksW) = fmt
@@ -117,6 +120,24 @@ def test_gemm_ws_product_spread_at_accumulator_bound(esb):
                           workspace=workspace(need))
     rows = np.array([0, 1, 777, M - 1], dtype=np.int64)
     st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 5, 3, 0.37, 5, 3, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+def test_gemm_ws_e2m1_spread_at_accumulator_bound(esb):
+    """ESB(4,1) on the E2M1 path: products m_A*m_B from 1 to 144 in one reduction and
+    K * 144 just below 2^24 (every partial sum exact in fp32)."""
+    M, N, K = 1536, 1536, 116480
+    A = extreme_codes(4, 2, (M, K), 5)
+    B = extreme_codes(4, 2, (N, K), 6)
+    need = esb.esb_gemm_workspace_size(M, N, K, 4, 2, 4, 2)
+    assert need > 0
+    log("gemm_ws e2m1 spread M=%d N=%d K=%d" % (M, N, K))
+    acc, y = esb.esb_gemm(dev(A), 4, 2, scalar(0.37), dev(B), 4, 2, scalar(0.021),
+                          workspace=workspace(need))
+    rows = np.array([0, 5, 1000, M - 1], dtype=np.int64)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 4, 2, 0.37, 4, 2, 0.021)
     assert st == 0
     np.testing.assert_array_equal(host(acc)[rows], oacc)
     assert_rel(host(y)[rows], oy, YREL, "y")
