@@ -412,7 +412,8 @@ def resnet18_bench(args):
                 yb = torch.empty((M, Nn), dtype=torch.float32, device="cuda")
                 c_ms = time_launches(lambda: esb.esb_gemm(t["codes"], 5, 3, t["alpha"], rec.fc_codes, 5, 3,
                                                           rec.fc_alpha, y=yb, want_acc=False,
-                                                          stream=stream), args.reps, stream)
+                                                          stream=stream, workspace=rec.cws),
+                                     args.reps, stream)
                 ops = 2.0 * M * Nn * K
                 nbytes = float(M * K + Nn * K + 4 * M * Nn)
             else:
@@ -423,7 +424,8 @@ def resnet18_bench(args):
                 c_ms = time_launches(lambda: esb.esb_conv2d(t["codes"], 5, 3, t["alpha"], L["codes"], 5, 3,
                                                             L["alpha"], stride=(L["stride"],) * 2,
                                                             pad=(L["pad"],) * 2, y=yb, want_acc=False,
-                                                            stream=stream), args.reps, stream)
+                                                            stream=stream, workspace=rec.cws),
+                                     args.reps, stream)
                 ops = 2.0 * Nb * P * Q * L["cout"] * L["k"] * L["k"] * C
                 nbytes = float(t["codes"].numel() + L["codes"].numel() + 4 * yb.numel())
             total_ops += ops

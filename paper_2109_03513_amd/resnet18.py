@@ -61,6 +61,15 @@ class ResNet18ESB:
         sizes["fc"] = batch * 512
         self.ws = {k: torch.empty(max(esb.esb_dda_workspace_size(v, n, k_sig, GRID_POINTS), 1),
                                   dtype=torch.uint8, device=dev) for k, v in sizes.items()}
+        # one contraction workspace for every layer (they run one after the other
+        # on one stream): operands decoded once where the layer has the work for it
+        need = esb.esb_gemm_workspace_size(batch, 1000, 512, n, k_sig, n, k_sig)
+        for name, L in self.layers.items():
+            side = input_side(name)
+            need = max(need, esb.esb_conv2d_workspace_size(
+                (batch, side, side, L["cin"]), (L["cout"], L["k"], L["k"], L["cin"]), n, k_sig, n,
+                k_sig, stride=(L["stride"],) * 2, pad=(L["pad"],) * 2))
+        self.cws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
         # weights, quantized once
         for name, L in self.layers.items():
             w = torch.from_numpy(np.ascontiguousarray(weights[name])).to(dev)
@@ -92,7 +101,7 @@ class ResNet18ESB:
         ax, cx = self._quantize(x, self.ws[name])
         acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"],
                                 stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
-                                want_acc=self.record, stream=self.sh)
+                                want_acc=self.record, stream=self.sh, workspace=self.cws)
         if self.record:
             self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
         return y
@@ -113,7 +122,8 @@ class ResNet18ESB:
         feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
         af, cf = self._quantize(feat, self.ws["fc"])
         acc, logits = esb.esb_gemm(cf, self.n, self.ks, af, self.fc_codes, self.n, self.ks,
-                                   self.fc_alpha, want_acc=self.record, stream=self.sh)
+                                   self.fc_alpha, want_acc=self.record, stream=self.sh,
+                                   workspace=self.cws)
         if self.record:
             self.trace.append(dict(name="fc", x=feat, alpha=af, codes=cf, acc=acc, y=logits))
         return logits
