@@ -138,6 +138,9 @@ typedef __attribute__((address_space(1))) const void gbl_cvoid_t;
 // its own wait on them is enough.  The memory clobber keeps the compiler from
 // moving LDS accesses across.
 __device__ __forceinline__ void lds_barrier() {
+    // the same wait as a builtin first: the compiler's wait tracking then knows
+    // that every LDS read issued so far is complete
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0), vmcnt and expcnt at their maxima
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
@@ -563,72 +566,106 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[i][j][r] = 0.0f;
 
+    // Each stage's MFMAs come in two parts.  E4M3: the A rows i < TI0, then the
+    // rest, over the same B fragments (kept for two stages, by stage parity);
+    // F4: the first and the second 64 values of the stage's 128.  Part 0 of stage s is issued before the
+    // barrier that ends the stage, part 1 after it, so the MFMAs keep running
+    // while the waves meet; the fragments of part 0 of stage s+1 are read right
+    // after that barrier, under the MFMAs of part 1.
+    constexpr int TI0 = (TI + 1) / 2;
     const int lr = lane & 31, lg = lane >> 5;
-    auto compute = [&](const uint8_t* d) {
+    v8i fa[TI], fb[2][TJ];        // E4M3 fragments: 32 bytes per lane
+    v4i ga[2][TI], gb[2][TJ];     // E2M1 fragments: 16 bytes = 32 values per lane, per part
+    auto frag8 = [&](const uint8_t* t, int row, int c0) {
+        const v4i lo = *(const v4i*)&t[lds_off(row, c0)];
+        const v4i hi = *(const v4i*)&t[lds_off(row, c0 + 1)];
+        return v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    };
+    auto frag4 = [&](const uint8_t* t, int row, int c0) { return *(const v4i*)&t[lds_off(row, c0)]; };
+    auto wide = [](v4i v) { return v8i{v[0], v[1], v[2], v[3], 0, 0, 0, 0}; };
+    // fragments of part 0 of the stage in slot d (B into buffer PAR)
+    auto read0 = [&](const uint8_t* d, auto PAR) {
+        constexpr int par = decltype(PAR)::value;
         const uint8_t* tA = d;
         const uint8_t* tB = d + BM * BK;
-        if (F4) {
+        if constexpr (F4) {
 #pragma unroll
-            for (int h = 0; h < 2; h++) {
-                const int c0 = 2 * h + lg;   // 16 bytes = 32 values per lane
-                v8i fb[TJ];
+            for (int j = 0; j < TJ; j++) gb[0][j] = frag4(tB, wc + 32 * j + lr, lg);
 #pragma unroll
-                for (int j = 0; j < TJ; j++) {
-                    const v4i v = *(const v4i*)&tB[lds_off(wc + 32 * j + lr, c0)];
-                    fb[j] = v8i{v[0], v[1], v[2], v[3], 0, 0, 0, 0};
-                }
-#pragma unroll
-                for (int i = 0; i < TI; i++) {
-                    const v4i v = *(const v4i*)&tA[lds_off(wr + 32 * i + lr, c0)];
-                    const v8i fa = v8i{v[0], v[1], v[2], v[3], 0, 0, 0, 0};
-#pragma unroll
-                    for (int j = 0; j < TJ; j++)
-                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            fa, fb[j], acc[i][j], 4, 4, 0, 127, 0, 127);
-                }
-            }
+            for (int i = 0; i < TI; i++) ga[0][i] = frag4(tA, wr + 32 * i + lr, lg);
         } else {
-            v8i fb[TJ];
-            const int c0 = 2 * lg;
 #pragma unroll
-            for (int j = 0; j < TJ; j++) {
-                const int row = wc + 32 * j + lr;
-                const v4i lo = *(const v4i*)&tB[lds_off(row, c0)];
-                const v4i hi = *(const v4i*)&tB[lds_off(row, c0 + 1)];
-                fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            }
+            for (int j = 0; j < TJ; j++) fb[par][j] = frag8(tB, wc + 32 * j + lr, 2 * lg);
 #pragma unroll
-            for (int i = 0; i < TI; i++) {
-                const int row = wr + 32 * i + lr;
-                const v4i lo = *(const v4i*)&tA[lds_off(row, c0)];
-                const v4i hi = *(const v4i*)&tA[lds_off(row, c0 + 1)];
-                const v8i fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            for (int i = 0; i < TI0; i++) fa[i] = frag8(tA, wr + 32 * i + lr, 2 * lg);
+        }
+    };
+    auto read1 = [&](const uint8_t* d) {
+        const uint8_t* tA = d;
+        const uint8_t* tB = d + BM * BK;
+        if constexpr (F4) {
+#pragma unroll
+            for (int j = 0; j < TJ; j++) gb[1][j] = frag4(tB, wc + 32 * j + lr, 2 + lg);
+#pragma unroll
+            for (int i = 0; i < TI; i++) ga[1][i] = frag4(tA, wr + 32 * i + lr, 2 + lg);
+        } else {
+#pragma unroll
+            for (int i = TI0; i < TI; i++) fa[i] = frag8(tA, wr + 32 * i + lr, 2 * lg);
+        }
+    };
+    auto mfma = [&](auto PART, auto PAR) {
+        constexpr int part = decltype(PART)::value, par = decltype(PAR)::value;
+        if constexpr (F4) {
+#pragma unroll
+            for (int i = 0; i < TI; i++)
 #pragma unroll
                 for (int j = 0; j < TJ; j++)
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[i][j], 0,
-                                                                                 0, 0, 127, 0, 127);
-            }
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        wide(ga[part][i]), wide(gb[part][j]), acc[i][j], 4, 4, 0, 127, 0, 127);
+        } else {
+#pragma unroll
+            for (int i = part ? TI0 : 0; i < (part ? TI : TI0); i++)
+#pragma unroll
+                for (int j = 0; j < TJ; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        fa[i], fb[par][j], acc[i][j], 0, 0, 0, 127, 0, 127);
         }
     };
 
+    // stage s lives in slot s % R; its fetch is issued R stages ahead, so at
+    // the barrier of stage s the fetches of stages s+2 .. s+R-1 may still be
+    // in flight (CT instructions each) while stage s+1 has landed
+    static_assert(R == 2 || R == 4, "ring depth");
     const int KT = (g.K + BK - 1) / BK;
-    static_for<0, R - 1>([&](auto Q) {
+    static_for<0, R>([&](auto Q) {
         constexpr int q = decltype(Q)::value;
         fetch(q * BK, ring + q * TILE);
     });
-    // stage s sits in slot s % R; at the top of stage s the fetches of stages
-    // s .. s+R-2 are in flight (CT instructions each)
-    for (int kt = 0; kt < KT; kt += R) {
-        static_for<0, R>([&](auto Q) {
-            constexpr int q = decltype(Q)::value;
-            if (kt + q < KT) {
-                vm_wait<(R - 2) * CT>();       // this thread's part of stage s landed
-                lds_barrier();                 // everyone's part landed; slot (s-1) % R is free
-                fetch((kt + q + R - 1) * BK, ring + ((q + R - 1) % R) * TILE);
-                compute(ring + q * TILE);
-            }
-        });
+    vm_wait<(R - 1) * CT>();   // stage 0 landed
+    lds_barrier();
+    read0(ring, ic<0>{});
+    // One stage; no branches inside, so that the compiler's waits track every
+    // fragment exactly.  Past the last stage read0 reads a slot it never uses.
+    auto stage = [&](int st, auto PAR) {
+        constexpr int par = decltype(PAR)::value;
+        uint8_t* slot = ring + (st & (R - 1)) * TILE;
+        mfma(ic<0>{}, PAR);
+        read1(slot);
+        __builtin_amdgcn_sched_barrier(0);
+        vm_wait<(R - 2) * CT>();       // this thread's part of stage st+1 landed
+        lds_barrier();                 // all of it; every read of this slot is done
+        fetch((st + R) * BK, slot);
+        read0(ring + ((st + 1) & (R - 1)) * TILE, ic<par ^ 1>{});
+        __builtin_amdgcn_sched_barrier(0);
+        mfma(ic<1>{}, PAR);
+    };
+    int st = 0;
+    for (; st + 1 < KT; st += 2) {
+        stage(st, ic<0>{});
+        stage(st + 1, ic<1>{});
     }
+    if (st < KT) stage(st, ic<0>{});
+    vm_wait<0>();   // the fetches past the end (+0 rows) land before the workgroup ends
 
     float s = 0.0f;
     if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
