@@ -27,13 +27,15 @@
 //   candidate: they add nothing (ReLU zeros never touch one LDS address).
 //   Values at or above the largest threshold (the unbounded top atom) and
 //   non-finite values land in the flagged last bin and are summed in fp64.
-//   At the end the block writes its packed cells as one row.
-// k_dda_reduce (only for many blocks): sums the rows in slices.
-// k_dda_finalize (1 block): per-atom sums, prefix sums over atoms, then per
-//   candidate A_j = sum_c Q_c (P1[end_c] - P1[start_c]), B_j likewise with P0 and
-//   Q_c^2, D_j = S2 + a (a B_j - 2 A_j); argmin with ties to the lowest index.
-// Integer sums are exact; fp64 sums run in a fixed order: the result is
-// deterministic.  Wave-level scans and reductions use DPP lane moves.
+//   At the end the block turns its own cells into its share of the objective:
+//   per-atom moments, prefix sums over atoms (counts in integers, sums of |x|
+//   in fp64), then per candidate A_j = sum_c Q_c (P1[end_c] - P1[start_c]) and
+//   B_j = sum_c Q_c^2 (P0[end_c] - P0[start_c]), written with the block's
+//   sum x^2 as one short vector.
+// k_dda_finalize (1 block): sums the block vectors in block order, D_j =
+//   S2 + a (a B_j - 2 A_j), argmin with ties to the lowest index.
+// Per-atom sums are exact integers; fp64 sums run in a fixed order: the result
+// is deterministic.  Wave-level scans and reductions use DPP lane moves.
 #include "esb_internal.h"
 
 namespace esb {
@@ -43,8 +45,6 @@ constexpr int kFinThreads = 1024;
 constexpr int kMaxSplits = 256;            // powers of two between thresholds (at most 254)
 constexpr int kRowElems = 4 * kHistThreads; // one float4 per thread
 constexpr int kMaxRowsPerBlock = 128;      // 2^19 elements: a packed cell cannot overflow
-constexpr int kPackedMaxBlocks = 32;       // above: k_dda_reduce sums the rows in slices
-constexpr int kReduceSlices = 16;
 constexpr uint32_t kFlagWalk = 1u << 31;   // bin holds two or more bounds
 constexpr uint32_t kFlagTop = 1u << 30;    // last bin: values >= the largest threshold
 constexpr uint32_t kAtomMask = (1u << 29) - 1u;
@@ -55,19 +55,19 @@ struct DdaArgs {
     int n, k;               // format (k fraction bits)
     int lbins;              // log2 of the bin count of the pass
     int nblk, rows_pb;      // blocks of k_dda_hist, rows of kRowElems per block
-    int nslice;             // slices of k_dda_reduce (0: the finalize reads the packed rows)
-    int rk_lds;             // the finalize keeps the cell starts in LDS
 };
 
-struct DdaWs {   // pointers into the caller's workspace
-    uint32_t* ubits;   // [Aa+4]: distinct sorted bounds U[0] = 0, U[1..Dp], then ~0
-    int32_t* rank;     // [A]: atom where cell c of candidate j starts (j*M + c-1)
-    uint32_t* meta;    // the top atom Dp (number of distinct bounds), twice
-    uint64_t* rows;    // [nblk][Aa+1] per block: count << 44 | significand sum
-    double* pscal;     // [nblk][4]: sum x^2, top-atom sum |x|, top count, flags
-    uint64_t* rcnt;    // [nslice][Aa+1] sliced sums (k_dda_reduce)
-    uint64_t* rsum;    // [nslice][Aa+1]
-};
+// Per block of k_dda_hist, 2G + 2 doubles: A_0 .. A_{G-1}, B_0 .. B_{G-1}, the
+// block's sum x^2, its flags (1: +-inf seen, 2: NaN seen).
+__host__ __device__ inline int part_stride(int G) { return 2 * G + 2; }
+// Above kGroupAbove blocks, k_dda_group first sums groups of kGroup
+// consecutive block vectors (many CUs, one round of loads each); the finalize
+// then reads the group vectors.
+constexpr int kGroup = 16;
+constexpr int kGroupAbove = 32;
+__host__ __device__ inline int dda_groups(int nblk) {
+    return nblk > kGroupAbove ? (nblk + kGroup - 1) / kGroup : 0;
+}
 
 __host__ __device__ static inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 __host__ __device__ static inline size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
@@ -96,33 +96,11 @@ bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L) {
     L->A = G * M;
     int rpb = 0;
     dda_blocks(len, &L->nblk, &rpb);
-    const size_t Aa1 = (size_t)L->A + kMaxSplits + 1;
-    const size_t ns = L->nblk > kPackedMaxBlocks ? kReduceSlices : 0;
-    size_t o = 0;
-    L->off_ubits = o; o = align256(o + sizeof(uint32_t) * (Aa1 + 3));
-    L->off_rank = o;  o = align256(o + sizeof(int32_t) * (size_t)L->A);
-    L->off_meta = o;  o = align256(o + sizeof(uint32_t) * 8);
-    L->off_pcnt = o;  o = align256(o + sizeof(uint64_t) * Aa1 * L->nblk);
-    L->off_psum = o;
-    L->off_pscal = o; o = align256(o + sizeof(double) * 4 * L->nblk);
-    L->off_s0 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
-    L->off_s1 = o;    o = align256(o + sizeof(uint64_t) * Aa1 * ns);
-    L->off_bins = 0;
-    L->total = o;
+    const size_t ps = sizeof(double) * (size_t)part_stride(G);
+    L->off_part = 0;
+    L->off_group = align256(ps * (size_t)L->nblk);
+    L->total = L->off_group + align256(ps * (size_t)dda_groups(L->nblk));
     return true;
-}
-
-static DdaWs ws_ptrs(void* ws, const DdaLayout& L) {
-    char* b = (char*)ws;
-    DdaWs w;
-    w.ubits = (uint32_t*)(b + L.off_ubits);
-    w.rank = (int32_t*)(b + L.off_rank);
-    w.meta = (uint32_t*)(b + L.off_meta);
-    w.rows = (uint64_t*)(b + L.off_pcnt);
-    w.pscal = (double*)(b + L.off_pscal);
-    w.rcnt = (uint64_t*)(b + L.off_s0);
-    w.rsum = (uint64_t*)(b + L.off_s1);
-    return w;
 }
 
 // ------------------------------------------------------------ wave primitives
@@ -229,30 +207,20 @@ __device__ __forceinline__ uint32_t med3_u32(uint32_t x, uint32_t lo, uint32_t h
 
 __device__ __forceinline__ bool alpha_ok(float a) { return a > 0.0f && a < __builtin_inff(); }
 
-__device__ __forceinline__ bool reaches(uint32_t xbits, float alpha, float mu) {
-    return __uint_as_float(xbits) / alpha >= mu;   // fl32(X / alpha) >= mu, IEEE division
-}
-
-// Smallest fp32 X >= 0 (as bits) with fl32(X / alpha) >= mu.  The predicate is
-// monotone in X, false at 0 (mu > 0) and true at +inf.  Local search from
-// fl32(alpha * mu), which is within a few ulps of the answer; bisection if the
-// walk does not settle.
-__device__ uint32_t threshold_bits(float alpha, float mu) {
-    uint32_t b = __float_as_uint(alpha * mu);
-    if (b > 0x7f800000u) b = 0x7f800000u;
-    int it = 0;
-    if (reaches(b, alpha, mu)) {
-        while (b > 0u && it < 32 && reaches(b - 1u, alpha, mu)) { b--; it++; }
-    } else {
-        while (it < 32 && !reaches(b, alpha, mu)) { b++; it++; }
-    }
-    if (it < 32) return b;
-    uint32_t lo = 0u, hi = 0x7f800000u;
-    while (hi - lo > 1u) {
-        const uint32_t mid = lo + ((hi - lo) >> 1);
-        if (reaches(mid, alpha, mu)) hi = mid; else lo = mid;
-    }
-    return hi;
+// Smallest fp32 X >= 0 (as bits) with fl32(X / alpha) >= mu (IEEE division,
+// round to nearest even), for alpha > 0 finite and mu a positive normal fp32
+// whose significand is even (a set midpoint has at most k + 2 significant
+// bits).  With p the fp32 just below mu, the quotient rounds to mu or above
+// exactly when X / alpha >= m = (p + mu) / 2 (a tie goes to the even mu), that
+// is X >= alpha * m.  That product has at most 24 + 25 significant bits, so it
+// is exact in fp64, and X is its rounding up to fp32 (+inf past the largest).
+__device__ __forceinline__ uint32_t threshold_bits(float alpha, float mu) {
+    const double m = 0.5 * ((double)__uint_as_float(__float_as_uint(mu) - 1u) + (double)mu);
+    const double t = (double)alpha * m;
+    const float f = (float)t;
+    uint32_t b = __float_as_uint(f);
+    if ((double)f < t) b++;
+    return b > 0x7f800000u ? 0x7f800000u : b;
 }
 
 // Bins of the pass: more bins make crowded bins (two or more bounds, a walk)
@@ -287,7 +255,7 @@ __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
 
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restrict__ x, int64_t len,
                                                            const float* __restrict__ grid,
-                                                           DdaArgs a, DdaWs w) {
+                                                           DdaArgs a, double* __restrict__ part) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int nbins = 1 << a.lbins;
@@ -301,7 +269,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     uint64_t* hist = KH;
     __shared__ float s_mid[128];
     __shared__ uint32_t s_u[4][16];
-    __shared__ double s_d[2][16];
+    __shared__ double s_d[3][16];
 
     // ---- 0. requests first: this thread's candidate scales and the first chunk
     //         of x, so that both latencies overlap the clearing of the bins.
@@ -632,253 +600,223 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     }
     lds_barrier();
 
-    // ---- 8. the block's row, its scalars; block 0 also publishes the tables
-    uint64_t* row = w.rows + (int64_t)blockIdx.x * (a.Aa + 1);
-    for (uint32_t i = tid; i <= Dp; i += kHistThreads) {
-        uint64_t v = 0;
-        for (uint32_t c = 0; c < (1u << lcop); c++) v += hist[(i << lcop) + c];   // fields stay apart
-        row[i] = v;
+    // ---- 8. the block's share of the objective.  Per atom: S0 = count, S1 =
+    //         sum |x| (the significand sums carry the binade of the atom's lower
+    //         bound U[at]).  Atom 0 has q = 0 for every candidate (its values went
+    //         to the spare cells); the top atom Dp is taken from the fp64 sums.
+    //         Exclusive prefix sums over atoms 0 .. Dp: P0 (u32) over U, P1
+    //         (fp64) over the histogram, once both are read.
+    constexpr int kPerMax = (kDdaMaxThresholds + kMaxSplits + 2 + kHistThreads - 1) / kHistThreads;
+    const int per = (int)((Dp + 2u + kHistThreads - 1) / kHistThreads);   // atoms 0 .. Dp+1
+    uint32_t c0[kPerMax];
+    double c1[kPerMax];
+    uint32_t m0 = 0;
+    double m1 = 0.0;
+#pragma unroll
+    for (int e = 0; e < kPerMax; e++) {
+        const uint32_t at = (uint32_t)(tid * per + e);
+        c0[e] = 0u;
+        c1[e] = 0.0;
+        if (e < per && at >= 1u && at < Dp) {
+            uint64_t v = 0;
+            for (uint32_t c = 0; c < (1u << lcop); c++) v += hist[(at << lcop) + c];   // fields stay apart
+            const uint32_t cnt = (uint32_t)(v >> 44);
+            uint64_t t = v & kSumMask;
+            const uint32_t ex = U[at] >> 23;
+            if (ex) t += (uint64_t)cnt << 23;            // the implicit bit of a normal binade
+            c0[e] = cnt;
+            c1[e] = ldexp((double)t, (int)max(ex, 1u) - 150);
+        }
+        m0 += c0[e];
+        m1 += c1[e];
     }
     {
+        const uint32_t i0 = wave_scan_add(m0);
+        const double i1 = wave_scan_add(m1);
         const double ss = wave_scan_add(ss0 + ss1), t1 = wave_scan_add(top_s1);
         const uint32_t tc = wave_scan_add(top_cnt), fl = wave_scan_or(flags);
-        if (lane == 63) { s_d[0][wid] = ss; s_d[1][wid] = t1; s_u[0][wid] = tc; s_u[1][wid] = fl; }
-    }
-    if (blockIdx.x == 0) {
-        for (uint32_t i = tid; i <= Dp + 3u; i += kHistThreads) w.ubits[i] = U[i];
-        for (int i = tid; i < A; i += kHistThreads) w.rank[i] = (int32_t)TH[i];
-        if (tid == 0) { w.meta[0] = Dp; w.meta[1] = Dp; }
+        if (lane == 63) {
+            s_u[0][wid] = i0; s_d[0][wid] = i1;
+            s_u[1][wid] = tc; s_u[2][wid] = fl; s_d[1][wid] = ss; s_d[2][wid] = t1;
+        }
+        lds_barrier();   // wave totals published; every read of the histogram and U is done
+        uint32_t r0 = i0 - m0;
+        double r1 = i1 - m1;
+        for (int v = 0; v < wid; v++) { r0 += s_u[0][v]; r1 += s_d[0][v]; }
+        uint32_t* P0 = U;
+        double* P1 = (double*)KH;
+#pragma unroll
+        for (int e = 0; e < kPerMax; e++) {
+            const uint32_t at = (uint32_t)(tid * per + e);
+            if (e < per && at <= Dp + 1u) {
+                P0[at] = r0;
+                P1[at] = r1;
+                r0 += c0[e];
+                r1 += c1[e];
+            }
+        }
     }
     lds_barrier();
-    if (tid == 0) {
-        double ss = 0.0, t1 = 0.0;
-        uint32_t tc = 0, fl = 0;
+
+    // ---- 9. per cell (j, c), c >= 1: atoms [start_c, start_{c+1}), the last
+    //         one up to Dp; the top atom joins the cell that holds Dp.  One
+    //         thread per cell writes Q_c S1 and Q_c^2 S0 of the cell; thread j
+    //         then sums the cells of candidate j in order.  Cells are taken
+    //         1024 at a time; the terms live where the bin entries were.
+    {
+        const uint32_t* P0 = U;
+        const double* P1 = (const double*)KH;
+        double2* T = (double2*)smem;                 // [kHistThreads], 16 KB <= the entries
+        double ssb = 0.0, t1b = 0.0;
+        uint32_t tcb = 0, flb = 0;
+#pragma unroll
         for (int v = 0; v < kHistThreads / 64; v++) {
-            ss += s_d[0][v]; t1 += s_d[1][v]; tc += s_u[0][v]; fl |= s_u[1][v];
+            ssb += s_d[1][v]; t1b += s_d[2][v]; tcb += s_u[1][v]; flb |= s_u[2][v];
         }
-        double* ps = w.pscal + 4 * (int64_t)blockIdx.x;
-        ps[0] = ss; ps[1] = t1; ps[2] = (double)tc; ps[3] = (double)fl;
+        const uint32_t end = Dp + 1u;
+        double Aj = 0.0, Bj = 0.0;
+        for (int i0 = 0; i0 < A; i0 += kHistThreads) {
+            const int i = i0 + tid;
+            if (i < A) {
+                const int j = i / M, c = i - j * M + 1;
+                const uint32_t st = min(TH[i], end);
+                const uint32_t nx = (c < M) ? min(TH[i + 1], end) : end;
+                const double q = (double)set_value(c, a.k);
+                double d1 = P1[nx] - P1[st];
+                uint32_t d0 = P0[nx] - P0[st];
+                if (st <= Dp && Dp < nx) { d1 += t1b; d0 += tcb; }
+                T[tid] = make_double2(q * d1, (q * q) * (double)d0);
+            }
+            lds_barrier();
+            if (tid < a.G) {
+                const int lo = max(tid * M, i0), hi = min(tid * M + M, i0 + kHistThreads);
+                for (int c = lo; c < hi; c += 4) {     // four reads in flight, sums in order
+                    double2 t[4];
+#pragma unroll
+                    for (int u = 0; u < 4; u++) t[u] = T[min(c + u, hi - 1) - i0];
+#pragma unroll
+                    for (int u = 0; u < 4; u++)
+                        if (c + u < hi) { Aj += t[u].x; Bj += t[u].y; }
+                }
+            }
+            lds_barrier();
+        }
+        double* out = part + (int64_t)blockIdx.x * part_stride(a.G);
+        if (tid < a.G) {
+            out[tid] = Aj;
+            out[a.G + tid] = Bj;
+        }
+        if (tid == 0) {
+            out[2 * a.G] = ssb;
+            out[2 * a.G + 1] = (double)flb;
+        }
     }
 }
 
-// -------------------------------------------------------------------- reduce
-// Slice s of the block rows, per atom: integer sums of counts and significand
-// sums (entries past the last bound are summed too and never read).
-__global__ __launch_bounds__(256) void k_dda_reduce(DdaArgs a, DdaWs w) {
-    const int at = blockIdx.x * 256 + threadIdx.x;
-    const int Aa1 = a.Aa + 1;
-    if (at >= Aa1) return;
-    const int s = blockIdx.y, per = (a.nblk + a.nslice - 1) / a.nslice;
-    const int b0 = s * per, b1 = min(a.nblk, b0 + per);
-    uint64_t c = 0, t = 0;
-#pragma unroll 4
-    for (int b = b0; b < b1; b++) {
-        const uint64_t v = w.rows[(int64_t)b * Aa1 + at];
-        c += v >> 44;
-        t += v & kSumMask;
+// --------------------------------------------------------------------- group
+// Group g: the sums of block vectors kGroup g .. kGroup g + kGroup - 1 in block
+// order (flags or-ed), one thread per vector entry.
+__global__ __launch_bounds__(256) void k_dda_group(DdaArgs a, const double* __restrict__ part,
+                                                   double* __restrict__ grp) {
+    const int ps = part_stride(a.G), g = blockIdx.x;
+    const int b0 = g * kGroup, nb = min(kGroup, a.nblk - b0);
+    for (int e = threadIdx.x; e < ps; e += 256) {
+        double v[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; u++) v[u] = part[(int64_t)(b0 + min(u, nb - 1)) * ps + e];
+        double t = 0.0;
+        uint32_t fl = 0;
+#pragma unroll
+        for (int u = 0; u < kGroup; u++)
+            if (u < nb) { t += v[u]; fl |= (uint32_t)v[u]; }
+        grp[(int64_t)g * ps + e] = (e == ps - 1) ? (double)fl : t;
     }
-    w.rcnt[(int64_t)s * Aa1 + at] = c;
-    w.rsum[(int64_t)s * Aa1 + at] = t;
 }
 
 // ------------------------------------------------------------------ finalize
-// Dynamic LDS: C0 u64[Aa+2] (counts, then prefix sums of counts as fp64),
-// C1 u64[Aa+2] (significand sums, then prefix sums of |x|), Dv double[G],
-// rk i32[A] (cell starts, when they fit).
+// Threads per candidate: enough that no thread sums more than 8 block vectors,
+// at most 16 and at most kFinThreads / G.
+__host__ __device__ inline int fin_split(int G, int nblk) {
+    int S = 1;
+    while (S < 16 && S * 8 < nblk && 2 * S * G <= kFinThreads) S *= 2;
+    return S;
+}
+
+// One block of G * S threads (rounded up to whole waves).  Thread (j, p) sums
+// the vectors of blocks p, p + S, p + 2S, ... in that order, then the S partial
+// sums of a candidate combine in a fixed butterfly; D_j = S2 + a (a B_j - 2 A_j)
+// and the argmin over (isnan(D), D, j), ties to the lowest index.
 __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
-                                                              DdaArgs a, DdaWs w,
+                                                              DdaArgs a,
+                                                              const double* __restrict__ part,
                                                               float* __restrict__ alpha_out,
                                                               double* __restrict__ D_out) {
-    extern __shared__ __align__(16) unsigned char smem[];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int G = a.G, M = a.M, A = a.A;
-    const int S = a.Aa + 1;                 // row stride; atoms 0 .. Ap <= Aa
-    const int NA = a.Aa + 2;                // prefix entries 0 .. Aa+1
-    uint64_t* C0 = (uint64_t*)smem;
-    uint64_t* C1 = C0 + NA;
-    double* P0 = (double*)C0;
-    double* P1 = (double*)C1;
-    double* Dv = (double*)(C1 + NA);
-    int32_t* rk = (int32_t*)(Dv + G);
-    __shared__ double s_d[3][16];
-    __shared__ uint32_t s_u[16];
-    __shared__ float s_q[128];
-    __shared__ float s_grid[kDdaMaxG];
-
-    // ---- 1. every global read is requested before any is used: the row
-    //         entries of this thread's first atom, the candidate scales, the
-    //         block scalars, the bounds of this thread's atoms (the contiguous
-    //         range of step 3), the cell starts
-    const uint32_t afin = w.meta[0];
-    const bool sliced = a.nslice > 0;
-    static_assert(2 * kReduceSlices <= kPackedMaxBlocks, "slice counts and sums share rv");
-    uint64_t rv[kPackedMaxBlocks];     // packed rows, or the slice counts then sums
-    if (tid < S) {
-        if (sliced) {
-#pragma unroll
-            for (int r = 0; r < kReduceSlices; r++) {
-                rv[r] = w.rcnt[(int64_t)r * S + tid];
-                rv[kReduceSlices + r] = w.rsum[(int64_t)r * S + tid];
-            }
-        } else {
-#pragma unroll
-            for (int r = 0; r < kPackedMaxBlocks; r++)
-                rv[r] = r < a.nblk ? w.rows[(int64_t)r * S + tid] : 0ull;
-        }
-    }
-    for (int j = tid; j < G; j += kFinThreads) s_grid[j] = grid[j];
-    constexpr int kPerMax = 9;                       // atoms per thread, (Aa+2)/1024 <= 9
-    const int per = (NA + kFinThreads - 1) / kFinThreads;
-    uint32_t ub[kPerMax];
-#pragma unroll
-    for (int e = 0; e < kPerMax; e++) {
-        const int at = tid * per + e;
-        ub[e] = (e < per && at < NA) ? w.ubits[at] : 0u;
-    }
-    double sc[3] = {0.0, 0.0, 0.0};
+    const int G = a.G, nb = a.nblk, ps = part_stride(G);
+    const int S = fin_split(G, nb);
+    const int p = tid & (S - 1), j = tid / S;
+    const bool live = j < G;
+    const float al = live ? grid[j] : 0.0f;
+    double A = 0.0, B = 0.0, S2 = 0.0;
     uint32_t fl = 0;
-    for (int b = tid; b < a.nblk; b += kFinThreads) {
-        const double* ps = w.pscal + 4 * (int64_t)b;
-        sc[0] += ps[0]; sc[1] += ps[1]; sc[2] += ps[2]; fl |= (uint32_t)ps[3];
-    }
-    if (a.rk_lds)
-        for (int i = tid; i < A; i += kFinThreads) rk[i] = w.rank[i];
-    if (tid <= M) s_q[tid] = set_value(tid, a.k);
-
-    // ---- 2. per-atom integer sums over the packed rows or the slices, one
-    //         thread per atom (coalesced across threads)
-    if (tid < S) {
-        uint64_t c = 0, t = 0;
-        if (sliced) {
+    if (live) {
+        for (int b0 = p; b0 < nb; b0 += 8 * S) {    // eight vectors in flight
+            double v[8][4];
 #pragma unroll
-            for (int r = 0; r < kReduceSlices; r++) { c += rv[r]; t += rv[kReduceSlices + r]; }
-        } else {
-#pragma unroll
-            for (int r = 0; r < kPackedMaxBlocks; r++) { c += rv[r] >> 44; t += rv[r] & kSumMask; }
-        }
-        C0[tid] = c;
-        C1[tid] = t;
-    }
-    for (int at = tid + kFinThreads; at < S; at += kFinThreads) {
-        uint64_t c = 0, t = 0;
-        if (sliced) {
-#pragma unroll 8
-            for (int r = 0; r < a.nslice; r++) {
-                c += w.rcnt[(int64_t)r * S + at];
-                t += w.rsum[(int64_t)r * S + at];
+            for (int u = 0; u < 8; u++) {
+                const int b = min(b0 + u * S, nb - 1);
+                const double* r = part + (int64_t)b * ps;
+                v[u][0] = r[j]; v[u][1] = r[G + j]; v[u][2] = r[2 * G]; v[u][3] = r[2 * G + 1];
             }
-        } else {
-#pragma unroll 8
-            for (int r = 0; r < a.nblk; r++) {
-                const uint64_t v = w.rows[(int64_t)r * S + at];
-                c += v >> 44;
-                t += v & kSumMask;
-            }
-        }
-        C0[at] = c;
-        C1[at] = t;
-    }
-    // block scalars: fixed-order reduction
-    {
-        const double r0 = wave_scan_add(sc[0]), r1 = wave_scan_add(sc[1]), r2 = wave_scan_add(sc[2]);
-        const uint32_t rf = wave_scan_or(fl);
-        if (lane == 63) { s_d[0][wid] = r0; s_d[1][wid] = r1; s_d[2][wid] = r2; s_u[wid] = rf; }
-    }
-    lds_barrier();
-    double sumsq = 0.0, top_s1 = 0.0, top_c = 0.0;
-    uint32_t flags = 0;
 #pragma unroll
-    for (int v = 0; v < kFinThreads / 64; v++) {
-        sumsq += s_d[0][v]; top_s1 += s_d[1][v]; top_c += s_d[2][v]; flags |= s_u[v];
-    }
-
-    // ---- 3. per-atom S0, S1 (atom 0 carries q = 0 for everyone; the top atom
-    //         its fp64 sums) and exclusive prefix sums over atoms 0 .. afin+1
-    double s0[kPerMax], s1[kPerMax];
-    double m0 = 0.0, m1 = 0.0;
-#pragma unroll
-    for (int e = 0; e < kPerMax; e++) {
-        const int at = tid * per + e;
-        s0[e] = 0.0;
-        s1[e] = 0.0;
-        if (e < per && at < NA) {
-            if (at >= 1 && (uint32_t)at < afin) {
-                const uint64_t c = C0[at];
-                uint64_t t = C1[at];
-                const uint32_t ex = ub[e] >> 23;
-                if (ex) t += c << 23;                // the implicit bit of a normal binade
-                s0[e] = (double)c;
-                s1[e] = ldexp((double)t, (int)max(ex, 1u) - 150);
-            } else if (afin > 0 && (uint32_t)at == afin) {
-                s0[e] = top_c;
-                s1[e] = top_s1;
-            }
-            m0 += s0[e];
-            m1 += s1[e];
+            for (int u = 0; u < 8; u++)
+                if (b0 + u * S < nb) {
+                    A += v[u][0]; B += v[u][1]; S2 += v[u][2]; fl |= (uint32_t)v[u][3];
+                }
         }
     }
-    {
-        const double i0 = wave_scan_add(m0), i1 = wave_scan_add(m1);
-        lds_barrier();   // s_d reused; C0/C1 reads above are done
-        if (lane == 63) { s_d[0][wid] = i0; s_d[1][wid] = i1; }
-        lds_barrier();
-        double r0 = i0 - m0, r1 = i1 - m1;
-        for (int v = 0; v < wid; v++) { r0 += s_d[0][v]; r1 += s_d[1][v]; }
-#pragma unroll
-        for (int e = 0; e < kPerMax; e++) {
-            const int at = tid * per + e;
-            if (e < per && at < NA) {
-                P0[at] = r0;
-                P1[at] = r1;
-                r0 += s0[e];
-                r1 += s1[e];
-            }
-        }
+    for (int o = 1; o < S; o <<= 1) {               // the S lanes of a candidate are adjacent
+        A += __shfl_xor(A, o);
+        B += __shfl_xor(B, o);
+        S2 += __shfl_xor(S2, o);
+        fl |= (uint32_t)__shfl_xor((int)fl, o);
     }
-    lds_barrier();
-
-    // ---- 4. per candidate: cells as atom ranges [start_c, start_{c+1}), the last to afin+1
-    const int32_t* rks = a.rk_lds ? rk : w.rank;
-    for (int j = tid; j < G; j += kFinThreads) {
-        const int32_t* rkj = rks + (int64_t)j * M;
-        const int end = (int)afin + 1;
-        double Aj = 0.0, Bj = 0.0;
-        int start = min(rkj[0], end);
-        for (int c = 1; c <= M; c++) {
-            const int next = (c < M) ? min(rkj[c], end) : end;
-            const double q = (double)s_q[c];
-            Aj = fma(q, P1[next] - P1[start], Aj);
-            Bj = fma(q * q, P0[next] - P0[start], Bj);
-            start = next;
-        }
-        const float al = s_grid[j];
+    double bd = __builtin_nan("");
+    int bj = 0x7fffffff;                            // none
+    float ba = 0.0f;
+    if (live && p == 0) {
         const double ad = (double)al;
-        double D = fma(ad, fma(ad, Bj, -2.0 * Aj), sumsq);
-        if (!alpha_ok(al) || (flags & 2u)) D = __builtin_nan("");
-        else if (flags & 1u) D = __builtin_inf();
-        Dv[j] = D;
+        double D = fma(ad, fma(ad, B, -2.0 * A), S2);
+        if (!alpha_ok(al) || (fl & 2u)) D = __builtin_nan("");
+        else if (fl & 1u) D = __builtin_inf();
         if (D_out) D_out[j] = D;
+        bd = D; bj = j; ba = al;
     }
+    auto pick = [](double& bd, int& bj, float& ba, double od, int oj, float oa) {
+        const bool onan = od != od, mnan = bd != bd;
+        const bool better = (oj != 0x7fffffff) &&
+                            ((bj == 0x7fffffff) || (!onan && mnan) ||
+                             (onan == mnan && (od < bd || (od == bd && oj < bj))));
+        if (better) { bd = od; bj = oj; ba = oa; }
+    };
+    for (int off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_xor(bd, off);
+        const int oj = __shfl_xor(bj, off);
+        const float oa = __shfl_xor(ba, off);
+        pick(bd, bj, ba, od, oj, oa);
+    }
+    if (blockDim.x == 64) {
+        if (lane == 0) *alpha_out = ba;
+        return;
+    }
+    __shared__ double s_bd[kFinThreads / 64];
+    __shared__ int s_bj[kFinThreads / 64];
+    __shared__ float s_ba[kFinThreads / 64];
+    if (lane == 0) { s_bd[wid] = bd; s_bj[wid] = bj; s_ba[wid] = ba; }
     lds_barrier();
-    if (tid < 64) {
-        // argmin over (isnan(D), D, j) in lexicographic order: the smallest index
-        // with the least D, NaN ranking above every number
-        double bd = __builtin_nan("");
-        int bj = 0x7fffffff;
-        for (int jj = tid; jj < G; jj += 64) {
-            const double d = Dv[jj];
-            const bool better = (d < bd) || (bd != bd && d == d) || (bj == 0x7fffffff);
-            if (better) { bd = d; bj = jj; }
-        }
-        for (int off = 32; off > 0; off >>= 1) {
-            const double od = __shfl_xor(bd, off);
-            const int oj = __shfl_xor(bj, off);
-            const bool onan = od != od, mnan = bd != bd;
-            const bool better = (!onan && mnan) || (onan == mnan && (od < bd || (od == bd && oj < bj))) ||
-                                (onan && mnan && oj < bj);
-            if (better) { bd = od; bj = oj; }
-        }
-        if (tid == 0) *alpha_out = s_grid[bj];
+    if (tid == 0) {
+        for (int v = 1; v < (int)(blockDim.x / 64); v++) pick(bd, bj, ba, s_bd[v], s_bj[v], s_ba[v]);
+        *alpha_out = ba;
     }
 }
 
@@ -890,29 +828,25 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
     a.n = f.n; a.k = f.k;
     dda_blocks(len, &a.nblk, &a.rows_pb);
     a.lbins = hist_lbins(L.A, a.rows_pb >= 8);
-    a.nslice = a.nblk > kPackedMaxBlocks ? kReduceSlices : 0;
-    a.rk_lds = 0;
-    const DdaWs w = ws_ptrs(ws, L);
+    double* part = (double*)((char*)ws + L.off_part);
+    double* grp = (double*)((char*)ws + L.off_group);
     static bool lds_attr_set[64] = {false};
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
         hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 156 * 1024);
         if (e != hipSuccess) return e;
-        e = hipFuncSetAttribute((const void*)k_dda_finalize,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
-        if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
-    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A, a.lbins).total, s>>>(x, len, grid, a, w);
-    if (a.nslice > 0) {
-        dim3 rg((a.Aa + 1 + 255) / 256, a.nslice);
-        k_dda_reduce<<<rg, 256, 0, s>>>(a, w);
+    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A, a.lbins).total, s>>>(x, len, grid, a, part);
+    const int ng = dda_groups(a.nblk);
+    if (ng > 0) {
+        k_dda_group<<<ng, 256, 0, s>>>(a, part, grp);
+        part = grp;
+        a.nblk = ng;                 // the finalize reads the group vectors
     }
-    size_t fin_lds = sizeof(uint64_t) * 2 * (size_t)(a.Aa + 2) + sizeof(double) * (size_t)G;
-    a.rk_lds = fin_lds + sizeof(int32_t) * (size_t)a.A <= 150 * 1024;
-    if (a.rk_lds) fin_lds += sizeof(int32_t) * (size_t)a.A;
-    k_dda_finalize<<<1, kFinThreads, fin_lds, s>>>(grid, a, w, alpha_out, D_out);
+    const int nt = (G * fin_split(G, a.nblk) + 63) / 64 * 64;   // <= kFinThreads
+    k_dda_finalize<<<1, nt, 0, s>>>(grid, a, part, alpha_out, D_out);
     return hipGetLastError();
 }
 

@@ -51,8 +51,7 @@ constexpr int kDdaMaxBlocks = 256;
 struct DdaLayout {
     int G, M, A;            // candidates, midpoints per candidate, thresholds (G*M)
     int nblk;               // blocks of the one-pass histogram kernel
-    size_t off_ubits, off_rank, off_bins, off_meta, off_pcnt, off_psum, off_pscal,
-        off_s0, off_s1, total;
+    size_t off_part, off_group, total;   // block and group partial objectives; bytes
 };
 bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L);
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
