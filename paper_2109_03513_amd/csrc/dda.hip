@@ -242,7 +242,7 @@ static inline int hist_lbins(int A, bool large) {
 struct HistLds {
     size_t u, th, kh, total;
 };
-__host__ __device__ static inline int hist_lcopies(int A) { return A <= 960 ? 2 : 0; }
+__host__ __device__ static inline int hist_lcopies(int A) { return A <= 256 ? 4 : (A <= 960 ? 2 : 0); }
 __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
     HistLds h;
     const size_t Aa = (size_t)A + kMaxSplits;
