@@ -177,7 +177,7 @@ def main():
         "project_w": ("esb_project(w): k_project_vec", "hbm", 5.0 * nel_w),
         "project_x": ("esb_project(x): k_project_vec", "hbm", 5.0 * nel_x),
         # conv: codes of x and w read once, fp32 y written once (AI below the int8 ridge)
-        "conv2d": ("esb_conv2d: k_contract", "hbm", 1.0 * nel_x + 1.0 * nel_w + 4.0 * M * Ncol),
+        "conv2d": ("esb_conv2d: k_mma 64x64", "hbm", 1.0 * nel_x + 1.0 * nel_w + 4.0 * M * Ncol),
     }
     dom = int(np.argmax(stage_ms))
     kname, bound, nbytes = groups[stages[dom]]

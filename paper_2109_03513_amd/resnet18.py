@@ -14,6 +14,9 @@ average pool) is plain tensor work done with torch on the same stream: the
 average is a float64 sum of the 7x7 window divided by 49 and rounded to fp32
 once.  No batch normalization (the weights are He-initialized).
 
+A downsample conv reads the same block input as the block's first conv, so it
+reuses that conv's alpha and codes instead of quantizing the tensor again.
+
 Activations are NHWC fp32; codes NHWC uint8; weights KRSC.
 """
 import numpy as np
@@ -96,14 +99,17 @@ class ResNet18ESB:
         codes = esb.esb_project(x, alpha, self.n, self.ks, stream=self.sh)
         return alpha, codes
 
-    def conv(self, name, x):
+    def conv(self, name, x, quantized=None):
+        """The layer on input x; `quantized` = (alpha, codes) of x when another layer
+        already quantized this same tensor (the DDA and the projection depend on x only)."""
         L = self.layers[name]
-        ax, cx = self._quantize(x, self.ws[name])
+        ax, cx = quantized if quantized is not None else self._quantize(x, self.ws[name])
         acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"],
                                 stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
                                 want_acc=self.record, stream=self.sh, workspace=self.cws)
         if self.record:
             self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
+        self.last_q = (ax, cx)
         return y
 
     def forward(self, x):
@@ -116,8 +122,10 @@ class ResNet18ESB:
             for blk in (0, 1):
                 p = "l%d.%d." % (stage, blk)
                 out = torch.relu(self.conv(p + "c1", a))
+                qa = self.last_q                     # the block input, quantized for c1
                 out = self.conv(p + "c2", out)
-                sc = self.conv(p + "ds", a) if (p + "ds") in self.layers else a
+                # the downsample conv reads the same block input: its quantization is reused
+                sc = self.conv(p + "ds", a, quantized=qa) if (p + "ds") in self.layers else a
                 a = torch.relu(out + sc)
         feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
         af, cf = self._quantize(feat, self.ws["fc"])
