@@ -172,12 +172,14 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
     if (lda > 0x7fffffff) return ESB_E_INVALID;
     const int op = mma_choose(fa, fb, K);
+    // decode-once formats: packed E2M1 where both formats fit it, else packed E2M3, else E4M3
     const bool f4 = mma_f4ok(fa, fb, K) && K % 32 == 0;
+    const bool f6 = !f4 && mma_f6ok(fa, fb, K) && K % 64 == 0 && mma_f6_tiles(M, N, 1);
     const hipStream_t s = (hipStream_t)stream;
     const bool fits = mma_fits(g, A, K, 1, B, ldb, b_layout);
     if (ws && fits && (f4 || op == 1) && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
         return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb, alphaB,
-                                         acc, y, ldc, f4, ws, s));
+                                         acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, s));
     if (op >= 0 && fits)
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
                                      ldc, s));
@@ -253,12 +255,13 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
         return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
     const int op = mma_choose(fx, fw, kred);
     const bool f4 = mma_f4ok(fx, fw, kred) && g.Cg % 32 == 0;
+    const bool f6 = !f4 && mma_f6ok(fx, fw, kred) && g.Cg % 64 == 0 && mma_f6_tiles(Mrows, Kg, d->groups);
     const bool fits = mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK);
     const int64_t xel = (int64_t)d->N * d->H * d->W * d->C, wel = (int64_t)d->K * kred;
     if (ws && fits && (f4 || op == 1) && pre_worth(Mrows, d->K, kred, xel, wel))
         return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
                                          (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w, d->K,
-                                         kred, fw, alphaW, acc, y, d->K, f4, ws, s));
+                                         kred, fw, alphaW, acc, y, d->K, f4 ? 1 : (f6 ? 2 : 0), ws, s));
     if (op >= 0 && fits)
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
                                      kred, fw, alphaW, acc, y, d->K, s));

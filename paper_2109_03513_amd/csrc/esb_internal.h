@@ -101,17 +101,22 @@ hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& g
 // E4M3 into a workspace of mma_pre_workspace() bytes; A is a_rows rows of a_cols
 // codes with pitch a_pitch (GEMM: M x K; convolution: the N*H*W pixels of C
 // channels), B is b_rows rows of K codes with pitch ldb.
-// f4: both formats lie inside OCP E2M1 (mma_f4ok) and the operands are decoded
-// to packed E2M1 instead (half the bytes, fp4 MFMAs); a_cols and K are then
-// multiples of 32.
+// mode 1: both formats lie inside OCP E2M1 (mma_f4ok) and the operands are
+// decoded to packed E2M1 instead (half the bytes, fp4 MFMAs); a_cols and K are
+// then multiples of 32.  mode 2: both inside OCP E2M3 (mma_f6ok), packed E2M3
+// (3/4 of the bytes, fp6 MFMAs); K a multiple of 64 and, for a convolution,
+// the channels per group too.  mode 0: E4M3.
 size_t mma_pre_workspace(int64_t a_rows, int64_t a_cols, int64_t b_rows, int64_t K);
 MmaDecode mma_decode_f4(const Fmt& f);
 bool mma_f4ok(const Fmt& fa, const Fmt& fb, int64_t K);
+MmaDecode mma_decode_f6(const Fmt& f);
+bool mma_f6ok(const Fmt& fa, const Fmt& fb, int64_t K);
+bool mma_f6_tiles(int64_t M, int64_t N, int groups);
 hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, const uint8_t* A,
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          bool f4, void* ws, hipStream_t s);
+                          int mode, void* ws, hipStream_t s);
 
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,

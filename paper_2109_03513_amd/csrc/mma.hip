@@ -50,6 +50,7 @@ struct FastParams {
     const uint8_t* A;
     const uint8_t* B;
     int64_t ldb;
+    int64_t blkA, blkB;     // packed E2M3: bytes of one 48-byte stage block of every row
     MmaDecode da, db;
     const float* alphaA;
     const float* alphaB;
@@ -72,6 +73,17 @@ __device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
 __device__ __forceinline__ uint32_t dec_f4(uint32_t c, const MmaDecode& d) {
     const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;
     return ((c << d.shs) & 0x08080808u) | t;
+}
+
+// Four codes to four OCP E2M3 values (low six bits of each byte), value q
+// exactly: the exponent-field increment on a 3-bit fraction, sign to bit 5.
+__device__ __forceinline__ uint32_t dec_f6(uint32_t c, const MmaDecode& d) {
+    const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;
+    return ((c << d.shs) & 0x20202020u) | t;
+}
+// Four 6-bit values (one per byte) into the low 24 bits, value 0 lowest.
+__device__ __forceinline__ uint32_t pack6(uint32_t v) {
+    return (v & 0x3fu) | ((v >> 2) & 0xfc0u) | ((v >> 4) & 0x3f000u) | ((v >> 6) & 0xfc0000u);
 }
 
 __device__ __forceinline__ uint32_t dec_i8(uint32_t c, const MmaDecode& d) {
@@ -462,6 +474,44 @@ __global__ __launch_bounds__(256) void k_decode_fp4(DecodeJob j0, DecodeJob j1) 
     }
 }
 
+// Rows of codes to packed E2M3 in stage blocks: the 64 codes 64b .. 64b+63 of
+// row r become 48 bytes at dst + (b * rows + r) * 48, so that the rows of one
+// contraction stage are one contiguous run of memory.  Within each 24-byte
+// half, value i sits at bits 6i .. 6i+5 (little endian).  One item per (block,
+// row), rows fastest, so that a wave writes 3 KB of contiguous memory; here
+// cols16 counts blocks of 64 codes per row.
+__device__ __forceinline__ void pack24(const uint4& a, const uint4& b, const MmaDecode& d, uint32_t* o) {
+    const uint32_t w0 = pack6(dec_f6(a.x, d)), w1 = pack6(dec_f6(a.y, d));
+    const uint32_t w2 = pack6(dec_f6(a.z, d)), w3 = pack6(dec_f6(a.w, d));
+    const uint32_t w4 = pack6(dec_f6(b.x, d)), w5 = pack6(dec_f6(b.y, d));
+    const uint32_t w6 = pack6(dec_f6(b.z, d)), w7 = pack6(dec_f6(b.w, d));
+    o[0] = w0 | (w1 << 24);
+    o[1] = (w1 >> 8) | (w2 << 16);
+    o[2] = (w2 >> 16) | (w3 << 8);
+    o[3] = w4 | (w5 << 24);
+    o[4] = (w5 >> 8) | (w6 << 16);
+    o[5] = (w6 >> 16) | (w7 << 8);
+}
+__global__ __launch_bounds__(256) void k_decode_fp6(DecodeJob j0, DecodeJob j1) {
+    const int64_t n0 = j0.rows * j0.cols16, n = n0 + j1.rows * j1.cols16;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
+        const bool second = t >= n0;
+        const DecodeJob& j = second ? j1 : j0;
+        const int64_t u = second ? t - n0 : t;
+        const int64_t b = u / j.rows, r = u - b * j.rows;
+        const uint4* p = (const uint4*)(j.src + r * j.pitch + 64 * b);
+        const uint4 c0 = p[0], c1 = p[1], c2 = p[2], c3 = p[3];
+        uint32_t o[12];
+        pack24(c0, c1, j.d, o);
+        pack24(c2, c3, j.d, o + 6);
+        uint4* q = (uint4*)(j.dst + u * 48);
+        q[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        q[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        q[2] = make_uint4(o[8], o[9], o[10], o[11]);
+    }
+}
+
 // DMA layout: one global_load_lds of a wave writes 1 KB = 16 tile rows of 64
 // bytes; lane l lands at row 16 q + l / 4, physical chunk l % 4, which under
 // the swizzle of lds_off holds logical chunk (l % 4) ^ ((l / 16) % 4) — the same
@@ -686,6 +736,208 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
             }
 }
 
+// Packed E2M3 operands (fp6): a stage is 64 reduction values = 48 bytes of
+// every tile row, kept unswizzled in LDS (rows of 48 bytes, 12 banks apart:
+// at most two lanes of a half-wave share a bank).  The DMA of a stage is
+// (BM + BN) * 48 / 1024 wave instructions, CT per wave; each lane serves one
+// 16-byte piece of one row per instruction.  An instruction never straddles
+// the A/B boundary (BM * 48 is a multiple of 1024).  In the stage-blocked
+// layout of k_decode_fp6 consecutive rows of a stage are contiguous, so an
+// instruction reads whole 64-byte segments.  Convolution needs Cg % 64 == 0,
+// so that a stage lies inside one filter tap (r, s): every lane of a stage
+// then shares (r, s, channel block).  MFMA: 32x32x64 with
+// cbsz = blgp = 2 (E2M3), six operand VGPRs; the MFMAs of a stage come in two
+// parts around the barrier as in k_mma_pre.
+template <int BM, int BN, int WGM, int WGN, int CONV, int R>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_mma_f6(FastParams g) {
+    constexpr int NW = WGM * WGN;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int TI = WM / 32, TJ = WN / 32;
+    constexpr int RB = 48;                                // bytes per row per stage
+    constexpr int NI = (BM + BN) * RB / 1024, CT = NI / NW;
+    static_assert(CT * NW == NI && (BM * RB) % 1024 == 0, "whole DMA instructions per wave");
+    constexpr int TILE = (BM + BN) * RB;
+    static_assert(R >= 2 && R <= 6, "ring depth");
+    __shared__ __align__(16) uint8_t ring[R * TILE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int tm, tn;
+    tile_of(g, tm, tn);
+    const int grp = blockIdx.z;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int wr = (wave / WGN) * WM, wc = (wave % WGN) * WN;
+    const ConvGeom& cg = g.ga;
+    const int64_t brow0 = (int64_t)grp * g.N;
+
+    // per DMA instruction i of this wave: operand, row, 16-byte piece of the lane
+    int64_t off[CT];       // A: pixel-row or row byte offset; B: row byte offset (+ piece)
+    int ih0[CT], iw0[CT];  // convolution: input position of the output pixel
+    bool isa[CT], rok[CT];
+    int piece[CT];
+#pragma unroll
+    for (int i = 0; i < CT; i++) {
+        const int o = 1024 * (wave + i * NW) + 16 * lane;
+        isa[i] = o < BM * RB;
+        const int ob = isa[i] ? o : o - BM * RB;
+        const int row = ob / RB;
+        piece[i] = ob - row * RB;
+        ih0[i] = iw0[i] = 0;
+        if (isa[i]) {
+            const int m = m0 + row;
+            rok[i] = m < g.M;
+            if (CONV) {
+                const int mm = rok[i] ? m : 0;
+                const int pq = cg.P * cg.Q;
+                const int img = mm / pq, rem = mm - img * pq;
+                const int p = rem / cg.Q, q = rem - p * cg.Q;
+                ih0[i] = rok[i] ? p * cg.sh - cg.ph : -0x40000000;
+                iw0[i] = q * cg.sw - cg.pw;
+                off[i] = (((int64_t)img * cg.H + ih0[i]) * cg.W + iw0[i]) * RB + piece[i];
+            } else {
+                off[i] = (int64_t)(rok[i] ? m : 0) * RB + piece[i];
+            }
+        } else {
+            const int nn = n0 + row;
+            rok[i] = nn < g.N;
+            off[i] = (brow0 + (rok[i] ? nn : 0)) * RB + piece[i];
+        }
+    }
+    const uint8_t* z = kZeroRows.b[kZeroRowE4M3];   // 0x00: E2M3 +0
+    const int KT = g.K / RB;                          // whole stages (K % 64 == 0 values)
+    const int nbc = cg.Cg / RB;                       // convolution: stage blocks per tap
+    int kr = 0, ks = 0, kb = 0;                       // convolution: tap and block of the next fetch
+
+    auto fetch = [&](int st, uint8_t* slot) {
+        const bool kin = st < KT;
+        const int64_t kA = (int64_t)st * g.blkA, kB = (int64_t)st * g.blkB;
+        int64_t koff = 0;
+        if (CONV) koff = ((int64_t)kr * cg.W + ks) * RB + (int64_t)(grp * nbc + kb) * g.blkA;
+#pragma unroll
+        for (int i = 0; i < CT; i++) {
+            bool ok = kin && rok[i];
+            const uint8_t* src;
+            if (isa[i]) {
+                if (CONV) {
+                    const int ih = ih0[i] + kr, iw = iw0[i] + ks;
+                    ok = ok && (unsigned)ih < (unsigned)cg.H && (unsigned)iw < (unsigned)cg.W;
+                    src = g.A + off[i] + koff;
+                } else {
+                    src = g.A + off[i] + kA;
+                }
+            } else {
+                src = g.B + off[i] + kB;
+            }
+            dma16(ok ? src : z, slot + 1024 * (wave + i * NW));
+        }
+        if (CONV) {
+            if (++kb == nbc) {
+                kb = 0;
+                if (++ks == cg.S) { ks = 0; ++kr; }
+            }
+        }
+    };
+
+    v16f acc[TI][TJ];
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[i][j][r] = 0.0f;
+
+    constexpr int TI0 = (TI + 1) / 2;
+    const int lr = lane & 31, lg = lane >> 5;
+    v8i fa[TI], fb[2][TJ];
+    // (native vector loads through pointers into the ring: with HIP's struct
+    // uint2 the compiler loses track of the address and waits for every DMA in
+    // flight before the read)
+    typedef int v2i __attribute__((ext_vector_type(2)));
+    auto frag6 = [&](const uint8_t* t, int row) {   // 24 bytes: 32 values of this half of the stage
+        const v2i* p = (const v2i*)(t + row * RB + 24 * lg);
+        const v2i x0 = p[0], x1 = p[1], x2 = p[2];
+        return v8i{x0[0], x0[1], x1[0], x1[1], x2[0], x2[1], 0, 0};
+    };
+    auto read0 = [&](const uint8_t* d, auto PAR) {
+        constexpr int par = decltype(PAR)::value;
+#pragma unroll
+        for (int j = 0; j < TJ; j++) fb[par][j] = frag6(d + BM * RB, wc + 32 * j + lr);
+#pragma unroll
+        for (int i = 0; i < TI0; i++) fa[i] = frag6(d, wr + 32 * i + lr);
+    };
+    auto read1 = [&](const uint8_t* d) {
+#pragma unroll
+        for (int i = TI0; i < TI; i++) fa[i] = frag6(d, wr + 32 * i + lr);
+    };
+    auto mfma = [&](auto PART, auto PAR) {
+        constexpr int part = decltype(PART)::value, par = decltype(PAR)::value;
+#pragma unroll
+        for (int i = part ? TI0 : 0; i < (part ? TI : TI0); i++)
+#pragma unroll
+            for (int j = 0; j < TJ; j++)
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[par][j], acc[i][j],
+                                                                             2, 2, 0, 127, 0, 127);
+    };
+
+    static_for<0, R>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        fetch(q, ring + q * TILE);
+    });
+    vm_wait<(R - 1) * CT>();   // stage 0 landed
+    lds_barrier();
+    read0(ring, ic<0>{});
+    auto stage = [&](int st, auto PAR) {
+        constexpr int par = decltype(PAR)::value;
+        uint8_t* slot = ring + (st % R) * TILE;
+        mfma(ic<0>{}, PAR);
+        read1(slot);
+        __builtin_amdgcn_sched_barrier(0);
+        vm_wait<(R - 2) * CT>();       // this thread's part of stage st+1 landed
+        lds_barrier();                 // all of it; every read of this slot is done
+        fetch(st + R, slot);
+        read0(ring + ((st + 1) % R) * TILE, ic<par ^ 1>{});
+        __builtin_amdgcn_sched_barrier(0);
+        mfma(ic<1>{}, PAR);
+    };
+    int st = 0;
+    for (; st + 1 < KT; st += 2) {
+        stage(st, ic<0>{});
+        stage(st + 1, ic<1>{});
+    }
+    if (st < KT) stage(st, ic<0>{});
+    vm_wait<0>();   // the fetches past the end (+0 rows) land before the workgroup ends
+
+    float s = 0.0f;
+    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int row = m0 + wr + 32 * i + 8 * (r >> 2) + 4 * lg + (r & 3);
+                const int col = n0 + wc + 32 * j + lr;
+                if (row < g.M && col < g.N) {
+                    const float fv = ldexpf(acc[i][j][r], g.out_shift);
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    if (g.acc) g.acc[o] = (int32_t)fv;
+                    if (g.y) g.y[o] = s * fv;
+                }
+            }
+}
+
+template <int BM, int BN, int WGM, int WGN, int R>
+hipError_t launch_f6_t(FastParams g, int groups, bool conv, hipStream_t s) {
+    g.tiles_m = (g.M + BM - 1) / BM;
+    g.tiles_n = (g.N + BN - 1) / BN;
+    g.ntiles = g.tiles_m * g.tiles_n;
+    dim3 grid(g.ntiles, 1, groups);
+    const int nt = 64 * WGM * WGN;
+    if (conv) k_mma_f6<BM, BN, WGM, WGN, 1, R><<<grid, nt, 0, s>>>(g);
+    else k_mma_f6<BM, BN, WGM, WGN, 0, R><<<grid, nt, 0, s>>>(g);
+    return hipGetLastError();
+}
+
 template <int BM, int BN, int WGM, int WGN, int R>
 hipError_t launch_pre_t(FastParams g, int groups, bool conv, bool f4, hipStream_t s) {
     g.tiles_m = (g.M + BM - 1) / BM;
@@ -783,6 +1035,30 @@ bool mma_f4ok(const Fmt& fa, const Fmt& fb, int64_t K) {
     return (double)K * (double)fa.max_int * (double)fb.max_int < 16777216.0;
 }
 
+// The fp6 path only for shapes that fill the chip with 256 x 256 tiles: there
+// it matches the E4M3 path (kernel ~7 % faster, decode as fast); the smaller
+// tiles that would fit its 48-byte rows run on four or two waves and lose.
+bool mma_f6_tiles(int64_t M, int64_t N, int groups) {
+    return N > 128 && ((M + 255) / 256) * ((N + 255) / 256) * groups >= num_cus();
+}
+
+MmaDecode mma_decode_f6(const Fmt& f) {
+    MmaDecode d{};
+    const uint32_t rep = 0x01010101u;
+    d.shf = 3 - f.k;                                     // fraction to E2M3's three bits
+    d.lm = ((1u << (f.n - 1)) - 1u) * rep;
+    d.inc = 0x08u * rep;                                 // + 1 in the exponent field
+    d.lmf = (((1u << (f.n - 1)) - 1u) << d.shf) * rep;
+    d.shs = 6 - f.n;                                     // sign to bit 5
+    return d;
+}
+
+bool mma_f6ok(const Fmt& fa, const Fmt& fb, int64_t K) {
+    auto in_e2m3 = [](const Fmt& f) { return f.ebits <= 2 && f.k <= 3; };
+    if (!in_e2m3(fa) || !in_e2m3(fb)) return false;
+    return (double)K * (double)fa.max_int * (double)fb.max_int < 16777216.0;
+}
+
 bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const uint8_t* B,
               int64_t ldb, int b_layout) {
     return b_layout == 0 && K > 0 && ga.Cg >= 16 && ga.Cg % 16 == 0 && ga.pitch % 16 == 0 &&
@@ -800,41 +1076,49 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          bool f4, void* ws, hipStream_t s) {
+                          int mode, void* ws, hipStream_t s) {
     if (M <= 0 || N <= 0) return hipSuccess;
     const bool conv = !(ga.H == 1 && ga.W == 1 && ga.R == 1 && ga.S == 1 && ga.ph == 0 && ga.pw == 0 &&
                         ga.Cg == K && groups == 1);
-    // decoded bytes per code: 1 (E4M3) or 1/2 (E2M1); lengths below are in bytes
-    const int sh = f4 ? 1 : 0;
-    const int64_t a_bytes = a_cols >> sh, kbytes = (int64_t)K >> sh;
+    const bool f4 = mode == 1, f6 = mode == 2;
+    // decoded bytes per code: 1 (E4M3), 1/2 (E2M1) or 3/4 (E2M3); lengths below are in bytes
+    auto bytes = [&](int64_t codes) { return f4 ? codes / 2 : (f6 ? codes / 4 * 3 : codes); };
+    const int64_t a_bytes = bytes(a_cols), kbytes = bytes(K);
     uint8_t* dA = (uint8_t*)ws;
     uint8_t* dB = dA + (((size_t)a_rows * (size_t)a_bytes + 255) & ~(size_t)255);
-    const int grp = f4 ? 32 : 16;    // codes per decode item
-    DecodeJob j0{A, a_rows, a_cols / grp, a_pitch, f4 ? mma_decode_f4(fa) : mma_decode(fa, 1), dA};
-    DecodeJob j1{B, b_rows, (int64_t)K / grp, ldb, f4 ? mma_decode_f4(fb) : mma_decode(fb, 1), dB};
+    const int grp = f6 ? 64 : (f4 ? 32 : 16);    // codes per decode item
+    const MmaDecode da = f4 ? mma_decode_f4(fa) : (f6 ? mma_decode_f6(fa) : mma_decode(fa, 1));
+    const MmaDecode db = f4 ? mma_decode_f4(fb) : (f6 ? mma_decode_f6(fb) : mma_decode(fb, 1));
+    DecodeJob j0{A, a_rows, a_cols / grp, a_pitch, da, dA};
+    DecodeJob j1{B, b_rows, (int64_t)K / grp, ldb, db, dB};
     const int64_t items = j0.rows * j0.cols16 + j1.rows * j1.cols16;
     int64_t blocks = (items + 255) / 256;
     const int64_t cap = (int64_t)num_cus() * 16;
     if (blocks > cap) blocks = cap;
-    if (f4) k_decode_fp4<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
-    else k_decode_e4m3<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
+    const unsigned nb = (unsigned)(blocks < 1 ? 1 : blocks);
+    if (f4) k_decode_fp4<<<nb, 256, 0, s>>>(j0, j1);
+    else if (f6) k_decode_fp6<<<nb, 256, 0, s>>>(j0, j1);
+    else k_decode_e4m3<<<nb, 256, 0, s>>>(j0, j1);
     FastParams g;
     g.M = M; g.N = N; g.K = (int)kbytes; g.ga = ga;
     g.ga.pitch = (int)a_bytes;
-    g.ga.Cg = ga.Cg >> sh;
+    g.ga.Cg = (int)bytes(ga.Cg);
     g.A = dA; g.B = dB; g.ldb = kbytes;
+    g.blkA = a_rows * 48;
+    g.blkB = b_rows * 48;
     g.da = j0.d;
     g.db = j1.d;
     g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
     g.kA = fa.k; g.kB = fb.k;
-    // E4M3 holds q * 2^-6 per operand; E2M1 holds q itself
-    g.out_shift = fa.k + fb.k + (f4 ? 0 : 12);
+    // E4M3 holds q * 2^-6 per operand; E2M1 and E2M3 hold q itself
+    g.out_shift = fa.k + fb.k + ((f4 || f6) ? 0 : 12);
     g.zrowA = g.zrowB = kZeroRowE4M3;
     g.tiles_m = g.tiles_n = g.ntiles = 0;
     const int64_t cus = num_cus();
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn) * groups;
     };
+    if (f6) return launch_f6_t<256, 256, 2, 4, 4>(g, groups, conv, s);   // see mma_f6_tiles
     if (N > 128 && tiles(256, 256) >= cus) return launch_pre_t<256, 256, 2, 4, 4>(g, groups, conv, f4, s);
     if (N > 64 && tiles(256, 128) >= cus) return launch_pre_t<256, 128, 4, 2, 4>(g, groups, conv, f4, s);
     if (N > 64 && tiles(128, 128) >= cus / 2) return launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, f4, s);

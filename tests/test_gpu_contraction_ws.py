@@ -1,7 +1,8 @@
 """GPU contraction with a caller workspace (esb_gemm_ws, esb_conv2d_ws), where
-shapes with enough work per operand byte decode both operands once to E4M3
-ahead of the contraction: bit-exact int32 accumulators and fp32 outputs within
-1e-6 relative against the oracle, like the plain calls."""
+shapes with enough work per operand byte decode both operands once (to packed
+E2M1, packed E2M3 or E4M3, whichever holds both formats) ahead of the
+contraction: bit-exact int32 accumulators and fp32 outputs within 1e-6
+relative against the oracle, like the plain calls."""
 import numpy as np
 import pytest
 
@@ -40,6 +41,10 @@ def sampled_rows(M, tile):
     (2049, 2050, 416, (4, 2), (4, 2)),     # E2M1 (fp4) path: ESB(4,1) is exactly E2M1
     (2048, 2080, 576, (3, 2), (3, 1)),     # E2M1 path for the 3-bit formats
     (1537, 1600, 1024, (2, 1), (4, 2)),    # E2M1 path, mixed formats
+    (4097, 4100, 576, (5, 3), (5, 3)),     # E2M3 (fp6) path (256 x 256 tiles): nine stages, ragged
+    (4100, 4097, 1024, (6, 4), (6, 4)),    # E2M3 path, three fraction bits
+    (4097, 4100, 640, (5, 3), (3, 2)),     # E2M3 path, mixed formats
+    (2049, 2050, 576, (5, 3), (5, 3)),     # too few 256 x 256 tiles for the E2M3 path: E4M3
 ])
 def test_gemm_ws_sampled(esb, M, N, K, fa, fb):
     (bA, ksA), (bB, ksB) = fa, fb
@@ -75,6 +80,7 @@ def test_gemm_ws_equals_plain_and_reuse(esb):
     (8, 14, 14, 256, 256, 3, 1, 1),        # ResNet18 layer3 3x3 at batch 8
     (4, 15, 13, 128, 320, 3, 2, 1),        # stride 2, odd sizes, ragged N tile
     (2, 7, 7, 512, 512, 3, 1, 1),          # layer4 3x3
+    (64, 56, 56, 64, 256, 3, 1, 1),        # 784 tiles of 256 x 256: the E2M3 path for ESB(5,2)
 ])
 @pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1))])
 def test_conv_ws_parity(esb, case, fmt):
@@ -138,6 +144,24 @@ def test_gemm_ws_e2m1_spread_at_accumulator_bound(esb):
                           workspace=workspace(need))
     rows = np.array([0, 5, 1000, M - 1], dtype=np.int64)
     st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 4, 2, 0.37, 4, 2, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+def test_gemm_ws_e2m3_spread_at_accumulator_bound(esb):
+    """ESB(5,2) on the E2M3 (fp6) path (K % 64 == 0): products m_A*m_B from 1 to 784 in
+    one reduction and K * 784 just below 2^24 (every partial sum exact in fp32)."""
+    M, N, K = 4096, 4096, 21376
+    A = extreme_codes(5, 3, (M, K), 7)
+    B = extreme_codes(5, 3, (N, K), 8)
+    need = esb.esb_gemm_workspace_size(M, N, K, 5, 3, 5, 3)
+    assert need > 0
+    log("gemm_ws e2m3 spread M=%d N=%d K=%d" % (M, N, K))
+    acc, y = esb.esb_gemm(dev(A), 5, 3, scalar(0.37), dev(B), 5, 3, scalar(0.021),
+                          workspace=workspace(need))
+    rows = np.array([0, 3, 999, M - 1], dtype=np.int64)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 5, 3, 0.37, 5, 3, 0.021)
     assert st == 0
     np.testing.assert_array_equal(host(acc)[rows], oacc)
     assert_rel(host(y)[rows], oy, YREL, "y")
