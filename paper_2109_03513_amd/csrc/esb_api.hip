@@ -180,9 +180,9 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     if (ws && fits && (f4 || op == 1) && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
         return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb, alphaB,
                                          acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, s));
-    if (op >= 0 && fits)
+    if (op >= 0 && fits)   // with a workspace, skinny shapes split the reduction
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
-                                     ldc, s));
+                                     ldc, (int32_t*)ws, s));
     return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
                                          decode_info(fb), alphaB, acc, y, ldc, N, s));
 }
@@ -190,8 +190,19 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
 size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig) {
     if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig) || M < 0 || N < 0 || K < 0) return 0;
     const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
-    if (mma_choose(fa, fb, K) != 1 && !(mma_f4ok(fa, fb, K) && K % 32 == 0)) return 0;
-    return mma_pre_workspace(M, K, N, K);   // E4M3 size; packed E2M1 needs half
+    const int op = mma_choose(fa, fb, K);
+    size_t need = 0;
+    if (op == 1 || (mma_f4ok(fa, fb, K) && K % 32 == 0))
+        need = mma_pre_workspace(M, K, N, K);   // E4M3 size; packed E2M1 / E2M3 need less
+    if (op >= 0 && K % 16 == 0) {               // split reduction: int32 partial sums
+        int kc = K;
+        const int ks = mma_splitk(M, N, K, &kc);
+        if (ks > 1) {
+            const size_t p = (size_t)ks * (size_t)M * (size_t)N * sizeof(int32_t);
+            if (p > need) need = p;
+        }
+    }
+    return need;
 }
 
 int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
@@ -264,7 +275,7 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
                                          kred, fw, alphaW, acc, y, d->K, f4 ? 1 : (f6 ? 2 : 0), ws, s));
     if (op >= 0 && fits)
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
-                                     kred, fw, alphaW, acc, y, d->K, s));
+                                     kred, fw, alphaW, acc, y, d->K, nullptr, s));
     return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
                                          alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
                                          d->K, Kg, s));

@@ -92,10 +92,15 @@ int mma_choose(const Fmt& fa, const Fmt& fb, int64_t K);
 // Layout conditions of the path: 16-byte chunks of codes on both operands.
 bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const uint8_t* B,
               int64_t ldb, int b_layout);
+// part: a workspace of at least mma_splitk(...) * M * N int32 for a dense GEMM
+// whose reduction is split (NULL: no split).
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
                       const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
                       int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
-                      int64_t ldc, hipStream_t s);
+                      int64_t ldc, int32_t* part, hipStream_t s);
+// Ranges of the reduction split for a dense GEMM of this shape (1: none), and
+// their length.
+int mma_splitk(int64_t M, int64_t N, int64_t K, int* kchunk);
 
 // The same contraction (op 1 formats) with both operands first decoded once to
 // E4M3 into a workspace of mma_pre_workspace() bytes; A is a_rows rows of a_cols

@@ -51,6 +51,8 @@ struct FastParams {
     const uint8_t* B;
     int64_t ldb;
     int64_t blkA, blkB;     // packed E2M3: bytes of one 48-byte stage block of every row
+    int ksplit, kchunk;     // k_mma on a dense GEMM: reduction split in ksplit ranges of kchunk
+    int32_t* part;          // [ksplit][M][N] int32 partial sums (ksplit > 1)
     MmaDecode da, db;
     const float* alphaA;
     const float* alphaB;
@@ -230,7 +232,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int tm, tn;
     tile_of(g, tm, tn);
-    const int grp = blockIdx.z;
+    // convolution: blockIdx.z is the group; dense GEMM: the reduction range
+    const int grp = CONV ? (int)blockIdx.z : 0;
+    const int kz = CONV ? 0 : (int)blockIdx.z;
+    const int kbeg = kz * g.kchunk;
+    const int Kl = CONV ? g.K : min(g.K - kbeg, g.kchunk);   // reduction length of this workgroup
     const int m0 = tm * BM, n0 = tn * BN;
     const int wr = (wave / WGN) * WM, wc = (wave % WGN) * WN;
     const ConvGeom& cg = g.ga;
@@ -263,10 +269,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
         kr = rs / cg.S;
         ks = rs - kr * cg.S;
     }
-    const uint8_t* aptr = g.A + (int64_t)(m0 + row0) * cg.pitch + 16 * ch;
+    const uint8_t* aptr = g.A + (int64_t)(m0 + row0) * cg.pitch + 16 * ch + kbeg;
     const int64_t astep = (int64_t)RSTEP * cg.pitch;
     const int mrem = g.M - m0 - row0;   // dense: chunk i of A is inside M iff i * RSTEP < mrem
-    const uint8_t* bptr = g.B + (brow0 + n0 + row0) * g.ldb + 16 * ch;
+    const uint8_t* bptr = g.B + (brow0 + n0 + row0) * g.ldb + 16 * ch + kbeg;
     const int64_t bstep = (int64_t)RSTEP * g.ldb;
     const int nrem = g.N - n0 - row0;
     const uint8_t* zA = kZeroRows.b[g.zrowA];
@@ -274,7 +280,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
 
     // fetch the codes of reduction offset k0 into a raw buffer
     auto fetch = [&](int k0, uint8_t* rawbuf) {
-        const bool kin = k0 + 16 * ch < g.K;
+        const bool kin = k0 + 16 * ch < Kl;
         uint8_t* base = rawbuf + wave * 64 * 16;
         if (CONV) {
             const int64_t koff = ((int64_t)kr * cg.W + ks) * cg.pitch + kc;
@@ -373,7 +379,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
         }
     };
 
-    const int KT = (g.K + BK - 1) / BK;
+    const int KT = (Kl + BK - 1) / BK;
     static_for<0, R>([&](auto Q) { fetch(decltype(Q)::value * BK, RAW(Q)); });
     vm_wait<(R - 1) * CT>();   // stage 0 landed
     read_raw(RAW(ic<0>{}));
@@ -420,11 +426,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
                         iv = (int32_t)acc[i][j][r];
                         fv = (float)iv;
                     }
+                    if (!CONV && g.ksplit > 1) {          // partial sum of this range
+                        g.part[((int64_t)kz * g.M + row) * g.N + col] = iv;
+                        continue;
+                    }
                     const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = iv;
                     if (g.y) g.y[o] = s * fv;
                 }
             }
+}
+
+// Sum of the ksplit partial sums of every output, in range order (int32 and
+// exact: every partial and the total obey the accumulator bound), then the
+// epilogue of the contraction.
+__global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
+    const int64_t MN = (int64_t)g.M * g.N;
+    float s = 0.0f;
+    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < MN; e += stride) {
+        uint32_t u = 0;                                  // two's complement wrap-around
+        for (int z = 0; z < g.ksplit; z++) u += (uint32_t)g.part[z * MN + e];
+        const int32_t t = (int32_t)u;
+        const int64_t row = e / g.N, col = e - row * g.N;
+        const int64_t o = row * g.ldc + col;
+        if (g.acc) g.acc[o] = t;
+        if (g.y) g.y[o] = s * (float)t;
+    }
 }
 
 // ------------------------------------------------------ pre-decoded operands
@@ -962,14 +991,22 @@ hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
     g.tiles_m = (g.M + BM - 1) / BM;
     g.tiles_n = (g.N + BN - 1) / BN;
     g.ntiles = g.tiles_m * g.tiles_n;
-    dim3 grid(g.ntiles, 1, groups);
+    dim3 grid(g.ntiles, 1, conv ? groups : g.ksplit);
     if (conv) k_mma<BM, BN, WGM, WGN, OP, 1, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
     else k_mma<BM, BN, WGM, WGN, OP, 0, R><<<grid, 64 * WGM * WGN, 0, s>>>(g);
+    if (!conv && g.ksplit > 1) {
+        const int64_t MN = (int64_t)g.M * g.N;
+        int64_t nb = (MN + 255) / 256;
+        if (nb > 4 * num_cus()) nb = 4 * num_cus();
+        k_splitk_sum<<<(unsigned)nb, 256, 0, s>>>(g);
+    }
     return hipGetLastError();
 }
 
 template <int OP>
 hipError_t launch_op(const FastParams& g, int groups, hipStream_t s) {
+    if (g.ksplit > 1)   // the tiles mma_splitk planned with
+        return g.M > 64 ? launch_t<128, 64, 2, 2, OP, 4>(g, groups, s) : launch_t<64, 64, 2, 2, OP, 4>(g, groups, s);
     const int64_t cus = num_cus();
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * groups;
@@ -1104,6 +1141,7 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
     g.ga.pitch = (int)a_bytes;
     g.ga.Cg = (int)bytes(ga.Cg);
     g.A = dA; g.B = dB; g.ldb = kbytes;
+    g.ksplit = 1; g.kchunk = (int)kbytes; g.part = nullptr;
     g.blkA = a_rows * 48;
     g.blkB = b_rows * 48;
     g.da = j0.d;
@@ -1126,14 +1164,41 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
     return launch_pre_t<64, 64, 2, 2, 4>(g, groups, conv, f4, s);
 }
 
+// Split of the reduction for a dense GEMM with too few output tiles to fill
+// the chip (skinny shapes such as a fully connected layer at a small batch):
+// ranges of kchunk (a multiple of 64, at least 4 stages) so that tiles x
+// ranges reaches about two workgroups per CU; 1 when no split pays.
+int mma_splitk(int64_t M, int64_t N, int64_t K, int* kchunk) {
+    *kchunk = (int)K;
+    const int64_t cus = num_cus();
+    const int64_t bm = M > 64 ? 128 : 64;
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + 63) / 64);
+    if (2.0 * (double)M * (double)N * (double)K < 2147483648.0 || tiles * 2 >= cus) return 1;
+    int64_t ks = (2 * cus + tiles - 1) / tiles;
+    if (ks > K / 256) ks = K / 256;
+    if (ks > 16) ks = 16;
+    if (ks < 2) return 1;
+    const int64_t kc = ((K + ks - 1) / ks + 63) / 64 * 64;
+    *kchunk = (int)kc;
+    return (int)((K + kc - 1) / kc);
+}
+
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
                       const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
                       int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
-                      int64_t ldc, hipStream_t s) {
+                      int64_t ldc, int32_t* part, hipStream_t s) {
     if (M <= 0 || N <= 0) return hipSuccess;
     FastParams g;
     g.M = M; g.N = N; g.K = K; g.ga = ga;
     g.A = A; g.B = B; g.ldb = ldb;
+    g.ksplit = 1;
+    g.kchunk = K;
+    g.part = nullptr;
+    if (part && groups == 1) {
+        int kc = K;
+        const int ks = mma_splitk(M, N, K, &kc);
+        if (ks > 1) { g.ksplit = ks; g.kchunk = kc; g.part = part; }
+    }
     g.da = mma_decode(fa, op);
     g.db = mma_decode(fb, op);
     g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;

@@ -45,6 +45,9 @@ def sampled_rows(M, tile):
     (4100, 4097, 1024, (6, 4), (6, 4)),    # E2M3 path, three fraction bits
     (4097, 4100, 640, (5, 3), (3, 2)),     # E2M3 path, mixed formats
     (2049, 2050, 576, (5, 3), (5, 3)),     # too few 256 x 256 tiles for the E2M3 path: E4M3
+    (128, 4096, 9216, (3, 2), (3, 1)),     # AlexNet FC at batch 128: reduction split in 8 ranges
+    (100, 3000, 4160, (5, 3), (5, 3)),     # split reduction, E4M3 decode in LDS, ragged last range
+    (64, 2048, 8192, (3, 2), (3, 1)),      # 64 x 64 tiles, 16 ranges
 ])
 def test_gemm_ws_sampled(esb, M, N, K, fa, fb):
     (bA, ksA), (bB, ksB) = fa, fb
