@@ -1006,7 +1006,7 @@ hipError_t launch_t(FastParams g, int groups, hipStream_t s) {
 template <int OP>
 hipError_t launch_op(const FastParams& g, int groups, hipStream_t s) {
     if (g.ksplit > 1)   // the tiles mma_splitk planned with
-        return g.M > 64 ? launch_t<128, 64, 2, 2, OP, 4>(g, groups, s) : launch_t<64, 64, 2, 2, OP, 4>(g, groups, s);
+        return g.M > 64 ? launch_t<128, 128, 2, 4, OP, 4>(g, groups, s) : launch_t<64, 64, 2, 2, OP, 4>(g, groups, s);
     const int64_t cus = num_cus();
     auto tiles = [&](int bm, int bn) {
         return (int64_t)((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * groups;
@@ -1168,13 +1168,15 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
 // the chip (skinny shapes such as a fully connected layer at a small batch):
 // ranges of kchunk (a multiple of 64, at least 4 stages) so that tiles x
 // ranges reaches about one workgroup per CU (measured on the AlexNet FC at
-// batch 128: 4 ranges 24.5 us, 8 ranges 26.3, 16 ranges 36.5; more partial
-// sums cost more than the extra workgroups gain); 1 when no split pays.
+// batch 128 with 128 x 64 tiles: 4 ranges 24.5 us, 8 ranges 26.3, 16 ranges
+// 36.5; more partial sums cost more than the extra workgroups gain; 128 x 128
+// tiles on eight waves with 8 ranges: 24.0 us); 1 when no split pays.
 int mma_splitk(int64_t M, int64_t N, int64_t K, int* kchunk) {
     *kchunk = (int)K;
     const int64_t cus = num_cus();
     const int64_t bm = M > 64 ? 128 : 64;
-    const int64_t tiles = ((M + bm - 1) / bm) * ((N + 63) / 64);
+    const int64_t bn = M > 64 ? 128 : 64;
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (2.0 * (double)M * (double)N * (double)K < 2147483648.0 || tiles * 2 >= cus) return 1;
     int64_t ks = (cus + tiles - 1) / tiles;
     if (ks > K / 256) ks = K / 256;
