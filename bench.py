@@ -318,6 +318,18 @@ def sweep(args):
                                args.reps, stream)
             emit("gemm_" + name, ms, nbytes=float(M * K + N * K + 4 * M * N), ops=2.0 * M * N * K,
                  ms_without_workspace=round(ms0, 5))
+            if esb.esb_pack_size(N, K, fb[0], fb[1]) and esb.esb_gemm_packed_workspace_size(
+                    M, N, K, fa[0], fa[1], fb[0], fb[1]):
+                # weights packed once (4-bit storage), read in place by every call
+                Bp = esb.esb_pack(B, fb[0], fb[1])
+                wsp = torch.empty(esb.esb_gemm_packed_workspace_size(M, N, K, fa[0], fa[1], fb[0],
+                                                                     fb[1]),
+                                  dtype=torch.uint8, device=dev)
+                msp = time_launches(lambda: esb.esb_gemm_packed(A, fa[0], fa[1], a, Bp, fb[0], fb[1],
+                                                                a, wsp, y=y, want_acc=False,
+                                                                stream=sh), args.reps, stream)
+                emit("gemm_" + name + "_packed_weights", msp,
+                     nbytes=float(M * K + N * K // 2 + 4 * M * N), ops=2.0 * M * N * K)
     if want("conv"):
         cases = [("resnet18_conv1_b64", 64, 224, 224, 3, 64, 7, 2, 3, 1),
                  ("resnet18_l1_3x3_b64", 64, 56, 56, 64, 64, 3, 1, 1, 1),

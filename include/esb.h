@@ -42,9 +42,10 @@ extern "C" {
 #define ESB_OK 0
 #define ESB_E_INVALID (-1)     /* bad n/k_sig, sizes, NULL pointer, layout, descriptor */
 #define ESB_E_OVERFLOW (-3)    /* reduction length * max|mA| * max|mB| > 2^31 - 1 */
-#define ESB_E_UNSUPPORTED (-4) /* decoded integers exceed the split int8 range (|m| > 32639) */
+#define ESB_E_UNSUPPORTED (-4) /* decoded integers exceed the split int8 range (|m| > 32639),
+                                  or a format / length outside the packed 4-bit storage */
 #define ESB_E_HIP (-5)         /* HIP launch / runtime failure, see esb_last_hip_error() */
-#define ESB_E_WORKSPACE (-6)   /* workspace NULL or smaller than esb_dda_workspace_size() */
+#define ESB_E_WORKSPACE (-6)   /* workspace NULL or smaller than its *_workspace_size() */
 
 #define ESB_B_NK 0 /* B stored N x K, row-major (K contiguous) */
 #define ESB_B_KN 1 /* B stored K x N, row-major (N contiguous) */
@@ -141,20 +142,23 @@ int esb_gemm(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_
              void* stream);
 
 /*
- * Bytes of device workspace that esb_gemm_ws may use to decode both operands
- * once ahead of the contraction (0 when the formats do not take that path: it
- * applies to pairs of formats whose values are exact in OCP E4M3 and whose
- * products and partial sums over K stay exact in the fp32 accumulation of the
- * fp8 matrix cores).  Deterministic in its arguments.
+ * Bytes of device workspace that esb_gemm_ws may use (0 when it would use
+ * none).  Two uses: decoding both operands once ahead of the contraction, for
+ * pairs of formats whose values are exact in OCP E4M3 (or E2M3, E2M1) and
+ * whose products and partial sums over K stay exact in the fp32 accumulation
+ * of the fp8/fp6/fp4 matrix cores; and int32 partial sums when a GEMM with too
+ * few output tiles to fill the GPU splits its reduction.  Deterministic in
+ * its arguments.
  */
 size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig);
 
 /*
  * esb_gemm with a caller workspace (device, at least esb_gemm_workspace_size()
  * bytes, or NULL).  Results are bit-identical to esb_gemm.  For shapes with
- * enough work per operand byte the codes of A and B are first decoded to E4M3
- * into the workspace (one extra pass, 1 byte read and written per code) and the
- * contraction reads the decoded bytes; otherwise the workspace is unused.
+ * enough work per operand byte the codes of A and B are first decoded (to
+ * packed E2M1, packed E2M3 or E4M3) into the workspace and the contraction
+ * reads the decoded bytes; skinny shapes split the reduction and keep exact
+ * int32 partial sums there; otherwise the workspace is unused.
  * ESB_E_WORKSPACE if workspace is non-NULL and ws_bytes is too small.  The
  * workspace carries nothing between calls; concurrent calls need distinct ones.
  */
@@ -162,6 +166,42 @@ int esb_gemm_ws(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int 
                 const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
                 const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
                 void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Packed 4-bit code storage (the b-bit format of Sec. 4.1 at b <= 4, two codes
+ * per byte).  For formats inside OCP FP4 E2M1 (at most 2 exponent bits and
+ * k_sig <= 2: ESB(4,1) itself, every ESB(3,.) and ESB(2,.)), each code becomes
+ * its E2M1 nibble with the same value q, 32 codes of a row per 16 bytes in a
+ * fixed order (byte i of dword w holds codes 8w+i, low nibble, and 8w+4+i),
+ * which is the operand layout of the fp4 matrix cores: a weight matrix packed
+ * once is read in place by esb_gemm_packed, at half the bytes of one code per
+ * byte and with no decoding in the contraction.
+ *   esb_pack_size  bytes of `rows` packed rows of K codes: rows * K/2, or 0 when
+ *                  the format is not inside E2M1 or K % 32 != 0;
+ *   esb_pack       codes: device, rows x K codes with row pitch ld >= K (both
+ *                  16-byte aligned); packed: device, esb_pack_size bytes, rows of
+ *                  K/2 bytes.  ESB_E_UNSUPPORTED for formats outside E2M1 or
+ *                  K % 32 != 0.
+ */
+size_t esb_pack_size(int rows, int K, int n, int k_sig);
+int esb_pack(const uint8_t* codes, int rows, int K, int64_t ld, int n, int k_sig,
+             uint8_t* packed, void* stream);
+
+/*
+ * GEMM with B given packed by esb_pack (N rows of K/2 bytes), A as codes (packed
+ * per call into the workspace), results bit-identical to esb_gemm with
+ * ESB_B_NK.  Both formats inside E2M1, K % 32 == 0, K * max|mA| * max|mB| < 2^24
+ * (else ESB_E_UNSUPPORTED / ESB_E_OVERFLOW).  Skinny shapes split the reduction
+ * over more workgroups, with exact int32 partial sums in the workspace.
+ *   workspace  device, at least esb_gemm_packed_workspace_size() bytes
+ *              (ESB_E_WORKSPACE otherwise); A 16-byte aligned, lda % 16 == 0.
+ */
+size_t esb_gemm_packed_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB,
+                                      int kB_sig);
+int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                    const float* alphaA, const uint8_t* B_packed, int nB, int kB_sig,
+                    const float* alphaB, int32_t* acc, float* y, int64_t ldc, void* workspace,
+                    size_t ws_bytes, void* stream);
 
 /* Convolution geometry.  Output P = (H + 2*pad_h - R)/stride_h + 1, Q likewise. */
 typedef struct esb_conv_desc {

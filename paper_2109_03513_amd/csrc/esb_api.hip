@@ -179,7 +179,7 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     const bool fits = mma_fits(g, A, K, 1, B, ldb, b_layout);
     if (ws && fits && (f4 || op == 1) && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
         return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb, alphaB,
-                                         acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, s));
+                                         acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, nullptr, false, s));
     if (op >= 0 && fits)   // with a workspace, skinny shapes split the reduction
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
                                      ldc, (int32_t*)ws, s));
@@ -272,7 +272,8 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
     if (ws && fits && (f4 || op == 1) && pre_worth(Mrows, d->K, kred, xel, wel))
         return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
                                          (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w, d->K,
-                                         kred, fw, alphaW, acc, y, d->K, f4 ? 1 : (f6 ? 2 : 0), ws, s));
+                                         kred, fw, alphaW, acc, y, d->K, f4 ? 1 : (f6 ? 2 : 0), ws, nullptr,
+                                         false, s));
     if (op >= 0 && fits)
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
                                      kred, fw, alphaW, acc, y, d->K, nullptr, s));
@@ -302,6 +303,66 @@ int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, 
                   void* workspace, size_t ws_bytes, void* stream) {
     return conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, acc, y, workspace, ws_bytes,
                      stream);
+}
+
+
+// ------------------------------------------------------------ packed codes
+static bool packable(const Fmt& f) { return f.ebits <= 2 && f.k <= 1; }   // inside OCP E2M1
+
+size_t esb_pack_size(int rows, int K, int n, int k_sig) {
+    if (!valid_fmt(n, k_sig) || rows < 0 || K <= 0 || K % 32 != 0) return 0;
+    if (!packable(make_fmt(n, k_sig))) return 0;
+    return (size_t)rows * (size_t)(K / 2);
+}
+
+int esb_pack(const uint8_t* codes, int rows, int K, int64_t ld, int n, int k_sig, uint8_t* packed,
+             void* stream) {
+    if (!valid_fmt(n, k_sig) || rows < 0 || K <= 0 || ld < K) return ESB_E_INVALID;
+    const Fmt f = make_fmt(n, k_sig);
+    if (!packable(f) || K % 32 != 0) return ESB_E_UNSUPPORTED;
+    if (rows == 0) return ESB_OK;
+    if (!codes || !packed || (uintptr_t)codes % 16 != 0 || ld % 16 != 0 || (uintptr_t)packed % 16 != 0)
+        return ESB_E_INVALID;
+    return hip_status(launch_pack_fp4(codes, rows, K, ld, f, packed, (hipStream_t)stream));
+}
+
+size_t esb_gemm_packed_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig) {
+    if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig) || M < 0 || N < 0 || K <= 0) return 0;
+    const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
+    if (!mma_f4ok(fa, fb, K) || K % 32 != 0) return 0;
+    const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    size_t need = al((size_t)M * (size_t)(K / 2));            // A, packed per call
+    int kc = K;
+    const int ks = mma_splitk(M, N, K, &kc);
+    if (ks > 1) need += (size_t)ks * (size_t)M * (size_t)N * sizeof(int32_t);
+    return need > 0 ? need : 1;
+}
+
+int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                    const float* alphaA, const uint8_t* B_packed, int nB, int kB_sig,
+                    const float* alphaB, int32_t* acc, float* y, int64_t ldc, void* workspace,
+                    size_t ws_bytes, void* stream) {
+    if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig)) return ESB_E_INVALID;
+    if (M < 0 || N < 0 || K <= 0 || lda < K || ldc < N) return ESB_E_INVALID;
+    if (!acc && !y) return ESB_E_INVALID;
+    if (y && (!alphaA || !alphaB)) return ESB_E_INVALID;
+    const Fmt fa = make_fmt(nA, kA_sig), fb = make_fmt(nB, kB_sig);
+    if (!packable(fa) || !packable(fb) || K % 32 != 0) return ESB_E_UNSUPPORTED;
+    const int st = contraction_contract(K, fa, fb);
+    if (st) return st;
+    if (!mma_f4ok(fa, fb, K)) return ESB_E_OVERFLOW;   // fp32 sums exact only below 2^24
+    const size_t need = esb_gemm_packed_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig);
+    if (!workspace || ws_bytes < need) return ESB_E_WORKSPACE;
+    if (M == 0 || N == 0) return ESB_OK;
+    if (!A || !B_packed || (uintptr_t)A % 16 != 0 || lda % 16 != 0 || (uintptr_t)B_packed % 16 != 0)
+        return ESB_E_INVALID;
+    if (lda > 0x7fffffff) return ESB_E_INVALID;
+    ConvGeom g;
+    g.Nb = M; g.H = 1; g.W = 1; g.C = K; g.pitch = (int)lda;
+    g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
+    return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, nullptr, N, K / 2, fb,
+                                     alphaB, acc, y, ldc, 1, workspace, B_packed, true,
+                                     (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -121,7 +121,12 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          int mode, void* ws, hipStream_t s);
+                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s);
+// b_packed: B given in packed E2M1 (mode 1 only), not decoded; split: a dense
+// GEMM with too few tiles splits its reduction (mma_splitk), the int32 partial
+// sums after the decoded operands in ws (see esb_gemm_packed_workspace_size).
+hipError_t launch_pack_fp4(const uint8_t* codes, int64_t rows, int64_t K, int64_t ld, const Fmt& f,
+                           uint8_t* packed, hipStream_t s);
 
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,

@@ -438,15 +438,45 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
 }
 
 // Sum of the ksplit partial sums of every output, in range order (int32 and
-// exact: every partial and the total obey the accumulator bound), then the
-// epilogue of the contraction.
+// exact: every partial and the total obey the accumulator bound; two's
+// complement wrap-around), then the epilogue of the contraction.  Four
+// consecutive outputs per thread when N % 4 == 0 (16-byte loads, the loads of
+// eight ranges in flight together), else one.
 __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
     const int64_t MN = (int64_t)g.M * g.N;
     float s = 0.0f;
     if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < MN; e += stride) {
-        uint32_t u = 0;                                  // two's complement wrap-around
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g.N % 4 == 0) {
+        const int4* p = (const int4*)g.part;
+        const int64_t MN4 = MN / 4;
+        for (int64_t e = t0; e < MN4; e += stride) {
+            uint32_t u0 = 0, u1 = 0, u2 = 0, u3 = 0;
+            for (int z0 = 0; z0 < g.ksplit; z0 += 8) {
+                int4 v[8];
+#pragma unroll
+                for (int z = 0; z < 8; z++) v[z] = p[(int64_t)min(z0 + z, g.ksplit - 1) * MN4 + e];
+#pragma unroll
+                for (int z = 0; z < 8; z++)
+                    if (z0 + z < g.ksplit) {
+                        u0 += (uint32_t)v[z].x; u1 += (uint32_t)v[z].y;
+                        u2 += (uint32_t)v[z].z; u3 += (uint32_t)v[z].w;
+                    }
+            }
+            const int64_t row = (4 * e) / g.N, col = 4 * e - row * g.N;
+            const int64_t o = row * g.ldc + col;
+            const int32_t t[4] = {(int32_t)u0, (int32_t)u1, (int32_t)u2, (int32_t)u3};
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                if (g.acc) g.acc[o + c] = t[c];
+                if (g.y) g.y[o + c] = s * (float)t[c];
+            }
+        }
+        return;
+    }
+    for (int64_t e = t0; e < MN; e += stride) {
+        uint32_t u = 0;
         for (int z = 0; z < g.ksplit; z++) u += (uint32_t)g.part[z * MN + e];
         const int32_t t = (int32_t)u;
         const int64_t row = e / g.N, col = e - row * g.N;
@@ -564,7 +594,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int tm, tn;
     tile_of(g, tm, tn);
-    const int grp = blockIdx.z;
+    // convolution: blockIdx.z is the group; dense GEMM: the reduction range
+    const int grp = CONV ? (int)blockIdx.z : 0;
+    const int kz = CONV ? 0 : (int)blockIdx.z;
+    const int kbeg = kz * g.kchunk;                                   // bytes
+    const int Kl = CONV ? g.K : min(g.K - kbeg, g.kchunk);
     const int m0 = tm * BM, n0 = tn * BN;
     const int wr = (wave / WGN) * WM, wc = (wave % WGN) * WN;
     const ConvGeom& cg = g.ga;
@@ -591,7 +625,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
             a_iw[i] = q * cg.sw - cg.pw;
             a_off[i] = (((int64_t)img * cg.H + a_ih[i]) * cg.W + a_iw[i]) * cg.pitch + goffA;
         } else {
-            a_off[i] = (int64_t)(ok ? m : 0) * cg.pitch + 16 * lc;
+            a_off[i] = (int64_t)(ok ? m : 0) * cg.pitch + 16 * lc + kbeg;
         }
     }
     if (CONV) {
@@ -606,13 +640,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     for (int i = 0; i < CHB; i++) {
         const int nn = n0 + 16 * (wave + i * NW) + rsub;
         brow_ok[i] = nn < g.N;
-        b_off[i] = (brow0 + (brow_ok[i] ? nn : 0)) * g.ldb + 16 * lc;
+        b_off[i] = (brow0 + (brow_ok[i] ? nn : 0)) * g.ldb + 16 * lc + (CONV ? 0 : kbeg);
     }
     const uint8_t* z = kZeroRows.b[kZeroRowE4M3];
 
     // the E4M3 bytes of reduction offset k0 into a ring slot (stages in order)
     auto fetch = [&](int k0, uint8_t* slot) {
-        const bool kin = k0 + 16 * lc < g.K;
+        const bool kin = k0 + 16 * lc < Kl;
         if (CONV) {
             const int64_t koff = ((int64_t)kr * cg.W + ks) * cg.pitch + kc;
 #pragma unroll
@@ -715,7 +749,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     // the barrier of stage s the fetches of stages s+2 .. s+R-1 may still be
     // in flight (CT instructions each) while stage s+1 has landed
     static_assert(R == 2 || R == 4, "ring depth");
-    const int KT = (g.K + BK - 1) / BK;
+    const int KT = (Kl + BK - 1) / BK;
     static_for<0, R>([&](auto Q) {
         constexpr int q = decltype(Q)::value;
         fetch(q * BK, ring + q * TILE);
@@ -758,6 +792,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
                 const int col = n0 + wc + 32 * j + lr;
                 if (row < g.M && col < g.N) {
                     const float fv = ldexpf(acc[i][j][r], g.out_shift);
+                    if (!CONV && g.ksplit > 1) {          // partial sum of this range
+                        g.part[((int64_t)kz * g.M + row) * g.N + col] = (int32_t)fv;
+                        continue;
+                    }
                     const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = (int32_t)fv;
                     if (g.y) g.y[o] = s * fv;
@@ -972,7 +1010,7 @@ hipError_t launch_pre_t(FastParams g, int groups, bool conv, bool f4, hipStream_
     g.tiles_m = (g.M + BM - 1) / BM;
     g.tiles_n = (g.N + BN - 1) / BN;
     g.ntiles = g.tiles_m * g.tiles_n;
-    dim3 grid(g.ntiles, 1, groups);
+    dim3 grid(g.ntiles, 1, conv ? groups : g.ksplit);
     const int nt = 64 * WGM * WGN;
     if (f4) {
         if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R, 1><<<grid, nt, 0, s>>>(g);
@@ -980,6 +1018,12 @@ hipError_t launch_pre_t(FastParams g, int groups, bool conv, bool f4, hipStream_
     } else {
         if (conv) k_mma_pre<BM, BN, WGM, WGN, 1, R, 0><<<grid, nt, 0, s>>>(g);
         else k_mma_pre<BM, BN, WGM, WGN, 0, R, 0><<<grid, nt, 0, s>>>(g);
+    }
+    if (!conv && g.ksplit > 1) {
+        const int64_t MN = (int64_t)g.M * g.N;
+        int64_t nb = (MN + 255) / 256;
+        if (nb > 4 * num_cus()) nb = 4 * num_cus();
+        k_splitk_sum<<<(unsigned)nb, 256, 0, s>>>(g);
     }
     return hipGetLastError();
 }
@@ -1109,11 +1153,24 @@ size_t mma_pre_workspace(int64_t a_rows, int64_t a_cols, int64_t b_rows, int64_t
     return al((size_t)a_rows * (size_t)a_cols) + al((size_t)b_rows * (size_t)K);
 }
 
+// Packed E2M1 rows (esb_pack): 32 codes to 16 bytes, the layout k_mma_pre reads.
+hipError_t launch_pack_fp4(const uint8_t* codes, int64_t rows, int64_t K, int64_t ld, const Fmt& f,
+                           uint8_t* packed, hipStream_t s) {
+    if (rows <= 0 || K <= 0) return hipSuccess;
+    DecodeJob j0{codes, rows, K / 32, ld, mma_decode_f4(f), packed};
+    DecodeJob j1{codes, 0, 0, ld, mma_decode_f4(f), packed};
+    int64_t blocks = (j0.rows * j0.cols16 + 255) / 256;
+    const int64_t cap = (int64_t)num_cus() * 16;
+    if (blocks > cap) blocks = cap;
+    k_decode_fp4<<<(unsigned)(blocks < 1 ? 1 : blocks), 256, 0, s>>>(j0, j1);
+    return hipGetLastError();
+}
+
 hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, const uint8_t* A,
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          int mode, void* ws, hipStream_t s) {
+                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s) {
     if (M <= 0 || N <= 0) return hipSuccess;
     const bool conv = !(ga.H == 1 && ga.W == 1 && ga.R == 1 && ga.S == 1 && ga.ph == 0 && ga.pw == 0 &&
                         ga.Cg == K && groups == 1);
@@ -1121,13 +1178,17 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
     // decoded bytes per code: 1 (E4M3), 1/2 (E2M1) or 3/4 (E2M3); lengths below are in bytes
     auto bytes = [&](int64_t codes) { return f4 ? codes / 2 : (f6 ? codes / 4 * 3 : codes); };
     const int64_t a_bytes = bytes(a_cols), kbytes = bytes(K);
+    const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
     uint8_t* dA = (uint8_t*)ws;
-    uint8_t* dB = dA + (((size_t)a_rows * (size_t)a_bytes + 255) & ~(size_t)255);
+    uint8_t* dBw = dA + al((size_t)a_rows * (size_t)a_bytes);
+    // B packed by esb_pack (E2M1 rows of K/2 bytes): used in place, not decoded
+    uint8_t* dB = b_packed ? (uint8_t*)b_packed : dBw;
+    int32_t* part = (int32_t*)(b_packed ? dBw : dBw + al((size_t)b_rows * (size_t)kbytes));
     const int grp = f6 ? 64 : (f4 ? 32 : 16);    // codes per decode item
     const MmaDecode da = f4 ? mma_decode_f4(fa) : (f6 ? mma_decode_f6(fa) : mma_decode(fa, 1));
     const MmaDecode db = f4 ? mma_decode_f4(fb) : (f6 ? mma_decode_f6(fb) : mma_decode(fb, 1));
     DecodeJob j0{A, a_rows, a_cols / grp, a_pitch, da, dA};
-    DecodeJob j1{B, b_rows, (int64_t)K / grp, ldb, db, dB};
+    DecodeJob j1{B, b_packed ? 0 : b_rows, (int64_t)K / grp, ldb, db, dB};
     const int64_t items = j0.rows * j0.cols16 + j1.rows * j1.cols16;
     int64_t blocks = (items + 255) / 256;
     const int64_t cap = (int64_t)num_cus() * 16;
@@ -1142,6 +1203,16 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
     g.ga.Cg = (int)bytes(ga.Cg);
     g.A = dA; g.B = dB; g.ldb = kbytes;
     g.ksplit = 1; g.kchunk = (int)kbytes; g.part = nullptr;
+    if (split && !conv && !f6) {
+        int kc = K;
+        const int ks = mma_splitk(M, N, K, &kc);
+        if (ks > 1) {   // the same number of ranges, in 64-byte stages of decoded bytes
+            const int64_t kcb = ((kbytes + ks - 1) / ks + 63) / 64 * 64;
+            g.kchunk = (int)kcb;
+            g.ksplit = (int)((kbytes + kcb - 1) / kcb);
+            g.part = part;
+        }
+    }
     g.blkA = a_rows * 48;
     g.blkB = b_rows * 48;
     g.da = j0.d;
@@ -1157,6 +1228,9 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
         return (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn) * groups;
     };
     if (f6) return launch_f6_t<256, 256, 2, 4, 4>(g, groups, conv, s);   // see mma_f6_tiles
+    if (g.ksplit > 1)   // the tiles mma_splitk planned with
+        return M > 64 ? launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, f4, s)
+                      : launch_pre_t<64, 64, 2, 2, 4>(g, groups, conv, f4, s);
     if (N > 128 && tiles(256, 256) >= cus) return launch_pre_t<256, 256, 2, 4, 4>(g, groups, conv, f4, s);
     if (N > 64 && tiles(256, 128) >= cus) return launch_pre_t<256, 128, 4, 2, 4>(g, groups, conv, f4, s);
     if (N > 64 && tiles(128, 128) >= cus / 2) return launch_pre_t<128, 128, 2, 4, 4>(g, groups, conv, f4, s);

@@ -71,6 +71,11 @@ def lib():
             "esb_conv2d_workspace_size": (sz, [ctypes.POINTER(ConvDesc), i32, i32, i32, i32]),
             "esb_conv2d_ws": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
                                     P, sz, P]),
+            "esb_pack_size": (sz, [i32, i32, i32, i32]),
+            "esb_pack": (i32, [P, i32, i32, i64, i32, i32, P, P]),
+            "esb_gemm_packed_workspace_size": (sz, [i32, i32, i32, i32, i32, i32, i32]),
+            "esb_gemm_packed": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i32, i32, P, P, P, i64,
+                                      P, sz, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -216,6 +221,48 @@ def esb_gemm(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, b_layout=ESB_B_NK, ac
         _check("esb_gemm_ws", lib().esb_gemm_ws(M, N, K, _ptr(A), lda, nA, kA_sig, _ptr(alphaA),
                                                 _ptr(B), ldb, nB, kB_sig, _ptr(alphaB), b_layout,
                                                 _ptr(acc), _ptr(y), N, wp, wb, _stream(stream)))
+    return acc, y
+
+
+def esb_pack_size(rows, K, n, k_sig):
+    return int(lib().esb_pack_size(rows, K, n, k_sig))
+
+
+def esb_pack(codes, n, k_sig, packed=None, stream=None):
+    """codes: rows x K (K % 32 == 0, format inside OCP E2M1) -> rows x K/2 packed bytes."""
+    import torch
+    _dev_tensor(codes, torch.uint8, "codes")
+    rows, K = codes.shape
+    if packed is None:
+        packed = torch.empty((rows, K // 2), dtype=torch.uint8, device=codes.device)
+    ld = codes.stride(0) if rows else K
+    _check("esb_pack", lib().esb_pack(_ptr(codes), rows, K, ld, n, k_sig, _ptr(packed),
+                                      _stream(stream)))
+    return packed
+
+
+def esb_gemm_packed_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig):
+    return int(lib().esb_gemm_packed_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig))
+
+
+def esb_gemm_packed(A, nA, kA_sig, alphaA, B_packed, nB, kB_sig, alphaB, workspace, acc=None,
+                    y=None, want_acc=True, want_y=True, stream=None):
+    """A: M x K codes; B_packed: N x K/2 bytes from esb_pack.  Returns (acc, y)."""
+    import torch
+    _dev_tensor(A, torch.uint8, "A")
+    _dev_tensor(B_packed, torch.uint8, "B_packed")
+    M, K = A.shape
+    N = B_packed.shape[0]
+    dev = A.device
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=dev)
+    if y is None and want_y:
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    lda = A.stride(0) if M else K
+    wp, wb = _ws(workspace)
+    _check("esb_gemm_packed", lib().esb_gemm_packed(M, N, K, _ptr(A), lda, nA, kA_sig, _ptr(alphaA),
+                                                    _ptr(B_packed), nB, kB_sig, _ptr(alphaB),
+                                                    _ptr(acc), _ptr(y), N, wp, wb, _stream(stream)))
     return acc, y
 
 

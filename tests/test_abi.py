@@ -131,3 +131,30 @@ def test_contraction_workspace_sizes_and_errors(L):
     assert L.esb_conv2d_workspace_size(ctypes.byref(dw), 5, 3, 5, 3) == 0
     assert esb.esb_conv2d_workspace_size((64, 14, 14, 256), (256, 3, 3, 256), 5, 3, 5, 3,
                                          pad=(1, 1)) == cneed
+
+
+def test_packed_sizes_and_errors(L):
+    """Packed 4-bit storage: sizes for formats inside OCP E2M1 only, refusals before any
+    launch (formats outside E2M1, K % 32, too small workspace, bad pitch)."""
+    fake = ctypes.c_void_p(0x1000)
+    assert L.esb_pack_size(10, 64, 4, 2) == 10 * 32          # ESB(4,1) = E2M1
+    assert L.esb_pack_size(7, 9216, 3, 1) == 7 * 4608         # ESB(3,0)
+    assert L.esb_pack_size(10, 48, 4, 2) == 0                 # K % 32 != 0
+    assert L.esb_pack_size(10, 64, 5, 3) == 0                 # ESB(5,2): two fraction bits
+    assert L.esb_pack_size(10, 64, 4, 3) == 0                 # ESB(4,2)
+    assert L.esb_pack(fake, 10, 64, 64, 5, 3, fake, None) == -4     # ESB_E_UNSUPPORTED
+    assert L.esb_pack(fake, 10, 64, 63, 4, 2, fake, None) == -1     # ld < K
+    assert L.esb_pack(fake, 10, 48, 48, 4, 2, fake, None) == -4     # K % 32
+    M, N, K = 128, 4096, 9216
+    need = L.esb_gemm_packed_workspace_size(M, N, K, 3, 2, 3, 1)
+    assert need >= M * K // 2
+    assert L.esb_gemm_packed_workspace_size(M, N, K, 5, 3, 3, 1) == 0
+    gp = L.esb_gemm_packed
+    assert gp(M, N, K, fake, K, 3, 2, fake, fake, 3, 1, fake, fake, None, N, fake, need - 1,
+              None) == -6
+    assert gp(M, N, K, fake, K, 3, 2, fake, fake, 3, 1, fake, fake, None, N, None, need,
+              None) == -6
+    assert gp(M, N, K, fake, K, 5, 3, fake, fake, 3, 1, fake, fake, None, N, fake, need,
+              None) == -4
+    assert gp(M, N, K, fake, K - 1, 3, 2, fake, fake, 3, 1, fake, fake, None, N, fake, need,
+              None) == -1
