@@ -59,6 +59,8 @@ def lib():
             "eso_dequantize": (i32, [P, i64, f32, i32, i32, P]),
             "eso_dda": (i32, [P, i64, i32, i32, P, i32, P]),
             "eso_dda_normal": (f64, [f64, i32, i32]),
+            "eso_dn_stats": (i32, [P, i64, P, P]),
+            "eso_project_dn": (i32, [P, i64, f32, f32, f32, i32, i32, P]),
             "eso_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, f32, P, i64, i32, i32, f32, i32,
                                P, P, i64]),
             "eso_conv2d": (i32, [i32] * 12 + [P, i32, i32, f32, P, i32, i32, f32, P, P]),
@@ -166,6 +168,26 @@ def dda(x, b, k_sig, grid):
 def dda_normal(alpha, b, k_sig):
     """Analytic one-sided D(alpha, b, k) for p = N(0, 1) (eq. (9))."""
     return lib().eso_dda_normal(float(alpha), b, k_sig)
+
+
+def dn_stats(x):
+    """(mean, population std) of x in long double (the DN equation), as floats."""
+    x = _f32(x)
+    m = ctypes.c_double()
+    sd = ctypes.c_double()
+    st = lib().eso_dn_stats(_p(x), x.size, ctypes.byref(m), ctypes.byref(sd))
+    assert st == 0
+    return m.value, sd.value
+
+
+def project_dn(x, mean, std, alpha, b, k_sig):
+    """Codes of fl32(fl32(x - mean) / fl32(std + 1e-7)) under alpha (binary32 mean, std)."""
+    x = _f32(x)
+    out = np.empty(x.shape, dtype=np.uint8)
+    st = lib().eso_project_dn(_p(x), x.size, float(np.float32(mean)), float(np.float32(std)),
+                              float(np.float32(alpha)), b, k_sig, _p(out))
+    assert st == 0
+    return out
 
 
 def gemm(A, B, bA, ksA, alphaA, bB, ksB, alphaB, b_layout=0, want_acc=True, want_y=True):

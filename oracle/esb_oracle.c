@@ -276,6 +276,46 @@ double eso_dda_normal(double alpha, int b, int k_sig) {
     return D;
 }
 
+/*
+ * Data normalization, Sec. 3.4 ("Normalization", the DN equation): the mean
+ * and the population standard deviation sqrt((1/d) sum (x - mu)^2), two passes
+ * in long double.  n == 0 gives NaN for both.
+ */
+int eso_dn_stats(const float* x, int64_t n, double* mean, double* std) {
+    if (n < 0) return ESO_E_INVALID;
+    if (n == 0) { *mean = NAN; *std = NAN; return ESO_OK; }
+    long double s = 0.0L;
+    for (int64_t i = 0; i < n; i++) s += (long double)x[i];
+    const long double mu = s / (long double)n;
+    long double v = 0.0L;
+    for (int64_t i = 0; i < n; i++) {
+        const long double d = (long double)x[i] - mu;
+        v += d * d;
+    }
+    *mean = (double)mu;
+    *std = (double)sqrtl(v / (long double)n);
+    return ESO_OK;
+}
+
+/*
+ * Projection of normalized data (Alg. 1: ESB(DN(W))), in binary32 with the
+ * given statistics (binary32 too) and epsilon = 1e-7 of the DN equation:
+ *   xh = fl32( fl32(x - mean) / fl32(std + fl32(1e-7)) ),   code = Pi(xh)
+ * with the projection of eso_project under alpha.
+ */
+int eso_project_dn(const float* x, int64_t n, float mean, float std, float alpha, int b, int k_sig,
+                   uint8_t* codes) {
+    if (!valid_bk(b, k_sig) || n < 0) return ESO_E_INVALID;
+    volatile float eps = 1e-7f;
+    const float den = std + eps;
+    for (int64_t i = 0; i < n; i++) {
+        volatile float d = x[i] - mean;
+        const float xh = d / den;
+        codes[i] = (uint8_t)eso_encode(eso_project_value(xh, alpha, b, k_sig), b, k_sig);
+    }
+    return ESO_OK;
+}
+
 /* Exact integer of a code: m = q * 2^k (eq. (14)-(15): fraction bits made integral). */
 static int64_t code_int(int code, int b, int k_sig) {
     return (int64_t)ldexp(eso_decode(code, b, k_sig), k_sig - 1);
