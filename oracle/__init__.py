@@ -59,6 +59,7 @@ def lib():
             "eso_dequantize": (i32, [P, i64, f32, i32, i32, P]),
             "eso_dda": (i32, [P, i64, i32, i32, P, i32, P]),
             "eso_dda_normal": (f64, [f64, i32, i32]),
+            "eso_dda_normal_deriv": (f64, [f64, i32, i32]),
             "eso_dn_stats": (i32, [P, i64, P, P]),
             "eso_project_dn": (i32, [P, i64, f32, f32, f32, i32, i32, P]),
             "eso_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, f32, P, i64, i32, i32, f32, i32,
@@ -168,6 +169,11 @@ def dda(x, b, k_sig, grid):
 def dda_normal(alpha, b, k_sig):
     """Analytic one-sided D(alpha, b, k) for p = N(0, 1) (eq. (9))."""
     return lib().eso_dda_normal(float(alpha), b, k_sig)
+
+
+def dda_normal_deriv(alpha, b, k_sig):
+    """dD/dalpha of dda_normal (Sec. 3.4, "Resolving extremum")."""
+    return lib().eso_dda_normal_deriv(float(alpha), b, k_sig)
 
 
 def dn_stats(x):

@@ -277,6 +277,29 @@ double eso_dda_normal(double alpha, int b, int k_sig) {
 }
 
 /*
+ * Derivative dD/dalpha of the analytic objective above (the quantity whose
+ * zeros Sec. 3.4, "Resolving extremum", looks for).  Each cell's integrand
+ * (t - alpha q_c)^2 phi(t) depends on alpha through alpha q_c and through the
+ * cell ends alpha m_c; at an end shared by two nearest-neighbour cells the two
+ * integrands are equal (the end is the midpoint), so the moving ends cancel and
+ *   dD/dalpha = -2 sum_c q_c (M1_c - alpha q_c M0_c).
+ */
+double eso_dda_normal_deriv(double alpha, int b, int k_sig) {
+    double vals[128];
+    int n = eso_valueset(b, k_sig, vals, 128);
+    if (n < 0 || !(alpha > 0)) return NAN;
+    double d = 0.0;
+    for (int c = 0; c < n; c++) {
+        double lo = (c == 0) ? 0.0 : 0.5 * alpha * (vals[c - 1] + vals[c]);
+        double hi = (c == n - 1) ? INFINITY : 0.5 * alpha * (vals[c] + vals[c + 1]);
+        double M0 = nPhi_upper(lo) - nPhi_upper(hi);
+        double M1 = nphi(lo) - nphi(hi);
+        d += -2.0 * vals[c] * (M1 - alpha * vals[c] * M0);
+    }
+    return d;
+}
+
+/*
  * Data normalization, Sec. 3.4 ("Normalization", the DN equation): the mean
  * and the population standard deviation sqrt((1/d) sum (x - mu)^2), two passes
  * in long double.  n == 0 gives NaN for both.

@@ -114,3 +114,25 @@ def test_nonfinite_data():
     x = np.array([0.1, np.nan, -0.3], dtype=np.float32)
     j, Dv = oracle.dda(x, 4, 2, np.array([0.5, 1.0], dtype=np.float32))
     assert np.isnan(Dv).all() and j == 0
+
+
+@pytest.mark.parametrize("b,ks", [(3, 1), (3, 2), (4, 1), (4, 2), (5, 3), (6, 2), (8, 5), (8, 7)])
+def test_deriv_is_the_slope_of_D(b, ks):
+    """The closed-form dD/dalpha against central differences of D itself."""
+    h = 1e-5
+    for a in [0.05, 0.31, 0.7, 1.3, 2.2, 2.9]:
+        fd = (oracle.dda_normal(a + h, b, ks) - oracle.dda_normal(a - h, b, ks)) / (2 * h)
+        d = oracle.dda_normal_deriv(a, b, ks)
+        assert abs(d - fd) <= 1e-8 + 1e-6 * abs(d), (b, ks, a, d, fd)
+
+
+@pytest.mark.parametrize("b,k,dda,alpha_star", TABLE1)
+def test_deriv_vanishes_at_table1_alpha_star(b, k, dda, alpha_star):
+    """Table 1's alpha* (printed to 4 decimals) is a zero of dD/dalpha: the slope there is
+    within the curvature times the print rounding, and changes sign across it."""
+    d2 = (oracle.dda_normal_deriv(alpha_star + 1e-4, b, k + 1)
+          - oracle.dda_normal_deriv(alpha_star - 1e-4, b, k + 1)) / 2e-4
+    assert d2 > 0
+    assert abs(oracle.dda_normal_deriv(alpha_star, b, k + 1)) <= d2 * 0.5e-4 * 1.01 + 1e-12
+    assert oracle.dda_normal_deriv(alpha_star - 2e-4, b, k + 1) < 0
+    assert oracle.dda_normal_deriv(alpha_star + 2e-4, b, k + 1) > 0
