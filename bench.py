@@ -283,7 +283,7 @@ def sweep(args):
                                                          workspace=ws, stream=sh), args.reps, stream)
             emit("dda_small_n4_k2_G64_len%d" % length, ms, nbytes=4.0 * length)
     big = 1 << 27
-    if want("project") or want("dda"):
+    if want("project") or want("dda") or want("dn"):
         x = torch.randn(big, device=dev, generator=g)
         alpha = torch.tensor([0.4871], device=dev)
         codes = torch.empty(big, dtype=torch.uint8, device=dev)
@@ -300,6 +300,24 @@ def sweep(args):
                 ms = time_launches(lambda: esb.esb_dda_align(x, n, ks, grid, alpha_out=ao, D_out=Do,
                                                              workspace=ws, stream=sh), args.reps, stream)
                 emit("dda_n%d_k%d_G64_2^27" % (n, ks), ms, nbytes=4.0 * big)
+        if want("dn"):
+            # normalization statistics (two passes), projection of normalized data, and the
+            # analytic aligner over 4096 candidates (Alg. 1: W_q = ESB(DN(W)))
+            st = torch.empty(2, device=dev)
+            wsd = torch.empty(esb.lib().esb_dn_workspace_size(big), dtype=torch.uint8, device=dev)
+            ms = time_launches(lambda: esb.esb_dn_stats(x, stats=st, workspace=wsd, stream=sh),
+                               args.reps, stream)
+            emit("dn_stats_2^27", ms, nbytes=4.0 * big)
+            ms = time_launches(lambda: esb.esb_project_dn(x, st, alpha, 4, 2, codes=codes, stream=sh),
+                               args.reps, stream)
+            emit("project_dn_n4_k2_2^27", ms, nbytes=5.0 * big)
+            cand = torch.linspace(0.005, 3.0, 4096, device=dev)
+            ao = torch.empty(1, device=dev)
+            Do = torch.empty(4096, dtype=torch.float64, device=dev)
+            for (n, ks) in [(4, 2), (8, 6)]:
+                ms = time_launches(lambda: esb.esb_dda_normal(n, ks, cand, alpha_out=ao, D_out=Do,
+                                                              stream=sh), args.reps, stream)
+                emit("dda_normal_n%d_k%d_G4096" % (n, ks), ms)
         del x, codes
     if want("gemm"):
         for (M, N, K, fa, fb, name) in [(128, 4096, 9216, (3, 2), (3, 1), "alexnet_fc_b128"),

@@ -203,6 +203,40 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
                     const float* alphaB, int32_t* acc, float* y, int64_t ldc, void* workspace,
                     size_t ws_bytes, void* stream);
 
+/*
+ * Data normalization (Sec. 3.4, the DN equation) and the aligner in its analytic
+ * form (eq. (9), (13) with p = N(0,1), "Resolving extremum"), the paper's own
+ * flow of Alg. 1: W_q = ESB(DN(W)) with alpha* found offline for N(0,1).
+ *
+ * esb_dn_stats: stats_out (device, two fp32) = the mean and the population
+ *   standard deviation sqrt((1/d) sum (x - mean)^2) of x, from one read of x:
+ *   fp64 sums and squared deviations per chunk of 16384 elements, combined by
+ *   the pairwise update in a fixed order (deterministic), rounded to binary32;
+ *   NaN, NaN for len == 0.  workspace: device, 8-byte aligned, at least
+ *   esb_dn_workspace_size(len) bytes (16 per chunk; ESB_E_WORKSPACE otherwise).
+ * esb_project_dn: codes of the normalized values
+ *   xh = fl32( fl32(x - mean) / fl32(std + 1e-7) ),   code = esb_project(xh, alpha),
+ *   stats (device, two fp32 mean, std: e.g. from esb_dn_stats, or running
+ *   averages kept by the caller); alpha device, as esb_project.
+ * esb_dda_normal: for each candidate grid[j] (device, G >= 1 fp32), the
+ *   one-sided analytic objective D_j = E[(t - Pi(t))^2; t >= 0], t ~ N(0,1),
+ *   with nearest-neighbour cells [alpha mid_c, alpha mid_{c+1}) (the top cell
+ *   open), in fp64 (erfc, exp); Table 1 of the paper prints 2 * D.  D_out
+ *   (device, G doubles, required); dD_out (device, G doubles, may be NULL)
+ *   = dD/dalpha at each candidate, -2 sum_c q_c (M1_c - alpha q_c M0_c) with
+ *   M0, M1 the cell's probability and first moment (the zeros the paper's
+ *   "Resolving extremum" looks for); alpha_out (device, one fp32) = grid[j*],
+ *   j* the smallest index with the least D; non-positive or non-finite
+ *   candidates get NaN and rank last.
+ */
+size_t esb_dn_workspace_size(int64_t len);
+int esb_dn_stats(const float* x, int64_t len, float* stats_out, void* workspace, size_t ws_bytes,
+                 void* stream);
+int esb_project_dn(const float* x, int64_t len, const float* stats, const float* alpha, int n,
+                   int k_sig, uint8_t* codes, void* stream);
+int esb_dda_normal(int n, int k_sig, const float* grid, int G, float* alpha_out, double* D_out,
+                   double* dD_out, void* stream);
+
 /* Convolution geometry.  Output P = (H + 2*pad_h - R)/stride_h + 1, Q likewise. */
 typedef struct esb_conv_desc {
     int N, H, W, C;          /* input batch, height, width, channels (NHWC) */

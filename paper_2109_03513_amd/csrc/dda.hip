@@ -185,18 +185,6 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// ---------------------------------------------------------------- format math
-// Non-negative set value number c (ascending, c = 0 .. 2^(n-1)-1) of ESB(n, k):
-// binade j = c >> k, fraction f; j = 0 is the subnormal binade f * 2^-k, else
-// 2^(j-1) * (1 + f 2^-k).  Exact in fp32.
-__host__ __device__ inline float set_value(int c, int k) {
-    const int j = c >> k, f = c & ((1 << k) - 1);
-    return j == 0 ? ldexpf((float)f, -k) : ldexpf((float)((1 << k) + f), j - 1 - k);
-}
-// Midpoint between values c-1 and c (k+2 significant bits: exact in fp32).
-__host__ __device__ inline float set_mid(int c, int k) {
-    return 0.5f * (set_value(c - 1, k) + set_value(c, k));
-}
 
 // Median of three (v_med3_u32): x clamped to [lo, hi] when lo <= hi.
 __device__ __forceinline__ uint32_t med3_u32(uint32_t x, uint32_t lo, uint32_t hi) {

@@ -110,7 +110,8 @@ int esb_project(const float* x, int64_t len, const float* alpha, int n, int k_si
                 void* stream) {
     if (!valid_fmt(n, k_sig) || len < 0 || !alpha) return ESB_E_INVALID;
     if (len > 0 && (!x || !codes)) return ESB_E_INVALID;
-    return hip_status(launch_project(x, len, alpha, make_fmt(n, k_sig), codes, (hipStream_t)stream));
+    return hip_status(launch_project(x, len, alpha, make_fmt(n, k_sig), codes, nullptr,
+                                     (hipStream_t)stream));
 }
 
 int esb_dequantize(const uint8_t* codes, int64_t len, const float* alpha, int n, int k_sig,
@@ -363,6 +364,31 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
     return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, nullptr, N, K / 2, fb,
                                      alphaB, acc, y, ldc, 1, workspace, B_packed, true,
                                      (hipStream_t)stream));
+}
+
+// ------------------------------------------- normalization and analytic DDA
+size_t esb_dn_workspace_size(int64_t len) { return len < 0 ? 0 : dn_workspace(len); }
+
+int esb_dn_stats(const float* x, int64_t len, float* stats_out, void* workspace, size_t ws_bytes,
+                 void* stream) {
+    if (len < 0 || !stats_out || (len > 0 && !x)) return ESB_E_INVALID;
+    if (!workspace || ws_bytes < dn_workspace(len)) return ESB_E_WORKSPACE;
+    return hip_status(launch_dn_stats(x, len, stats_out, workspace, (hipStream_t)stream));
+}
+
+int esb_project_dn(const float* x, int64_t len, const float* stats, const float* alpha, int n,
+                   int k_sig, uint8_t* codes, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !alpha || !stats) return ESB_E_INVALID;
+    if (len > 0 && (!x || !codes)) return ESB_E_INVALID;
+    return hip_status(launch_project(x, len, alpha, make_fmt(n, k_sig), codes, stats,
+                                     (hipStream_t)stream));
+}
+
+int esb_dda_normal(int n, int k_sig, const float* grid, int G, float* alpha_out, double* D_out,
+                   double* dD_out, void* stream) {
+    if (!valid_fmt(n, k_sig) || G < 1 || !grid || !alpha_out || !D_out) return ESB_E_INVALID;
+    return hip_status(launch_dda_normal(make_fmt(n, k_sig), grid, G, alpha_out, D_out,
+                                        dD_out, (hipStream_t)stream));
 }
 
 }  // extern "C"

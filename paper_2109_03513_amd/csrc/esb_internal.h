@@ -25,6 +25,18 @@ struct Fmt {
     int max_int;          // largest |m|, m = q * 2^k the exact integer of a code
 };
 
+// Non-negative set value number c (ascending, c = 0 .. 2^(n-1)-1) of ESB(n, k):
+// binade j = c >> k, fraction f; j = 0 is the subnormal binade f * 2^-k, else
+// 2^(j-1) * (1 + f 2^-k) (eq. (4)-(5)).  Exact in fp32.
+__host__ __device__ inline float set_value(int c, int k) {
+    const int j = c >> k, f = c & ((1 << k) - 1);
+    return j == 0 ? ldexpf((float)f, -k) : ldexpf((float)((1 << k) + f), j - 1 - k);
+}
+// Midpoint between values c-1 and c (k+2 significant bits: exact in fp32).
+__host__ __device__ inline float set_mid(int c, int k) {
+    return 0.5f * (set_value(c - 1, k) + set_value(c, k));
+}
+
 bool valid_fmt(int n, int k_sig);
 Fmt make_fmt(int n, int k_sig);
 int decode_int(const Fmt& f, uint32_t code);   // m = q * 2^k (host)
@@ -32,13 +44,21 @@ double decode_value(const Fmt& f, uint32_t code);
 int num_cus();
 
 // ----------------------------------------------------------------- projection
+// dn (device, two fp32: mean, standard deviation, or NULL): project the
+// normalized values fl32(fl32(x - mean) / fl32(std + 1e-7)) instead of x.
 struct ProjParams {
     uint32_t k, zero_code, c_code, c_bits, sign_bit, one;   // one = 2^k
 };
 ProjParams proj_params(const Fmt& f);
 
 hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,
-                          uint8_t* codes, hipStream_t s);
+                          uint8_t* codes, const float* dn, hipStream_t s);
+
+// ------------------------------------------------------ normalization, analytic DDA
+size_t dn_workspace(int64_t len);
+hipError_t launch_dn_stats(const float* x, int64_t len, float* stats, void* ws, hipStream_t s);
+hipError_t launch_dda_normal(const Fmt& f, const float* grid, int G, float* alpha_out,
+                             double* D_out, double* dD_out, hipStream_t s);
 hipError_t launch_dequantize(const uint8_t* codes, int64_t len, const float* alpha, const Fmt& f,
                              float* out, hipStream_t s);
 

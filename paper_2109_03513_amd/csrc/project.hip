@@ -108,10 +108,50 @@ __device__ __forceinline__ uint32_t code4(const f32x4 v, float alpha, float r, b
 // at ~6.1 TB/s where a grid-stride loop stays at ~5.1.
 constexpr int kTile4 = 4 * 256;
 
+// Data normalization of Alg. 1 (DN before ESB): fl32(fl32(x - mean) / den),
+// den = fl32(std + 1e-7), the IEEE binary32 division.  Fast form: with
+// rd = fl32(1 / den), q = fl32(a rd), the residual a - den q is exact in one
+// fma and fl32(q + residual rd) is the correctly rounded a / den (Markstein,
+// IBM J. Res. Develop. 34(1), 1990: rd correctly rounded, q within an ulp),
+// provided nothing underflows or overflows: den in [2^-24, 2^24] and
+// |a| in [2^-100, 2^100] (zero, Inf and NaN excluded); other elements take the
+// IEEE division.
+struct DnArgs {
+    float mean, den, rd;
+    bool fast;
+};
+__device__ __forceinline__ DnArgs dn_args(const float* dn) {
+    DnArgs a;
+    a.mean = dn[0];
+    a.den = dn[1] + 1e-7f;
+    a.rd = 1.0f / a.den;
+    a.fast = a.den >= 0x1p-24f && a.den <= 0x1p24f;
+    return a;
+}
+__device__ __forceinline__ bool dn_in_range(float a) {
+    const uint32_t e = __float_as_uint(a) & 0x7fffffffu;
+    return e - 0x0d800000u <= 0x71800000u - 0x0d800000u;   // 2^-100 <= |a| <= 2^100
+}
+__device__ __forceinline__ float dn_fast(float a, const DnArgs& d) {
+    const float q = a * d.rd;
+    const float r = __builtin_fmaf(-q, d.den, a);
+    return __builtin_fmaf(r, d.rd, q);
+}
+__device__ __forceinline__ f32x4 dn4(f32x4 v, const DnArgs& a) {
+    const f32x4 c{v.x - a.mean, v.y - a.mean, v.z - a.mean, v.w - a.mean};
+    if (a.fast && dn_in_range(c.x) && dn_in_range(c.y) && dn_in_range(c.z) && dn_in_range(c.w))
+        return f32x4{dn_fast(c.x, a), dn_fast(c.y, a), dn_fast(c.z, a), dn_fast(c.w, a)};
+    return f32x4{c.x / a.den, c.y / a.den, c.z / a.den, c.w / a.den};
+}
+
+template <int DN>
 __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x4, int64_t n4,
                                                      const float* __restrict__ alpha_p,
-                                                     ProjParams p, uint32_t* __restrict__ out4) {
+                                                     ProjParams p, uint32_t* __restrict__ out4,
+                                                     const float* __restrict__ dn) {
     const float alpha = *alpha_p;
+    DnArgs da{0.0f, 1.0f, 1.0f, false};
+    if (DN) da = dn_args(dn);
     const bool ok = alpha_valid(alpha);
     const bool fast = fast_scale(alpha);
     const float r = 1.0f / alpha;
@@ -121,6 +161,10 @@ __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x
         f32x4 v[4];
 #pragma unroll
         for (int u = 0; u < 4; u++) v[u] = __builtin_nontemporal_load(&x4[i0 + u * 256]);
+        if (DN) {
+#pragma unroll
+            for (int u = 0; u < 4; u++) v[u] = dn4(v[u], da);
+        }
 #pragma unroll
         for (int u = 0; u < 4; u++)
             __builtin_nontemporal_store(ok ? code4(v[u], alpha, r, fast, p) : z4, &out4[i0 + u * 256]);
@@ -128,20 +172,26 @@ __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x
 #pragma unroll
         for (int u = 0; u < 4; u++) {
             const int64_t i = i0 + u * 256;
-            if (i < n4) out4[i] = ok ? code4(x4[i], alpha, r, fast, p) : z4;
+            if (i < n4) out4[i] = ok ? code4(DN ? dn4(x4[i], da) : x4[i], alpha, r, fast, p) : z4;
         }
     }
 }
 
 // Scalar path: unaligned pointers and the tail of the vector path.
+template <int DN>
 __global__ __launch_bounds__(256) void k_project_scalar(const float* __restrict__ x, int64_t len,
                                                         const float* __restrict__ alpha_p,
-                                                        ProjParams p, uint8_t* __restrict__ out) {
+                                                        ProjParams p, uint8_t* __restrict__ out,
+                                                        const float* __restrict__ dn) {
     const float alpha = *alpha_p;
     const bool ok = alpha_valid(alpha);
+    DnArgs da{0.0f, 1.0f, 1.0f, false};
+    if (DN) da = dn_args(dn);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += stride)
-        out[i] = (uint8_t)(ok ? esb_code(x[i], alpha, p) : p.zero_code);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += stride) {
+        const float xi = DN ? (x[i] - da.mean) / da.den : x[i];
+        out[i] = (uint8_t)(ok ? esb_code(xi, alpha, p) : p.zero_code);
+    }
 }
 
 static int grid_for(int64_t work, int per_block) {
@@ -152,7 +202,7 @@ static int grid_for(int64_t work, int per_block) {
 }
 
 hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,
-                          uint8_t* codes, hipStream_t s) {
+                          uint8_t* codes, const float* dn, hipStream_t s) {
     if (len <= 0) return hipSuccess;
     const ProjParams p = proj_params(f);
     const bool aligned = ((uintptr_t)x % 16 == 0) && ((uintptr_t)codes % 4 == 0);
@@ -161,13 +211,18 @@ hipError_t launch_project(const float* x, int64_t len, const float* alpha, const
         const int64_t n4 = len / 4;
         const int64_t tiles = (n4 + kTile4 - 1) / kTile4;
         if (tiles > 0x7fffffff) return hipErrorInvalidValue;
-        k_project_vec<<<(unsigned)tiles, 256, 0, s>>>((const f32x4*)x, n4, alpha, p,
-                                                      (uint32_t*)codes);
+        if (dn) k_project_vec<1><<<(unsigned)tiles, 256, 0, s>>>((const f32x4*)x, n4, alpha, p,
+                                                                 (uint32_t*)codes, dn);
+        else k_project_vec<0><<<(unsigned)tiles, 256, 0, s>>>((const f32x4*)x, n4, alpha, p,
+                                                              (uint32_t*)codes, dn);
         head = n4 * 4;
     }
-    if (head < len)
-        k_project_scalar<<<grid_for(len - head, 256), 256, 0, s>>>(x + head, len - head, alpha,
-                                                                   p, codes + head);
+    if (head < len) {
+        if (dn) k_project_scalar<1><<<grid_for(len - head, 256), 256, 0, s>>>(
+                    x + head, len - head, alpha, p, codes + head, dn);
+        else k_project_scalar<0><<<grid_for(len - head, 256), 256, 0, s>>>(
+                    x + head, len - head, alpha, p, codes + head, dn);
+    }
     return hipGetLastError();
 }
 

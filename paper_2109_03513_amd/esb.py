@@ -74,6 +74,10 @@ def lib():
             "esb_pack_size": (sz, [i32, i32, i32, i32]),
             "esb_pack": (i32, [P, i32, i32, i64, i32, i32, P, P]),
             "esb_gemm_packed_workspace_size": (sz, [i32, i32, i32, i32, i32, i32, i32]),
+            "esb_dn_workspace_size": (sz, [i64]),
+            "esb_dn_stats": (i32, [P, i64, P, P, sz, P]),
+            "esb_project_dn": (i32, [P, i64, P, P, i32, i32, P, P]),
+            "esb_dda_normal": (i32, [i32, i32, P, i32, P, P, P, P]),
             "esb_gemm_packed": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i32, i32, P, P, P, i64,
                                       P, sz, P]),
         }
@@ -264,6 +268,46 @@ def esb_gemm_packed(A, nA, kA_sig, alphaA, B_packed, nB, kB_sig, alphaB, workspa
                                                     _ptr(B_packed), nB, kB_sig, _ptr(alphaB),
                                                     _ptr(acc), _ptr(y), N, wp, wb, _stream(stream)))
     return acc, y
+
+
+def esb_dn_stats(x, stats=None, workspace=None, stream=None):
+    """Device fp32 [mean, std] of x (population standard deviation)."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    n = x.numel()
+    if stats is None:
+        stats = torch.empty(2, dtype=torch.float32, device=x.device)
+    if workspace is None:
+        workspace = torch.empty(int(lib().esb_dn_workspace_size(n)), dtype=torch.uint8,
+                                device=x.device)
+    wp, wb = _ws(workspace)
+    _check("esb_dn_stats", lib().esb_dn_stats(_ptr(x), n, _ptr(stats), wp, wb, _stream(stream)))
+    return stats
+
+
+def esb_project_dn(x, stats, alpha, n, k_sig, codes=None, stream=None):
+    """Codes of fl32(fl32(x - mean) / fl32(std + 1e-7)) under alpha; stats = [mean, std]."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    if codes is None:
+        codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _check("esb_project_dn", lib().esb_project_dn(_ptr(x), x.numel(), _ptr(stats), _ptr(alpha), n,
+                                                  k_sig, _ptr(codes), _stream(stream)))
+    return codes
+
+
+def esb_dda_normal(n, k_sig, grid, alpha_out=None, D_out=None, dD_out=None, stream=None):
+    """Analytic one-sided D_j for N(0,1) over the candidates grid (device fp32); dD_out
+    (optional device fp64 tensor of grid's size) receives dD/dalpha."""
+    import torch
+    G = grid.numel()
+    if alpha_out is None:
+        alpha_out = torch.empty(1, dtype=torch.float32, device=grid.device)
+    if D_out is None:
+        D_out = torch.empty(G, dtype=torch.float64, device=grid.device)
+    _check("esb_dda_normal", lib().esb_dda_normal(n, k_sig, _ptr(grid), G, _ptr(alpha_out),
+                                                  _ptr(D_out), _ptr(dD_out), _stream(stream)))
+    return alpha_out, D_out
 
 
 def conv_out_hw(H, W, R, S, stride, pad):

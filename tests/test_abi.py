@@ -158,3 +158,24 @@ def test_packed_sizes_and_errors(L):
               None) == -4
     assert gp(M, N, K, fake, K - 1, 3, 2, fake, fake, 3, 1, fake, fake, None, N, fake, need,
               None) == -1
+
+
+def test_dn_and_dda_normal_refusals(L):
+    """Normalization and the analytic aligner refuse bad arguments before any launch."""
+    fake = ctypes.c_void_p(0x1000)
+    need = L.esb_dn_workspace_size(1 << 20)
+    assert need >= 8
+    assert L.esb_dn_workspace_size(-1) == 0
+    assert L.esb_dn_stats(fake, -1, fake, fake, need, None) == -1
+    assert L.esb_dn_stats(fake, 10, None, fake, need, None) == -1
+    assert L.esb_dn_stats(None, 10, fake, fake, need, None) == -1
+    assert L.esb_dn_stats(fake, 1 << 20, fake, fake, need - 1, None) == -6
+    assert L.esb_dn_stats(fake, 1 << 20, fake, None, need, None) == -6
+    assert L.esb_project_dn(fake, 10, fake, fake, 9, 2, fake, None) == -1   # n > 8
+    assert L.esb_project_dn(fake, 10, None, fake, 4, 2, fake, None) == -1
+    assert L.esb_project_dn(fake, -1, fake, fake, 4, 2, fake, None) == -1
+    assert L.esb_dda_normal(4, 2, fake, 0, fake, None, None, None) == -1
+    assert L.esb_dda_normal(4, 4, fake, 10, fake, None, None, None) == -1          # k_sig >= n
+    assert L.esb_dda_normal(4, 2, None, 10, fake, None, None, None) == -1
+    assert L.esb_dda_normal(4, 2, fake, 10, None, fake, None, None) == -1
+    assert L.esb_dda_normal(4, 2, fake, 10, fake, None, fake, None) == -1   # D_out required
