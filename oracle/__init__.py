@@ -60,6 +60,7 @@ def lib():
             "eso_dda": (i32, [P, i64, i32, i32, P, i32, P]),
             "eso_dda_normal": (f64, [f64, i32, i32]),
             "eso_dda_normal_deriv": (f64, [f64, i32, i32]),
+            "eso_post": (i32, [P, i64, i64, i64, P, P, P, i32, f32, i32, i32, P, P]),
             "eso_dn_stats": (i32, [P, i64, P, P]),
             "eso_project_dn": (i32, [P, i64, f32, f32, f32, i32, i32, P]),
             "eso_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, f32, P, i64, i32, i32, f32, i32,
@@ -194,6 +195,24 @@ def project_dn(x, mean, std, alpha, b, k_sig):
                               float(np.float32(alpha)), b, k_sig, _p(out))
     assert st == 0
     return out
+
+
+def post(y, b, k_sig, alpha, a=None, bias=None, res=None, relu=False):
+    """Fused post-processing of a 2-D output y (channels = columns): returns (z, codes)."""
+    y = _f32(y)
+    assert y.ndim == 2
+    rows, cols = y.shape
+    av = None if a is None else _f32(a)
+    bv = None if bias is None else _f32(bias)
+    rv = None if res is None else _f32(res)
+    z = np.empty_like(y)
+    codes = np.empty(y.shape, dtype=np.uint8)
+    st = lib().eso_post(_p(y), rows, cols, cols, None if av is None else _p(av),
+                        None if bv is None else _p(bv), None if rv is None else _p(rv),
+                        int(bool(relu)), float(np.float32(alpha)), b, k_sig, _p(z), _p(codes))
+    if st:
+        raise ValueError("eso_post: %d" % st)
+    return z, codes
 
 
 def gemm(A, B, bA, ksA, alphaA, bB, ksB, alphaB, b_layout=0, want_acc=True, want_y=True):

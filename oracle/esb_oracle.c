@@ -339,6 +339,33 @@ int eso_project_dn(const float* x, int64_t n, float mean, float std, float alpha
     return ESO_OK;
 }
 
+/*
+ * Post-processing of a contraction output (Sec. 4.2, the "BN and DN" step of
+ * eq. (16) folded into a per-channel a x + b, then the "ESB quantization"
+ * step): for the scaled output y of row i, channel j (row-major, pitch ld),
+ *   z = fma(a_j, y, b_j)            one rounding; a_j = 1, b_j = 0 when absent,
+ *   z = fl32(z + res_ij)            when a residual is given,
+ *   z = z > 0 ? z : 0               when relu (NaN gives 0),
+ *   code = projection of z with alpha (eq. (6)-(8)),
+ * writing z to z_out and the code to codes_out (either may be NULL).
+ */
+int eso_post(const float* y, int64_t rows, int64_t cols, int64_t ld, const float* a,
+             const float* bias, const float* res, int relu, float alpha, int b, int k_sig,
+             float* z_out, uint8_t* codes_out) {
+    if (!valid_bk(b, k_sig) || rows < 0 || cols < 0 || ld < cols) return ESO_E_INVALID;
+    for (int64_t i = 0; i < rows; i++)
+        for (int64_t j = 0; j < cols; j++) {
+            const int64_t o = i * ld + j;
+            float z = fmaf(a ? a[j] : 1.0f, y[o], bias ? bias[j] : 0.0f);
+            if (res) z = z + res[o];
+            if (relu) z = z > 0.0f ? z : 0.0f;
+            if (z_out) z_out[o] = z;
+            if (codes_out)
+                codes_out[o] = (uint8_t)eso_encode(eso_project_value(z, alpha, b, k_sig), b, k_sig);
+        }
+    return ESO_OK;
+}
+
 /* Exact integer of a code: m = q * 2^k (eq. (14)-(15): fraction bits made integral). */
 static int64_t code_int(int code, int b, int k_sig) {
     return (int64_t)ldexp(eso_decode(code, b, k_sig), k_sig - 1);
