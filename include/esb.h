@@ -273,6 +273,49 @@ int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
                   const float* alphaW, int32_t* acc, float* y, void* workspace,
                   size_t ws_bytes, void* stream);
 
+/*
+ * Fused post-processing of a contraction's outputs (Sec. 4.2: the "BN and DN"
+ * step of eq. (16), folded offline into a per-channel a x + b, then the "ESB
+ * quantization" step that hands the next layer its codes), in the epilogue of
+ * the contraction kernels, so that the next layer's input is written as codes
+ * (1 byte per output) instead of fp32.  For each output with scaled value
+ * y0 = fl32(s fl32(acc)) (s as in esb_gemm) in channel j (the output column of
+ * a GEMM, the output channel of a convolution):
+ *   z = fma(a[j], y0, b[j])     one rounding; a[j] = 1 when a is NULL, b[j] = 0
+ *                               when b is NULL (so -0 becomes +0);
+ *   z = fl32(z + residual[o])   when residual is not NULL;
+ *   z = z > 0 ? z : 0           when relu is nonzero (NaN gives 0);
+ *   y[o] = z                    when y is not NULL (instead of y0);
+ *   codes[o] = code of z under *alpha in ESB(n, k_sig), as esb_project, when
+ *              codes is not NULL.
+ * residual and codes have the layout of y (GEMM: M rows of pitch ldc; conv:
+ * NHWC [N, P, Q, K]); residual may be the same buffer as y (read before the
+ * write of the same element).  acc, when not NULL, still receives the integer
+ * sums.  The scale of the outputs must be known before the layer (the
+ * paper's offline / running-average scales): alpha is a device scalar.
+ * Errors: ESB_E_INVALID if post is given without alphaA / alphaB, if codes is
+ * given without alpha or with an invalid (n, k_sig), or if acc, y and codes are
+ * all NULL; otherwise as esb_gemm_ws / esb_conv2d_ws (workspace may be NULL).
+ */
+typedef struct esb_post {
+    const float* a;         /* device, one fp32 per output channel, or NULL */
+    const float* b;         /* device, one fp32 per output channel, or NULL */
+    const float* residual;  /* device fp32 in the layout of y, or NULL */
+    int relu;               /* nonzero: clamp at 0 */
+    const float* alpha;     /* device scalar: scale of the output codes */
+    int n, k_sig;           /* format of the output codes */
+    uint8_t* codes;         /* device, one code per output in the layout of y, or NULL */
+} esb_post;
+
+int esb_gemm_post(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                  const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+                  const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+                  const esb_post* post, void* workspace, size_t ws_bytes, void* stream);
+int esb_conv2d_post(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+                    const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+                    const float* alphaW, int32_t* acc, float* y, const esb_post* post,
+                    void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -17,6 +17,7 @@ struct DwParams {
     int32_t* acc;
     float* y;
     int kx, kw;
+    Post post;         // fused post-processing of the outputs (post.on == 0: none)
     int16_t tx[256];   // exact integer of every activation code
     int16_t tw[256];   // exact integer of every filter code
 };
@@ -34,7 +35,8 @@ __global__ __launch_bounds__(kDwThreads) void k_dwconv(DwParams p) {
     tx[threadIdx.x] = p.tx[threadIdx.x];
     __syncthreads();
     float s = 0.0f;
-    if (p.y) s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kx + p.kw));
+    if (p.y || p.post.on) s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kx + p.kw));
+    const float qa = p.post.on ? post_alpha(p.post) : 0.0f;
     const int CV = VEC ? C / 4 : C;                 // channel groups per pixel
     const int64_t total = (int64_t)g.Nb * g.P * g.Q * CV;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -68,20 +70,28 @@ __global__ __launch_bounds__(kDwThreads) void k_dwconv(DwParams p) {
         const int64_t o = pix * C + c0;
         if (VEC) {
             if (p.acc) *(int4*)(p.acc + o) = make_int4(a0, a1, a2, a3);
-            if (p.y) *(float4*)(p.y + o) = make_float4(s * (float)a0, s * (float)a1, s * (float)a2,
-                                                        s * (float)a3);
+            if (p.post.on) {
+                post_store(p.post, p.y, o, c0, s * (float)a0, qa);
+                post_store(p.post, p.y, o + 1, c0 + 1, s * (float)a1, qa);
+                post_store(p.post, p.y, o + 2, c0 + 2, s * (float)a2, qa);
+                post_store(p.post, p.y, o + 3, c0 + 3, s * (float)a3, qa);
+            } else if (p.y) {
+                *(float4*)(p.y + o) = make_float4(s * (float)a0, s * (float)a1, s * (float)a2,
+                                                  s * (float)a3);
+            }
         } else {
             if (p.acc) p.acc[o] = a0;
-            if (p.y) p.y[o] = s * (float)a0;
+            out_store(p.post, p.y, o, c0, s * (float)a0, qa);
         }
     }
 }
 
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,
-                         float* y, hipStream_t s) {
+                         float* y, hipStream_t s, const Post* post) {
     DwParams p;
     p.g = g; p.x = x; p.w = w; p.alphaX = alphaX; p.alphaW = alphaW; p.acc = acc; p.y = y;
+    p.post = post ? *post : Post{};
     p.kx = fx.k; p.kw = fw.k;
     for (int c = 0; c < 256; c++) {
         p.tx[c] = (int16_t)decode_int(fx, (uint32_t)c);

@@ -153,13 +153,39 @@ static bool pre_worth(int64_t M, int64_t N, int64_t K, int64_t a_elems, int64_t 
     return ops >= 1500.0 * (double)(a_elems + b_elems);
 }
 
+// Fused post-processing: the output scale needs both alphas; codes need their
+// format and scale.
+static bool post_ok(const esb_post* p, const float* alphaA, const float* alphaB) {
+    if (!p) return true;
+    if (!alphaA || !alphaB) return false;
+    if (p->codes && (!p->alpha || !valid_fmt(p->n, p->k_sig))) return false;
+    return true;
+}
+
+static Post make_post(const esb_post* p) {
+    Post q{};
+    if (!p) return q;
+    q.a = p->a;
+    q.b = p->b;
+    q.res = p->residual;
+    q.alpha = p->alpha;
+    q.codes = p->codes;
+    q.relu = p->relu != 0;
+    q.on = 1;
+    if (p->codes) q.pp = proj_params(make_fmt(p->n, p->k_sig));
+    return q;
+}
+
 static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
                      const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
                      const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
-                     void* ws, size_t ws_bytes, void* stream) {
+                     void* ws, size_t ws_bytes, void* stream, const esb_post* post = nullptr) {
     if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig)) return ESB_E_INVALID;
     if (M < 0 || N < 0 || K < 0 || (b_layout != ESB_B_NK && b_layout != ESB_B_KN)) return ESB_E_INVALID;
-    if (!acc && !y) return ESB_E_INVALID;
+    if (!post_ok(post, alphaA, alphaB)) return ESB_E_INVALID;
+    if (!acc && !y && !(post && post->codes)) return ESB_E_INVALID;
+    const Post P = make_post(post);
+    const Post* pp = post ? &P : nullptr;
     if (ldc < N || lda < K || (b_layout == ESB_B_NK ? ldb < K : ldb < N)) return ESB_E_INVALID;
     if (y && (!alphaA || !alphaB)) return ESB_E_INVALID;
     if ((int64_t)M * N > 0 && K > 0 && (!A || !B)) return ESB_E_INVALID;
@@ -180,12 +206,13 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     const bool fits = mma_fits(g, A, K, 1, B, ldb, b_layout);
     if (ws && fits && (f4 || op == 1) && pre_worth(M, N, K, (int64_t)M * K, (int64_t)N * K))
         return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, B, N, ldb, fb, alphaB,
-                                         acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, nullptr, false, s));
+                                         acc, y, ldc, f4 ? 1 : (f6 ? 2 : 0), ws, nullptr, false, s,
+                                         pp));
     if (op >= 0 && fits)   // with a workspace, skinny shapes split the reduction
         return hip_status(launch_mma(op, M, N, K, 1, g, A, fa, alphaA, B, ldb, fb, alphaB, acc, y,
-                                     ldc, (int32_t*)ws, s));
+                                     ldc, (int32_t*)ws, s, pp));
     return hip_status(launch_contraction(M, N, K, 1, g, A, decode_info(fa), alphaA, B, ldb, b_layout,
-                                         decode_info(fb), alphaB, acc, y, ldc, N, s));
+                                         decode_info(fb), alphaB, acc, y, ldc, N, s, pp));
 }
 
 size_t esb_gemm_workspace_size(int M, int N, int K, int nA, int kA_sig, int nB, int kB_sig) {
@@ -248,9 +275,12 @@ static bool conv_is_depthwise(const esb_conv_desc* d) {
 
 static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, const float* alphaX,
                      const uint8_t* w, int nW, int kW_sig, const float* alphaW, int32_t* acc, float* y,
-                     void* ws, size_t ws_bytes, void* stream) {
+                     void* ws, size_t ws_bytes, void* stream, const esb_post* post = nullptr) {
     if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return ESB_E_INVALID;
-    if (!acc && !y) return ESB_E_INVALID;
+    if (!post_ok(post, alphaX, alphaW)) return ESB_E_INVALID;
+    if (!acc && !y && !(post && post->codes)) return ESB_E_INVALID;
+    const Post P = make_post(post);
+    const Post* pp = post ? &P : nullptr;
     if (y && (!alphaX || !alphaW)) return ESB_E_INVALID;
     ConvGeom g;
     int64_t Mrows = 0, kred = 0;
@@ -264,7 +294,7 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
     if (Mrows == 0) return ESB_OK;
     const hipStream_t s = (hipStream_t)stream;
     if (conv_is_depthwise(d))
-        return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s));
+        return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s, pp));
     const int op = mma_choose(fx, fw, kred);
     const bool f4 = mma_f4ok(fx, fw, kred) && g.Cg % 32 == 0;
     const bool f6 = !f4 && mma_f6ok(fx, fw, kred) && g.Cg % 64 == 0 && mma_f6_tiles(Mrows, Kg, d->groups);
@@ -274,13 +304,13 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
         return hip_status(launch_mma_pre((int)Mrows, Kg, (int)kred, d->groups, g, x,
                                          (int64_t)d->N * d->H * d->W, d->C, d->C, fx, alphaX, w, d->K,
                                          kred, fw, alphaW, acc, y, d->K, f4 ? 1 : (f6 ? 2 : 0), ws, nullptr,
-                                         false, s));
+                                         false, s, pp));
     if (op >= 0 && fits)
         return hip_status(launch_mma(op, (int)Mrows, Kg, (int)kred, d->groups, g, x, fx, alphaX, w,
-                                     kred, fw, alphaW, acc, y, d->K, nullptr, s));
+                                     kred, fw, alphaW, acc, y, d->K, nullptr, s, pp));
     return hip_status(launch_contraction((int)Mrows, Kg, (int)kred, d->groups, g, x, decode_info(fx),
                                          alphaX, w, kred, ESB_B_NK, decode_info(fw), alphaW, acc, y,
-                                         d->K, Kg, s));
+                                         d->K, Kg, s, pp));
 }
 
 size_t esb_conv2d_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int nW, int kW_sig) {
@@ -304,6 +334,22 @@ int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig, 
                   void* workspace, size_t ws_bytes, void* stream) {
     return conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, acc, y, workspace, ws_bytes,
                      stream);
+}
+
+int esb_gemm_post(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,
+                  const float* alphaA, const uint8_t* B, int64_t ldb, int nB, int kB_sig,
+                  const float* alphaB, int b_layout, int32_t* acc, float* y, int64_t ldc,
+                  const esb_post* post, void* workspace, size_t ws_bytes, void* stream) {
+    return gemm_impl(M, N, K, A, lda, nA, kA_sig, alphaA, B, ldb, nB, kB_sig, alphaB, b_layout, acc, y,
+                     ldc, workspace, ws_bytes, stream, post);
+}
+
+int esb_conv2d_post(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+                    const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+                    const float* alphaW, int32_t* acc, float* y, const esb_post* post,
+                    void* workspace, size_t ws_bytes, void* stream) {
+    return conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, acc, y, workspace, ws_bytes,
+                     stream, post);
 }
 
 

@@ -51,6 +51,75 @@ struct ProjParams {
 };
 ProjParams proj_params(const Fmt& f);
 
+// Code of x under scale alpha (eq. (6)-(8)): v = fl32(x / alpha) with the IEEE
+// binary32 division, then the shift-round of eq. (7) on the bit pattern of |v|:
+//   |v| >= 1: keep the leading 1 and k fraction bits, adding half an ulp of the
+//             kept precision before truncating (ties go to the larger magnitude);
+//             the carry into the exponent field is the round-up to the next binade;
+//   |v| <  1: the step is fixed at 2^-k (the subnormal binade, eq. (5));
+//   |v| >= C: clip to C (eq. (8)); NaN gives +0.
+// For |v| >= 1 the rounded bit pattern is the code itself: the biased fp32
+// exponent minus 127 is the ESB exponent field, the kept fraction bits the
+// ESB fraction field.
+__device__ __forceinline__ uint32_t esb_code(float x, float alpha, const ProjParams& p) {
+    const float v = x / alpha;   // correctly rounded binary32 division
+    const uint32_t vb = __float_as_uint(v);
+    const uint32_t ab = vb & 0x7fffffffu;
+    const uint32_t ef = ab >> 23;
+    // |v| in [1, C): round to k fraction bits; the result is (e+127) << k | f.
+    const uint32_t shA = 23u - p.k;
+    const uint32_t codeA = ((ab + (1u << (shA - 1u))) >> shA) - (127u << p.k);
+    // |v| < 1: m = round(|v| * 2^k) in [0, 2^k]; m == 2^k is the value 1 (code 0).
+    const uint32_t mant = (ab & 0x7fffffu) | (ef ? 0x800000u : 0u);
+    const uint32_t sB = min(150u - max(ef, 1u) - p.k, 25u);   // >= 17 for |v| < 1
+    const uint32_t m = (mant + (1u << (sB - 1u))) >> sB;       // sB == 25 gives 0
+    const uint32_t codeB = (m >= p.one) ? 0u : (p.zero_code | m);
+    uint32_t code = (ef >= 127u) ? codeA : codeB;
+    code = (ab >= p.c_bits) ? p.c_code : code;            // clip (covers +-Inf)
+    code = (ab > 0x7f800000u) ? p.zero_code : code;       // NaN
+    code |= ((vb >> 31) && code != p.zero_code) ? p.sign_bit : 0u;
+    return code;
+}
+
+__device__ __forceinline__ bool alpha_valid(float a) { return a > 0.0f && a < __builtin_inff(); }
+
+// Fused post-processing of a contraction output (Sec. 4.2: the "BN and DN"
+// step of eq. (16) folded into a per-channel a x + b, then the "ESB
+// quantization" step), applied to the scaled output y0 = fl32(s fl32(acc)):
+//   z = fma(a_ch, y0, b_ch)   (a_ch = 1, b_ch = 0 when absent; one rounding)
+//   z = fl32(z + res_o)       (when a residual is given)
+//   z = z > 0 ? z : 0         (relu; NaN gives 0)
+// z goes to y (when given) and its code under *alpha to codes (when given);
+// res, y and codes share the output indexing.  on == 0: the plain epilogue.
+struct Post {
+    const float* a;
+    const float* b;
+    const float* res;
+    const float* alpha;
+    uint8_t* codes;
+    ProjParams pp;
+    int relu;
+    int on;
+};
+
+__device__ __forceinline__ float post_alpha(const Post& P) { return P.codes ? *P.alpha : 0.0f; }
+
+__device__ __forceinline__ void post_store(const Post& P, float* y, int64_t o, int64_t ch, float y0,
+                                           float qa) {
+    float z = __builtin_fmaf(P.a ? P.a[ch] : 1.0f, y0, P.b ? P.b[ch] : 0.0f);
+    if (P.res) z = z + P.res[o];
+    if (P.relu) z = z > 0.0f ? z : 0.0f;
+    if (y) y[o] = z;
+    if (P.codes) P.codes[o] = (uint8_t)(alpha_valid(qa) ? esb_code(z, qa, P.pp) : P.pp.zero_code);
+}
+
+// The epilogue store of one output: the plain scaled value, or the fused post-processing.
+__device__ __forceinline__ void out_store(const Post& P, float* y, int64_t o, int64_t ch, float y0,
+                                          float qa) {
+    if (P.on) post_store(P, y, o, ch, y0, qa);
+    else if (y) y[o] = y0;
+}
+
 hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,
                           uint8_t* codes, const float* dn, hipStream_t s);
 
@@ -96,7 +165,7 @@ hipError_t launch_contraction(int M, int N, int K, int groups, const ConvGeom& g
                               const uint8_t* A, const DecodeInfo& da, const float* alphaA,
                               const uint8_t* B, int64_t ldb, int b_layout, const DecodeInfo& db,
                               const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                              int out_col_per_group, hipStream_t s);
+                              int out_col_per_group, hipStream_t s, const Post* post = nullptr);
 
 // Large-tile path on the 32x32 MFMA shapes.  op 1: codes decoded to E4M3,
 // fp32 accumulation; op 0: codes of n <= 3 bits decoded to int8 by one
@@ -117,7 +186,7 @@ bool mma_fits(const ConvGeom& ga, const uint8_t* A, int64_t K, int groups, const
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
                       const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
                       int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
-                      int64_t ldc, int32_t* part, hipStream_t s);
+                      int64_t ldc, int32_t* part, hipStream_t s, const Post* post = nullptr);
 // Ranges of the reduction split for a dense GEMM of this shape (1: none), and
 // their length.
 int mma_splitk(int64_t M, int64_t N, int64_t K, int* kchunk);
@@ -141,7 +210,8 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s);
+                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s,
+                          const Post* post = nullptr);
 // b_packed: B given in packed E2M1 (mode 1 only), not decoded; split: a dense
 // GEMM with too few tiles splits its reduction (mma_splitk), the int32 partial
 // sums after the decoded operands in ws (see esb_gemm_packed_workspace_size).
@@ -151,6 +221,6 @@ hipError_t launch_pack_fp4(const uint8_t* codes, int64_t rows, int64_t K, int64_
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,
-                         float* y, hipStream_t s);
+                         float* y, hipStream_t s, const Post* post = nullptr);
 
 }  // namespace esb

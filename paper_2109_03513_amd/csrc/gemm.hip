@@ -37,6 +37,7 @@ struct GemmParams {
     float* y;
     int64_t ldc;
     uint32_t zeroA, zeroB;  // the +0 code of each operand (padding / out of range)
+    Post post;              // fused post-processing of the outputs (post.on == 0: none)
 };
 
 // ------------------------------------------------------------------ decode
@@ -347,7 +348,8 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
 
     // epilogue: lane holds rows 4*(lane>>4) + r, column lane & 15 of each 16x16 block
     float s = 0.0f;
-    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.da.k + g.db.k));
+    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.da.k + g.db.k));
+    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -361,9 +363,10 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
                     if (NACC > 1) v += (uint32_t)acc[NACC > 1 ? 1 : 0][i][j][r] << 8;
                     if (NACC > 2) v += (uint32_t)acc[NACC > 2 ? 2 : 0][i][j][r] << 16;
                     const int32_t iv = (int32_t)v;
-                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    const int64_t ch = (int64_t)grp * g.N + col;
+                    const int64_t o = (int64_t)row * g.ldc + ch;
                     if (g.acc) g.acc[o] = iv;
-                    if (g.y) g.y[o] = s * (float)iv;
+                    out_store(g.post, g.y, o, ch, s * (float)iv, qa);
                 }
             }
 }
@@ -417,12 +420,13 @@ hipError_t launch_contraction(int M, int N, int K, int groups, const ConvGeom& g
                               const uint8_t* A, const DecodeInfo& da, const float* alphaA,
                               const uint8_t* B, int64_t ldb, int b_layout, const DecodeInfo& db,
                               const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                              int /*out_col_per_group*/, hipStream_t s) {
+                              int /*out_col_per_group*/, hipStream_t s, const Post* post) {
     if (M <= 0 || N <= 0) return hipSuccess;
     GemmParams g;
     g.M = M; g.N = N; g.K = K; g.ga = ga;
     g.A = A; g.B = B; g.ldb = ldb; g.da = da; g.db = db;
     g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.post = post ? *post : Post{};
     g.zeroA = (uint32_t)da.emax << da.k;
     g.zeroB = (uint32_t)db.emax << db.k;
     const bool a16 = (K > 0) && (ga.Cg >= 16) && (ga.Cg % 16 == 0) && (ga.pitch % 16 == 0) &&

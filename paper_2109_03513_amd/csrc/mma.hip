@@ -62,6 +62,7 @@ struct FastParams {
     int out_shift;          // F8: acc_int = acc_f32 * 2^out_shift
     int kA, kB;
     int zrowA, zrowB;       // rows of kZeroRows holding each operand's +0 code
+    Post post;              // fused post-processing of the outputs (post.on == 0: none)
 };
 constexpr int kZeroRowE4M3 = 7 * 8;
 
@@ -407,7 +408,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     // epilogue: register r of a 32x32 block holds row 8*(r/4) + 4*(lane/32) + r%4,
     // column lane % 32.
     float s = 0.0f;
-    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -430,9 +432,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
                         g.part[((int64_t)kz * g.M + row) * g.N + col] = iv;
                         continue;
                     }
-                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    const int64_t ch = (int64_t)grp * g.N + col;
+                    const int64_t o = (int64_t)row * g.ldc + ch;
                     if (g.acc) g.acc[o] = iv;
-                    if (g.y) g.y[o] = s * fv;
+                    out_store(g.post, g.y, o, ch, s * fv, qa);
                 }
             }
 }
@@ -445,7 +448,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
 __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
     const int64_t MN = (int64_t)g.M * g.N;
     float s = 0.0f;
-    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (g.N % 4 == 0) {
@@ -470,7 +474,7 @@ __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
                 if (g.acc) g.acc[o + c] = t[c];
-                if (g.y) g.y[o + c] = s * (float)t[c];
+                out_store(g.post, g.y, o + c, col + c, s * (float)t[c], qa);
             }
         }
         return;
@@ -482,7 +486,7 @@ __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
         const int64_t row = e / g.N, col = e - row * g.N;
         const int64_t o = row * g.ldc + col;
         if (g.acc) g.acc[o] = t;
-        if (g.y) g.y[o] = s * (float)t;
+        out_store(g.post, g.y, o, col, s * (float)t, qa);
     }
 }
 
@@ -781,7 +785,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
     vm_wait<0>();   // the fetches past the end (+0 rows) land before the workgroup ends
 
     float s = 0.0f;
-    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -796,9 +801,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
                         g.part[((int64_t)kz * g.M + row) * g.N + col] = (int32_t)fv;
                         continue;
                     }
-                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    const int64_t ch = (int64_t)grp * g.N + col;
+                    const int64_t o = (int64_t)row * g.ldc + ch;
                     if (g.acc) g.acc[o] = (int32_t)fv;
-                    if (g.y) g.y[o] = s * fv;
+                    out_store(g.post, g.y, o, ch, s * fv, qa);
                 }
             }
 }
@@ -975,7 +981,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_f6(FastParams g) {
     vm_wait<0>();   // the fetches past the end (+0 rows) land before the workgroup ends
 
     float s = 0.0f;
-    if (g.y) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
+    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -986,9 +993,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_f6(FastParams g) {
                 const int col = n0 + wc + 32 * j + lr;
                 if (row < g.M && col < g.N) {
                     const float fv = ldexpf(acc[i][j][r], g.out_shift);
-                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
+                    const int64_t ch = (int64_t)grp * g.N + col;
+                    const int64_t o = (int64_t)row * g.ldc + ch;
                     if (g.acc) g.acc[o] = (int32_t)fv;
-                    if (g.y) g.y[o] = s * fv;
+                    out_store(g.post, g.y, o, ch, s * fv, qa);
                 }
             }
 }
@@ -1170,7 +1178,8 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
                           int64_t a_rows, int64_t a_cols, int64_t a_pitch, const Fmt& fa,
                           const float* alphaA, const uint8_t* B, int64_t b_rows, int64_t ldb,
                           const Fmt& fb, const float* alphaB, int32_t* acc, float* y, int64_t ldc,
-                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s) {
+                          int mode, void* ws, const uint8_t* b_packed, bool split, hipStream_t s,
+                          const Post* post) {
     if (M <= 0 || N <= 0) return hipSuccess;
     const bool conv = !(ga.H == 1 && ga.W == 1 && ga.R == 1 && ga.S == 1 && ga.ph == 0 && ga.pw == 0 &&
                         ga.Cg == K && groups == 1);
@@ -1218,6 +1227,7 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
     g.da = j0.d;
     g.db = j1.d;
     g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.post = post ? *post : Post{};
     g.kA = fa.k; g.kB = fb.k;
     // E4M3 holds q * 2^-6 per operand; E2M1 and E2M3 hold q itself
     g.out_shift = fa.k + fb.k + ((f4 || f6) ? 0 : 12);
@@ -1264,7 +1274,7 @@ int mma_splitk(int64_t M, int64_t N, int64_t K, int* kchunk) {
 hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& ga,
                       const uint8_t* A, const Fmt& fa, const float* alphaA, const uint8_t* B,
                       int64_t ldb, const Fmt& fb, const float* alphaB, int32_t* acc, float* y,
-                      int64_t ldc, int32_t* part, hipStream_t s) {
+                      int64_t ldc, int32_t* part, hipStream_t s, const Post* post) {
     if (M <= 0 || N <= 0) return hipSuccess;
     FastParams g;
     g.M = M; g.N = N; g.K = K; g.ga = ga;
@@ -1280,6 +1290,7 @@ hipError_t launch_mma(int op, int M, int N, int K, int groups, const ConvGeom& g
     g.da = mma_decode(fa, op);
     g.db = mma_decode(fb, op);
     g.alphaA = alphaA; g.alphaB = alphaB; g.acc = acc; g.y = y; g.ldc = ldc;
+    g.post = post ? *post : Post{};
     g.kA = fa.k; g.kB = fb.k;
     g.out_shift = fa.k + fb.k + 12;
     g.zrowA = (fa.n - 2) * 8 + fa.k;

@@ -38,28 +38,6 @@ ProjParams proj_params(const Fmt& f) {
     return p;
 }
 
-__device__ __forceinline__ uint32_t esb_code(float x, float alpha, const ProjParams& p) {
-    const float v = x / alpha;   // correctly rounded binary32 division
-    const uint32_t vb = __float_as_uint(v);
-    const uint32_t ab = vb & 0x7fffffffu;
-    const uint32_t ef = ab >> 23;
-    // |v| in [1, C): round to k fraction bits; the result is (e+127) << k | f.
-    const uint32_t shA = 23u - p.k;
-    const uint32_t codeA = ((ab + (1u << (shA - 1u))) >> shA) - (127u << p.k);
-    // |v| < 1: m = round(|v| * 2^k) in [0, 2^k]; m == 2^k is the value 1 (code 0).
-    const uint32_t mant = (ab & 0x7fffffu) | (ef ? 0x800000u : 0u);
-    const uint32_t sB = min(150u - max(ef, 1u) - p.k, 25u);   // >= 17 for |v| < 1
-    const uint32_t m = (mant + (1u << (sB - 1u))) >> sB;       // sB == 25 gives 0
-    const uint32_t codeB = (m >= p.one) ? 0u : (p.zero_code | m);
-    uint32_t code = (ef >= 127u) ? codeA : codeB;
-    code = (ab >= p.c_bits) ? p.c_code : code;            // clip (covers +-Inf)
-    code = (ab > 0x7f800000u) ? p.zero_code : code;       // NaN
-    code |= ((vb >> 31) && code != p.zero_code) ? p.sign_bit : 0u;
-    return code;
-}
-
-__device__ __forceinline__ bool alpha_valid(float a) { return a > 0.0f && a < __builtin_inff(); }
-
 // Fast code of x given r = fl32(1/alpha); sets `risky` if q0 is within 4 ulps
 // of a midpoint (the caller then recomputes with esb_code).
 __device__ __forceinline__ uint32_t esb_code_fast(float x, float r, const ProjParams& p,

@@ -40,6 +40,12 @@ class ConvDesc(ctypes.Structure):
                  "groups")]
 
 
+class PostDesc(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("relu", ctypes.c_int), ("alpha", ctypes.c_void_p), ("n", ctypes.c_int),
+                ("k_sig", ctypes.c_int), ("codes", ctypes.c_void_p)]
+
+
 def lib():
     """Load libesb.so (after torch, so that both share one HIP runtime)."""
     global _lib
@@ -74,6 +80,10 @@ def lib():
             "esb_pack_size": (sz, [i32, i32, i32, i32]),
             "esb_pack": (i32, [P, i32, i32, i64, i32, i32, P, P]),
             "esb_gemm_packed_workspace_size": (sz, [i32, i32, i32, i32, i32, i32, i32]),
+            "esb_gemm_post": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32,
+                                    P, P, i64, ctypes.POINTER(PostDesc), P, sz, P]),
+            "esb_conv2d_post": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P,
+                                      P, ctypes.POINTER(PostDesc), P, sz, P]),
             "esb_dn_workspace_size": (sz, [i64]),
             "esb_dn_stats": (i32, [P, i64, P, P, sz, P]),
             "esb_project_dn": (i32, [P, i64, P, P, i32, i32, P, P]),
@@ -226,6 +236,73 @@ def esb_gemm(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, b_layout=ESB_B_NK, ac
                                                 _ptr(B), ldb, nB, kB_sig, _ptr(alphaB), b_layout,
                                                 _ptr(acc), _ptr(y), N, wp, wb, _stream(stream)))
     return acc, y
+
+
+def _addr(t):
+    return None if t is None else t.data_ptr()
+
+
+def post_desc(alpha, n, k_sig, codes=None, a=None, b=None, residual=None, relu=False):
+    """esb_post of device tensors: per-channel a, b, a residual in the output layout, relu, and
+    the output codes (uint8, output layout) under the device scalar alpha in ESB(n, k_sig)."""
+    return PostDesc(_addr(a), _addr(b), _addr(residual), int(bool(relu)), _addr(alpha), n, k_sig,
+                    _addr(codes))
+
+
+def esb_gemm_post(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, out_alpha, out_n, out_k_sig,
+                  a=None, b=None, residual=None, relu=False, b_layout=ESB_B_NK, codes=None,
+                  want_codes=True, acc=None, want_acc=False, y=None, want_y=False, workspace=None,
+                  stream=None):
+    """Contraction with the fused post-processing; returns (acc, y, codes), M x N each."""
+    import torch
+    _dev_tensor(A, torch.uint8, "A")
+    _dev_tensor(B, torch.uint8, "B")
+    M, K = A.shape
+    N = B.shape[0] if b_layout == ESB_B_NK else B.shape[1]
+    dev = A.device
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=dev)
+    if y is None and want_y:
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    if codes is None and want_codes:
+        codes = torch.empty((M, N), dtype=torch.uint8, device=dev)
+    d = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu)
+    lda = A.stride(0) if M else K
+    ldb = B.stride(0) if B.shape[0] else 0
+    wp, wb = _ws(workspace)
+    _check("esb_gemm_post", lib().esb_gemm_post(M, N, K, _ptr(A), lda, nA, kA_sig, _ptr(alphaA),
+                                                _ptr(B), ldb, nB, kB_sig, _ptr(alphaB), b_layout,
+                                                _ptr(acc), _ptr(y), N, ctypes.byref(d), wp, wb,
+                                                _stream(stream)))
+    return acc, y, codes
+
+
+def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out_n, out_k_sig,
+                    a=None, b=None, residual=None, relu=False, stride=(1, 1), pad=(0, 0),
+                    groups=1, codes=None, want_codes=True, acc=None, want_acc=False, y=None,
+                    want_y=False, workspace=None, stream=None):
+    """Convolution with the fused post-processing; returns (acc, y, codes), NHWC each."""
+    import torch
+    _dev_tensor(x, torch.uint8, "x")
+    _dev_tensor(w, torch.uint8, "w")
+    Nb, H, W, C = x.shape
+    K, R, S, _ = w.shape
+    P, Q = conv_out_hw(H, W, R, S, stride, pad)
+    dev = x.device
+    if acc is None and want_acc:
+        acc = torch.empty((Nb, P, Q, K), dtype=torch.int32, device=dev)
+    if y is None and want_y:
+        y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
+    if codes is None and want_codes:
+        codes = torch.empty((Nb, P, Q, K), dtype=torch.uint8, device=dev)
+    pd = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu)
+    d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], groups)
+    wp, wb = _ws(workspace)
+    _check("esb_conv2d_post", lib().esb_conv2d_post(ctypes.byref(d), _ptr(x), nX, kX_sig,
+                                                    _ptr(alphaX), _ptr(w), nW, kW_sig,
+                                                    _ptr(alphaW), _ptr(acc), _ptr(y),
+                                                    ctypes.byref(pd), wp, wb, _stream(stream)))
+    return acc, y, codes
 
 
 def esb_pack_size(rows, K, n, k_sig):

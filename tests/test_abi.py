@@ -179,3 +179,22 @@ def test_dn_and_dda_normal_refusals(L):
     assert L.esb_dda_normal(4, 2, None, 10, fake, None, None, None) == -1
     assert L.esb_dda_normal(4, 2, fake, 10, None, fake, None, None) == -1
     assert L.esb_dda_normal(4, 2, fake, 10, fake, None, fake, None) == -1   # D_out required
+
+
+def test_post_refusals(L):
+    """The fused post-processing refuses bad arguments before any launch."""
+    from paper_2109_03513_amd.esb import PostDesc
+    fake = ctypes.c_void_p(0x1000)
+    M = N = K = 64
+    gp = L.esb_gemm_post
+
+    def call(post, acc=fake, y=fake, alphaA=fake):
+        return gp(M, N, K, fake, K, 4, 2, alphaA, fake, K, 4, 2, fake, 0, acc, y, N,
+                  None if post is None else ctypes.byref(post), None, 0, None)
+
+    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 2, 0x1000), alphaA=None) == -1
+    assert call(PostDesc(None, None, None, 0, None, 4, 2, 0x1000)) == -1      # codes, no alpha
+    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 4, 0x1000)) == -1    # bad format
+    assert call(PostDesc(None, None, None, 0, 0x1000, 9, 2, 0x1000)) == -1
+    assert call(PostDesc(None, None, None, 1, None, 0, 0, None), acc=None, y=None) == -1
+    assert call(None, acc=None, y=None) == -1
