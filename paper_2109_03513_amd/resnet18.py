@@ -18,6 +18,14 @@ A downsample conv reads the same block input as the block's first conv, so it
 reuses that conv's alpha and codes instead of quantizing the tensor again.
 
 Activations are NHWC fp32; codes NHWC uint8; weights KRSC.
+
+forward_fused(x) is the inference flow of the paper (Alg. 1 at inference, Sec.
+4.2): every layer input's scale is fixed beforehand (here: the scales the DDA
+chose in the last forward(), the calibration), so each contraction's epilogue
+applies the ReLU and the residual sum and writes the next layer's codes
+directly (esb_conv2d_post); fp32 activations are written only where the glue
+needs them (the max pool input, the identity of the next block, the average
+pool input).  On the calibration batch its logits equal forward()'s bit for bit.
 """
 import numpy as np
 
@@ -53,6 +61,7 @@ class ResNet18ESB:
         self.sh = stream.cuda_stream if stream is not None else None
         self.record = record
         self.trace = []
+        self.calib = {}   # layer name -> device scale of its input, from the last forward()
         dev = "cuda"
         self.cmax = value_max(n, k_sig)
         self.cgrid = torch.from_numpy(workloads.maxabs_grid_factors(self.cmax, GRID_POINTS)).to(dev)
@@ -109,6 +118,7 @@ class ResNet18ESB:
                                 want_acc=self.record, stream=self.sh, workspace=self.cws)
         if self.record:
             self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
+        self.calib[name] = ax
         self.last_q = (ax, cx)
         return y
 
@@ -129,9 +139,55 @@ class ResNet18ESB:
                 a = torch.relu(out + sc)
         feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
         af, cf = self._quantize(feat, self.ws["fc"])
+        self.calib["fc"] = af
         acc, logits = esb.esb_gemm(cf, self.n, self.ks, af, self.fc_codes, self.n, self.ks,
                                    self.fc_alpha, want_acc=self.record, stream=self.sh,
                                    workspace=self.cws)
         if self.record:
             self.trace.append(dict(name="fc", x=feat, alpha=af, codes=cf, acc=acc, y=logits))
+        return logits
+
+    def conv_post(self, name, cx, out_alpha=None, residual=None, relu=False, want_y=False):
+        """The layer on input codes cx (scale calib[name]), with the fused epilogue: ReLU,
+        residual, and the next layer's codes under out_alpha when it is given."""
+        L = self.layers[name]
+        _, y, codes = esb.esb_conv2d_post(
+            cx, self.n, self.ks, self.calib[name], L["codes"], self.n, self.ks, L["alpha"],
+            out_alpha, self.n, self.ks, residual=residual, relu=relu,
+            stride=(L["stride"],) * 2, pad=(L["pad"],) * 2, want_codes=out_alpha is not None,
+            want_y=want_y, stream=self.sh, workspace=self.cws)
+        return y, codes
+
+    def forward_fused(self, x):
+        """Forward pass with the scales of the last forward() fixed (see the module notes)."""
+        torch = self.torch
+        F = torch.nn.functional
+        A = self.calib
+        if "fc" not in A:
+            raise RuntimeError("forward_fused needs the scales of a forward() first")
+        cx = esb.esb_project(x, A["conv1"], self.n, self.ks, stream=self.sh)
+        a, _ = self.conv_post("conv1", cx, relu=True, want_y=True)
+        a = F.max_pool2d(a.permute(0, 3, 1, 2), 3, 2, 1).permute(0, 2, 3, 1).contiguous()
+        ca = esb.esb_project(a, A["l1.0.c1"], self.n, self.ks, stream=self.sh)
+        blocks = [(s, b) for s in (1, 2, 3, 4) for b in (0, 1)]
+        for i, (stage, blk) in enumerate(blocks):
+            p = "l%d.%d." % (stage, blk)
+            _, mid = self.conv_post(p + "c1", ca, out_alpha=A[p + "c2"], relu=True)
+            if (p + "ds") in self.layers:   # reads the block input's codes (scale of c1)
+                L = self.layers[p + "ds"]
+                _, sc = esb.esb_conv2d(ca, self.n, self.ks, A[p + "c1"], L["codes"], self.n,
+                                       self.ks, L["alpha"], stride=(L["stride"],) * 2,
+                                       pad=(L["pad"],) * 2, want_acc=False, stream=self.sh,
+                                       workspace=self.cws)
+            else:
+                sc = a
+            nxt = None
+            if i + 1 < len(blocks):
+                nxt = A["l%d.%d.c1" % blocks[i + 1]]
+            a, ca = self.conv_post(p + "c2", mid, out_alpha=nxt, residual=sc, relu=True,
+                                   want_y=True)
+        feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
+        cf = esb.esb_project(feat, A["fc"], self.n, self.ks, stream=self.sh)
+        _, logits = esb.esb_gemm(cf, self.n, self.ks, A["fc"], self.fc_codes, self.n, self.ks,
+                                 self.fc_alpha, want_acc=False, stream=self.sh, workspace=self.cws)
         return logits

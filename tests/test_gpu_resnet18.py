@@ -95,3 +95,22 @@ def test_resnet18_stack_matches_oracle(batch):
     y = layer("fc", feat, None, 1, 0, wq["fc"])
     assert_rel(logits, y, 1e-6, "logits")
     assert np.all(np.isfinite(logits))
+
+
+def test_resnet18_fused_equals_dda_forward():
+    """With the scales of a DDA forward fixed (calibration on the same batch), the fused
+    forward (epilogues writing the next layer's codes) gives the same logits bit for bit:
+    the epilogue's residual sum and ReLU are the glue's own fp32 operations."""
+    import torch
+    from paper_2109_03513_amd import resnet18
+    batch = 2
+    weights = wl.resnet18_weights(0)
+    x = torch.from_numpy(wl.resnet18_input(1, batch)).cuda()
+    model = resnet18.ResNet18ESB(weights, batch)
+    log("resnet18 fused: calibration forward")
+    ref = host(model.forward(x))
+    log("resnet18 fused: fused forward")
+    got = host(model.forward_fused(x))
+    np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+    again = host(model.forward_fused(x))
+    np.testing.assert_array_equal(again.view(np.uint32), ref.view(np.uint32))
