@@ -113,6 +113,56 @@ __device__ __forceinline__ void post_store(const Post& P, float* y, int64_t o, i
     if (P.codes) P.codes[o] = (uint8_t)(alpha_valid(qa) ? esb_code(z, qa, P.pp) : P.pp.zero_code);
 }
 
+// Four consecutive outputs o .. o+3 (channels ch .. ch+3; nv of them inside the
+// output) through the fused post-processing; 16-byte residual / y accesses and
+// one 4-byte code store where the addresses allow.
+__device__ __forceinline__ void post_store4(const Post& P, float* y, int64_t o, int64_t ch, f32x4 v,
+                                            int nv, float qa) {
+    if (nv < 4) {
+        for (int c = 0; c < nv; c++) post_store(P, y, o + c, ch + c, v[c], qa);
+        return;
+    }
+    f32x4 z;
+#pragma unroll
+    for (int c = 0; c < 4; c++)
+        z[c] = __builtin_fmaf(P.a ? P.a[ch + c] : 1.0f, v[c], P.b ? P.b[ch + c] : 0.0f);
+    if (P.res) {
+        f32x4 r;
+        if (((uintptr_t)(P.res + o) & 15) == 0) {
+            r = *(const f32x4*)(P.res + o);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; c++) r[c] = P.res[o + c];
+        }
+#pragma unroll
+        for (int c = 0; c < 4; c++) z[c] = z[c] + r[c];
+    }
+    if (P.relu) {
+#pragma unroll
+        for (int c = 0; c < 4; c++) z[c] = z[c] > 0.0f ? z[c] : 0.0f;
+    }
+    if (y) {
+        if (((uintptr_t)(y + o) & 15) == 0) {
+            *(f32x4*)(y + o) = z;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; c++) y[o + c] = z[c];
+        }
+    }
+    if (P.codes) {
+        const bool ok = alpha_valid(qa);
+        uint32_t q[4];
+#pragma unroll
+        for (int c = 0; c < 4; c++) q[c] = ok ? esb_code(z[c], qa, P.pp) : P.pp.zero_code;
+        if (((uintptr_t)(P.codes + o) & 3) == 0) {
+            *(uint32_t*)(P.codes + o) = q[0] | (q[1] << 8) | (q[2] << 16) | (q[3] << 24);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; c++) P.codes[o + c] = (uint8_t)q[c];
+        }
+    }
+}
+
 // The epilogue store of one output: the plain scaled value, or the fused post-processing.
 __device__ __forceinline__ void out_store(const Post& P, float* y, int64_t o, int64_t ch, float y0,
                                           float qa) {

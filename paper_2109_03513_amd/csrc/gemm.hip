@@ -232,7 +232,9 @@ __device__ __forceinline__ uint4 b_load(const GemmParams& g, int n, int k_start,
 }
 
 // ------------------------------------------------------------------ kernel
-template <int BM, int BN, int WM, int WN, int PA, int PB, int AV, int BV>
+// POST: the fused post-processing epilogue (a separate instantiation, so that
+// the plain kernel keeps its register budget).
+template <int BM, int BN, int WM, int WN, int PA, int PB, int AV, int BV, bool POST>
 __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
     static_assert((BM / WM) * (BN / WN) == NT / 64, "4 waves per workgroup");
     constexpr int CA = (BM * 4 + NT - 1) / NT;   // A chunks per thread per stage
@@ -348,8 +350,48 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
 
     // epilogue: lane holds rows 4*(lane>>4) + r, column lane & 15 of each 16x16 block
     float s = 0.0f;
-    if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.da.k + g.db.k));
-    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
+    if (g.y || POST) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.da.k + g.db.k));
+    auto ival = [&](int i, int j, int r) {
+        uint32_t v = (uint32_t)acc[0][i][j][r];
+        if (NACC > 1) v += (uint32_t)acc[NACC > 1 ? 1 : 0][i][j][r] << 8;
+        if (NACC > 2) v += (uint32_t)acc[NACC > 2 ? 2 : 0][i][j][r] << 16;
+        return (int32_t)v;
+    };
+    if constexpr (POST) {
+        // fused post-processing through LDS, one row of 16x16 blocks at a time: each
+        // wave's 16 x WN slab of scaled values is read back four outputs per lane, so
+        // the post-processing code stays outside the unrolled register loops
+        static_assert(NT / 64 * 16 * WN * 4 <= sizeof(sA), "post slabs fit the A buffers");
+        float* slab = (float*)&sA[0][0][0] + wave * 16 * WN;
+        const float qa = post_alpha(g.post);
+#pragma unroll
+        for (int i = 0; i < TI; i++) {
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < TJ; j++)
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const int rl = 4 * (lane >> 4) + r, cl = 16 * j + (lane & 15);
+                    const int row = m0 + wr + 16 * i + rl, col = n0 + wc + cl;
+                    const int32_t iv = ival(i, j, r);
+                    if (g.acc && row < g.M && col < g.N)
+                        g.acc[(int64_t)row * g.ldc + (int64_t)grp * g.N + col] = iv;
+                    slab[rl * WN + cl] = s * (float)iv;
+                }
+            __syncthreads();
+#pragma unroll 1
+            for (int e = 4 * lane; e < 16 * WN; e += 256) {
+                const int rl = e / WN, cl = e - rl * WN;
+                const int row = m0 + wr + 16 * i + rl, col = n0 + wc + cl;
+                if (row < g.M && col < g.N) {
+                    const int64_t ch = (int64_t)grp * g.N + col;
+                    post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch,
+                                *(const f32x4*)(slab + e), min(4, g.N - col), qa);
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -359,14 +401,10 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
                 const int row = m0 + wr + 16 * i + 4 * (lane >> 4) + r;
                 const int col = n0 + wc + 16 * j + (lane & 15);
                 if (row < g.M && col < g.N) {
-                    uint32_t v = (uint32_t)acc[0][i][j][r];
-                    if (NACC > 1) v += (uint32_t)acc[NACC > 1 ? 1 : 0][i][j][r] << 8;
-                    if (NACC > 2) v += (uint32_t)acc[NACC > 2 ? 2 : 0][i][j][r] << 16;
-                    const int32_t iv = (int32_t)v;
-                    const int64_t ch = (int64_t)grp * g.N + col;
-                    const int64_t o = (int64_t)row * g.ldc + ch;
+                    const int32_t iv = ival(i, j, r);
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = iv;
-                    out_store(g.post, g.y, o, ch, s * (float)iv, qa);
+                    if (g.y) g.y[o] = s * (float)iv;
                 }
             }
 }
@@ -394,7 +432,8 @@ DecodeInfo decode_info(const Fmt& f) {
 template <int BM, int BN, int WM, int WN, int PA, int PB, int AV, int BV>
 static void launch_t(const GemmParams& g, int groups, hipStream_t s) {
     dim3 grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, groups);
-    k_contract<BM, BN, WM, WN, PA, PB, AV, BV><<<grid, NT, 0, s>>>(g);
+    if (g.post.on) k_contract<BM, BN, WM, WN, PA, PB, AV, BV, true><<<grid, NT, 0, s>>>(g);
+    else k_contract<BM, BN, WM, WN, PA, PB, AV, BV, false><<<grid, NT, 0, s>>>(g);
 }
 
 template <int BM, int BN, int WM, int WN>

@@ -66,6 +66,60 @@ struct FastParams {
 };
 constexpr int kZeroRowE4M3 = 7 * 8;
 
+// The int32 sums of a wave's 32x32 blocks (register r of a block is row
+// 8(r/4) + 4(lane/32) + r%4, column lane%32), `iv(i, j, r)` the value.
+template <int TI, int TJ, class IV>
+__device__ __forceinline__ void store_acc(const FastParams& g, int lane, int row0, int col0, int grp,
+                                          IV iv) {
+    const int lr = lane & 31, lg = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < TI; i++)
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int row = row0 + 32 * i + 8 * (r >> 2) + 4 * lg + (r & 3);
+                const int col = col0 + 32 * j + lr;
+                if (row < g.M && col < g.N) g.acc[(int64_t)row * g.ldc + (int64_t)grp * g.N + col] = iv(i, j, r);
+            }
+}
+
+// Epilogue of the 32x32-block MFMA kernels with the fused post-processing.
+// One row of blocks (index i) at a time, each wave writes its TJ blocks of
+// scaled values y0(i, j, r) (register r of a block is row 8(r/4) + 4(lane/32)
+// + r%4, column lane%32) to its own LDS slab of 32 x 32TJ floats, then reads
+// them back as four consecutive outputs per lane: the post-processing code is
+// emitted once per row of blocks, outside the unrolled register loops (whose
+// full unrolling keeps the accumulators in registers), and its global
+// accesses are contiguous.  Every thread of the workgroup calls this.
+template <int TI, int TJ, class Y0>
+__device__ __forceinline__ void post_epilogue(const FastParams& g, float* slab, int lane, int row0,
+                                              int col0, int grp, Y0 y0) {
+    constexpr int W = 32 * TJ;
+    const int lr = lane & 31, lg = lane >> 5;
+    const float qa = post_alpha(g.post);
+#pragma unroll
+    for (int i = 0; i < TI; i++) {
+        __syncthreads();   // the LDS is free: main loop or previous row done everywhere
+#pragma unroll
+        for (int j = 0; j < TJ; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++)
+                slab[(8 * (r >> 2) + 4 * lg + (r & 3)) * W + 32 * j + lr] = y0(i, j, r);
+        __syncthreads();
+#pragma unroll 1
+        for (int e = 4 * lane; e < 32 * W; e += 256) {
+            const int rl = e / W, cl = e - rl * W;
+            const int row = row0 + 32 * i + rl, col = col0 + cl;
+            if (row < g.M && col < g.N) {
+                const int64_t ch = (int64_t)grp * g.N + col;
+                post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch, *(const f32x4*)(slab + e),
+                            min(4, g.N - col), qa);
+            }
+        }
+    }
+}
+
 __device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
     const uint32_t t = (((c & d.lm) << d.shf) + d.inc) & d.lmf;   // exponent + 1 (mod 2^ebits)
     return ((c << d.shs) & 0x80808080u) | t;                       // sign to bit 7
@@ -409,7 +463,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
     // column lane % 32.
     float s = 0.0f;
     if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
-    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
+    if (g.post.on && (CONV || g.ksplit == 1)) {
+        // two LDS buffers of TILE bytes each hold the slabs of half the waves
+        constexpr int NW = WGM * WGN;
+        static_assert((NW / 2) * 32 * 32 * TJ * 4 <= TILE, "post slabs fit the decode buffers");
+        if (g.acc)
+            store_acc<TI, TJ>(g, lane, m0 + wr, n0 + wc, grp, [&](int i, int j, int r) {
+                return OP == 1 ? (int32_t)ldexpf((float)acc[i][j][r], g.out_shift) : (int32_t)acc[i][j][r];
+            });
+        float* slab = (float*)(wave < NW / 2 ? dec0 : dec1) + (wave % (NW / 2)) * (32 * 32 * TJ);
+        post_epilogue<TI, TJ>(g, slab, lane, m0 + wr, n0 + wc, grp, [&](int i, int j, int r) {
+            return OP == 1 ? s * ldexpf((float)acc[i][j][r], g.out_shift) : s * (float)(int32_t)acc[i][j][r];
+        });
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -432,10 +499,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma(FastParams g) {
                         g.part[((int64_t)kz * g.M + row) * g.N + col] = iv;
                         continue;
                     }
-                    const int64_t ch = (int64_t)grp * g.N + col;
-                    const int64_t o = (int64_t)row * g.ldc + ch;
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = iv;
-                    out_store(g.post, g.y, o, ch, s * fv, qa);
+                    if (g.y) g.y[o] = s * fv;
                 }
             }
 }
@@ -786,7 +852,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
 
     float s = 0.0f;
     if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
-    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
+    if (g.post.on && (CONV || g.ksplit == 1)) {
+        static_assert(NW * 32 * 32 * TJ * 4 <= R * TILE, "post slabs fit the ring");
+        if (g.acc)
+            store_acc<TI, TJ>(g, lane, m0 + wr, n0 + wc, grp, [&](int i, int j, int r) {
+                return (int32_t)ldexpf(acc[i][j][r], g.out_shift);
+            });
+        post_epilogue<TI, TJ>(g, (float*)ring + wave * (32 * 32 * TJ), lane, m0 + wr, n0 + wc, grp,
+                              [&](int i, int j, int r) { return s * ldexpf(acc[i][j][r], g.out_shift); });
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -801,10 +876,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_pre(FastParams g) {
                         g.part[((int64_t)kz * g.M + row) * g.N + col] = (int32_t)fv;
                         continue;
                     }
-                    const int64_t ch = (int64_t)grp * g.N + col;
-                    const int64_t o = (int64_t)row * g.ldc + ch;
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = (int32_t)fv;
-                    out_store(g.post, g.y, o, ch, s * fv, qa);
+                    if (g.y) g.y[o] = s * fv;
                 }
             }
 }
@@ -982,7 +1056,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_f6(FastParams g) {
 
     float s = 0.0f;
     if (g.y || g.post.on) s = ldexpf(g.alphaA[0] * g.alphaB[0], -(g.kA + g.kB));
-    const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
+    if (g.post.on && (CONV || g.ksplit == 1)) {
+        static_assert(NW * 32 * 32 * TJ * 4 <= R * TILE, "post slabs fit the ring");
+        if (g.acc)
+            store_acc<TI, TJ>(g, lane, m0 + wr, n0 + wc, grp, [&](int i, int j, int r) {
+                return (int32_t)ldexpf(acc[i][j][r], g.out_shift);
+            });
+        post_epilogue<TI, TJ>(g, (float*)ring + wave * (32 * 32 * TJ), lane, m0 + wr, n0 + wc, grp,
+                              [&](int i, int j, int r) { return s * ldexpf(acc[i][j][r], g.out_shift); });
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TI; i++)
 #pragma unroll
@@ -993,10 +1076,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_mma_f6(FastParams g) {
                 const int col = n0 + wc + 32 * j + lr;
                 if (row < g.M && col < g.N) {
                     const float fv = ldexpf(acc[i][j][r], g.out_shift);
-                    const int64_t ch = (int64_t)grp * g.N + col;
-                    const int64_t o = (int64_t)row * g.ldc + ch;
+                    const int64_t o = (int64_t)row * g.ldc + (int64_t)grp * g.N + col;
                     if (g.acc) g.acc[o] = (int32_t)fv;
-                    out_store(g.post, g.y, o, ch, s * fv, qa);
+                    if (g.y) g.y[o] = s * fv;
                 }
             }
 }
