@@ -97,32 +97,32 @@ def main():
     ax = torch.empty(1, dtype=torch.float32, device=dev)
     Dw = torch.empty(64, dtype=torch.float64, device=dev)
     Dx = torch.empty(64, dtype=torch.float64, device=dev)
-    wsw = torch.empty(esb.esb_dda_workspace_size(w.numel(), n, ks, 64), dtype=torch.uint8, device=dev)
-    wsx = torch.empty(esb.esb_dda_workspace_size(x.numel(), n, ks, 64), dtype=torch.uint8, device=dev)
     cw = torch.empty(w.shape, dtype=torch.uint8, device=dev)
     cx = torch.empty(x.shape, dtype=torch.uint8, device=dev)
     y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
 
-    stages = ["dda_w", "dda_x", "project_w", "project_x", "conv2d"]
+    stages = ["dda", "project", "conv2d"]
+    # the weights and the activations: independent problems, one launch group each
+    dda_jobs = esb.dda_jobs([(w, n, ks, gw, aw, Dw), (x, n, ks, gx, ax, Dx)])
+    wsd = torch.empty(esb.esb_dda_batch_workspace_size(dda_jobs), dtype=torch.uint8, device=dev)
+    proj_jobs = esb.project_jobs([(w, aw, n, ks, cw), (x, ax, n, ks, cx)])
 
     def run_stage(i, st=sh):
         if i == 0:
-            esb.esb_dda_align(w, n, ks, gw, alpha_out=aw, D_out=Dw, workspace=wsw, stream=st)
+            esb.esb_dda_align_batch(dda_jobs, wsd, stream=st)
         elif i == 1:
-            esb.esb_dda_align(x, n, ks, gx, alpha_out=ax, D_out=Dx, workspace=wsx, stream=st)
-        elif i == 2:
-            esb.esb_project(w, aw, n, ks, codes=cw, stream=st)
-        elif i == 3:
-            esb.esb_project(x, ax, n, ks, codes=cx, stream=st)
+            esb.esb_project_batch(proj_jobs, stream=st)
         else:
             esb.esb_conv2d(cx, n, ks, ax, cw, n, ks, aw, stride=c["stride"], pad=c["pad"], y=y,
                            want_acc=False, stream=st)
 
-    # One chain on one stream: a HIP graph with the weight and activation
-    # branches on two streams ran them one after the other anyway and paid for
-    # the fork and join (measured 70.3 us per step against 58.7 us chained).
+    # One chain on one stream.  DDA(w) and DDA(x) share one launch of each DDA
+    # kernel (as do the two projections): each alone leaves most CUs idle, and
+    # a HIP graph with the two branches on two streams ran them one after the
+    # other anyway and paid for the fork and join (measured 70.3 us per step
+    # against 58.7 us chained).
     def step():
-        for i in (0, 2, 1, 3, 4):
+        for i in (0, 1, 2):
             run_stage(i)
 
     with torch.cuda.stream(stream):
@@ -151,7 +151,7 @@ def main():
         # per launch group: a graph of INNER back-to-back copies of one stage
         INNER, REPS = 20, 5
         stage_ms = []
-        for i in range(5):
+        for i in range(len(stages)):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=stream):
                 for _ in range(INNER):
@@ -172,10 +172,9 @@ def main():
     # roofline of the dominant launch group
     nel_w, nel_x = w.numel(), x.numel()
     groups = {
-        "dda_w": ("esb_dda_align(w): k_dda_hist + k_dda_finalize", "hbm", 4.0 * nel_w),
-        "dda_x": ("esb_dda_align(x): k_dda_hist + k_dda_finalize", "hbm", 4.0 * nel_x),
-        "project_w": ("esb_project(w): k_project_vec", "hbm", 5.0 * nel_w),
-        "project_x": ("esb_project(x): k_project_vec", "hbm", 5.0 * nel_x),
+        "dda": ("esb_dda_align_batch(w, x): k_dda_hist + k_dda_finalize", "hbm",
+                4.0 * (nel_w + nel_x)),
+        "project": ("esb_project_batch(w, x): k_project_batch", "hbm", 5.0 * (nel_w + nel_x)),
         # conv: codes of x and w read once, fp32 y written once (AI below the int8 ridge)
         "conv2d": ("esb_conv2d: k_mma 64x64", "hbm", 1.0 * nel_x + 1.0 * nel_w + 4.0 * M * Ncol),
     }
@@ -186,15 +185,15 @@ def main():
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
             "traffic": measured_traffic(kname.split(":")[0] + "@" + c["name"]),
             "algorithmic_bytes": nbytes, "launch_us": round(stage_ms[dom] * 1e3, 3)}
-    conv_ms = stage_ms[4]
+    conv_ms = stage_ms[2]
     extra = {
         "stage_launch_us": {k: round(v * 1e3, 3) for k, v in zip(stages, stage_ms)},
         "conv_int_tops": round(ops / (conv_ms * 1e-3) / 1e12, 3),
         "conv_frac_int8_peak": round(ops / (conv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 6),
-        "project_x_gbps": round(5.0 * nel_x / (stage_ms[3] * 1e-3) / 1e9, 2),
-        "dda_x_gbps": round(4.0 * nel_x / (stage_ms[1] * 1e-3) / 1e9, 2),
-        "timing": "whole step replayed as one HIP graph (one stream: DDA(w), project(w), DDA(x), "
-                  "project(x), conv2d); launch groups as graphs of 20 copies",
+        "project_gbps": round(5.0 * (nel_w + nel_x) / (stage_ms[1] * 1e-3) / 1e9, 2),
+        "dda_gbps": round(4.0 * (nel_w + nel_x) / (stage_ms[0] * 1e-3) / 1e9, 2),
+        "timing": "whole step replayed as one HIP graph (one stream: DDA(w, x) batched, "
+                  "project(w, x) batched, conv2d); launch groups as graphs of 20 copies",
     }
 
     cpu = None
@@ -207,7 +206,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
         "config": {"workload": c["name"] + "_esb4k2_dda64",
-                   "note": "DDA(w), project(w), DDA(x), project(x), conv2d per step"},
+                   "note": "DDA(w), DDA(x), project(w), project(x), conv2d per step; the two "
+                           "DDAs and the two projections each share one launch group"},
         "roofline": roof, "cpu_baseline": cpu, "detail": extra,
     }
     print(json.dumps(rec), flush=True)

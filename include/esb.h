@@ -204,6 +204,40 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
                     size_t ws_bytes, void* stream);
 
 /*
+ * Batches of independent problems in one launch of each kernel: the DDA or the
+ * projection of several tensors (for example a layer's weights and its input,
+ * or every layer's weights), each with its own format, grid and outputs, with
+ * results identical to one esb_dda_align / esb_project call per job.  Small
+ * tensors leave most of the GPU idle and pay a fixed latency per launch; a
+ * batch pays it once.  jobs: host array of count entries.  The DDA workspace
+ * (device) holds every job's workspace, 256-byte aligned, in job order:
+ * esb_dda_batch_workspace_size() bytes (0 for an invalid job).  Errors as the
+ * single calls; a job that fails validation fails the whole batch before any
+ * launch.
+ */
+typedef struct esb_dda_job {
+    const float* x;     /* device, len fp32 */
+    int64_t len;
+    int n, k_sig;
+    const float* grid;  /* device, G fp32 candidates */
+    int G;
+    float* alpha_out;   /* device, one fp32 */
+    double* D_out;      /* device, G doubles, or NULL */
+} esb_dda_job;
+size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs);
+int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, size_t ws_bytes,
+                        void* stream);
+
+typedef struct esb_project_job {
+    const float* x;      /* device, len fp32 */
+    int64_t len;
+    const float* alpha;  /* device scalar */
+    int n, k_sig;
+    uint8_t* codes;      /* device, len codes */
+} esb_project_job;
+int esb_project_batch(int count, const esb_project_job* jobs, void* stream);
+
+/*
  * Data normalization (Sec. 3.4, the DN equation) and the aligner in its analytic
  * form (eq. (9), (13) with p = N(0,1), "Resolving extremum"), the paper's own
  * flow of Alg. 1: W_q = ESB(DN(W)) with alpha* found offline for N(0,1).

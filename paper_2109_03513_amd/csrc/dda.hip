@@ -241,9 +241,10 @@ __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
     return h;
 }
 
-__global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restrict__ x, int64_t len,
-                                                           const float* __restrict__ grid,
-                                                           DdaArgs a, double* __restrict__ part) {
+// One block (local index bid of its job) of the histogram pass.
+__device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int64_t len,
+                                               const float* __restrict__ grid, const DdaArgs a,
+                                               double* __restrict__ part, const int bid) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int nbins = 1 << a.lbins;
@@ -269,7 +270,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         al[r] = (i < A) ? grid[i / M] : 1.0f;
     }
     const bool vec = ((uintptr_t)x & 15) == 0;
-    const int64_t e0 = (int64_t)blockIdx.x * a.rows_pb * kRowElems;
+    const int64_t e0 = (int64_t)bid * a.rows_pb * kRowElems;
     const int64_t e1 = min(len, e0 + (int64_t)a.rows_pb * kRowElems);
     // element range of the vector path: whole float4 only; the last block takes
     // the len % 4 tail separately
@@ -579,7 +580,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
         visit(g);
         if (c + 2 * 4 * kHistThreads < v1) visit(g + 8);   // rows 2, 3 of the chunk
     }
-    if (vec && blockIdx.x == gridDim.x - 1 && tid < (int)(len & 3)) {   // tail of the vector path
+    if (vec && bid == a.nblk - 1 && tid < (int)(len & 3)) {   // tail of the vector path
         uint32_t g[E];
         g[0] = __float_as_uint(x[(len & ~(int64_t)3) + tid]);
 #pragma unroll
@@ -689,7 +690,7 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
             }
             lds_barrier();
         }
-        double* out = part + (int64_t)blockIdx.x * part_stride(a.G);
+        double* out = part + (int64_t)bid * part_stride(a.G);
         if (tid < a.G) {
             out[tid] = Aj;
             out[a.G + tid] = Bj;
@@ -701,12 +702,54 @@ __global__ __launch_bounds__(kHistThreads) void k_dda_hist(const float* __restri
     }
 }
 
+// ---------------------------------------------------------------- batches
+// Several independent problems in one launch of each kernel: the blocks of job
+// i are blk0 .. blk0 + nblk - 1 of the histogram grid (groups: grp0 ..), and
+// block i of the finalize grid.  Small tensors leave most CUs idle and the
+// fixed latency of the set-up, epilogue and finalize dominates, so running
+// them side by side costs about as much as one.
+constexpr int kDdaMaxJobs = 8;
+struct DdaJob {
+    const float* x;
+    int64_t len;
+    const float* grid;
+    float* alpha_out;
+    double* D_out;
+    double* part;       // block vectors
+    double* grp;        // group vectors (jobs with groups)
+    DdaArgs a;
+    int blk0, grp0, ngrp;
+};
+struct DdaBatch {
+    DdaJob job[kDdaMaxJobs];
+    int count;
+};
+
+__device__ __forceinline__ int dda_job_of_block(const DdaBatch& B, int b) {
+    int j = 0;
+    for (int i = 1; i < B.count; i++)
+        if (B.job[i].blk0 <= b) j = i;
+    return j;
+}
+
+__global__ __launch_bounds__(kHistThreads) void k_dda_hist(DdaBatch B) {
+    const int j = dda_job_of_block(B, (int)blockIdx.x);
+    const DdaJob& J = B.job[j];
+    dda_hist_block(J.x, J.len, J.grid, J.a, J.part, (int)blockIdx.x - J.blk0);
+}
+
 // --------------------------------------------------------------------- group
 // Group g: the sums of block vectors kGroup g .. kGroup g + kGroup - 1 in block
 // order (flags or-ed), one thread per vector entry.
-__global__ __launch_bounds__(256) void k_dda_group(DdaArgs a, const double* __restrict__ part,
-                                                   double* __restrict__ grp) {
-    const int ps = part_stride(a.G), g = blockIdx.x;
+__global__ __launch_bounds__(256) void k_dda_group(DdaBatch B) {
+    int jb = 0;
+    for (int i = 1; i < B.count; i++)
+        if (B.job[i].ngrp > 0 && B.job[i].grp0 <= (int)blockIdx.x) jb = i;
+    const DdaJob& J = B.job[jb];
+    const DdaArgs a = J.a;
+    const double* __restrict__ part = J.part;
+    double* __restrict__ grp = J.grp;
+    const int ps = part_stride(a.G), g = (int)blockIdx.x - J.grp0;
     const int b0 = g * kGroup, nb = min(kGroup, a.nblk - b0);
     for (int e = threadIdx.x; e < ps; e += 256) {
         double v[kGroup];
@@ -734,13 +777,16 @@ __host__ __device__ inline int fin_split(int G, int nblk) {
 // the vectors of blocks p, p + S, p + 2S, ... in that order, then the S partial
 // sums of a candidate combine in a fixed butterfly; D_j = S2 + a (a B_j - 2 A_j)
 // and the argmin over (isnan(D), D, j), ties to the lowest index.
-__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __restrict__ grid,
-                                                              DdaArgs a,
-                                                              const double* __restrict__ part,
-                                                              float* __restrict__ alpha_out,
-                                                              double* __restrict__ D_out) {
+// Block i of the grid finalizes job i (block vectors, or group vectors when
+// the job has groups).
+__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
+    const DdaJob& J = jobs.job[blockIdx.x];
+    const float* __restrict__ grid = J.grid;
+    float* __restrict__ alpha_out = J.alpha_out;
+    double* __restrict__ D_out = J.D_out;
+    const double* __restrict__ part = J.ngrp > 0 ? J.grp : J.part;
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int G = a.G, nb = a.nblk, ps = part_stride(G);
+    const int G = J.a.G, nb = J.ngrp > 0 ? J.ngrp : J.a.nblk, ps = part_stride(G);
     const int S = fin_split(G, nb);
     const int p = tid & (S - 1), j = tid / S;
     const bool live = j < G;
@@ -808,16 +854,8 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(const float* __res
     }
 }
 
-hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
-                      float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
-                      hipStream_t s) {
-    DdaArgs a;
-    a.G = G; a.M = L.M; a.A = L.A; a.Aa = L.A + kMaxSplits;
-    a.n = f.n; a.k = f.k;
-    dda_blocks(len, &a.nblk, &a.rows_pb);
-    a.lbins = hist_lbins(L.A, a.rows_pb >= 8);
-    double* part = (double*)((char*)ws + L.off_part);
-    double* grp = (double*)((char*)ws + L.off_group);
+static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, int nhist, int ngroups,
+                              hipStream_t s) {
     static bool lds_attr_set[64] = {false};
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
@@ -826,16 +864,49 @@ hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* gr
         if (e != hipSuccess) return e;
         lds_attr_set[dev] = true;
     }
-    k_dda_hist<<<a.nblk, kHistThreads, hist_lds(L.A, a.lbins).total, s>>>(x, len, grid, a, part);
-    const int ng = dda_groups(a.nblk);
-    if (ng > 0) {
-        k_dda_group<<<ng, 256, 0, s>>>(a, part, grp);
-        part = grp;
-        a.nblk = ng;                 // the finalize reads the group vectors
-    }
-    const int nt = (G * fin_split(G, a.nblk) + 63) / 64 * 64;   // <= kFinThreads
-    k_dda_finalize<<<1, nt, 0, s>>>(grid, a, part, alpha_out, D_out);
+    k_dda_hist<<<nhist, kHistThreads, max_lds, s>>>(B);
+    if (ngroups > 0) k_dda_group<<<ngroups, 256, 0, s>>>(B);
+    k_dda_finalize<<<B.count, max_fin_threads, 0, s>>>(B);
     return hipGetLastError();
+}
+
+hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
+    for (int c0 = 0; c0 < count; c0 += kDdaMaxJobs) {
+        DdaBatch B;
+        B.count = count - c0 < kDdaMaxJobs ? count - c0 : kDdaMaxJobs;
+        int nhist = 0, ngroups = 0, max_lds = 0, max_fin = 64;
+        for (int i = 0; i < B.count; i++) {
+            const DdaJobDesc& d = jobs[c0 + i];
+            DdaJob& J = B.job[i];
+            DdaArgs& a = J.a;
+            a.G = d.G; a.M = d.L.M; a.A = d.L.A; a.Aa = d.L.A + kMaxSplits;
+            a.n = d.f.n; a.k = d.f.k;
+            dda_blocks(d.len, &a.nblk, &a.rows_pb);
+            a.lbins = hist_lbins(d.L.A, a.rows_pb >= 8);
+            J.x = d.x; J.len = d.len; J.grid = d.grid; J.alpha_out = d.alpha_out; J.D_out = d.D_out;
+            J.part = (double*)((char*)d.ws + d.L.off_part);
+            J.grp = (double*)((char*)d.ws + d.L.off_group);
+            J.blk0 = nhist;
+            nhist += a.nblk;
+            J.ngrp = dda_groups(a.nblk);
+            J.grp0 = ngroups;
+            ngroups += J.ngrp;
+            const int lds = (int)hist_lds(d.L.A, a.lbins).total;
+            if (lds > max_lds) max_lds = lds;
+            const int nt = (d.G * fin_split(d.G, J.ngrp > 0 ? J.ngrp : a.nblk) + 63) / 64 * 64;
+            if (nt > max_fin) max_fin = nt;   // <= kFinThreads
+        }
+        const hipError_t e = launch_batch(B, max_lds, max_fin, nhist, ngroups, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
+                      float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
+                      hipStream_t s) {
+    const DdaJobDesc d{x, len, f, grid, G, alpha_out, D_out, ws, L};
+    return launch_dda_batch(&d, 1, s);
 }
 
 }  // namespace esb

@@ -3,6 +3,8 @@
 #include <string.h>
 
 #include "../../include/esb.h"
+#include <vector>
+
 #include "esb_internal.h"
 
 namespace esb {
@@ -137,6 +139,54 @@ int esb_dda_align(const float* x, int64_t len, int n, int k_sig, const float* gr
     if (!dda_layout(len, f, G, &L)) return ESB_E_INVALID;
     if (!workspace || ws_bytes < L.total) return ESB_E_WORKSPACE;
     return hip_status(launch_dda(x, len, f, grid, G, alpha_out, D_out, workspace, L, (hipStream_t)stream));
+}
+
+size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs) {
+    if (count < 0 || (count > 0 && !jobs)) return 0;
+    size_t total = 0;
+    for (int i = 0; i < count; i++) {
+        const esb_dda_job& j = jobs[i];
+        if (!valid_fmt(j.n, j.k_sig)) return 0;
+        DdaLayout L;
+        if (!dda_layout(j.len, make_fmt(j.n, j.k_sig), j.G, &L)) return 0;
+        total += (L.total + 255) & ~(size_t)255;
+    }
+    return total;
+}
+
+int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, size_t ws_bytes,
+                        void* stream) {
+    if (count < 0 || (count > 0 && !jobs)) return ESB_E_INVALID;
+    if (count == 0) return ESB_OK;
+    std::vector<DdaJobDesc> d((size_t)count);
+    size_t off = 0;
+    for (int i = 0; i < count; i++) {
+        const esb_dda_job& j = jobs[i];
+        if (!valid_fmt(j.n, j.k_sig) || j.len < 0 || !j.grid || !j.alpha_out) return ESB_E_INVALID;
+        if (j.len > 0 && !j.x) return ESB_E_INVALID;
+        DdaJobDesc& e = d[(size_t)i];
+        e.f = make_fmt(j.n, j.k_sig);
+        if (!dda_layout(j.len, e.f, j.G, &e.L)) return ESB_E_INVALID;
+        e.x = j.x; e.len = j.len; e.grid = j.grid; e.G = j.G;
+        e.alpha_out = j.alpha_out; e.D_out = j.D_out;
+        e.ws = (char*)workspace + off;
+        off += (e.L.total + 255) & ~(size_t)255;
+    }
+    if (!workspace || ws_bytes < off) return ESB_E_WORKSPACE;
+    return hip_status(launch_dda_batch(d.data(), count, (hipStream_t)stream));
+}
+
+int esb_project_batch(int count, const esb_project_job* jobs, void* stream) {
+    if (count < 0 || (count > 0 && !jobs)) return ESB_E_INVALID;
+    std::vector<ProjJobDesc> d((size_t)count);
+    for (int i = 0; i < count; i++) {
+        const esb_project_job& j = jobs[i];
+        if (!valid_fmt(j.n, j.k_sig) || j.len < 0 || !j.alpha) return ESB_E_INVALID;
+        if (j.len > 0 && (!j.x || !j.codes)) return ESB_E_INVALID;
+        d[(size_t)i] = ProjJobDesc{j.x, j.len, j.alpha, make_fmt(j.n, j.k_sig), j.codes};
+    }
+    if (count == 0) return ESB_OK;
+    return hip_status(launch_project_batch(d.data(), count, (hipStream_t)stream));
 }
 
 static int contraction_contract(int64_t kred, const Fmt& a, const Fmt& b) {

@@ -172,6 +172,14 @@ __device__ __forceinline__ void out_store(const Post& P, float* y, int64_t o, in
 
 hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,
                           uint8_t* codes, const float* dn, hipStream_t s);
+struct ProjJobDesc {
+    const float* x;
+    int64_t len;
+    const float* alpha;
+    Fmt f;
+    uint8_t* codes;
+};
+hipError_t launch_project_batch(const ProjJobDesc* jobs, int count, hipStream_t s);
 
 // ------------------------------------------------------ normalization, analytic DDA
 size_t dn_workspace(int64_t len);
@@ -196,6 +204,19 @@ bool dda_layout(int64_t len, const Fmt& f, int G, DdaLayout* L);
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
                       float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
                       hipStream_t s);
+// Several independent problems; each job's workspace ws holds L.total bytes.
+struct DdaJobDesc {
+    const float* x;
+    int64_t len;
+    Fmt f;
+    const float* grid;
+    int G;
+    float* alpha_out;
+    double* D_out;
+    void* ws;
+    DdaLayout L;
+};
+hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s);
 
 // ---------------------------------------------------------------- contraction
 // Decoding of one operand's codes to exact integers.

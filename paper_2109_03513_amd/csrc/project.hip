@@ -123,10 +123,10 @@ __device__ __forceinline__ f32x4 dn4(f32x4 v, const DnArgs& a) {
 }
 
 template <int DN>
-__global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x4, int64_t n4,
-                                                     const float* __restrict__ alpha_p,
-                                                     ProjParams p, uint32_t* __restrict__ out4,
-                                                     const float* __restrict__ dn) {
+__device__ __forceinline__ void project_tile(const f32x4* __restrict__ x4, int64_t n4,
+                                             const float* __restrict__ alpha_p, const ProjParams& p,
+                                             uint32_t* __restrict__ out4, const float* __restrict__ dn,
+                                             int64_t tile) {
     const float alpha = *alpha_p;
     DnArgs da{0.0f, 1.0f, 1.0f, false};
     if (DN) da = dn_args(dn);
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x
     const bool fast = fast_scale(alpha);
     const float r = 1.0f / alpha;
     const uint32_t z4 = p.zero_code * 0x01010101u;
-    const int64_t i0 = (int64_t)blockIdx.x * kTile4 + threadIdx.x;
+    const int64_t i0 = tile * kTile4 + threadIdx.x;
     if (i0 + 3 * 256 < n4) {
         f32x4 v[4];
 #pragma unroll
@@ -153,6 +153,38 @@ __global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x
             if (i < n4) out4[i] = ok ? code4(DN ? dn4(x4[i], da) : x4[i], alpha, r, fast, p) : z4;
         }
     }
+}
+
+template <int DN>
+__global__ __launch_bounds__(256) void k_project_vec(const f32x4* __restrict__ x4, int64_t n4,
+                                                     const float* __restrict__ alpha_p,
+                                                     ProjParams p, uint32_t* __restrict__ out4,
+                                                     const float* __restrict__ dn) {
+    project_tile<DN>(x4, n4, alpha_p, p, out4, dn, (int64_t)blockIdx.x);
+}
+
+// Several tensors in one launch: tiles tile0 .. of the grid belong to job i
+// (the vector part of each tensor; tails go to k_project_scalar).
+constexpr int kProjMaxJobs = 8;
+struct ProjJob {
+    const f32x4* x4;
+    int64_t n4;
+    const float* alpha;
+    uint32_t* out4;
+    int64_t tile0;
+    ProjParams p;
+};
+struct ProjBatch {
+    ProjJob job[kProjMaxJobs];
+    int count;
+};
+
+__global__ __launch_bounds__(256) void k_project_batch(ProjBatch B) {
+    int j = 0;
+    for (int i = 1; i < B.count; i++)
+        if (B.job[i].tile0 <= (int64_t)blockIdx.x) j = i;
+    const ProjJob& J = B.job[j];
+    project_tile<0>(J.x4, J.n4, J.alpha, J.p, J.out4, nullptr, (int64_t)blockIdx.x - J.tile0);
 }
 
 // Scalar path: unaligned pointers and the tail of the vector path.
@@ -200,6 +232,40 @@ hipError_t launch_project(const float* x, int64_t len, const float* alpha, const
                     x + head, len - head, alpha, p, codes + head, dn);
         else k_project_scalar<0><<<grid_for(len - head, 256), 256, 0, s>>>(
                     x + head, len - head, alpha, p, codes + head, dn);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_project_batch(const ProjJobDesc* jobs, int count, hipStream_t s) {
+    for (int c0 = 0; c0 < count; c0 += kProjMaxJobs) {
+        ProjBatch B;
+        B.count = 0;
+        int64_t tiles = 0;
+        for (int i = c0; i < count && i < c0 + kProjMaxJobs; i++) {
+            const ProjJobDesc& d = jobs[i];
+            if (d.len <= 0) continue;
+            const ProjParams p = proj_params(d.f);
+            const bool aligned = ((uintptr_t)d.x % 16 == 0) && ((uintptr_t)d.codes % 4 == 0);
+            int64_t head = 0;
+            if (aligned && d.len >= 4) {
+                ProjJob& J = B.job[B.count++];
+                J.x4 = (const f32x4*)d.x;
+                J.n4 = d.len / 4;
+                J.alpha = d.alpha;
+                J.out4 = (uint32_t*)d.codes;
+                J.tile0 = tiles;
+                J.p = p;
+                tiles += (J.n4 + kTile4 - 1) / kTile4;
+                head = J.n4 * 4;
+            }
+            if (head < d.len)
+                k_project_scalar<0><<<grid_for(d.len - head, 256), 256, 0, s>>>(
+                    d.x + head, d.len - head, d.alpha, p, d.codes + head, nullptr);
+        }
+        if (B.count > 0) {
+            if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+            k_project_batch<<<(unsigned)tiles, 256, 0, s>>>(B);
+        }
     }
     return hipGetLastError();
 }

@@ -40,6 +40,17 @@ class ConvDesc(ctypes.Structure):
                  "groups")]
 
 
+class DdaJob(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("len", ctypes.c_int64), ("n", ctypes.c_int),
+                ("k_sig", ctypes.c_int), ("grid", ctypes.c_void_p), ("G", ctypes.c_int),
+                ("alpha_out", ctypes.c_void_p), ("D_out", ctypes.c_void_p)]
+
+
+class ProjectJob(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("len", ctypes.c_int64), ("alpha", ctypes.c_void_p),
+                ("n", ctypes.c_int), ("k_sig", ctypes.c_int), ("codes", ctypes.c_void_p)]
+
+
 class PostDesc(ctypes.Structure):
     _fields_ = [("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("residual", ctypes.c_void_p),
                 ("relu", ctypes.c_int), ("alpha", ctypes.c_void_p), ("n", ctypes.c_int),
@@ -84,6 +95,9 @@ def lib():
                                     P, P, i64, ctypes.POINTER(PostDesc), P, sz, P]),
             "esb_conv2d_post": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P,
                                       P, ctypes.POINTER(PostDesc), P, sz, P]),
+            "esb_dda_batch_workspace_size": (sz, [i32, ctypes.POINTER(DdaJob)]),
+            "esb_dda_align_batch": (i32, [i32, ctypes.POINTER(DdaJob), P, sz, P]),
+            "esb_project_batch": (i32, [i32, ctypes.POINTER(ProjectJob), P]),
             "esb_dn_workspace_size": (sz, [i64]),
             "esb_dn_stats": (i32, [P, i64, P, P, sz, P]),
             "esb_project_dn": (i32, [P, i64, P, P, i32, i32, P, P]),
@@ -303,6 +317,39 @@ def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out
                                                     _ptr(alphaW), _ptr(acc), _ptr(y),
                                                     ctypes.byref(pd), wp, wb, _stream(stream)))
     return acc, y, codes
+
+
+def dda_jobs(specs):
+    """ctypes array of esb_dda_job from (x, n, k_sig, grid, alpha_out, D_out) tuples."""
+    arr = (DdaJob * len(specs))()
+    for i, (x, n, k_sig, grid, alpha_out, D_out) in enumerate(specs):
+        arr[i] = DdaJob(_addr(x), x.numel(), n, k_sig, _addr(grid), grid.numel(), _addr(alpha_out),
+                        _addr(D_out))
+    return arr
+
+
+def esb_dda_batch_workspace_size(jobs):
+    return int(lib().esb_dda_batch_workspace_size(len(jobs), jobs))
+
+
+def esb_dda_align_batch(jobs, workspace, stream=None):
+    """DDA of every job (a dda_jobs() array) in one launch of each kernel."""
+    wp, wb = _ws(workspace)
+    _check("esb_dda_align_batch", lib().esb_dda_align_batch(len(jobs), jobs, wp, wb,
+                                                            _stream(stream)))
+
+
+def project_jobs(specs):
+    """ctypes array of esb_project_job from (x, alpha, n, k_sig, codes) tuples."""
+    arr = (ProjectJob * len(specs))()
+    for i, (x, alpha, n, k_sig, codes) in enumerate(specs):
+        arr[i] = ProjectJob(_addr(x), x.numel(), _addr(alpha), n, k_sig, _addr(codes))
+    return arr
+
+
+def esb_project_batch(jobs, stream=None):
+    """Projection of every job (a project_jobs() array) in one launch."""
+    _check("esb_project_batch", lib().esb_project_batch(len(jobs), jobs, _stream(stream)))
 
 
 def esb_pack_size(rows, K, n, k_sig):

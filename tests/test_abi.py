@@ -198,3 +198,24 @@ def test_post_refusals(L):
     assert call(PostDesc(None, None, None, 0, 0x1000, 9, 2, 0x1000)) == -1
     assert call(PostDesc(None, None, None, 1, None, 0, 0, None), acc=None, y=None) == -1
     assert call(None, acc=None, y=None) == -1
+
+
+def test_batch_refusals(L):
+    """Batched DDA and projection validate every job before any launch."""
+    from paper_2109_03513_amd.esb import DdaJob, ProjectJob
+    jobs = (DdaJob * 2)(DdaJob(0x1000, 100, 4, 2, 0x1000, 64, 0x1000, None),
+                        DdaJob(0x1000, 5000, 5, 3, 0x1000, 17, 0x1000, 0x1000))
+    need = L.esb_dda_batch_workspace_size(2, jobs)
+    single = L.esb_dda_workspace_size(100, 4, 2, 64) + L.esb_dda_workspace_size(5000, 5, 3, 17)
+    assert need >= single > 0
+    assert L.esb_dda_align_batch(2, jobs, ctypes.c_void_p(0x1000), need - 1, None) == -6
+    assert L.esb_dda_align_batch(2, jobs, None, need, None) == -6
+    bad = (DdaJob * 2)(jobs[0], DdaJob(0x1000, 5000, 5, 5, 0x1000, 17, 0x1000, None))
+    assert L.esb_dda_batch_workspace_size(2, bad) == 0
+    assert L.esb_dda_align_batch(2, bad, ctypes.c_void_p(0x1000), need, None) == -1
+    assert L.esb_dda_align_batch(0, None, None, 0, None) == 0
+    assert L.esb_dda_align_batch(-1, jobs, None, 0, None) == -1
+    pj = (ProjectJob * 2)(ProjectJob(0x1000, 10, 0x1000, 4, 2, 0x1000),
+                          ProjectJob(0x1000, 10, None, 4, 2, 0x1000))
+    assert L.esb_project_batch(2, pj, None) == -1
+    assert L.esb_project_batch(0, None, None) == 0
