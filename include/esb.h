@@ -322,14 +322,19 @@ int esb_conv2d_ws(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
  *   y[o] = z                    when y is not NULL (instead of y0);
  *   codes[o] = code of z under *alpha in ESB(n, k_sig), as esb_project, when
  *              codes is not NULL.
+ *   *absmax_out = max(*absmax_out, |z|) over every output, when absmax_out is
+ *              not NULL: the next layer's max|x| (e.g. for a DDA grid scaled by
+ *              it) without another pass; the comparison is on the fp32 bit
+ *              patterns, so a NaN z leaves a NaN; the caller sets the initial
+ *              value (0 to start).
  * residual and codes have the layout of y (GEMM: M rows of pitch ldc; conv:
  * NHWC [N, P, Q, K]); residual may be the same buffer as y (read before the
  * write of the same element).  acc, when not NULL, still receives the integer
  * sums.  The scale of the outputs must be known before the layer (the
  * paper's offline / running-average scales): alpha is a device scalar.
  * Errors: ESB_E_INVALID if post is given without alphaA / alphaB, if codes is
- * given without alpha or with an invalid (n, k_sig), or if acc, y and codes are
- * all NULL; otherwise as esb_gemm_ws / esb_conv2d_ws (workspace may be NULL).
+ * given without alpha or with an invalid (n, k_sig), or if acc, y, codes and
+ * absmax_out are all NULL; otherwise as esb_gemm_ws / esb_conv2d_ws (workspace may be NULL).
  */
 typedef struct esb_post {
     const float* a;         /* device, one fp32 per output channel, or NULL */
@@ -339,6 +344,7 @@ typedef struct esb_post {
     const float* alpha;     /* device scalar: scale of the output codes */
     int n, k_sig;           /* format of the output codes */
     uint8_t* codes;         /* device, one code per output in the layout of y, or NULL */
+    float* absmax_out;      /* device scalar, or NULL: raised to max |z| of this call */
 } esb_post;
 
 int esb_gemm_post(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, int kA_sig,

@@ -40,6 +40,7 @@ __global__ __launch_bounds__(kDwThreads) void k_dwconv(DwParams p) {
     const int CV = VEC ? C / 4 : C;                 // channel groups per pixel
     const int64_t total = (int64_t)g.Nb * g.P * g.Q * CV;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    uint32_t amax = 0;
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
         const int cv = (int)(t % CV);
         const int64_t pix = t / CV;
@@ -71,19 +72,20 @@ __global__ __launch_bounds__(kDwThreads) void k_dwconv(DwParams p) {
         if (VEC) {
             if (p.acc) *(int4*)(p.acc + o) = make_int4(a0, a1, a2, a3);
             if (p.post.on) {
-                post_store(p.post, p.y, o, c0, s * (float)a0, qa);
-                post_store(p.post, p.y, o + 1, c0 + 1, s * (float)a1, qa);
-                post_store(p.post, p.y, o + 2, c0 + 2, s * (float)a2, qa);
-                post_store(p.post, p.y, o + 3, c0 + 3, s * (float)a3, qa);
+                amax = max(amax, post_store(p.post, p.y, o, c0, s * (float)a0, qa));
+                amax = max(amax, post_store(p.post, p.y, o + 1, c0 + 1, s * (float)a1, qa));
+                amax = max(amax, post_store(p.post, p.y, o + 2, c0 + 2, s * (float)a2, qa));
+                amax = max(amax, post_store(p.post, p.y, o + 3, c0 + 3, s * (float)a3, qa));
             } else if (p.y) {
                 *(float4*)(p.y + o) = make_float4(s * (float)a0, s * (float)a1, s * (float)a2,
                                                   s * (float)a3);
             }
         } else {
             if (p.acc) p.acc[o] = a0;
-            out_store(p.post, p.y, o, c0, s * (float)a0, qa);
+            amax = max(amax, out_store(p.post, p.y, o, c0, s * (float)a0, qa));
         }
     }
+    post_absmax_flush(p.post, amax);
 }
 
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,

@@ -220,6 +220,7 @@ static Post make_post(const esb_post* p) {
     q.res = p->residual;
     q.alpha = p->alpha;
     q.codes = p->codes;
+    q.absmax = (uint32_t*)p->absmax_out;
     q.relu = p->relu != 0;
     q.on = 1;
     if (p->codes) q.pp = proj_params(make_fmt(p->n, p->k_sig));
@@ -233,7 +234,7 @@ static int gemm_impl(int M, int N, int K, const uint8_t* A, int64_t lda, int nA,
     if (!valid_fmt(nA, kA_sig) || !valid_fmt(nB, kB_sig)) return ESB_E_INVALID;
     if (M < 0 || N < 0 || K < 0 || (b_layout != ESB_B_NK && b_layout != ESB_B_KN)) return ESB_E_INVALID;
     if (!post_ok(post, alphaA, alphaB)) return ESB_E_INVALID;
-    if (!acc && !y && !(post && post->codes)) return ESB_E_INVALID;
+    if (!acc && !y && !(post && (post->codes || post->absmax_out))) return ESB_E_INVALID;
     const Post P = make_post(post);
     const Post* pp = post ? &P : nullptr;
     if (ldc < N || lda < K || (b_layout == ESB_B_NK ? ldb < K : ldb < N)) return ESB_E_INVALID;
@@ -328,7 +329,7 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
                      void* ws, size_t ws_bytes, void* stream, const esb_post* post = nullptr) {
     if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return ESB_E_INVALID;
     if (!post_ok(post, alphaX, alphaW)) return ESB_E_INVALID;
-    if (!acc && !y && !(post && post->codes)) return ESB_E_INVALID;
+    if (!acc && !y && !(post && (post->codes || post->absmax_out))) return ESB_E_INVALID;
     const Post P = make_post(post);
     const Post* pp = post ? &P : nullptr;
     if (y && (!alphaX || !alphaW)) return ESB_E_INVALID;

@@ -90,13 +90,17 @@ __device__ __forceinline__ bool alpha_valid(float a) { return a > 0.0f && a < __
 //   z = fl32(z + res_o)       (when a residual is given)
 //   z = z > 0 ? z : 0         (relu; NaN gives 0)
 // z goes to y (when given) and its code under *alpha to codes (when given);
-// res, y and codes share the output indexing.  on == 0: the plain epilogue.
+// res, y and codes share the output indexing.  absmax (when given): the
+// largest |z| over the call, as the fp32 bit pattern (a NaN wins over every
+// number), combined into *absmax with an unsigned atomic maximum (the caller
+// clears it).  on == 0: the plain epilogue.
 struct Post {
     const float* a;
     const float* b;
     const float* res;
     const float* alpha;
     uint8_t* codes;
+    uint32_t* absmax;
     ProjParams pp;
     int relu;
     int on;
@@ -104,23 +108,26 @@ struct Post {
 
 __device__ __forceinline__ float post_alpha(const Post& P) { return P.codes ? *P.alpha : 0.0f; }
 
-__device__ __forceinline__ void post_store(const Post& P, float* y, int64_t o, int64_t ch, float y0,
-                                           float qa) {
+// Returns the bit pattern of |z| (0 when absmax is not requested).
+__device__ __forceinline__ uint32_t post_store(const Post& P, float* y, int64_t o, int64_t ch,
+                                               float y0, float qa) {
     float z = __builtin_fmaf(P.a ? P.a[ch] : 1.0f, y0, P.b ? P.b[ch] : 0.0f);
     if (P.res) z = z + P.res[o];
     if (P.relu) z = z > 0.0f ? z : 0.0f;
     if (y) y[o] = z;
     if (P.codes) P.codes[o] = (uint8_t)(alpha_valid(qa) ? esb_code(z, qa, P.pp) : P.pp.zero_code);
+    return P.absmax ? (__float_as_uint(z) & 0x7fffffffu) : 0u;
 }
 
 // Four consecutive outputs o .. o+3 (channels ch .. ch+3; nv of them inside the
 // output) through the fused post-processing; 16-byte residual / y accesses and
 // one 4-byte code store where the addresses allow.
-__device__ __forceinline__ void post_store4(const Post& P, float* y, int64_t o, int64_t ch, f32x4 v,
-                                            int nv, float qa) {
+__device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t o, int64_t ch,
+                                                f32x4 v, int nv, float qa) {
     if (nv < 4) {
-        for (int c = 0; c < nv; c++) post_store(P, y, o + c, ch + c, v[c], qa);
-        return;
+        uint32_t m = 0;
+        for (int c = 0; c < nv; c++) m = max(m, post_store(P, y, o + c, ch + c, v[c], qa));
+        return m;
     }
     f32x4 z;
 #pragma unroll
@@ -161,13 +168,35 @@ __device__ __forceinline__ void post_store4(const Post& P, float* y, int64_t o, 
             for (int c = 0; c < 4; c++) P.codes[o + c] = (uint8_t)q[c];
         }
     }
+    uint32_t m = 0;
+    if (P.absmax) {
+#pragma unroll
+        for (int c = 0; c < 4; c++) m = max(m, __float_as_uint(z[c]) & 0x7fffffffu);
+    }
+    return m;
+}
+
+// The running |z| maxima of a wave into *absmax.  Every lane of the wave calls
+// this.  Thousands of waves meet on one address, so a wave first reads the
+// current value from the L2 (an atomic load) and issues its atomic maximum only
+// when its own maximum is larger: a stale read costs one unneeded atomic, never
+// a wrong result.
+__device__ __forceinline__ void post_absmax_flush(const Post& P, uint32_t m) {
+    if (!P.absmax) return;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+    if ((threadIdx.x & 63) == 0) {
+        const uint32_t cur = __hip_atomic_load(P.absmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (m > cur) atomicMax(P.absmax, m);
+    }
 }
 
 // The epilogue store of one output: the plain scaled value, or the fused post-processing.
-__device__ __forceinline__ void out_store(const Post& P, float* y, int64_t o, int64_t ch, float y0,
-                                          float qa) {
-    if (P.on) post_store(P, y, o, ch, y0, qa);
-    else if (y) y[o] = y0;
+__device__ __forceinline__ uint32_t out_store(const Post& P, float* y, int64_t o, int64_t ch,
+                                              float y0, float qa) {
+    if (P.on) return post_store(P, y, o, ch, y0, qa);
+    if (y) y[o] = y0;
+    return 0u;
 }
 
 hipError_t launch_project(const float* x, int64_t len, const float* alpha, const Fmt& f,

@@ -364,6 +364,7 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
         static_assert(NT / 64 * 16 * WN * 4 <= sizeof(sA), "post slabs fit the A buffers");
         float* slab = (float*)&sA[0][0][0] + wave * 16 * WN;
         const float qa = post_alpha(g.post);
+        uint32_t amax = 0;
 #pragma unroll
         for (int i = 0; i < TI; i++) {
             __syncthreads();
@@ -385,11 +386,12 @@ __global__ __launch_bounds__(NT) void k_contract(GemmParams g) {
                 const int row = m0 + wr + 16 * i + rl, col = n0 + wc + cl;
                 if (row < g.M && col < g.N) {
                     const int64_t ch = (int64_t)grp * g.N + col;
-                    post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch,
-                                *(const f32x4*)(slab + e), min(4, g.N - col), qa);
+                    amax = max(amax, post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch,
+                                                 *(const f32x4*)(slab + e), min(4, g.N - col), qa));
                 }
             }
         }
+        post_absmax_flush(g.post, amax);
         return;
     }
 #pragma unroll

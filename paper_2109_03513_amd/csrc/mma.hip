@@ -98,6 +98,7 @@ __device__ __forceinline__ void post_epilogue(const FastParams& g, float* slab, 
     constexpr int W = 32 * TJ;
     const int lr = lane & 31, lg = lane >> 5;
     const float qa = post_alpha(g.post);
+    uint32_t amax = 0;
 #pragma unroll
     for (int i = 0; i < TI; i++) {
         __syncthreads();   // the LDS is free: main loop or previous row done everywhere
@@ -113,11 +114,12 @@ __device__ __forceinline__ void post_epilogue(const FastParams& g, float* slab, 
             const int row = row0 + 32 * i + rl, col = col0 + cl;
             if (row < g.M && col < g.N) {
                 const int64_t ch = (int64_t)grp * g.N + col;
-                post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch, *(const f32x4*)(slab + e),
-                            min(4, g.N - col), qa);
+                amax = max(amax, post_store4(g.post, g.y, (int64_t)row * g.ldc + ch, ch,
+                                             *(const f32x4*)(slab + e), min(4, g.N - col), qa));
             }
         }
     }
+    post_absmax_flush(g.post, amax);
 }
 
 __device__ __forceinline__ uint32_t dec_f8(uint32_t c, const MmaDecode& d) {
@@ -518,6 +520,7 @@ __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
     const float qa = g.post.on ? post_alpha(g.post) : 0.0f;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t amax = 0;
     if (g.N % 4 == 0) {
         const int4* p = (const int4*)g.part;
         const int64_t MN4 = MN / 4;
@@ -540,9 +543,10 @@ __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
 #pragma unroll
             for (int c = 0; c < 4; c++) {
                 if (g.acc) g.acc[o + c] = t[c];
-                out_store(g.post, g.y, o + c, col + c, s * (float)t[c], qa);
+                amax = max(amax, out_store(g.post, g.y, o + c, col + c, s * (float)t[c], qa));
             }
         }
+        post_absmax_flush(g.post, amax);
         return;
     }
     for (int64_t e = t0; e < MN; e += stride) {
@@ -552,8 +556,9 @@ __global__ __launch_bounds__(256) void k_splitk_sum(FastParams g) {
         const int64_t row = e / g.N, col = e - row * g.N;
         const int64_t o = row * g.ldc + col;
         if (g.acc) g.acc[o] = t;
-        out_store(g.post, g.y, o, col, s * (float)t, qa);
+        amax = max(amax, out_store(g.post, g.y, o, col, s * (float)t, qa));
     }
+    post_absmax_flush(g.post, amax);
 }
 
 // ------------------------------------------------------ pre-decoded operands

@@ -54,7 +54,7 @@ class ProjectJob(ctypes.Structure):
 class PostDesc(ctypes.Structure):
     _fields_ = [("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("residual", ctypes.c_void_p),
                 ("relu", ctypes.c_int), ("alpha", ctypes.c_void_p), ("n", ctypes.c_int),
-                ("k_sig", ctypes.c_int), ("codes", ctypes.c_void_p)]
+                ("k_sig", ctypes.c_int), ("codes", ctypes.c_void_p), ("absmax_out", ctypes.c_void_p)]
 
 
 def lib():
@@ -256,17 +256,18 @@ def _addr(t):
     return None if t is None else t.data_ptr()
 
 
-def post_desc(alpha, n, k_sig, codes=None, a=None, b=None, residual=None, relu=False):
-    """esb_post of device tensors: per-channel a, b, a residual in the output layout, relu, and
-    the output codes (uint8, output layout) under the device scalar alpha in ESB(n, k_sig)."""
+def post_desc(alpha, n, k_sig, codes=None, a=None, b=None, residual=None, relu=False, absmax=None):
+    """esb_post of device tensors: per-channel a, b, a residual in the output layout, relu, the
+    output codes (uint8, output layout) under the device scalar alpha in ESB(n, k_sig), and a
+    device fp32 scalar raised to max|z|."""
     return PostDesc(_addr(a), _addr(b), _addr(residual), int(bool(relu)), _addr(alpha), n, k_sig,
-                    _addr(codes))
+                    _addr(codes), _addr(absmax))
 
 
 def esb_gemm_post(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, out_alpha, out_n, out_k_sig,
                   a=None, b=None, residual=None, relu=False, b_layout=ESB_B_NK, codes=None,
                   want_codes=True, acc=None, want_acc=False, y=None, want_y=False, workspace=None,
-                  stream=None):
+                  stream=None, absmax=None):
     """Contraction with the fused post-processing; returns (acc, y, codes), M x N each."""
     import torch
     _dev_tensor(A, torch.uint8, "A")
@@ -280,7 +281,7 @@ def esb_gemm_post(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, out_alpha, out_n
         y = torch.empty((M, N), dtype=torch.float32, device=dev)
     if codes is None and want_codes:
         codes = torch.empty((M, N), dtype=torch.uint8, device=dev)
-    d = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu)
+    d = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu, absmax)
     lda = A.stride(0) if M else K
     ldb = B.stride(0) if B.shape[0] else 0
     wp, wb = _ws(workspace)
@@ -294,7 +295,7 @@ def esb_gemm_post(A, nA, kA_sig, alphaA, B, nB, kB_sig, alphaB, out_alpha, out_n
 def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out_n, out_k_sig,
                     a=None, b=None, residual=None, relu=False, stride=(1, 1), pad=(0, 0),
                     groups=1, codes=None, want_codes=True, acc=None, want_acc=False, y=None,
-                    want_y=False, workspace=None, stream=None):
+                    want_y=False, workspace=None, stream=None, absmax=None):
     """Convolution with the fused post-processing; returns (acc, y, codes), NHWC each."""
     import torch
     _dev_tensor(x, torch.uint8, "x")
@@ -309,7 +310,7 @@ def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out
         y = torch.empty((Nb, P, Q, K), dtype=torch.float32, device=dev)
     if codes is None and want_codes:
         codes = torch.empty((Nb, P, Q, K), dtype=torch.uint8, device=dev)
-    pd = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu)
+    pd = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, residual, relu, absmax)
     d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], groups)
     wp, wb = _ws(workspace)
     _check("esb_conv2d_post", lib().esb_conv2d_post(ctypes.byref(d), _ptr(x), nX, kX_sig,

@@ -8,11 +8,15 @@ largest set value, so the grid spans (0, max|x| / C]), projected to ESB codes
 (eq. (8)) and contracted with the pre-quantized weights (eq. (15)) into fp32
 outputs.  Weights are quantized once, the same way, when the model is built.
 
-Only the library's calls touch the ESB arithmetic.  The glue between layers
-(ReLU, the 3x3 / stride-2 max pool after conv1, residual additions, the global
-average pool) is plain tensor work done with torch on the same stream: the
-average is a float64 sum of the 7x7 window divided by 49 and rounded to fp32
-once.  No batch normalization (the weights are He-initialized).
+Only the library's calls touch the ESB arithmetic.  The ReLUs and the
+residual additions run in the convolutions' epilogues (esb_conv2d_post: the
+same fp32 operations), which also raise a device scalar to the max |x| of the
+next layer's input, so that its DDA grid needs no separate reduction; the
+3x3 / stride-2 max pool after conv1 and the global average pool are torch on
+the same stream (the pool keeps the maximum: the ReLU'd values are >= 0 and
+every element lies in some window).  The average is a float64 sum of the 7x7
+window divided by 49 and rounded to fp32 once.  No batch normalization (the
+weights are He-initialized).
 
 A downsample conv reads the same block input as the block's first conv, so it
 reuses that conv's alpha and codes instead of quantizing the tensor again.
@@ -82,6 +86,7 @@ class ResNet18ESB:
                 (batch, side, side, L["cin"]), (L["cout"], L["k"], L["k"], L["cin"]), n, k_sig, n,
                 k_sig, stride=(L["stride"],) * 2, pad=(L["pad"],) * 2))
         self.cws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        self.amax = torch.zeros(32, dtype=torch.float32, device=dev)   # max |x| per layer input
         # weights, quantized once
         for name, L in self.layers.items():
             w = torch.from_numpy(np.ascontiguousarray(weights[name])).to(dev)
@@ -94,28 +99,38 @@ class ResNet18ESB:
         need = esb.esb_dda_workspace_size(t.numel(), self.n, self.ks, GRID_POINTS)
         return self.torch.empty(max(need, 1), dtype=self.torch.uint8, device=t.device)
 
-    def grid(self, x):
-        """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product)."""
-        m = self.torch.linalg.vector_norm(x, float("inf"))   # max |x|, one reduction
+    def grid(self, x, xmax=None):
+        """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product); xmax:
+        a device scalar already holding max|x| (from the producing epilogue)."""
+        m = self.torch.linalg.vector_norm(x, float("inf")) if xmax is None else xmax
         return m.reshape(1) * self.cgrid
 
-    def _quantize(self, x, ws):
+    def _quantize(self, x, ws, xmax=None):
         torch = self.torch
-        g = self.grid(x)
+        g = self.grid(x, xmax)
         alpha = torch.empty(1, dtype=torch.float32, device=x.device)
         esb.esb_dda_align(x, self.n, self.ks, g, alpha_out=alpha, D_out=None, workspace=ws,
                           stream=self.sh, want_D=False)
         codes = esb.esb_project(x, alpha, self.n, self.ks, stream=self.sh)
         return alpha, codes
 
-    def conv(self, name, x, quantized=None):
+    def conv(self, name, x, quantized=None, xmax=None, residual=None, relu=False, absmax=None):
         """The layer on input x; `quantized` = (alpha, codes) of x when another layer
-        already quantized this same tensor (the DDA and the projection depend on x only)."""
+        already quantized this same tensor (the DDA and the projection depend on x only);
+        xmax: device max|x| for the DDA grid.  With residual / relu / absmax the epilogue adds
+        the residual, applies the ReLU and raises absmax to the max |output|."""
         L = self.layers[name]
-        ax, cx = quantized if quantized is not None else self._quantize(x, self.ws[name])
-        acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"],
-                                stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
-                                want_acc=self.record, stream=self.sh, workspace=self.cws)
+        ax, cx = quantized if quantized is not None else self._quantize(x, self.ws[name], xmax)
+        if residual is None and not relu and absmax is None:
+            acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks,
+                                    L["alpha"], stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
+                                    want_acc=self.record, stream=self.sh, workspace=self.cws)
+        else:
+            acc, y, _ = esb.esb_conv2d_post(
+                cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"], None, self.n,
+                self.ks, residual=residual, relu=relu, stride=(L["stride"],) * 2,
+                pad=(L["pad"],) * 2, want_codes=False, want_acc=self.record, want_y=True,
+                stream=self.sh, workspace=self.cws, absmax=absmax)
         if self.record:
             self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
         self.calib[name] = ax
@@ -125,18 +140,27 @@ class ResNet18ESB:
     def forward(self, x):
         torch = self.torch
         F = torch.nn.functional
-        a = torch.relu(self.conv("conv1", x))
-        # 3x3 max pool, stride 2, pad 1 (padding never wins: -inf)
+        self.amax.zero_()
+        slots = iter(range(self.amax.numel()))
+
+        def slot():
+            i = next(slots)
+            return self.amax[i:i + 1]
+
+        m = slot()
+        a = self.conv("conv1", x, relu=True, absmax=m)
+        # 3x3 max pool, stride 2, pad 1 (padding never wins: -inf); max|a| is unchanged
         a = F.max_pool2d(a.permute(0, 3, 1, 2), 3, 2, 1).permute(0, 2, 3, 1).contiguous()
         for stage in (1, 2, 3, 4):
             for blk in (0, 1):
                 p = "l%d.%d." % (stage, blk)
-                out = torch.relu(self.conv(p + "c1", a))
+                m1 = slot()
+                out = self.conv(p + "c1", a, xmax=m, relu=True, absmax=m1)
                 qa = self.last_q                     # the block input, quantized for c1
-                out = self.conv(p + "c2", out)
                 # the downsample conv reads the same block input: its quantization is reused
                 sc = self.conv(p + "ds", a, quantized=qa) if (p + "ds") in self.layers else a
-                a = torch.relu(out + sc)
+                m = slot()
+                a = self.conv(p + "c2", out, xmax=m1, residual=sc, relu=True, absmax=m)
         feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
         af, cf = self._quantize(feat, self.ws["fc"])
         self.calib["fc"] = af

@@ -192,11 +192,11 @@ def test_post_refusals(L):
         return gp(M, N, K, fake, K, 4, 2, alphaA, fake, K, 4, 2, fake, 0, acc, y, N,
                   None if post is None else ctypes.byref(post), None, 0, None)
 
-    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 2, 0x1000), alphaA=None) == -1
-    assert call(PostDesc(None, None, None, 0, None, 4, 2, 0x1000)) == -1      # codes, no alpha
-    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 4, 0x1000)) == -1    # bad format
-    assert call(PostDesc(None, None, None, 0, 0x1000, 9, 2, 0x1000)) == -1
-    assert call(PostDesc(None, None, None, 1, None, 0, 0, None), acc=None, y=None) == -1
+    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 2, 0x1000, None), alphaA=None) == -1
+    assert call(PostDesc(None, None, None, 0, None, 4, 2, 0x1000, None)) == -1      # codes, no alpha
+    assert call(PostDesc(None, None, None, 0, 0x1000, 4, 4, 0x1000, None)) == -1    # bad format
+    assert call(PostDesc(None, None, None, 0, 0x1000, 9, 2, 0x1000, None)) == -1
+    assert call(PostDesc(None, None, None, 1, None, 0, 0, None, None), acc=None, y=None) == -1
     assert call(None, acc=None, y=None) == -1
 
 

@@ -82,14 +82,26 @@ def test_gemm_post(esb, M, N, K, fa, fb, ws, variant, out):
     w = workspace(esb.esb_gemm_workspace_size(M, N, K, bA, ksA, bB, ksB)) if ws else None
     log("gemm_post M=%d N=%d K=%d A=%s B=%s ws=%s variant=%s out=%s" % (M, N, K, fa, fb, ws,
                                                                        variant, out))
+    amax = scalar(0.0)
     acc, y, codes = esb.esb_gemm_post(
         dev(A), bA, ksA, scalar(ALPHA_A), dev(B), bB, ksB, scalar(ALPHA_B), scalar(qa), out[0],
         out[1], a=None if a is None else dev(a), b=None if b is None else dev(b),
         residual=None if R is None else dev(R), relu=relu, want_acc=True, want_y=True,
-        workspace=w)
+        workspace=w, absmax=amax)
     np.testing.assert_array_equal(host(acc)[rows], oacc)
     np.testing.assert_array_equal(host(y)[rows].view(np.uint32), oz.view(np.uint32))
     np.testing.assert_array_equal(host(codes)[rows], ocodes)
+    check_absmax(host(amax)[0], oz, rows.size == M)
+
+
+def check_absmax(got, oz, complete):
+    """max |z| over the call: equal to the oracle's when every row was computed by the oracle,
+    else at least the sampled rows' maximum."""
+    want = np.float32(np.max(np.abs(oz))) if oz.size else np.float32(0)
+    if complete:
+        assert got == want, (got, want)
+    else:
+        assert got >= want
 
 
 def test_gemm_post_codes_only_and_in_place_residual(esb):
@@ -161,11 +173,32 @@ def test_conv2d_post(esb, Nb, H, W, C, K, R, S, stride, pad, groups, fx, fw, ws,
         wsz = lib().esb_conv2d_workspace_size(ctypes.byref(cd), bX, ksX, bW, ksW)
     log("conv_post %s groups=%d ws=%d variant=%s" % ((Nb, H, W, C, K, R, S, stride, pad), groups,
                                                      wsz, variant))
+    amax = scalar(0.0)
     acc, y, codes = esb.esb_conv2d_post(
         dev(x), bX, ksX, scalar(ALPHA_A), dev(w), bW, ksW, scalar(ALPHA_B), scalar(qa), 5, 3,
         a=None if a is None else dev(a), b=None if b is None else dev(b),
         residual=None if R_ is None else dev(R_), relu=relu, want_acc=True, want_y=True,
-        workspace=workspace(wsz) if ws else None, **d)
+        workspace=workspace(wsz) if ws else None, absmax=amax, **d)
     np.testing.assert_array_equal(host(acc), oacc)
     np.testing.assert_array_equal(host(y).reshape(-1, K).view(np.uint32), oz.view(np.uint32))
     np.testing.assert_array_equal(host(codes).reshape(-1, K), oc)
+    check_absmax(host(amax)[0], oz, True)
+
+
+def test_absmax_only_and_accumulation(esb):
+    """Only the maximum requested; a second call raises the same scalar further."""
+    M, N, K = 300, 200, 128
+    A = wl.random_codes(71, (M, K), 8)
+    B = wl.random_codes(72, (N, K), 8)
+    st, _, oy = oracle.gemm(A, B, 5, 3, ALPHA_A, 5, 3, ALPHA_B)
+    oz, _ = oracle.post(oy, 5, 3, 1.0, relu=True)
+    amax = scalar(0.0)
+    acc, y, codes = esb.esb_gemm_post(dev(A), 5, 3, scalar(ALPHA_A), dev(B), 5, 3, scalar(ALPHA_B),
+                                      None, 5, 3, relu=True, want_codes=False, absmax=amax)
+    assert acc is None and y is None and codes is None
+    assert host(amax)[0] == np.float32(np.max(np.abs(oz)))
+    big = np.float32(np.max(np.abs(oz)) * 4)
+    amax2 = scalar(big)
+    esb.esb_gemm_post(dev(A), 5, 3, scalar(ALPHA_A), dev(B), 5, 3, scalar(ALPHA_B), None, 5, 3,
+                      relu=True, want_codes=False, absmax=amax2)
+    assert host(amax2)[0] == big

@@ -54,7 +54,9 @@ def test_resnet18_stack_matches_oracle(batch):
     cmax = resnet18.value_max(N, KS)
     gpu = {t["name"]: t for t in model.trace}
 
-    def layer(name, a, w, stride, pad, wq):
+    def layer(name, a, w, stride, pad, wq, glue=None):
+        """The oracle layer; the GPU trace holds its output after the epilogue's glue (ReLU,
+        residual), which `glue` applies to the oracle's output in numpy fp32."""
         log("  oracle layer %s input %s" % (name, a.shape))
         alpha, codes = quantize_np(a, cmax)
         t = gpu[name]
@@ -67,8 +69,9 @@ def test_resnet18_stack_matches_oracle(batch):
                                        stride=(stride, stride), pad=(pad, pad))
         assert st == 0
         np.testing.assert_array_equal(host(t["acc"]), acc, err_msg=name)
-        assert_rel(host(t["y"]), y, 1e-6, name)
-        return y
+        z = y if glue is None else glue(y)
+        assert_rel(host(t["y"]), z, 1e-6, name)
+        return z
 
     wq = {}
     for name, cin, cout, k, st, pd in wl.RESNET18_CONVS:
@@ -79,18 +82,20 @@ def test_resnet18_stack_matches_oracle(batch):
     wq["fc"] = quantize_np(weights["fc"], cmax)
     geo = {name: (st, pd) for name, _, _, _, st, pd in wl.RESNET18_CONVS}
 
-    def conv(name, a):
-        return layer(name, a, None, geo[name][0], geo[name][1], wq[name])
+    def conv(name, a, glue=None):
+        return layer(name, a, None, geo[name][0], geo[name][1], wq[name], glue)
 
-    a = np.maximum(conv("conv1", x), 0.0).astype(np.float32)
+    def relu(v):
+        return np.maximum(v, 0.0).astype(np.float32)
+
+    a = conv("conv1", x, relu)
     a = maxpool_np(a)
     for stage in (1, 2, 3, 4):
         for blk in (0, 1):
             p = "l%d.%d." % (stage, blk)
-            out = np.maximum(conv(p + "c1", a), 0.0).astype(np.float32)
-            out = conv(p + "c2", out)
+            out = conv(p + "c1", a, relu)
             sc = conv(p + "ds", a) if (p + "ds") in geo else a
-            a = np.maximum(out + sc, 0.0).astype(np.float32)
+            a = conv(p + "c2", out, lambda v: relu(v + sc))
     feat = (a.astype(np.float64).sum(axis=(1, 2)) / float(a.shape[1] * a.shape[2])).astype(np.float32)
     y = layer("fc", feat, None, 1, 0, wq["fc"])
     assert_rel(logits, y, 1e-6, "logits")
