@@ -223,6 +223,9 @@ typedef struct esb_dda_job {
     int G;
     float* alpha_out;   /* device, one fp32 */
     double* D_out;      /* device, G doubles, or NULL */
+    const float* grid_scale;  /* device scalar, or NULL: candidate j is then
+                                 fl32(grid_scale[0] * grid[j]) (one rounding), e.g. a grid of
+                                 factors times a max|x| computed on the device */
 } esb_dda_job;
 size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs);
 int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, size_t ws_bytes,

@@ -243,7 +243,8 @@ __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
 
 // One block (local index bid of its job) of the histogram pass.
 __device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int64_t len,
-                                               const float* __restrict__ grid, const DdaArgs a,
+                                               const float* __restrict__ grid,
+                                               const float* __restrict__ gscale, const DdaArgs a,
                                                double* __restrict__ part, const int bid) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -263,11 +264,12 @@ __device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int6
     // ---- 0. requests first: this thread's candidate scales and the first chunk
     //         of x, so that both latencies overlap the clearing of the bins.
     constexpr int kMaxTpt = kDdaMaxThresholds / kHistThreads;   // thresholds per thread
+    const float gsc = gscale ? *gscale : 1.0f;   // candidates fl32(gsc * grid[j])
     float al[kMaxTpt];
 #pragma unroll
     for (int r = 0; r < kMaxTpt; r++) {
         const int i = tid + r * kHistThreads;
-        al[r] = (i < A) ? grid[i / M] : 1.0f;
+        al[r] = (i < A) ? (gscale ? gsc * grid[i / M] : grid[i / M]) : 1.0f;
     }
     const bool vec = ((uintptr_t)x & 15) == 0;
     const int64_t e0 = (int64_t)bid * a.rows_pb * kRowElems;
@@ -713,6 +715,7 @@ struct DdaJob {
     const float* x;
     int64_t len;
     const float* grid;
+    const float* gscale;   // NULL, or a device scalar multiplying every candidate
     float* alpha_out;
     double* D_out;
     double* part;       // block vectors
@@ -735,7 +738,7 @@ __device__ __forceinline__ int dda_job_of_block(const DdaBatch& B, int b) {
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(DdaBatch B) {
     const int j = dda_job_of_block(B, (int)blockIdx.x);
     const DdaJob& J = B.job[j];
-    dda_hist_block(J.x, J.len, J.grid, J.a, J.part, (int)blockIdx.x - J.blk0);
+    dda_hist_block(J.x, J.len, J.grid, J.gscale, J.a, J.part, (int)blockIdx.x - J.blk0);
 }
 
 // --------------------------------------------------------------------- group
@@ -790,7 +793,7 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
     const int S = fin_split(G, nb);
     const int p = tid & (S - 1), j = tid / S;
     const bool live = j < G;
-    const float al = live ? grid[j] : 0.0f;
+    const float al = live ? (J.gscale ? *J.gscale * grid[j] : grid[j]) : 0.0f;
     double A = 0.0, B = 0.0, S2 = 0.0;
     uint32_t fl = 0;
     if (live) {
@@ -883,7 +886,8 @@ hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
             a.n = d.f.n; a.k = d.f.k;
             dda_blocks(d.len, &a.nblk, &a.rows_pb);
             a.lbins = hist_lbins(d.L.A, a.rows_pb >= 8);
-            J.x = d.x; J.len = d.len; J.grid = d.grid; J.alpha_out = d.alpha_out; J.D_out = d.D_out;
+            J.x = d.x; J.len = d.len; J.grid = d.grid; J.gscale = d.gscale;
+            J.alpha_out = d.alpha_out; J.D_out = d.D_out;
             J.part = (double*)((char*)d.ws + d.L.off_part);
             J.grp = (double*)((char*)d.ws + d.L.off_group);
             J.blk0 = nhist;
@@ -905,7 +909,7 @@ hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
                       float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
                       hipStream_t s) {
-    const DdaJobDesc d{x, len, f, grid, G, alpha_out, D_out, ws, L};
+    const DdaJobDesc d{x, len, f, grid, G, alpha_out, D_out, ws, L, nullptr};
     return launch_dda_batch(&d, 1, s);
 }
 

@@ -169,6 +169,7 @@ int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, siz
         if (!dda_layout(j.len, e.f, j.G, &e.L)) return ESB_E_INVALID;
         e.x = j.x; e.len = j.len; e.grid = j.grid; e.G = j.G;
         e.alpha_out = j.alpha_out; e.D_out = j.D_out;
+        e.gscale = j.grid_scale;
         e.ws = (char*)workspace + off;
         off += (e.L.total + 255) & ~(size_t)255;
     }

@@ -244,6 +244,7 @@ struct DdaJobDesc {
     double* D_out;
     void* ws;
     DdaLayout L;
+    const float* gscale;   // NULL, or a device scalar: candidate j is fl32(*gscale * grid[j])
 };
 hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s);
 

@@ -43,7 +43,8 @@ class ConvDesc(ctypes.Structure):
 class DdaJob(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("len", ctypes.c_int64), ("n", ctypes.c_int),
                 ("k_sig", ctypes.c_int), ("grid", ctypes.c_void_p), ("G", ctypes.c_int),
-                ("alpha_out", ctypes.c_void_p), ("D_out", ctypes.c_void_p)]
+                ("alpha_out", ctypes.c_void_p), ("D_out", ctypes.c_void_p),
+                ("grid_scale", ctypes.c_void_p)]
 
 
 class ProjectJob(ctypes.Structure):
@@ -321,11 +322,14 @@ def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out
 
 
 def dda_jobs(specs):
-    """ctypes array of esb_dda_job from (x, n, k_sig, grid, alpha_out, D_out) tuples."""
+    """ctypes array of esb_dda_job from (x, n, k_sig, grid, alpha_out, D_out[, grid_scale])
+    tuples; with grid_scale (a device scalar) candidate j is fl32(grid_scale * grid[j])."""
     arr = (DdaJob * len(specs))()
-    for i, (x, n, k_sig, grid, alpha_out, D_out) in enumerate(specs):
+    for i, spec in enumerate(specs):
+        x, n, k_sig, grid, alpha_out, D_out = spec[:6]
+        gs = spec[6] if len(spec) > 6 else None
         arr[i] = DdaJob(_addr(x), x.numel(), n, k_sig, _addr(grid), grid.numel(), _addr(alpha_out),
-                        _addr(D_out))
+                        _addr(D_out), _addr(gs))
     return arr
 
 

@@ -107,10 +107,14 @@ class ResNet18ESB:
 
     def _quantize(self, x, ws, xmax=None):
         torch = self.torch
-        g = self.grid(x, xmax)
         alpha = torch.empty(1, dtype=torch.float32, device=x.device)
-        esb.esb_dda_align(x, self.n, self.ks, g, alpha_out=alpha, D_out=None, workspace=ws,
-                          stream=self.sh, want_D=False)
+        if xmax is None:
+            g = self.grid(x)
+            esb.esb_dda_align(x, self.n, self.ks, g, alpha_out=alpha, D_out=None, workspace=ws,
+                              stream=self.sh, want_D=False)
+        else:   # the DDA scales the factors by the device max|x| itself (same single rounding)
+            jobs = esb.dda_jobs([(x, self.n, self.ks, self.cgrid, alpha, None, xmax)])
+            esb.esb_dda_align_batch(jobs, ws, stream=self.sh)
         codes = esb.esb_project(x, alpha, self.n, self.ks, stream=self.sh)
         return alpha, codes
 

@@ -203,14 +203,14 @@ def test_post_refusals(L):
 def test_batch_refusals(L):
     """Batched DDA and projection validate every job before any launch."""
     from paper_2109_03513_amd.esb import DdaJob, ProjectJob
-    jobs = (DdaJob * 2)(DdaJob(0x1000, 100, 4, 2, 0x1000, 64, 0x1000, None),
-                        DdaJob(0x1000, 5000, 5, 3, 0x1000, 17, 0x1000, 0x1000))
+    jobs = (DdaJob * 2)(DdaJob(0x1000, 100, 4, 2, 0x1000, 64, 0x1000, None, None),
+                        DdaJob(0x1000, 5000, 5, 3, 0x1000, 17, 0x1000, 0x1000, 0x1000))
     need = L.esb_dda_batch_workspace_size(2, jobs)
     single = L.esb_dda_workspace_size(100, 4, 2, 64) + L.esb_dda_workspace_size(5000, 5, 3, 17)
     assert need >= single > 0
     assert L.esb_dda_align_batch(2, jobs, ctypes.c_void_p(0x1000), need - 1, None) == -6
     assert L.esb_dda_align_batch(2, jobs, None, need, None) == -6
-    bad = (DdaJob * 2)(jobs[0], DdaJob(0x1000, 5000, 5, 5, 0x1000, 17, 0x1000, None))
+    bad = (DdaJob * 2)(jobs[0], DdaJob(0x1000, 5000, 5, 5, 0x1000, 17, 0x1000, None, None))
     assert L.esb_dda_batch_workspace_size(2, bad) == 0
     assert L.esb_dda_align_batch(2, bad, ctypes.c_void_p(0x1000), need, None) == -1
     assert L.esb_dda_align_batch(0, None, None, 0, None) == 0

@@ -111,3 +111,24 @@ def test_project_batch(esb, count):
     esb.esb_project_batch(esb.project_jobs(rows))
     for (x, alpha, b, ks, cd) in keep:
         np.testing.assert_array_equal(host(cd), oracle.project(x, alpha, b, ks))
+
+
+def test_dda_batch_grid_scale(esb):
+    """Candidates given as factors times a device scalar equal the explicit grid
+    fl32(s * c_j), bit for bit, against the oracle."""
+    torch = torch_cuda()
+    r = np.random.default_rng(5)
+    x = np.maximum(r.standard_normal(50001), 0).astype(np.float32) * np.float32(3.7)
+    c = ((np.arange(64) + 1) / (64 * 6.0)).astype(np.float32)
+    s = np.float32(np.max(np.abs(x)))
+    grid = (s * c).astype(np.float32)
+    xd = dev(x)
+    a = torch.empty(1, dtype=torch.float32, device="cuda")
+    D = torch.empty(64, dtype=torch.float64, device="cuda")
+    cd, sd = dev(c), dev(np.array([s], dtype=np.float32))   # alive until the call has run
+    jobs = esb.dda_jobs([(xd, 5, 3, cd, a, D, sd)])
+    ws = torch.empty(esb.esb_dda_batch_workspace_size(jobs), dtype=torch.uint8, device="cuda")
+    esb.esb_dda_align_batch(jobs, ws)
+    j, Do = oracle.dda(x, 5, 3, grid)
+    assert_rel(host(D), Do, REL, "scaled grid")
+    assert host(a)[0] == grid[j]
