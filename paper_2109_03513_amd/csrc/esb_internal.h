@@ -83,6 +83,60 @@ __device__ __forceinline__ uint32_t esb_code(float x, float alpha, const ProjPar
 
 __device__ __forceinline__ bool alpha_valid(float a) { return a > 0.0f && a < __builtin_inff(); }
 
+// Fast projection: the IEEE division costs ~10 VALU operations per element and
+// makes a projection ALU bound, so the quotient is approximated by
+// q0 = fl32(x * r), r = fl32(1 / alpha).  |q0 - x/alpha| <= 2^-23 |q0| < 2
+// ulp(q0), and fl32(x/alpha) is within another half ulp, so the two round to
+// the same set value unless q0 lies within 3 ulps of a cell midpoint
+// (midpoints sit at least 2^-(k+2) of a binade away from binade edges, so the
+// check is on the bits the rounding discards).  Below 1 the rounding to the
+// fixed step 2^-k is done on w = |q0| + 1 (one more half ulp).  Groups with an
+// element within 4 ulps of a midpoint take the exact esb_code; this happens
+// with probability ~2^(k-20) per element.  Used only for scales with alpha and
+// 1/alpha normal (alpha in [2^-125, 2^125]).
+// Fast code of x given r = fl32(1/alpha); sets `risky` if q0 is within 4 ulps
+// of a midpoint (the caller then recomputes with esb_code).
+__device__ __forceinline__ uint32_t esb_code_fast(float x, float r, const ProjParams& p,
+                                                  uint32_t& risky) {
+    const float q0 = x * r;
+    const uint32_t qb = __float_as_uint(q0);
+    const uint32_t ab = qb & 0x7fffffffu;
+    const bool small = ab < 0x3f800000u;                       // |q0| < 1
+    const float w = small ? __uint_as_float(ab) + 1.0f : __uint_as_float(ab);
+    const uint32_t wb = __float_as_uint(w);
+    const uint32_t shA = 23u - p.k;
+    const uint32_t half = 1u << (shA - 1u);
+    const uint32_t c = ((wb + half) >> shA) - (127u << p.k);   // (e << k) | f, or m for small
+    const uint32_t d = wb & ((half << 1) - 1u);                  // discarded bits
+    risky |= (d - half + 4u) <= 8u;
+    // small: m = round((w - 1) * 2^k) in [0, 2^k]; zero + m wraps m == 2^k (the value 1) to 0
+    uint32_t code = small ? ((p.zero_code + c) & (p.sign_bit - 1u)) : c;
+    code = (ab >= p.c_bits) ? p.c_code : code;
+    code = (ab > 0x7f800000u) ? p.zero_code : code;
+    code |= (code != p.zero_code) ? ((qb >> 31) << (31u - __builtin_clz(p.sign_bit))) : 0u;
+    return code;
+}
+
+__device__ __forceinline__ bool fast_scale(float alpha) {
+    return alpha >= 0x1p-125f && alpha <= 0x1p125f;
+}
+
+// Vector path: 4 elements per 16-byte load, 4 codes per 4-byte store.
+__device__ __forceinline__ uint32_t code4(const f32x4 v, float alpha, float r, bool fast,
+                                          const ProjParams& p) {
+    if (fast) {
+        uint32_t risky = 0;
+        const uint32_t c0 = esb_code_fast(v.x, r, p, risky);
+        const uint32_t c1 = esb_code_fast(v.y, r, p, risky);
+        const uint32_t c2 = esb_code_fast(v.z, r, p, risky);
+        const uint32_t c3 = esb_code_fast(v.w, r, p, risky);
+        if (!risky) return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
+    }
+    return esb_code(v.x, alpha, p) | (esb_code(v.y, alpha, p) << 8) |
+           (esb_code(v.z, alpha, p) << 16) | (esb_code(v.w, alpha, p) << 24);
+}
+
+
 // Fused post-processing of a contraction output (Sec. 4.2: the "BN and DN"
 // step of eq. (16) folded into a per-channel a x + b, then the "ESB
 // quantization" step), applied to the scaled output y0 = fl32(s fl32(acc)):
@@ -157,15 +211,14 @@ __device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t
         }
     }
     if (P.codes) {
-        const bool ok = alpha_valid(qa);
-        uint32_t q[4];
-#pragma unroll
-        for (int c = 0; c < 4; c++) q[c] = ok ? esb_code(z[c], qa, P.pp) : P.pp.zero_code;
+        const uint32_t q4 = alpha_valid(qa)
+                                ? code4(z, qa, 1.0f / qa, fast_scale(qa), P.pp)
+                                : P.pp.zero_code * 0x01010101u;
         if (((uintptr_t)(P.codes + o) & 3) == 0) {
-            *(uint32_t*)(P.codes + o) = q[0] | (q[1] << 8) | (q[2] << 16) | (q[3] << 24);
+            *(uint32_t*)(P.codes + o) = q4;
         } else {
 #pragma unroll
-            for (int c = 0; c < 4; c++) P.codes[o + c] = (uint8_t)q[c];
+            for (int c = 0; c < 4; c++) P.codes[o + c] = (uint8_t)(q4 >> (8 * c));
         }
     }
     uint32_t m = 0;

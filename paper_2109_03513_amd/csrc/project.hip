@@ -11,17 +11,8 @@
 // exponent minus 127 is the ESB exponent field and the kept fraction bits are
 // the ESB fraction field.
 //
-// Fast path (esb_code_fast): the IEEE division costs ~10 VALU operations per
-// element and makes the kernel ALU bound, so the quotient is approximated by
-// q0 = fl32(x * r), r = fl32(1 / alpha).  |q0 - x/alpha| <= 2^-23 |q0| < 2
-// ulp(q0), and fl32(x/alpha) is within another half ulp, so the two round to
-// the same set value unless q0 lies within 3 ulps of a cell midpoint
-// (midpoints sit at least 2^-(k+2) of a binade away from binade edges, so the
-// check is on the bits discarded by the rounding).  Below 1 the rounding to
-// the fixed step 2^-k is done on w = |q0| + 1 (one more half-ulp of error).
-// Elements within 4 ulps of a midpoint take the exact path; this happens with
-// probability ~2^(k-20) per element.  The fast path is used only for scales
-// with alpha and 1/alpha normal (alpha in [2^-125, 2^125]).
+// Fast path: esb_code_fast / code4 in the internal header (shared with the
+// fused contraction epilogue), the exact esb_code near cell midpoints.
 // HBM bound: 4 B read + 1 B written per element.
 #include "esb_internal.h"
 
@@ -36,48 +27,6 @@ ProjParams proj_params(const Fmt& f) {
     p.sign_bit = f.sign_bit;
     p.one = 1u << f.k;
     return p;
-}
-
-// Fast code of x given r = fl32(1/alpha); sets `risky` if q0 is within 4 ulps
-// of a midpoint (the caller then recomputes with esb_code).
-__device__ __forceinline__ uint32_t esb_code_fast(float x, float r, const ProjParams& p,
-                                                  uint32_t& risky) {
-    const float q0 = x * r;
-    const uint32_t qb = __float_as_uint(q0);
-    const uint32_t ab = qb & 0x7fffffffu;
-    const bool small = ab < 0x3f800000u;                       // |q0| < 1
-    const float w = small ? __uint_as_float(ab) + 1.0f : __uint_as_float(ab);
-    const uint32_t wb = __float_as_uint(w);
-    const uint32_t shA = 23u - p.k;
-    const uint32_t half = 1u << (shA - 1u);
-    const uint32_t c = ((wb + half) >> shA) - (127u << p.k);   // (e << k) | f, or m for small
-    const uint32_t d = wb & ((half << 1) - 1u);                  // discarded bits
-    risky |= (d - half + 4u) <= 8u;
-    // small: m = round((w - 1) * 2^k) in [0, 2^k]; zero + m wraps m == 2^k (the value 1) to 0
-    uint32_t code = small ? ((p.zero_code + c) & (p.sign_bit - 1u)) : c;
-    code = (ab >= p.c_bits) ? p.c_code : code;
-    code = (ab > 0x7f800000u) ? p.zero_code : code;
-    code |= (code != p.zero_code) ? ((qb >> 31) << (31u - __builtin_clz(p.sign_bit))) : 0u;
-    return code;
-}
-
-__device__ __forceinline__ bool fast_scale(float alpha) {
-    return alpha >= 0x1p-125f && alpha <= 0x1p125f;
-}
-
-// Vector path: 4 elements per 16-byte load, 4 codes per 4-byte store.
-__device__ __forceinline__ uint32_t code4(const f32x4 v, float alpha, float r, bool fast,
-                                          const ProjParams& p) {
-    if (fast) {
-        uint32_t risky = 0;
-        const uint32_t c0 = esb_code_fast(v.x, r, p, risky);
-        const uint32_t c1 = esb_code_fast(v.y, r, p, risky);
-        const uint32_t c2 = esb_code_fast(v.z, r, p, risky);
-        const uint32_t c3 = esb_code_fast(v.w, r, p, risky);
-        if (!risky) return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
-    }
-    return esb_code(v.x, alpha, p) | (esb_code(v.y, alpha, p) << 8) |
-           (esb_code(v.z, alpha, p) << 16) | (esb_code(v.w, alpha, p) << 24);
 }
 
 // One contiguous tile of kTile4 = 4 x 256 float4 (16 KB in, 4 KB out) per
