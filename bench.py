@@ -60,7 +60,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one MI355X "
-              "(multi-GPU sharding is not part of this build); use --gpus 1", file=sys.stderr)
+              "(libesb has no multi-GPU path); use --gpus 1", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
