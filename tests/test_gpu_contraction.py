@@ -116,6 +116,10 @@ CONV_CASES = [
     (2, 8, 8, 144, 24, 1, 1, 0, 1),        # 1x1 project
     (2, 10, 10, 144, 144, 3, 1, 1, 144),   # depthwise
     (1, 9, 7, 6, 6, 3, 2, 1, 6),           # depthwise, C % 4 != 0
+    (3, 13, 11, 48, 48, 3, 2, 1, 48),      # depthwise, 16 channels per thread, stride 2
+    (1, 12, 12, 64, 64, 1, 1, 0, 64),      # depthwise 1x1
+    (2, 9, 9, 16, 16, 5, 1, 2, 16),        # depthwise 5x5 (25 taps: four channels per thread)
+    (1, 6, 7, 20, 20, 3, 1, 1, 20),        # depthwise, C % 16 != 0
     (1, 8, 8, 32, 32, 3, 1, 1, 2),         # grouped, C/groups = 16
     (1, 7, 7, 12, 8, 3, 1, 1, 4),          # grouped, C/groups = 3
 ]
