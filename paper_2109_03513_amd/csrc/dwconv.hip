@@ -1,9 +1,11 @@
 // Depthwise convolution over ESB codes (groups == C == K, one filter per
 // channel), gfx950.  R*S multiply-adds per output: far below the MFMA ridge, so
-// this is a VALU kernel bound by HBM (codes in, int32 / fp32 out).  Each thread
-// produces four consecutive channels of one output pixel; decoded filter taps
-// live in LDS as int16, activation codes are decoded through a 256-entry LDS
-// table of exact integers.
+// these are VALU kernels (codes in, int32 / fp32 out); at MobileNet sizes the
+// byte extraction, table lookups and multiply-adds bound them, not HBM.
+// k_dwconv16: sixteen channels of one output pixel per thread (C % 16 == 0);
+// k_dwconv: four channels (C % 4 == 0) or one.  Decoded filter taps live in
+// LDS as int16, activation codes are decoded through a 256-entry LDS table of
+// exact integers.
 #include "esb_internal.h"
 
 namespace esb {
