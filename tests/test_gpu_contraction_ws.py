@@ -84,6 +84,8 @@ def test_gemm_ws_equals_plain_and_reuse(esb):
     (4, 15, 13, 128, 320, 3, 2, 1),        # stride 2, odd sizes, ragged N tile
     (2, 7, 7, 512, 512, 3, 1, 1),          # layer4 3x3
     (64, 56, 56, 64, 256, 3, 1, 1),        # 784 tiles of 256 x 256: the E2M3 path for ESB(5,2)
+    (64, 7, 7, 512, 512, 3, 1, 1),         # ResNet18 layer4 at batch 64 (100 tiles of 128 x 128)
+    (64, 14, 14, 256, 512, 3, 2, 1),       # layer4's first conv (stride 2)
     (4, 224, 224, 3, 64, 7, 2, 3),         # image stem, C = 3: byte-gathering kernel
     (3, 33, 31, 24, 40, 1, 1, 0),          # C = 24 (1x1)
     (2, 57, 61, 5, 16, 3, 2, 1),           # C = 5, ragged everything

@@ -146,6 +146,7 @@ CONV_CASES = [
     (2, 20, 20, 32, 32, 3, 3, 1, 1, 32, (5, 3), (5, 3), False, "all"),  # depthwise, 4 channels
     (1, 11, 13, 7, 7, 3, 3, 2, 1, 7, (4, 2), (4, 2), False, "all"),     # depthwise, scalar path
     (2, 64, 64, 3, 64, 7, 7, 2, 3, 1, (5, 3), (5, 3), True, "all"),     # C = 3 stem, workspace
+    (16, 7, 7, 512, 512, 3, 3, 1, 1, 1, (5, 3), (5, 3), True, "all"),   # long reduction, few tiles
 ]
 
 
