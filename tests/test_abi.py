@@ -219,3 +219,12 @@ def test_batch_refusals(L):
                           ProjectJob(0x1000, 10, None, 4, 2, 0x1000))
     assert L.esb_project_batch(2, pj, None) == -1
     assert L.esb_project_batch(0, None, None) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without libesb.so the binding raises instead of computing anything elsewhere."""
+    from paper_2109_03513_amd import esb
+    monkeypatch.setattr(esb, "_lib", None)
+    monkeypatch.setattr(esb, "LIB_PATH", str(tmp_path / "libesb.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        esb.lib()
