@@ -72,7 +72,7 @@ static int hip_status(hipError_t e) {
 
 extern "C" {
 
-int esb_version(void) { return 100; }
+int esb_version(void) { return 200; }   // 0.2.0: fused epilogue, packed codes, DN, batches
 
 const char* esb_strerror(int status) {
     switch (status) {
