@@ -322,6 +322,29 @@ def sweep(args):
                                                               stream=sh), args.reps, stream)
                 emit("dda_normal_n%d_k%d_G4096" % (n, ks), ms)
         del x, codes
+    if want("dda_batch"):
+        # quantizing every ResNet18 weight tensor (20 convolutions and the classifier,
+        # ESB(5,2), 64-point grids): one call per tensor against batches of 8 per launch
+        wts = workloads.resnet18_weights(0)
+        tens = [torch.from_numpy(np.ascontiguousarray(v)).to(dev).reshape(-1) for v in wts.values()]
+        fac = torch.from_numpy(workloads.scale_grid(1.0)).to(dev)
+        grids = [(t.abs().max() * fac / 3.0).contiguous() for t in tens]
+        outs = [(torch.empty(1, device=dev), torch.empty(64, dtype=torch.float64, device=dev))
+                for _ in tens]
+        single_ws = [torch.empty(esb.esb_dda_workspace_size(t.numel(), 5, 3, 64), dtype=torch.uint8,
+                                 device=dev) for t in tens]
+        jobs = esb.dda_jobs([(t, 5, 3, gr, a_, d_) for t, gr, (a_, d_) in zip(tens, grids, outs)])
+        wsb = torch.empty(esb.esb_dda_batch_workspace_size(jobs), dtype=torch.uint8, device=dev)
+        nel = float(sum(t.numel() for t in tens))
+
+        def singles():
+            for t, gr, (a_, d_), w_ in zip(tens, grids, outs, single_ws):
+                esb.esb_dda_align(t, 5, 3, gr, alpha_out=a_, D_out=d_, workspace=w_, stream=sh)
+
+        ms1 = time_launches(singles, args.reps, stream)
+        ms2 = time_launches(lambda: esb.esb_dda_align_batch(jobs, wsb, stream=sh), args.reps, stream)
+        emit("dda_resnet18_weights_21_tensors_one_call_each", ms1, nbytes=4.0 * nel)
+        emit("dda_resnet18_weights_21_tensors_batched", ms2, nbytes=4.0 * nel)
     if want("gemm"):
         for (M, N, K, fa, fb, name) in [(128, 4096, 9216, (3, 2), (3, 1), "alexnet_fc_b128"),
                                         (4096, 4096, 4096, (4, 2), (4, 2), "square_4096"),
