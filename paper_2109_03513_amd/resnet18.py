@@ -87,17 +87,24 @@ class ResNet18ESB:
                 k_sig, stride=(L["stride"],) * 2, pad=(L["pad"],) * 2))
         self.cws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
         self.amax = torch.zeros(32, dtype=torch.float32, device=dev)   # max |x| per layer input
-        # weights, quantized once
-        for name, L in self.layers.items():
-            w = torch.from_numpy(np.ascontiguousarray(weights[name])).to(dev)
-            L["alpha"], L["codes"] = self._quantize(w, self._ws_for(w))
-        wfc = torch.from_numpy(np.ascontiguousarray(weights["fc"])).to(dev)
-        self.fc_alpha, self.fc_codes = self._quantize(wfc, self._ws_for(wfc))
+        # weights, quantized once: every tensor's DDA and projection as one batch
+        names = list(self.layers) + ["fc"]
+        ws = [torch.from_numpy(np.ascontiguousarray(weights[nm])).to(dev) for nm in names]
+        grids = [self.grid(w) for w in ws]
+        alphas = [torch.empty(1, dtype=torch.float32, device=dev) for _ in ws]
+        codes = [torch.empty(w.shape, dtype=torch.uint8, device=dev) for w in ws]
+        jobs = esb.dda_jobs([(w, n, k_sig, g, a_, None) for w, g, a_ in zip(ws, grids, alphas)])
+        wsb = torch.empty(max(esb.esb_dda_batch_workspace_size(jobs), 1), dtype=torch.uint8,
+                          device=dev)
+        esb.esb_dda_align_batch(jobs, wsb, stream=self.sh)
+        esb.esb_project_batch(esb.project_jobs([(w, a_, n, k_sig, c) for w, a_, c in
+                                                zip(ws, alphas, codes)]), stream=self.sh)
+        for nm, a_, c in zip(names, alphas, codes):
+            if nm == "fc":
+                self.fc_alpha, self.fc_codes = a_, c
+            else:
+                self.layers[nm]["alpha"], self.layers[nm]["codes"] = a_, c
         torch.cuda.synchronize()
-
-    def _ws_for(self, t):
-        need = esb.esb_dda_workspace_size(t.numel(), self.n, self.ks, GRID_POINTS)
-        return self.torch.empty(max(need, 1), dtype=self.torch.uint8, device=t.device)
 
     def grid(self, x, xmax=None):
         """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product); xmax:
