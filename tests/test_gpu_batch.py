@@ -132,3 +132,34 @@ def test_dda_batch_grid_scale(esb):
     j, Do = oracle.dda(x, 5, 3, grid)
     assert_rel(host(D), Do, REL, "scaled grid")
     assert host(a)[0] == grid[j]
+
+
+def test_dda_batch_mixed_grid_scales(esb):
+    """Jobs with and without a device grid scale in one batch; a scale that makes every
+    candidate invalid (0, NaN) gives NaN objectives and alpha = the first candidate's value,
+    like a grid of such candidates in a single call."""
+    torch = torch_cuda()
+    r = np.random.default_rng(8)
+    xs = [(r.standard_normal(n) * 0.7).astype(np.float32) for n in (30000, 7001, 123457, 64)]
+    c = ((np.arange(32) + 1) / 32.0).astype(np.float32)
+    scales = [np.float32(np.max(np.abs(xs[0]))), None, np.float32(0.0), np.float32(np.nan)]
+    keep, rows = [], []
+    for x, sc in zip(xs, scales):
+        xd = dev(x)
+        cd = dev(c if sc is not None else (c * np.float32(2.5)).astype(np.float32))
+        sd = None if sc is None else dev(np.array([sc], dtype=np.float32))
+        a = torch.empty(1, dtype=torch.float32, device="cuda")
+        D = torch.empty(32, dtype=torch.float64, device="cuda")
+        keep.append((xd, cd, sd, a, D))
+        rows.append((xd, 4, 2, cd, a, D, sd))
+    jobs = esb.dda_jobs(rows)
+    ws = torch.empty(esb.esb_dda_batch_workspace_size(jobs), dtype=torch.uint8, device="cuda")
+    esb.esb_dda_align_batch(jobs, ws)
+    for (x, sc), (_, _, _, a, D) in zip(zip(xs, scales), keep):
+        grid = (c if sc is not None else (c * np.float32(2.5))).astype(np.float32)
+        if sc is not None:
+            grid = (np.float32(sc) * grid).astype(np.float32)
+        j, Do = oracle.dda(x, 4, 2, grid)
+        assert_rel(host(D), Do, REL, "mixed scales")
+        # alpha is the chosen candidate's value: grid[0] (0 or NaN) when every one is invalid
+        np.testing.assert_array_equal(host(a)[:1], grid[j:j + 1])
