@@ -173,3 +173,22 @@ def test_dda_normal_invalid_candidates(esb):
     assert host(alpha)[0] == want
     alpha, D = esb.esb_dda_normal(4, 2, dev(np.array([np.nan, -2.0], dtype=np.float32)))
     assert np.isnan(host(D)).all() and np.isnan(host(alpha)[0])
+
+
+@pytest.mark.parametrize("length", [1, 1000, 300001])
+def test_dn_unaligned(esb, length):
+    """Statistics and normalized projection on an x that starts 4 bytes past a 16-byte
+    boundary (the scalar-load kernels) and codes at an odd address."""
+    torch = pytest.importorskip("torch")
+    r = np.random.default_rng([31, length])
+    x = (r.standard_normal(length) * 0.4 - 0.03).astype(np.float32)
+    log("dn unaligned len=%d" % length)
+    xd = dev(np.concatenate([[np.float32(7)], x]))[1:]
+    assert xd.data_ptr() % 16 != 0
+    st = esb.esb_dn_stats(xd)
+    got = host(st)
+    m, s = oracle.dn_stats(x)
+    assert ulps(got[0], np.float32(m)) <= 1 and ulps(got[1], np.float32(s)) <= 1
+    codes = torch.empty(length + 1, dtype=torch.uint8, device="cuda")[1:]
+    esb.esb_project_dn(xd, st, scalar(0.9), 4, 2, codes=codes)
+    np.testing.assert_array_equal(host(codes), oracle.project_dn(x, got[0], got[1], 0.9, 4, 2))
