@@ -41,7 +41,8 @@ SHAPES = [(1, 1, 1), (7, 5, 33), (16, 16, 64), (64, 64, 576), (65, 63, 130), (12
 
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("fmt", [((4, 2), (4, 2)), ((3, 2), (3, 1)), ((5, 3), (5, 3)),
-                                 ((2, 1), (8, 7)), ((7, 5), (6, 4))])
+                                 ((2, 1), (8, 7)), ((7, 5), (6, 4)), ((4, 1), (4, 1)),
+                                 ((4, 1), (5, 3))])
 def test_gemm_int8_path(esb, shape, fmt):
     gemm_case(esb, *shape, *fmt)
 

@@ -84,13 +84,15 @@ def test_gemm_ws_equals_plain_and_reuse(esb):
     (4, 15, 13, 128, 320, 3, 2, 1),        # stride 2, odd sizes, ragged N tile
     (2, 7, 7, 512, 512, 3, 1, 1),          # layer4 3x3
     (64, 56, 56, 64, 256, 3, 1, 1),        # 784 tiles of 256 x 256: the E2M3 path for ESB(5,2)
-    (64, 7, 7, 512, 512, 3, 1, 1),         # ResNet18 layer4 at batch 64 (100 tiles of 128 x 128)
+    (64, 7, 7, 512, 512, 3, 1, 1),         # ResNet18 layer4 at batch 64 (100 tiles of 128 x 128
+                                           # are under half the CUs: 64 x 64 tiles)
     (64, 14, 14, 256, 512, 3, 2, 1),       # layer4's first conv (stride 2)
     (4, 224, 224, 3, 64, 7, 2, 3),         # image stem, C = 3: byte-gathering kernel
     (3, 33, 31, 24, 40, 1, 1, 0),          # C = 24 (1x1)
     (2, 57, 61, 5, 16, 3, 2, 1),           # C = 5, ragged everything
 ])
-@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1))])
+@pytest.mark.parametrize("fmt", [((5, 3), (5, 3)), ((4, 2), (4, 2)), ((3, 2), (3, 1)),
+                                 ((4, 1), (4, 1))])
 def test_conv_ws_parity(esb, case, fmt):
     Nb, H, W, C, K, R, st, pd = case
     (bX, ksX), (bW, ksW) = fmt
@@ -173,3 +175,66 @@ def test_gemm_ws_e2m3_spread_at_accumulator_bound(esb):
     assert st == 0
     np.testing.assert_array_equal(host(acc)[rows], oacc)
     assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+# The E4M3 (fp8) path at the edge of what the dispatcher admits for it: every product
+# m_A * m_B at most 2^12 and K * max|m_A| * max|m_B| below 2^24.  ESB(4,0) (n = 4,
+# k_sig = 1, Table 1's 4-bit power-of-two row) reaches the product bound exactly
+# (m up to 64, p = 4096); ESB(6,3) (k_sig = 4) gives p = 60 * 60 = 3600.  Codes take the
+# largest and the smallest nonzero magnitude at random, with random signs, so every
+# 64-long slice of the reduction mixes products 2^12 apart, and K sits just below
+# 2^24 / p.
+FP8_EDGE = [
+    # fmt, K of the GEMM (K % 16 == 0), conv (C, R) with R * R * C just below 2^24 / p
+    ((4, 1), 4080, (448, 3)),
+    ((6, 4), 4656, (512, 3)),
+]
+
+
+@pytest.mark.parametrize("fmt,K,convRC", FP8_EDGE)
+@pytest.mark.parametrize("use_ws", [False, True])
+def test_gemm_fp8_path_at_admission_bound(esb, fmt, K, convRC, use_ws):
+    b, ks = fmt
+    M, N = 640, 576
+    MA = oracle.C(b, ks) * 2 ** (ks - 1)
+    assert K * MA * MA < 2 ** 24 <= (K + 16) * MA * MA   # the largest K % 16 == 0 admitted
+    A = extreme_codes(b, ks, (M, K), 11)
+    B = extreme_codes(b, ks, (N, K), 12)
+    ws = None
+    if use_ws:
+        need = esb.esb_gemm_workspace_size(M, N, K, b, ks, b, ks)
+        assert need > 0
+        ws = workspace(need)
+    log("gemm fp8 edge fmt=%s M=%d N=%d K=%d ws=%s" % (fmt, M, N, K, use_ws))
+    acc, y = esb.esb_gemm(dev(A), b, ks, scalar(0.37), dev(B), b, ks, scalar(0.021), workspace=ws)
+    rows = np.array([0, 1, 129, 300, M - 1], dtype=np.int64)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, b, ks, 0.37, b, ks, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+
+
+@pytest.mark.parametrize("fmt,K,convRC", FP8_EDGE)
+@pytest.mark.parametrize("use_ws", [False, True])
+def test_conv_fp8_path_at_admission_bound(esb, fmt, K, convRC, use_ws):
+    b, ks = fmt
+    C, R = convRC
+    Nb, H, W, Kout = 4, 14, 14, 256
+    x = extreme_codes(b, ks, (Nb, H, W, C), 13)
+    w = extreme_codes(b, ks, (Kout, R, R, C), 14)
+    ws = None
+    if use_ws:
+        need = esb.esb_conv2d_workspace_size(x.shape, w.shape, b, ks, b, ks, stride=(1, 1),
+                                             pad=(1, 1))
+        assert need > 0
+        ws = workspace(need)
+    log("conv fp8 edge fmt=%s x=%s w=%s ws=%s" % (fmt, x.shape, w.shape, use_ws))
+    acc, y = esb.esb_conv2d(dev(x), b, ks, scalar(0.5), dev(w), b, ks, scalar(0.03), stride=(1, 1),
+                            pad=(1, 1), workspace=ws)
+    acc, y = host(acc), host(y)
+    for img in (0, Nb - 1):
+        s, oacc, oy = oracle.conv2d(np.ascontiguousarray(x[img:img + 1]), w, b, ks, 0.5, b, ks, 0.03,
+                                    stride=(1, 1), pad=(1, 1))
+        assert s == 0
+        np.testing.assert_array_equal(acc[img:img + 1], oacc)
+        assert_rel(y[img:img + 1], oy, YREL, "y")

@@ -43,12 +43,13 @@ def maxpool_np(a):   # 3x3, stride 2, pad 1, NHWC
 
 
 @pytest.mark.parametrize("batch", [2])
-def test_resnet18_stack_matches_oracle(batch):
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_resnet18_stack_matches_oracle(batch, seed):
     import torch
     from paper_2109_03513_amd import resnet18
     weights = wl.resnet18_weights(0)
-    x = wl.resnet18_input(0, batch)
-    log("resnet18 stack batch=%d: GPU forward" % batch)
+    x = wl.resnet18_input(seed, batch)
+    log("resnet18 stack batch=%d seed=%d: GPU forward" % (batch, seed))
     model = resnet18.ResNet18ESB(weights, batch, record=True)
     logits = host(model.forward(torch.from_numpy(x).cuda()))
     cmax = resnet18.value_max(N, KS)
