@@ -9,7 +9,8 @@
  * a hipStream_t passed as void* (NULL = the null stream).  All device work is
  * enqueued asynchronously on `stream`; functions return once it is enqueued.
  * The caller owns every buffer; the library allocates no device memory.
- * Functions are stateless and thread-safe.
+ * Calls keep no state between them and may be made from several host
+ * threads; calls that share a workspace must not overlap.
  *
  * Errors: every call returns an int status.  Arguments are validated on the
  * host before any launch; on error nothing is enqueued.  ESB_E_HIP means a HIP

@@ -36,6 +36,8 @@
 //   S2 + a (a B_j - 2 A_j), argmin with ties to the lowest index.
 // Per-atom sums are exact integers; fp64 sums run in a fixed order: the result
 // is deterministic.  Wave-level scans and reductions use DPP lane moves.
+#include <atomic>
+
 #include "esb_internal.h"
 
 namespace esb {
@@ -859,13 +861,15 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
 
 static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, int nhist, int ngroups,
                               hipStream_t s) {
-    static bool lds_attr_set[64] = {false};
+    // set once per device; racing threads set the same attribute
+    static std::atomic<bool> lds_attr_set[64];
     int dev = 0;
-    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 && !lds_attr_set[dev]) {
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 &&
+        !lds_attr_set[dev].load(std::memory_order_acquire)) {
         hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 156 * 1024);
         if (e != hipSuccess) return e;
-        lds_attr_set[dev] = true;
+        lds_attr_set[dev].store(true, std::memory_order_release);
     }
     k_dda_hist<<<nhist, kHistThreads, max_lds, s>>>(B);
     if (ngroups > 0) k_dda_group<<<ngroups, 256, 0, s>>>(B);

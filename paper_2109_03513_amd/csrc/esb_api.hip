@@ -3,6 +3,7 @@
 #include <string.h>
 
 #include "../../include/esb.h"
+#include <atomic>
 #include <vector>
 
 #include "esb_internal.h"
@@ -46,16 +47,16 @@ int decode_int(const Fmt& f, uint32_t code) {
 }
 
 int num_cus() {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64];   // zero-initialized (static storage)
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int v = 0;
+    int v = cached[dev].load(std::memory_order_relaxed);
+    if (!v) {   // racing threads store the same value
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
             v = 256;
-        cached[dev] = v;
+        cached[dev].store(v, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return v;
 }
 
 }  // namespace esb
