@@ -8,9 +8,11 @@
  * on the current device; "host" pointers are ordinary CPU memory.  `stream` is
  * a hipStream_t passed as void* (NULL = the null stream).  All device work is
  * enqueued asynchronously on `stream`; functions return once it is enqueued.
- * The caller owns every buffer; the library allocates no device memory.
- * Calls keep no state between them and may be made from several host
- * threads; calls that share a workspace must not overlap.
+ * The caller owns every buffer; the library allocates no device memory (it
+ * holds one static scratch array per GPU for esb_dda_align_noalloc).  Calls
+ * keep no state between them and may be made from several host threads;
+ * calls that share a workspace (or, for esb_dda_align_noalloc, a GPU) must not
+ * overlap.
  *
  * Errors: every call returns an int status.  Arguments are validated on the
  * host before any launch; on error nothing is enqueued.  ESB_E_HIP means a HIP
@@ -47,6 +49,7 @@ extern "C" {
                                   or a format / length outside the packed 4-bit storage */
 #define ESB_E_HIP (-5)         /* HIP launch / runtime failure, see esb_last_hip_error() */
 #define ESB_E_WORKSPACE (-6)   /* workspace NULL or smaller than its *_workspace_size() */
+#define ESB_E_SCRATCH (-7)     /* input larger than the static scratch of a *_noalloc call */
 
 #define ESB_B_NK 0 /* B stored N x K, row-major (K contiguous) */
 #define ESB_B_KN 1 /* B stored K x N, row-major (N contiguous) */
@@ -203,6 +206,27 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
                     const float* alphaA, const uint8_t* B_packed, int nB, int kB_sig,
                     const float* alphaB, int32_t* acc, float* y, int64_t ldc, void* workspace,
                     size_t ws_bytes, void* stream);
+
+/*
+ * esb_dda_align for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, search and results as esb_dda_align (alpha and D
+ * bit-identical), without a workspace: the call's scratch (the per-block
+ * partial objectives) lives in a static device array of
+ * ESB_DDA_NOALLOC_SCRATCH bytes that the library holds on every GPU it runs
+ * on until the process ends; the call itself allocates nothing.
+ *   Limit: esb_dda_workspace_size(len, n, k_sig, G) <= ESB_DDA_NOALLOC_SCRATCH
+ *   (with G = 64 about 2^31 elements), else ESB_E_SCRATCH before any launch.
+ *   Sharing: every call on one GPU uses that GPU's one array, so calls that
+ *   overlap on a GPU (several streams or host threads) race; serialize them
+ *   on one stream.  Nothing carries over from one call to the next.
+ *   The first call on each device looks up that device's array address
+ *   (hipGetSymbolAddress, with the device current); a failure returns
+ *   ESB_E_HIP.
+ */
+#define ESB_DDA_NOALLOC_SCRATCH ((size_t)4 << 20)
+int esb_dda_align_noalloc(const float* x, int64_t len, int n, int k_sig, const float* grid, int G,
+                          float* alpha_out, double* D_out, void* stream);
 
 /*
  * Batches of independent problems in one launch of each kernel: the DDA or the

@@ -4,6 +4,7 @@
 
 #include "../../include/esb.h"
 #include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "esb_internal.h"
@@ -71,6 +72,36 @@ static int hip_status(hipError_t e) {
     return ESB_E_HIP;
 }
 
+// Scratch of the entry point that allocates nothing (esb_dda_align_noalloc):
+// one array per GPU, held until the process ends.  In host code `scratch` only
+// names the symbol; its device address comes from hipGetSymbolAddress, looked
+// up once per device with that device current.
+constexpr size_t kScratchBytes = ESB_DDA_NOALLOC_SCRATCH;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static std::atomic<void*> g_scratch_ptr[64];
+
+static hipError_t scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (!p) return hipErrorInvalidSymbol;
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return hipSuccess;
+}
+
 extern "C" {
 
 int esb_version(void) { return 200; }   // 0.2.0: fused epilogue, packed codes, DN, batches
@@ -83,6 +114,7 @@ const char* esb_strerror(int status) {
         case ESB_E_UNSUPPORTED: return "decoded integers exceed the split int8 range";
         case ESB_E_HIP: return "HIP runtime error";
         case ESB_E_WORKSPACE: return "workspace missing or too small";
+        case ESB_E_SCRATCH: return "input needs more scratch than the static device buffer holds";
         default: return "unknown status";
     }
 }
@@ -140,6 +172,20 @@ int esb_dda_align(const float* x, int64_t len, int n, int k_sig, const float* gr
     if (!dda_layout(len, f, G, &L)) return ESB_E_INVALID;
     if (!workspace || ws_bytes < L.total) return ESB_E_WORKSPACE;
     return hip_status(launch_dda(x, len, f, grid, G, alpha_out, D_out, workspace, L, (hipStream_t)stream));
+}
+
+int esb_dda_align_noalloc(const float* x, int64_t len, int n, int k_sig, const float* grid, int G,
+                          float* alpha_out, double* D_out, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !grid || !alpha_out) return ESB_E_INVALID;
+    if (len > 0 && !x) return ESB_E_INVALID;
+    const Fmt f = make_fmt(n, k_sig);
+    DdaLayout L;
+    if (!dda_layout(len, f, G, &L)) return ESB_E_INVALID;
+    if (L.total > kScratchBytes) return ESB_E_SCRATCH;
+    void* ws = nullptr;
+    const hipError_t e = scratch_address(&ws);
+    if (e != hipSuccess) return hip_status(e);
+    return hip_status(launch_dda(x, len, f, grid, G, alpha_out, D_out, ws, L, (hipStream_t)stream));
 }
 
 size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs) {

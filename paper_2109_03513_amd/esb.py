@@ -19,6 +19,8 @@ ESB_E_OVERFLOW = -3
 ESB_E_UNSUPPORTED = -4
 ESB_E_HIP = -5
 ESB_E_WORKSPACE = -6
+ESB_E_SCRATCH = -7
+ESB_DDA_NOALLOC_SCRATCH = 4 << 20
 ESB_B_NK = 0
 ESB_B_KN = 1
 
@@ -79,6 +81,7 @@ def lib():
             "esb_dequantize": (i32, [P, i64, P, i32, i32, P, P]),
             "esb_dda_workspace_size": (sz, [i64, i32, i32, i32]),
             "esb_dda_align": (i32, [P, i64, i32, i32, P, i32, P, P, P, sz, P]),
+            "esb_dda_align_noalloc": (i32, [P, i64, i32, i32, P, i32, P, P, P]),
             "esb_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32, P, P,
                                i64, P]),
             "esb_conv2d": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
@@ -203,6 +206,21 @@ def esb_dda_align(x, n, k_sig, grid, alpha_out=None, D_out=None, workspace=None,
                                                 _ptr(alpha_out), _ptr(D_out), _ptr(workspace),
                                                 workspace.numel() * workspace.element_size(),
                                                 _stream(stream)))
+    return alpha_out, D_out
+
+
+def esb_dda_align_noalloc(x, n, k_sig, grid, alpha_out, D_out=None, stream=None):
+    """esb_dda_align with the library's static scratch (no workspace); alpha_out (and D_out,
+    if given) are preallocated device tensors, so that the call allocates nothing."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(grid, torch.float32, "grid")
+    _dev_tensor(alpha_out, torch.float32, "alpha_out")
+    if D_out is not None:
+        _dev_tensor(D_out, torch.float64, "D_out")
+    _check("esb_dda_align_noalloc", lib().esb_dda_align_noalloc(
+        _ptr(x), x.numel(), n, k_sig, _ptr(grid), grid.numel(), _ptr(alpha_out), _ptr(D_out),
+        _stream(stream)))
     return alpha_out, D_out
 
 

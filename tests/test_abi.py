@@ -74,6 +74,15 @@ def test_argument_validation_without_launch(L):
     assert L.esb_dda_align(fake, 100, 4, 2, fake, 64, fake, None, fake, need - 1, None) == -6
     assert L.esb_dda_workspace_size(100, 4, 2, 0) == 0
     assert L.esb_dda_workspace_size(100, 8, 7, 65) == 0
+    # DDA with the static scratch: the same checks, and inputs beyond the scratch refused
+    na = L.esb_dda_align_noalloc
+    assert na(fake, 100, 8, 7, fake, 65, fake, None, None) == -1
+    assert na(fake, 100, 4, 2, None, 64, fake, None, None) == -1
+    assert na(None, 100, 4, 2, fake, 64, fake, None, None) == -1
+    big = 1 << 33
+    assert L.esb_dda_workspace_size(big, 4, 2, 64) > (4 << 20)
+    assert na(fake, big, 4, 2, fake, 64, fake, None, None) == -7
+    assert L.esb_strerror(-7) != L.esb_strerror(-99)
     # GEMM contract: unsupported magnitudes, overflow, bad pitches, no output
     g = L.esb_gemm
     assert g(4, 4, 8, fake, 8, 6, 2, fake, fake, 8, 6, 2, fake, 0, fake, None, 4, None) == -4
