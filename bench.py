@@ -1,15 +1,22 @@
 """Benchmark of the ESB hot path on one MI355X.
 
-One step = the whole hot path over one batch of the ResNet18-shaped 3x3
-convolution workload (64->64 channels, 56x56, stride 1, pad 1, batch 1,
-ESB n=4 / k_sig=2 for weights and activations):
-    DDA scale search (64 candidates) on the weights and on the activations,
-    projection of both to ESB codes, implicit-GEMM convolution over the codes
-    to scaled fp32 outputs.
+Default: the largest single-GPU workload, the ResNet18 stack at batch 64 with
+every convolution and the classifier quantized to ESB n=5 / k_sig=3 (the
+paper's ESB(5,2)), the input of every layer scaled by the DDA search over 64
+candidates on the device, projected to codes and contracted with the
+pre-quantized weights (one step = one forward pass over 64 synthetic
+224x224x3 images, replayed as a HIP graph).  `value` is the contraction's
+integer operations (2*M*N*K over all 21 layers, 232.2 G per forward) per
+second over the whole forward, in TOPS; images/s is in `detail`.
+`roofline` is that of the launch group with the largest share of the forward
+(each library call of one forward timed alone with HIP events).
+
+--conv3x3: the ResNet18-shaped 3x3 convolution at batch 1 (64->64, 56x56,
+ESB n=4 / k_sig=2): DDA of weights and activations, their projection and the
+convolution per step.  --sweep: every kernel at the large layer shapes.
 Inputs are synthetic, seeded and resident in HBM before timing starts.
 
-Prints ONE JSON line.  `value` is the convolution's integer operations
-(2*M*N*K) per second over the whole step, in TOPS.
+Prints ONE JSON line.
 """
 import argparse
 import json
@@ -27,8 +34,8 @@ INT8_PEAK_TOPS = 5000.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="approximate CPU time budget of the oracle baseline")
@@ -40,6 +47,10 @@ def parse():
     p.add_argument("--resnet18", action="store_true",
                    help="ResNet18 forward at batch 64 (ESB(5,2) everywhere): images/s and per-layer "
                         "times (one JSON line per layer, then a summary line)")
+    p.add_argument("--conv3x3", action="store_true",
+                   help="the ResNet18-shaped 3x3 convolution at batch 1 (DDA, projection, conv)")
+    p.add_argument("--cpu-images", type=int, default=32,
+                   help="images of the oracle's forward for the CPU baseline")
     p.add_argument("--batch", type=int, default=64)
     p.add_argument("--reps", type=int, default=20)
     return p.parse_args()
@@ -74,7 +85,17 @@ def main():
     if args.resnet18:
         resnet18_bench(args)
         return
+    if args.conv3x3:
+        print(json.dumps(conv3x3_step(args)), flush=True)
+        return
+    resnet18_headline(args)
 
+
+def conv3x3_step(args, with_cpu=True):
+    """The ResNet18-shaped 3x3 convolution at batch 1: one step = DDA(w), DDA(x),
+    project(w), project(x), conv2d.  Returns the JSON record."""
+    import numpy as np
+    import torch
     from paper_2109_03513_amd import esb, workloads
 
     torch.cuda.set_device(0)
@@ -200,7 +221,7 @@ def main():
     }
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if with_cpu and not args.no_cpu_baseline:
         cpu = cpu_baseline(c, ops, args.cpu_seconds)
 
     rec = {
@@ -213,7 +234,7 @@ def main():
                            "DDAs and the two projections each share one launch group"},
         "roofline": roof, "cpu_baseline": cpu, "detail": extra,
     }
-    print(json.dumps(rec), flush=True)
+    return rec
 
 
 def measured_traffic(key):
@@ -542,6 +563,245 @@ def resnet18_bench(args):
                       "graph_ms": None if fused_graph_ms is None else round(fused_graph_ms, 4),
                       "graph_replays_match_eager": fused_graph_ok,
                       "logits_equal_dda_forward": fused_equal, "data": "synthetic"}), flush=True)
+
+
+FP8_PEAK_TOPS = 5000.0      # dense E4M3 and int8 MFMA: the same 5.0 P(FL)OP/s
+
+
+def resnet18_ops(batch):
+    """Integer operations (2*M*N*K) of the ResNet18 contractions for one forward."""
+    from paper_2109_03513_amd import esb, resnet18, workloads
+    ops = 2.0 * batch * 1000 * 512
+    for name, cin, cout, k, st, pd in workloads.RESNET18_CONVS:
+        side = resnet18.input_side(name)
+        P, Q = esb.conv_out_hw(side, side, k, k, (st, st), (pd, pd))
+        ops += 2.0 * batch * P * Q * cout * k * k * cin
+    return ops
+
+
+# Which contractions share a kernel instance: layers of one geometry (input side, channels,
+# window, stride) get the same tiles from the dispatcher.
+def contraction_group(label):
+    from paper_2109_03513_amd import resnet18, workloads
+    if label == "fc":
+        return "fc 512->1000"
+    for name, cin, cout, k, st, pd in workloads.RESNET18_CONVS:
+        if name == label:
+            side = resnet18.input_side(name)
+            return "conv %dx%d/%d %d->%d at %dx%d" % (k, k, st, cin, cout, side, side)
+    return label
+
+
+def resnet18_headline(args):
+    """The largest single-GPU workload: ResNet18 at batch 64, per-layer DDA on the device."""
+    import numpy as np
+    import torch
+    from paper_2109_03513_amd import resnet18, workloads
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()      # default priority
+    B = args.batch
+    ops = resnet18_ops(B)
+    weights = workloads.resnet18_weights(0)
+    x = torch.from_numpy(workloads.resnet18_input(0, B)).cuda()
+    with torch.cuda.stream(stream):
+        model = resnet18.ResNet18ESB(weights, B, stream=stream)
+        ref = None
+        for _ in range(max(args.warmup, 1)):
+            ref = model.forward(x)
+        stream.synchronize()
+        ref = ref.clone()
+        # one forward per HIP graph, used only if every replay equals the eager logits
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            out = model.forward(x)
+        graph_ok = True
+        for _ in range(3):
+            g.replay()
+            stream.synchronize()
+            graph_ok = graph_ok and bool(torch.equal(out, ref))
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            if graph_ok:
+                g.replay()
+            else:
+                model.forward(x)
+        e1.record(stream)
+        e1.synchronize()
+        wall = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        ms_per_step = max(e0.elapsed_time(e1), 1e3 * wall) / args.steps
+        del g
+        # every library call of the forward timed in place: events around each call of an
+        # eager forward, queued behind a spin kernel so that the host runs ahead and the
+        # calls execute back to back as in a graph replay; the median of three forwards
+        runs = []
+        for _ in range(3):
+            units = []
+            torch.cuda._sleep(50_000_000)        # ~20 ms of spinning on this stream
+            model.forward(x, units=units)
+            stream.synchronize()
+            runs.append([u["events"][0].elapsed_time(u["events"][1]) for u in units])
+        for i, u in enumerate(units):
+            u["ms"] = float(np.median([r[i] for r in runs]))
+        # the fixed-scale inference flow (fused epilogues), eager, for the detail
+        model.forward_fused(x)
+        stream.synchronize()
+        f0 = torch.cuda.Event(enable_timing=True)
+        f1 = torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for _ in range(5):
+            model.forward_fused(x)
+        f1.record(stream)
+        f1.synchronize()
+        fused_ms = f0.elapsed_time(f1) / 5
+
+    groups = {}
+    for u in units:
+        key = contraction_group(u["label"]) if u["kind"] == "contraction" else u["kind"]
+        gr = groups.setdefault(key, dict(kind=u["kind"], ms=0.0, bytes=0.0, ops=0.0, calls=0,
+                                         layers=[]))
+        gr["ms"] += u["ms"]
+        gr["bytes"] += u["bytes"]
+        gr["ops"] += u["ops"]
+        gr["calls"] += 1
+        gr["layers"].append(u["label"])
+    units_ms = sum(gr["ms"] for gr in groups.values())
+    kernels = {
+        "dda": "esb_dda_align_batch per layer input: k_dda_hist (+ k_dda_group) + k_dda_finalize",
+        "project": "esb_project per layer input: k_project_vec",
+        "absmax": "esb_absmax: k_absmax",
+        "maxpool": "esb_maxpool2d: k_maxpool",
+        "avgpool": "esb_avgpool_global: k_avgpool",
+    }
+    dom_key = max(groups, key=lambda k: groups[k]["ms"])
+    dom = groups[dom_key]
+    per_launch_ms = dom["ms"] / dom["calls"]
+    if dom["kind"] == "contraction":
+        ai = dom["ops"] / dom["bytes"]
+        bound = "mfma" if ai >= FP8_PEAK_TOPS / (HBM_PEAK_GBS / 1e3) else "hbm"
+        label = "%s contraction (%s)" % (dom_key, ", ".join(dom["layers"]))
+    else:
+        bound = "hbm"
+        label = kernels.get(dom["kind"], dom["kind"])
+    if bound == "mfma":
+        achieved = dom["ops"] / (dom["ms"] * 1e-3) / 1e12
+        roof = {"kernel": label, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": FP8_PEAK_TOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TOPS, 5)}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = {"kernel": label, "bound": "hbm", "achieved": round(achieved, 2),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5)}
+    roof.update(traffic=measured_traffic("resnet18_b64:" + dom_key),
+                algorithmic_bytes_per_launch=round(dom["bytes"] / dom["calls"]),
+                ops_per_launch=round(dom["ops"] / dom["calls"]),
+                launches_per_forward=dom["calls"], launch_us=round(per_launch_ms * 1e3, 3),
+                share_of_forward=round(dom["ms"] / units_ms, 4))
+    table = []
+    for k, gr in sorted(groups.items(), key=lambda kv: -kv[1]["ms"]):
+        row = {"group": k, "calls": gr["calls"], "us": round(gr["ms"] * 1e3, 1),
+               "share": round(gr["ms"] / units_ms, 4)}
+        if gr["ops"]:
+            row["tops"] = round(gr["ops"] / (gr["ms"] * 1e-3) / 1e12, 1)
+        row["gbps"] = round(gr["bytes"] / (gr["ms"] * 1e-3) / 1e9, 1)
+        table.append(row)
+
+    value = ops / (ms_per_step * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = resnet18_cpu_baseline(weights, args.cpu_images, resnet18_ops(1))
+    step2 = conv3x3_step(argparse.Namespace(steps=10, warmup=2, no_cpu_baseline=True,
+                                            cpu_seconds=0.0), with_cpu=False)
+    rec = {
+        "metric": "ESB GEMM/conv int TOPS (% of int8 MFMA peak) + projection GB/s (% HBM)",
+        "value": round(value, 3), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp8(e4m3)+int8",
+        "data": "synthetic",
+        "config": {"workload": "resnet18_b%d_224x224_esb5k3_all_layers_dda64" % B,
+                   "batch": B, "note": "one step = one forward: per layer max|x|, DDA over 64 "
+                                       "candidates, projection, contraction (+ ReLU / residual "
+                                       "epilogues, max pool, average pool); value = contraction "
+                                       "ops of the forward per second"},
+        "roofline": roof, "cpu_baseline": cpu,
+        "detail": {
+            "images_per_s": round(B / (ms_per_step * 1e-3), 1),
+            "gop_per_forward": round(ops / 1e9, 2),
+            "frac_int8_peak_over_forward": round(value / INT8_PEAK_TOPS, 4),
+            "timing": "one forward per HIP graph replay (replays equal the eager logits: %s); "
+                      "groups: every library call timed in place by events around it in eager "
+                      "forwards queued behind a spin kernel (median of 3)" % graph_ok,
+            "units_sum_ms": round(units_ms, 4),
+            "groups": table,
+            "mfma_types": "E4M3 (fp8) MFMA on every contraction but conv1 (C = 3: int8 MFMA on "
+                          "the byte-gathering kernel); fp32 accumulation exact (integers < 2^24)",
+            "fixed_scale_inference_images_per_s": round(B / (fused_ms * 1e-3), 1),
+            "resnet18_conv3x3_b1_step": {k: step2[k] for k in ("value", "unit", "ms_per_step")},
+        },
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def resnet18_cpu_baseline(weights, images, ops_per_image):
+    """The oracle's forward over the first `images` images of the same batch (per-layer DDA
+    over those images' tensors, the glue in NumPy), on the host cores."""
+    import numpy as np
+    import oracle
+    from paper_2109_03513_amd import workloads as wl
+    N, KS = 5, 3
+    cmax = float(oracle.valueset(N, KS)[-1])
+    fac = wl.maxabs_grid_factors(cmax)
+
+    def quant(a):
+        g = (np.float32(np.max(np.abs(a))) * fac).astype(np.float32)
+        j, _ = oracle.dda(a, N, KS, g)
+        return g[j], oracle.project(a, g[j], N, KS)
+
+    wq = {k: quant(v) for k, v in weights.items()}      # weights: quantized once, untimed
+    geo = {n: (st, pd) for n, _, _, _, st, pd in wl.RESNET18_CONVS}
+    x = wl.resnet18_input(0, 64)[:images]
+
+    def conv(name, a):
+        al, c = quant(a)
+        st, _, y = oracle.conv2d(c, wq[name][1], N, KS, al, N, KS, wq[name][0],
+                                 stride=(geo[name][0],) * 2, pad=(geo[name][1],) * 2,
+                                 want_acc=False)
+        return y
+
+    def relu(v):
+        return np.maximum(v, 0.0).astype(np.float32)
+
+    t0 = time.perf_counter()
+    a = relu(conv("conv1", x))
+    Bn, H, W, C = a.shape
+    P = (H + 2 - 3) // 2 + 1
+    pad = np.full((Bn, H + 2, W + 2, C), -np.inf, dtype=np.float32)
+    pad[:, 1:-1, 1:-1] = a
+    pooled = np.full((Bn, P, P, C), -np.inf, dtype=np.float32)
+    for r in range(3):
+        for s_ in range(3):
+            pooled = np.maximum(pooled, pad[:, r:r + 2 * P:2, s_:s_ + 2 * P:2])
+    a = pooled
+    for stage in (1, 2, 3, 4):
+        for blk in (0, 1):
+            p = "l%d.%d." % (stage, blk)
+            out = relu(conv(p + "c1", a))
+            sc = conv(p + "ds", a) if (p + "ds") in geo else a
+            a = relu(conv(p + "c2", out) + sc)
+    flat = a.reshape(a.shape[0], -1, a.shape[3]).astype(np.float64)
+    feat = (flat.sum(axis=1) / flat.shape[1]).astype(np.float32)
+    al, c = quant(feat)
+    oracle.gemm(c, wq["fc"][1], N, KS, al, N, KS, wq["fc"][0], want_acc=False)
+    el = time.perf_counter() - t0
+    return {"value": round(images * ops_per_image / el / 1e12, 6), "unit": "TOPS",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "the oracle's forward over the first %d of the 64 images (per-layer DDA "
+                      "over those images, glue in NumPy): %.2f s, %.3f s per image; the rate "
+                      "per image is the figure" % (images, el, el / images)}
 
 
 def cpu_baseline(c, ops, budget_s):

@@ -299,6 +299,30 @@ int esb_project_dn(const float* x, int64_t len, const float* stats, const float*
 int esb_dda_normal(int n, int k_sig, const float* grid, int G, float* alpha_out, double* D_out,
                    double* dD_out, void* stream);
 
+/*
+ * Glue between quantized layers (Sec. 4.2: the post-processing after a
+ * convolution, "MP&ReLU", and the pooled features before the classifier), so
+ * that a forward pass between two contractions runs only library kernels.
+ * fp32, NHWC; every pointer device; asynchronous on `stream`.
+ * esb_maxpool2d: out[n][p][q][c] = max over the R x S window at
+ *   (p*stride - pad, q*stride - pad) of the input elements inside the image
+ *   (padding is never selected; requires pad < R and pad < S so that every
+ *   window holds one); a NaN in a window gives NaN.  out is [N, P, Q, C] with
+ *   P = (H + 2 pad - R)/stride + 1, Q likewise.
+ * esb_avgpool_global: out[n][c] = fl32( (sum over the HW positions, in
+ *   position order, of (double)x[n][i][c]) / HW ), x [N, HW, C], out [N, C];
+ *   absmax_out (or NULL) is raised to max |out| as below.
+ * esb_absmax: *absmax_out = max(*absmax_out, max_i |x_i|), compared as fp32 bit
+ *   patterns with the sign cleared (a NaN wins over every number); the caller
+ *   sets the initial value (0 to start).  A DDA grid scaled by this maximum
+ *   (esb_dda_job.grid_scale) needs no host round trip.
+ */
+int esb_maxpool2d(const float* x, int N, int H, int W, int C, int R, int S, int stride, int pad,
+                  float* out, void* stream);
+int esb_avgpool_global(const float* x, int N, int HW, int C, float* out, float* absmax_out,
+                       void* stream);
+int esb_absmax(const float* x, int64_t len, float* absmax_out, void* stream);
+
 /* Convolution geometry.  Output P = (H + 2*pad_h - R)/stride_h + 1, Q likewise. */
 typedef struct esb_conv_desc {
     int N, H, W, C;          /* input batch, height, width, channels (NHWC) */

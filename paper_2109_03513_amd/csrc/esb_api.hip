@@ -224,6 +224,32 @@ int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, siz
     return hip_status(launch_dda_batch(d.data(), count, (hipStream_t)stream));
 }
 
+int esb_maxpool2d(const float* x, int N, int H, int W, int C, int R, int S, int stride, int pad,
+                  float* out, void* stream) {
+    if (N < 0 || H < 1 || W < 1 || C < 1 || R < 1 || S < 1 || stride < 1 || pad < 0 ||
+        pad >= R || pad >= S || H + 2 * pad < R || W + 2 * pad < S)
+        return ESB_E_INVALID;
+    PoolGeom g;
+    g.N = N; g.H = H; g.W = W; g.C = C; g.R = R; g.S = S; g.sh = stride; g.sw = stride;
+    g.ph = pad; g.pw = pad;
+    g.P = (H + 2 * pad - R) / stride + 1;
+    g.Q = (W + 2 * pad - S) / stride + 1;
+    if ((int64_t)N * g.P * g.Q * C > 0 && (!x || !out)) return ESB_E_INVALID;
+    return hip_status(launch_maxpool(x, g, out, (hipStream_t)stream));
+}
+
+int esb_avgpool_global(const float* x, int N, int HW, int C, float* out, float* absmax_out,
+                       void* stream) {
+    if (N < 0 || HW < 1 || C < 1) return ESB_E_INVALID;
+    if (N > 0 && (!x || !out)) return ESB_E_INVALID;
+    return hip_status(launch_avgpool(x, N, HW, C, out, absmax_out, (hipStream_t)stream));
+}
+
+int esb_absmax(const float* x, int64_t len, float* absmax_out, void* stream) {
+    if (len < 0 || !absmax_out || (len > 0 && !x)) return ESB_E_INVALID;
+    return hip_status(launch_absmax(x, len, absmax_out, (hipStream_t)stream));
+}
+
 int esb_project_batch(int count, const esb_project_job* jobs, void* stream) {
     if (count < 0 || (count > 0 && !jobs)) return ESB_E_INVALID;
     std::vector<ProjJobDesc> d((size_t)count);

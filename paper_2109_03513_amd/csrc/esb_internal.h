@@ -229,19 +229,27 @@ __device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t
     return m;
 }
 
-// The running |z| maxima of a wave into *absmax.  Every lane of the wave calls
-// this.  Thousands of waves meet on one address, so a wave first reads the
-// current value from the L2 (an atomic load) and issues its atomic maximum only
-// when its own maximum is larger: a stale read costs one unneeded atomic, never
-// a wrong result.
-__device__ __forceinline__ void post_absmax_flush(const Post& P, uint32_t m) {
-    if (!P.absmax) return;
+// The running |z| maxima of a workgroup into *absmax.  Every thread of the
+// workgroup calls this (it holds a barrier).  Thousands of workgroups meet on
+// one address, so the waves' maxima first meet in LDS, and the one thread
+// that holds the workgroup's maximum reads the current value (an atomic load)
+// and issues its atomic maximum only when its own is larger: a stale read
+// costs one unneeded atomic, never a wrong result.
+__device__ __forceinline__ void absmax_flush_block(uint32_t* absmax, uint32_t m) {
+    __shared__ uint32_t s_amax[16];
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
-    if ((threadIdx.x & 63) == 0) {
-        const uint32_t cur = __hip_atomic_load(P.absmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (m > cur) atomicMax(P.absmax, m);
+    const int wave = threadIdx.x >> 6, nwaves = (blockDim.x + 63) >> 6;
+    if ((threadIdx.x & 63) == 0) s_amax[wave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < nwaves; w++) m = max(m, s_amax[w]);
+        const uint32_t cur = __hip_atomic_load(absmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (m > cur) atomicMax(absmax, m);
     }
+}
+__device__ __forceinline__ void post_absmax_flush(const Post& P, uint32_t m) {
+    if (P.absmax) absmax_flush_block(P.absmax, m);   // uniform: every thread takes the same branch
 }
 
 // The epilogue store of one output: the plain scaled value, or the fused post-processing.
@@ -371,6 +379,15 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
 // sums after the decoded operands in ws (see esb_gemm_packed_workspace_size).
 hipError_t launch_pack_fp4(const uint8_t* codes, int64_t rows, int64_t K, int64_t ld, const Fmt& f,
                            uint8_t* packed, hipStream_t s);
+
+// Glue between layers: NHWC max pooling, the global average pool, max |x|.
+struct PoolGeom {
+    int N, H, W, C, R, S, sh, sw, ph, pw, P, Q;
+};
+hipError_t launch_maxpool(const float* x, const PoolGeom& g, float* out, hipStream_t s);
+hipError_t launch_avgpool(const float* x, int N, int HW, int C, float* out, float* absmax,
+                          hipStream_t s);
+hipError_t launch_absmax(const float* x, int64_t len, float* absmax, hipStream_t s);
 
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,

@@ -102,6 +102,9 @@ def lib():
             "esb_dda_batch_workspace_size": (sz, [i32, ctypes.POINTER(DdaJob)]),
             "esb_dda_align_batch": (i32, [i32, ctypes.POINTER(DdaJob), P, sz, P]),
             "esb_project_batch": (i32, [i32, ctypes.POINTER(ProjectJob), P]),
+            "esb_maxpool2d": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P]),
+            "esb_avgpool_global": (i32, [P, i32, i32, i32, P, P, P]),
+            "esb_absmax": (i32, [P, i64, P, P]),
             "esb_dn_workspace_size": (sz, [i64]),
             "esb_dn_stats": (i32, [P, i64, P, P, sz, P]),
             "esb_project_dn": (i32, [P, i64, P, P, i32, i32, P, P]),
@@ -373,6 +376,43 @@ def project_jobs(specs):
 def esb_project_batch(jobs, stream=None):
     """Projection of every job (a project_jobs() array) in one launch."""
     _check("esb_project_batch", lib().esb_project_batch(len(jobs), jobs, _stream(stream)))
+
+
+def esb_maxpool2d(x, window, stride, pad, out=None, stream=None):
+    """NHWC fp32 max pool (padding never selected); returns out [N, P, Q, C]."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    N, H, W, C = x.shape
+    P, Q = conv_out_hw(H, W, window, window, (stride, stride), (pad, pad))
+    if out is None:
+        out = torch.empty((N, P, Q, C), dtype=torch.float32, device=x.device)
+    _dev_tensor(out, torch.float32, "out")
+    _check("esb_maxpool2d", lib().esb_maxpool2d(_ptr(x), N, H, W, C, window, window, stride, pad,
+                                                _ptr(out), _stream(stream)))
+    return out
+
+
+def esb_avgpool_global(x, out=None, absmax=None, stream=None):
+    """x [N, H, W, C] (or [N, HW, C]) fp32 -> out [N, C]: fp64 sums in position order / HW."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    N, C = x.shape[0], x.shape[-1]
+    HW = x.numel() // max(N * C, 1) if N * C else 1
+    if out is None:
+        out = torch.empty((N, C), dtype=torch.float32, device=x.device)
+    _dev_tensor(out, torch.float32, "out")
+    _check("esb_avgpool_global", lib().esb_avgpool_global(_ptr(x), N, HW, C, _ptr(out),
+                                                          _ptr(absmax), _stream(stream)))
+    return out
+
+
+def esb_absmax(x, absmax, stream=None):
+    """Raise the device fp32 scalar `absmax` to max |x| (the caller sets its start value)."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(absmax, torch.float32, "absmax")
+    _check("esb_absmax", lib().esb_absmax(_ptr(x), x.numel(), _ptr(absmax), _stream(stream)))
+    return absmax
 
 
 def esb_pack_size(rows, K, n, k_sig):

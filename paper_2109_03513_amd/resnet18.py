@@ -8,15 +8,17 @@ largest set value, so the grid spans (0, max|x| / C]), projected to ESB codes
 (eq. (8)) and contracted with the pre-quantized weights (eq. (15)) into fp32
 outputs.  Weights are quantized once, the same way, when the model is built.
 
-Only the library's calls touch the ESB arithmetic.  The ReLUs and the
-residual additions run in the convolutions' epilogues (esb_conv2d_post: the
-same fp32 operations), which also raise a device scalar to the max |x| of the
-next layer's input, so that its DDA grid needs no separate reduction; the
-3x3 / stride-2 max pool after conv1 and the global average pool are torch on
-the same stream (the pool keeps the maximum: the ReLU'd values are >= 0 and
-every element lies in some window).  The average is a float64 sum of the 7x7
-window divided by 49 and rounded to fp32 once.  No batch normalization (the
-weights are He-initialized).
+Every step runs in the library's kernels; torch only holds the buffers (and
+clears the running maxima at the start of a pass).  The ReLUs and the residual
+additions run in the convolutions' epilogues (esb_conv2d_post: the same fp32
+operations), which also raise a device scalar to the max |x| of the next
+layer's input, so that its DDA grid (esb_dda_job.grid_scale) needs no separate
+reduction; the image's maximum comes from esb_absmax.  The 3x3 / stride-2 max
+pool after conv1 is esb_maxpool2d (it keeps the maximum: the ReLU'd values are
+>= 0 and every element lies in some window) and the global average pool
+esb_avgpool_global (a float64 sum of the 7x7 positions in order, divided by 49
+and rounded to fp32 once), which raises the maximum of the pooled features.
+No batch normalization (the weights are He-initialized).
 
 A downsample conv reads the same block input as the block's first conv, so it
 reuses that conv's alpha and codes instead of quantizing the tensor again.
@@ -65,6 +67,7 @@ class ResNet18ESB:
         self.sh = stream.cuda_stream if stream is not None else None
         self.record = record
         self.trace = []
+        self.units = None
         self.calib = {}   # layer name -> device scale of its input, from the last forward()
         dev = "cuda"
         self.cmax = value_max(n, k_sig)
@@ -87,13 +90,17 @@ class ResNet18ESB:
                 k_sig, stride=(L["stride"],) * 2, pad=(L["pad"],) * 2))
         self.cws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
         self.amax = torch.zeros(32, dtype=torch.float32, device=dev)   # max |x| per layer input
+        self.spare = torch.zeros(1, dtype=torch.float32, device=dev)   # max |x| for _quantize(x)
         # weights, quantized once: every tensor's DDA and projection as one batch
         names = list(self.layers) + ["fc"]
         ws = [torch.from_numpy(np.ascontiguousarray(weights[nm])).to(dev) for nm in names]
-        grids = [self.grid(w) for w in ws]
+        wmax = torch.zeros(len(ws), dtype=torch.float32, device=dev)
+        for i, w in enumerate(ws):
+            esb.esb_absmax(w, wmax[i:i + 1], stream=self.sh)
         alphas = [torch.empty(1, dtype=torch.float32, device=dev) for _ in ws]
         codes = [torch.empty(w.shape, dtype=torch.uint8, device=dev) for w in ws]
-        jobs = esb.dda_jobs([(w, n, k_sig, g, a_, None) for w, g, a_ in zip(ws, grids, alphas)])
+        jobs = esb.dda_jobs([(w, n, k_sig, self.cgrid, a_, None, wmax[i:i + 1])
+                             for i, (w, a_) in enumerate(zip(ws, alphas))])
         wsb = torch.empty(max(esb.esb_dda_batch_workspace_size(jobs), 1), dtype=torch.uint8,
                           device=dev)
         esb.esb_dda_align_batch(jobs, wsb, stream=self.sh)
@@ -106,23 +113,42 @@ class ResNet18ESB:
                 self.layers[nm]["alpha"], self.layers[nm]["codes"] = a_, c
         torch.cuda.synchronize()
 
-    def grid(self, x, xmax=None):
-        """alpha_j = fl32(max|x| * c_j) on the device (one correctly rounded product); xmax:
-        a device scalar already holding max|x| (from the producing epilogue)."""
-        m = self.torch.linalg.vector_norm(x, float("inf")) if xmax is None else xmax
-        return m.reshape(1) * self.cgrid
+    def _call(self, kind, label, fn, nbytes=0.0, ops=0.0):
+        """Run one library call.  While self.units is a list (a forward run for the bench),
+        the call is bracketed by two timing events on the model's stream and kept there with
+        its algorithmic bytes and operations; fn writes only into buffers allocated before it,
+        so running it again repeats the same work."""
+        if self.units is None:
+            return fn()
+        torch = self.torch
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        st = self.stream if self.stream is not None else torch.cuda.current_stream()
+        e0.record(st)
+        out = fn()
+        e1.record(st)
+        self.units.append(dict(kind=kind, label=label, fn=fn, bytes=float(nbytes),
+                               ops=float(ops), events=(e0, e1)))
+        return out
 
-    def _quantize(self, x, ws, xmax=None):
+    def _quantize(self, x, ws, xmax=None, label=""):
+        """DDA over alpha_j = fl32(max|x| * c_j) (the DDA scales the factors c_j by the device
+        scalar xmax itself, one correctly rounded product each), then the projection.  xmax:
+        a device scalar already holding max|x| (from the producing epilogue), else esb_absmax."""
         torch = self.torch
         alpha = torch.empty(1, dtype=torch.float32, device=x.device)
+        codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+        nel = x.numel()
         if xmax is None:
-            g = self.grid(x)
-            esb.esb_dda_align(x, self.n, self.ks, g, alpha_out=alpha, D_out=None, workspace=ws,
-                              stream=self.sh, want_D=False)
-        else:   # the DDA scales the factors by the device max|x| itself (same single rounding)
-            jobs = esb.dda_jobs([(x, self.n, self.ks, self.cgrid, alpha, None, xmax)])
-            esb.esb_dda_align_batch(jobs, ws, stream=self.sh)
-        codes = esb.esb_project(x, alpha, self.n, self.ks, stream=self.sh)
+            xmax = self.spare
+            xmax.zero_()
+            self._call("absmax", label, lambda: esb.esb_absmax(x, xmax, stream=self.sh), 4 * nel)
+        jobs = esb.dda_jobs([(x, self.n, self.ks, self.cgrid, alpha, None, xmax)])
+        self._call("dda", label, lambda: esb.esb_dda_align_batch(jobs, ws, stream=self.sh),
+                   4 * nel)
+        self._call("project", label,
+                   lambda: esb.esb_project(x, alpha, self.n, self.ks, codes=codes, stream=self.sh),
+                   5 * nel)
         return alpha, codes
 
     def conv(self, name, x, quantized=None, xmax=None, residual=None, relu=False, absmax=None):
@@ -130,27 +156,40 @@ class ResNet18ESB:
         already quantized this same tensor (the DDA and the projection depend on x only);
         xmax: device max|x| for the DDA grid.  With residual / relu / absmax the epilogue adds
         the residual, applies the ReLU and raises absmax to the max |output|."""
+        torch = self.torch
         L = self.layers[name]
-        ax, cx = quantized if quantized is not None else self._quantize(x, self.ws[name], xmax)
+        ax, cx = quantized if quantized is not None else self._quantize(x, self.ws[name], xmax,
+                                                                        name)
+        Nb, H, W, C = cx.shape
+        st, pd = (L["stride"],) * 2, (L["pad"],) * 2
+        P, Q = esb.conv_out_hw(H, W, L["k"], L["k"], st, pd)
+        y = torch.empty((Nb, P, Q, L["cout"]), dtype=torch.float32, device=cx.device)
+        acc = (torch.empty((Nb, P, Q, L["cout"]), dtype=torch.int32, device=cx.device)
+               if self.record else None)
+        ops = 2.0 * Nb * P * Q * L["cout"] * L["k"] * L["k"] * C
+        nbytes = cx.numel() + L["codes"].numel() + 4 * y.numel() * (2 if residual is not None else 1)
         if residual is None and not relu and absmax is None:
-            acc, y = esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks,
-                                    L["alpha"], stride=(L["stride"],) * 2, pad=(L["pad"],) * 2,
-                                    want_acc=self.record, stream=self.sh, workspace=self.cws)
+            fn = lambda: esb.esb_conv2d(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks,
+                                        L["alpha"], stride=st, pad=pd, acc=acc, y=y,
+                                        want_acc=self.record, stream=self.sh, workspace=self.cws)
         else:
-            acc, y, _ = esb.esb_conv2d_post(
+            fn = lambda: esb.esb_conv2d_post(
                 cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"], None, self.n,
-                self.ks, residual=residual, relu=relu, stride=(L["stride"],) * 2,
-                pad=(L["pad"],) * 2, want_codes=False, want_acc=self.record, want_y=True,
-                stream=self.sh, workspace=self.cws, absmax=absmax)
+                self.ks, residual=residual, relu=relu, stride=st, pad=pd, want_codes=False,
+                acc=acc, want_acc=self.record, y=y, stream=self.sh, workspace=self.cws,
+                absmax=absmax)
+        self._call("contraction", name, fn, nbytes, ops)
         if self.record:
             self.trace.append(dict(name=name, x=x, alpha=ax, codes=cx, acc=acc, y=y))
         self.calib[name] = ax
         self.last_q = (ax, cx)
         return y
 
-    def forward(self, x):
+    def forward(self, x, units=None):
+        """The forward pass with per-layer DDA; units: a list that receives every library call
+        of the pass (see _call)."""
         torch = self.torch
-        F = torch.nn.functional
+        self.units = units
         self.amax.zero_()
         slots = iter(range(self.amax.numel()))
 
@@ -158,10 +197,19 @@ class ResNet18ESB:
             i = next(slots)
             return self.amax[i:i + 1]
 
+        m0 = slot()
+        self._call("absmax", "image", lambda: esb.esb_absmax(x, m0, stream=self.sh), 4 * x.numel())
         m = slot()
-        a = self.conv("conv1", x, relu=True, absmax=m)
-        # 3x3 max pool, stride 2, pad 1 (padding never wins: -inf); max|a| is unchanged
-        a = F.max_pool2d(a.permute(0, 3, 1, 2), 3, 2, 1).permute(0, 2, 3, 1).contiguous()
+        a = self.conv("conv1", x, xmax=m0, relu=True, absmax=m)
+        # 3x3 max pool, stride 2, pad 1 (padding never wins); max|a| is unchanged
+        Nb, H, W, C = a.shape
+        P = (H + 2 - 3) // 2 + 1
+        pooled = torch.empty((Nb, P, P, C), dtype=torch.float32, device=a.device)
+        a_in = a
+        self._call("maxpool", "stem",
+                   lambda: esb.esb_maxpool2d(a_in, 3, 2, 1, out=pooled, stream=self.sh),
+                   4 * (a_in.numel() + pooled.numel()))
+        a = pooled
         for stage in (1, 2, 3, 4):
             for blk in (0, 1):
                 p = "l%d.%d." % (stage, blk)
@@ -172,14 +220,26 @@ class ResNet18ESB:
                 sc = self.conv(p + "ds", a, quantized=qa) if (p + "ds") in self.layers else a
                 m = slot()
                 a = self.conv(p + "c2", out, xmax=m1, residual=sc, relu=True, absmax=m)
-        feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
-        af, cf = self._quantize(feat, self.ws["fc"])
+        mf = slot()
+        feat = torch.empty((a.shape[0], a.shape[3]), dtype=torch.float32, device=a.device)
+        a_last = a
+        self._call("avgpool", "head",
+                   lambda: esb.esb_avgpool_global(a_last, out=feat, absmax=mf, stream=self.sh),
+                   4 * (a_last.numel() + feat.numel()))
+        af, cf = self._quantize(feat, self.ws["fc"], xmax=mf, label="fc")
         self.calib["fc"] = af
-        acc, logits = esb.esb_gemm(cf, self.n, self.ks, af, self.fc_codes, self.n, self.ks,
-                                   self.fc_alpha, want_acc=self.record, stream=self.sh,
-                                   workspace=self.cws)
+        M, K = cf.shape
+        Nf = self.fc_codes.shape[0]
+        logits = torch.empty((M, Nf), dtype=torch.float32, device=cf.device)
+        acc = torch.empty((M, Nf), dtype=torch.int32, device=cf.device) if self.record else None
+        self._call("contraction", "fc",
+                   lambda: esb.esb_gemm(cf, self.n, self.ks, af, self.fc_codes, self.n, self.ks,
+                                        self.fc_alpha, acc=acc, y=logits, want_acc=self.record,
+                                        stream=self.sh, workspace=self.cws),
+                   M * K + Nf * K + 4 * M * Nf, 2.0 * M * Nf * K)
         if self.record:
             self.trace.append(dict(name="fc", x=feat, alpha=af, codes=cf, acc=acc, y=logits))
+        self.units = None
         return logits
 
     def conv_post(self, name, cx, out_alpha=None, residual=None, relu=False, want_y=False):
@@ -195,14 +255,12 @@ class ResNet18ESB:
 
     def forward_fused(self, x):
         """Forward pass with the scales of the last forward() fixed (see the module notes)."""
-        torch = self.torch
-        F = torch.nn.functional
         A = self.calib
         if "fc" not in A:
             raise RuntimeError("forward_fused needs the scales of a forward() first")
         cx = esb.esb_project(x, A["conv1"], self.n, self.ks, stream=self.sh)
         a, _ = self.conv_post("conv1", cx, relu=True, want_y=True)
-        a = F.max_pool2d(a.permute(0, 3, 1, 2), 3, 2, 1).permute(0, 2, 3, 1).contiguous()
+        a = esb.esb_maxpool2d(a, 3, 2, 1, stream=self.sh)
         ca = esb.esb_project(a, A["l1.0.c1"], self.n, self.ks, stream=self.sh)
         blocks = [(s, b) for s in (1, 2, 3, 4) for b in (0, 1)]
         for i, (stage, blk) in enumerate(blocks):
@@ -221,7 +279,7 @@ class ResNet18ESB:
                 nxt = A["l%d.%d.c1" % blocks[i + 1]]
             a, ca = self.conv_post(p + "c2", mid, out_alpha=nxt, residual=sc, relu=True,
                                    want_y=True)
-        feat = (a.double().sum(dim=(1, 2)) / float(a.shape[1] * a.shape[2])).float().contiguous()
+        feat = esb.esb_avgpool_global(a, stream=self.sh)
         cf = esb.esb_project(feat, A["fc"], self.n, self.ks, stream=self.sh)
         _, logits = esb.esb_gemm(cf, self.n, self.ks, A["fc"], self.fc_codes, self.n, self.ks,
                                  self.fc_alpha, want_acc=False, stream=self.sh, workspace=self.cws)

@@ -74,6 +74,18 @@ def test_argument_validation_without_launch(L):
     assert L.esb_dda_align(fake, 100, 4, 2, fake, 64, fake, None, fake, need - 1, None) == -6
     assert L.esb_dda_workspace_size(100, 4, 2, 0) == 0
     assert L.esb_dda_workspace_size(100, 8, 7, 65) == 0
+    # glue: windows made only of padding, bad sizes, missing pointers
+    mp = L.esb_maxpool2d
+    assert mp(fake, 1, 8, 8, 4, 3, 3, 2, 3, fake, None) == -1          # pad >= window
+    assert mp(fake, 1, 8, 8, 4, 3, 3, 0, 1, fake, None) == -1          # stride 0
+    assert mp(fake, 1, 2, 2, 4, 5, 5, 1, 1, fake, None) == -1          # window beyond padded input
+    assert mp(None, 1, 8, 8, 4, 3, 3, 2, 1, fake, None) == -1
+    assert mp(None, 0, 8, 8, 4, 3, 3, 2, 1, None, None) == 0           # empty batch: nothing to do
+    assert L.esb_avgpool_global(fake, 2, 0, 4, fake, None, None) == -1
+    assert L.esb_avgpool_global(None, 2, 49, 4, fake, None, None) == -1
+    assert L.esb_absmax(fake, 10, None, None) == -1
+    assert L.esb_absmax(None, 10, fake, None) == -1
+    assert L.esb_absmax(None, 0, fake, None) == 0
     # DDA with the static scratch: the same checks, and inputs beyond the scratch refused
     na = L.esb_dda_align_noalloc
     assert na(fake, 100, 8, 7, fake, 65, fake, None, None) == -1

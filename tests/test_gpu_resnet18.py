@@ -42,6 +42,15 @@ def maxpool_np(a):   # 3x3, stride 2, pad 1, NHWC
     return out
 
 
+def avgpool_np(a):   # global average: float64 sum in position order, / HW, one rounding
+    B, H, W, C = a.shape
+    flat = a.reshape(B, H * W, C).astype(np.float64)
+    acc = np.zeros((B, C), dtype=np.float64)
+    for i in range(H * W):
+        acc += flat[:, i, :]
+    return (acc / float(H * W)).astype(np.float32)
+
+
 @pytest.mark.parametrize("batch", [2])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_resnet18_stack_matches_oracle(batch, seed):
@@ -97,7 +106,7 @@ def test_resnet18_stack_matches_oracle(batch, seed):
             out = conv(p + "c1", a, relu)
             sc = conv(p + "ds", a) if (p + "ds") in geo else a
             a = conv(p + "c2", out, lambda v: relu(v + sc))
-    feat = (a.astype(np.float64).sum(axis=(1, 2)) / float(a.shape[1] * a.shape[2])).astype(np.float32)
+    feat = avgpool_np(a)
     y = layer("fc", feat, None, 1, 0, wq["fc"])
     assert_rel(logits, y, 1e-6, "logits")
     assert np.all(np.isfinite(logits))
