@@ -672,7 +672,7 @@ def resnet18_headline(args):
         gr["layers"].append(u["label"])
     units_ms = sum(gr["ms"] for gr in groups.values())
     kernels = {
-        "dda": "esb_dda_align_batch per layer input: k_dda_hist (+ k_dda_group) + k_dda_finalize",
+        "dda": "esb_dda_align_planned per layer input: k_dda_hist (+ k_dda_group) + k_dda_finalize",
         "project": "esb_project per layer input: k_project_vec",
         "absmax": "esb_absmax: k_absmax",
         "maxpool": "esb_maxpool2d: k_maxpool",
@@ -756,8 +756,9 @@ def resnet18_cpu_baseline(weights, images, ops_per_image):
     cmax = float(oracle.valueset(N, KS)[-1])
     fac = wl.maxabs_grid_factors(cmax)
 
-    def quant(a):
-        g = (np.float32(np.max(np.abs(a))) * fac).astype(np.float32)
+    def quant(a):   # grid 2^E c_j, E the binary exponent of max|a|
+        m = np.float32(np.max(np.abs(a)))
+        g = np.ldexp(fac, int(np.frexp(m)[1]) if m != 0 else 0).astype(np.float32)
         j, _ = oracle.dda(a, N, KS, g)
         return g[j], oracle.project(a, g[j], N, KS)
 

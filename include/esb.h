@@ -208,6 +208,40 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
                     size_t ws_bytes, void* stream);
 
 /*
+ * The aligner with its grid-only work done once: a plan.  Every call of
+ * esb_dda_align first derives, from the candidates alone, each candidate's
+ * exact cell thresholds, their merged sorted bounds and a bin table over them;
+ * for a small tensor that set-up takes as long as the pass over the data.
+ * esb_dda_plan builds it once, on the device, for candidates factors[j]
+ * (device, G fp32); esb_dda_align_planned then searches the candidates
+ *   alpha_j = 2^E * factors[j],   2^(E-1) <= |*scale| < 2^E   (E = 0 when *scale == 0),
+ * a data-dependent power-of-two multiple of the factors (for example factors
+ * spanning (0, 1/C] and *scale = max|x| from esb_absmax or an epilogue, so that
+ * the grid spans (0, 2^E/C] with 2^E in (max|x|, 2 max|x|]).  Multiplying a
+ * candidate by a power of two multiplies its exact thresholds by the same
+ * power, so the plan's tables are shifted in the exponent instead of being
+ * rebuilt; when the shifted tables would leave the normal fp32 range the call
+ * rebuilds them.  Results are those of esb_dda_align with grid[j] =
+ * ldexp(factors[j], E) (identical alpha, D within its stated accuracy and
+ * deterministic); a *scale that is not finite makes every candidate NaN
+ * (D_j = NaN, alpha_out = NaN).
+ *   esb_dda_plan_size    bytes of a plan (0 for invalid arguments);
+ *   esb_dda_plan         plan: device, 16-byte aligned, esb_dda_plan_size bytes
+ *                        (ESB_E_WORKSPACE otherwise); written on `stream`;
+ *   esb_dda_align_planned  n, k_sig, G as given to esb_dda_plan; scale: device
+ *                        scalar; workspace: esb_dda_workspace_size(len, n, k_sig,
+ *                        G) bytes.  A plan built for other arguments (or not a
+ *                        plan) is not used: the call then rebuilds the tables
+ *                        from the factors it finds there.
+ */
+size_t esb_dda_plan_size(int n, int k_sig, int G);
+int esb_dda_plan(int n, int k_sig, const float* factors, int G, void* plan, size_t plan_bytes,
+                 void* stream);
+int esb_dda_align_planned(const float* x, int64_t len, int n, int k_sig, const void* plan, int G,
+                          const float* scale, float* alpha_out, double* D_out, void* workspace,
+                          size_t ws_bytes, void* stream);
+
+/*
  * esb_dda_align for callers that cannot allocate device memory: code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, search and results as esb_dda_align (alpha and D
@@ -407,6 +441,34 @@ int esb_conv2d_post(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig
                     const float* alphaX, const uint8_t* w, int nW, int kW_sig,
                     const float* alphaW, int32_t* acc, float* y, const esb_post* post,
                     void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * A convolution followed by the post-processing of esb_conv2d_post with a
+ * ReLU and by max pooling (Sec. 4.2: the convolution stage, then "MP&ReLU"),
+ * the stem of a convolutional network:
+ *   z[n][p][q][k]  = relu(fma(a[k], fl32(s fl32(acc[n][p][q][k])), b[k]))  (as esb_conv2d_post)
+ *   y[n][i][j][k]  = max of z over the pool_window x pool_window window at
+ *                    (i pool_stride - pool_pad, j pool_stride - pool_pad), positions
+ *                    outside z left out (pool_pad < pool_window: every window holds one);
+ * y: device fp32 [N, PP, QQ, K] (PP = (P + 2 pool_pad - pool_window)/pool_stride + 1,
+ * QQ likewise), or NULL; post: relu nonzero, residual NULL, a / b optional; its codes
+ * (with alpha, n, k_sig) receive the codes of y and absmax_out is raised to max |y|.
+ * Where the fused kernel applies (stride 2, C <= 3, S*C <= 32, R <= 8, K == 64, pool
+ * 3 / 2 / 1, decoded integers within int8, x 4-byte aligned) nothing else is
+ * written: the full-resolution z never reaches memory.  Elsewhere z is computed into
+ * the workspace (device, esb_conv2d_relu_maxpool_workspace_size bytes, 0 where the
+ * fused kernel applies) and pooled from there, with the same results.
+ * Errors: ESB_E_INVALID for a missing post, relu == 0, a residual, a window made only
+ * of padding, or no output; otherwise as esb_conv2d_post.
+ */
+size_t esb_conv2d_relu_maxpool_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int nW,
+                                              int kW_sig, int pool_window, int pool_stride,
+                                              int pool_pad);
+int esb_conv2d_relu_maxpool(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+                            const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+                            const float* alphaW, const esb_post* post, int pool_window,
+                            int pool_stride, int pool_pad, float* y, void* workspace,
+                            size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

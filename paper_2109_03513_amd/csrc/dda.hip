@@ -243,11 +243,51 @@ __host__ __device__ static inline HistLds hist_lds(int A, int lbins) {
     return h;
 }
 
-// One block (local index bid of its job) of the histogram pass.
+// A plan: the grid-only part of the set-up for candidates factor_j (scale 1),
+// dumped from LDS once, so that a call with candidates 2^E factor_j loads it
+// instead of rebuilding it.  Multiplying a candidate by 2^E multiplies each of
+// its exact thresholds by 2^E (the quotient fl32(X / alpha) is unchanged when
+// X and alpha both scale and stay normal), and adding E << 23 to a normal fp32
+// bit pattern is that multiplication, so the loaded bounds are the bounds of
+// the scaled grid bit for bit while E lies in [emin, emax] (every threshold and
+// every candidate stays normal).  Layout: this header, the G factors, the bin
+// entries (nbins uint2), the distinct bounds U (A + 260 u32), the cell starts
+// TH (A u32), each 16-byte aligned.
+struct DdaPlanHead {
+    uint32_t magic;
+    int n, k, G, M, A, lbins;
+    uint32_t shift, base, nb, hi, Dp;
+    int emin, emax;
+};
+constexpr uint32_t kPlanMagic = 0x45534250u;   // "ESBP"
+__host__ __device__ inline size_t plan_factors_off() { return align16(sizeof(DdaPlanHead)); }
+__host__ __device__ inline size_t plan_ent_off(int G) {
+    return plan_factors_off() + align16(sizeof(float) * (size_t)G);
+}
+__host__ __device__ inline size_t plan_u_off(int G, int lbins) {
+    return plan_ent_off(G) + ((size_t)8 << lbins);
+}
+__host__ __device__ inline size_t plan_th_off(int G, int A, int lbins) {
+    return plan_u_off(G, lbins) + align16(sizeof(uint32_t) * ((size_t)A + kMaxSplits + 4));
+}
+__host__ __device__ inline size_t plan_total(int G, int A, int lbins) {
+    return plan_th_off(G, A, lbins) + align16(sizeof(uint32_t) * (size_t)A);
+}
+// Plans use the bins of large inputs (few crowded bins); loading them costs
+// the same at every size.
+inline int plan_lbins(int A) { return hist_lbins(A, true); }
+
+// One block (local index bid of its job) of the histogram pass.  plan_in: the
+// job's candidates are 2^E factor_j (factor_j = grid[j], E the binary exponent
+// of |*gscale|) and the grid-only tables come from this plan when E is inside
+// its range (else they are rebuilt as without a plan).  plan_out: build a plan
+// (x empty): dump the tables after the set-up and return.
 __device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int64_t len,
                                                const float* __restrict__ grid,
                                                const float* __restrict__ gscale, const DdaArgs a,
-                                               double* __restrict__ part, const int bid) {
+                                               double* __restrict__ part, const int bid,
+                                               const uint8_t* __restrict__ plan_in,
+                                               uint8_t* __restrict__ plan_out) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int A = a.A, M = a.M, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int nbins = 1 << a.lbins;
@@ -267,11 +307,30 @@ __device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int6
     //         of x, so that both latencies overlap the clearing of the bins.
     constexpr int kMaxTpt = kDdaMaxThresholds / kHistThreads;   // thresholds per thread
     const float gsc = gscale ? *gscale : 1.0f;   // candidates fl32(gsc * grid[j])
+    // planned: candidates 2^pe factor_j, 2^(pe-1) <= |gsc| < 2^pe (pe = 0 for 0); a
+    // scale that is not finite makes every candidate NaN
+    int pe = 0;
+    bool use_plan = false;
+    const bool sc_ok = __builtin_isfinite(gsc);
+    if (plan_in) {
+        frexpf(fabsf(gsc), &pe);
+        const DdaPlanHead& ph = *(const DdaPlanHead*)plan_in;
+        const bool head_ok = ph.magic == kPlanMagic && ph.n == a.n && ph.k == a.k && ph.G == a.G &&
+                             ph.M == M && ph.A == A && ph.lbins == a.lbins &&
+                             ph.nb <= (uint32_t)nbins && nbins <= (1 << 13) &&
+                             ph.Dp <= (uint32_t)a.Aa && ph.shift < 23u;
+        use_plan = head_ok && sc_ok && pe >= ph.emin && pe <= ph.emax;
+    }
     float al[kMaxTpt];
 #pragma unroll
     for (int r = 0; r < kMaxTpt; r++) {
         const int i = tid + r * kHistThreads;
-        al[r] = (i < A) ? (gscale ? gsc * grid[i / M] : grid[i / M]) : 1.0f;
+        float v = 1.0f;
+        if (i < A) {
+            if (plan_in) v = sc_ok ? ldexpf(grid[i / M], pe) : __builtin_nanf("");
+            else v = gscale ? gsc * grid[i / M] : grid[i / M];
+        }
+        al[r] = v;
     }
     const bool vec = ((uintptr_t)x & 15) == 0;
     const int64_t e0 = (int64_t)bid * a.rows_pb * kRowElems;
@@ -322,196 +381,300 @@ __device__ __forceinline__ void dda_hist_block(const float* __restrict__ x, int6
     constexpr int64_t kChunkElems = 4 * 4 * kHistThreads;
     if (e0 + kChunkElems <= v1) load_full(e0, gn);
     else if (e0 < v1) load_chunk(e0, gn);   // (x may be NULL when len == 0)
-    if (tid < M) s_mid[tid] = set_mid(tid + 1, a.k);
-    for (int b = tid; b < nbins; b += kHistThreads) binc[b] = 0u;
-    lds_barrier();
-
-    // ---- 1. thresholds, their finite range and count
-    {
-        uint32_t wlo = 0x7f800000u, whi = 0u, wn = 0u;
+    uint32_t shift = 0, base = 0, nb = 1, lo = 0x7f800000u, hi = 0x7f800000u, Dp = 0;
+    uint32_t ec_lo = 255u, ec_hi = 0u, plan_bad = 0u;   // plan building only
+    if (use_plan) {
+        // the tables of the plan, every bound multiplied by 2^pe (pe << 23 added to
+        // its bit pattern); padding (~0) and the zero lower bound of atom 0 stay
+        const DdaPlanHead& ph = *(const DdaPlanHead*)plan_in;
+        const uint32_t d = (uint32_t)pe << 23;
+        shift = ph.shift;
+        base = ph.base + (uint32_t)(pe * (1 << (23 - (int)ph.shift)));
+        nb = ph.nb;
+        hi = ph.hi + d;
+        Dp = ph.Dp;
+        const uint2* pe = (const uint2*)(plan_in + plan_ent_off(ph.G));
+        const uint32_t* pu = (const uint32_t*)(plan_in + plan_u_off(ph.G, ph.lbins));
+        const uint32_t* pt = (const uint32_t*)(plan_in + plan_th_off(ph.G, ph.A, ph.lbins));
+        // every load in flight before the first store (at most 8192 bins, A + 260
+        // bounds and A cell starts: 8, 9 and 8 per thread)
+        constexpr int kB = (1 << 13) / kHistThreads;
+        constexpr int kU = (kDdaMaxThresholds + kMaxSplits + 4 + kHistThreads - 1) / kHistThreads;
+        constexpr int kT = kDdaMaxThresholds / kHistThreads;
+        uint2 ev[kB];
+        uint32_t uv[kU], tv[kT];
 #pragma unroll
-        for (int r = 0; r < kMaxTpt; r++) {
-            const int i = tid + r * kHistThreads;
-            if (r * kHistThreads < A && i < A) {
-                const int c = i - (i / M) * M;
-                const uint32_t t = alpha_ok(al[r]) ? threshold_bits(al[r], s_mid[c]) : 0x7f800000u;
-                TH[i] = t;
-                if (t < 0x7f800000u) { wlo = min(wlo, t); whi = max(whi, t); wn++; }
+        for (int q = 0; q < kB; q++) {
+            const uint32_t b = (uint32_t)(tid + q * kHistThreads);
+            ev[q] = b < nb ? pe[b] : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int q = 0; q < kU; q++) {
+            const uint32_t i = (uint32_t)(tid + q * kHistThreads);
+            uv[q] = i < Dp + 4u ? pu[i] : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < kT; q++) {
+            const int i = tid + q * kHistThreads;
+            tv[q] = i < A ? pt[i] : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < kB; q++) {
+            const uint32_t b = (uint32_t)(tid + q * kHistThreads);
+            if (b < nb) {
+                uint2 e = ev[q];
+                e.y = e.y == 0xffffffffu ? e.y : e.y + d;
+                ENT[b] = e;
             }
         }
-        wlo = wave_scan_min(wlo);
-        whi = wave_scan_max(whi);
-        wn = wave_scan_add(wn);
-        if (lane == 63) { s_u[0][wid] = wlo; s_u[1][wid] = whi; s_u[2][wid] = wn; }
-    }
-    lds_barrier();
-    uint32_t lo = 0x7f800000u, hi = 0u, nfin = 0u;
 #pragma unroll
-    for (int v = 0; v < kHistThreads / 64; v++) {
-        lo = min(lo, s_u[0][v]);
-        hi = max(hi, s_u[1][v]);
-        nfin += s_u[2][v];
-    }
-    if (nfin == 0) { lo = 0x7f800000u; hi = 0x7f800000u; }
-    uint32_t shift = 0;
-    while (((hi >> shift) - (lo >> shift)) >= (uint32_t)(nbins - 1)) shift++;   // <= 21
-    const uint32_t base = lo >> shift;
-    const uint32_t nb = (hi >> shift) - base + 1u;
-    // binade starts strictly inside (lo, hi)
-    const uint32_t nsplit = (hi > lo) ? ((hi - 1u) >> 23) - (lo >> 23) : 0u;
-    const uint32_t Ap = nfin + nsplit;
-
-    // ---- 2. bounds per bin: finite thresholds and the powers of two in (lo, hi)
-    for (int i = tid; i < A; i += kHistThreads) {
-        const uint32_t t = TH[i];
-        if (t < 0x7f800000u) atomicAdd(&binc[(t >> shift) - base], 1u);
-    }
-    for (uint32_t e = tid; e < nsplit; e += kHistThreads)
-        atomicAdd(&binc[((((lo >> 23) + 1u + e) << 23) >> shift) - base], 1u);
-    lds_barrier();
-
-    // ---- 3. first atom of every bin: exclusive scan of the counts, P bins per thread
-    const int P = nbins / kHistThreads;   // 16, 8, 4 or 2 bins per thread
-    {
-        uint32_t cnt[16];
-        uint4* b4 = (uint4*)binc;
-#pragma unroll
-        for (int q = 0; q < 4; q++) {
-            if (4 * q < P && P >= 4) {
-                const uint4 u = b4[tid * (P / 4) + q];
-                cnt[4 * q] = u.x; cnt[4 * q + 1] = u.y; cnt[4 * q + 2] = u.z; cnt[4 * q + 3] = u.w;
-            } else {
-                cnt[4 * q] = cnt[4 * q + 1] = cnt[4 * q + 2] = cnt[4 * q + 3] = 0u;
-            }
-        }
-        if (P == 2) {
-            const uint2 u = ((const uint2*)binc)[tid];
-            cnt[0] = u.x; cnt[1] = u.y;
-        }
-        uint32_t mine = 0;
-#pragma unroll
-        for (int e = 0; e < 16; e++) mine += cnt[e];
-        const uint32_t incl = wave_scan_add(mine);
-        if (lane == 63) s_u[3][wid] = incl;
-        lds_barrier();
-        uint32_t run = incl - mine;
-        for (int v = 0; v < wid; v++) run += s_u[3][v];
-        uint32_t st[16];                        // fill counter (high half) starts at 0
-#pragma unroll
-        for (int e = 0; e < 16; e++) { st[e] = run; run += cnt[e]; }
-#pragma unroll
-        for (int q = 0; q < 4; q++)
-            if (4 * q < P && P >= 4)
-                b4[tid * (P / 4) + q] = make_uint4(st[4 * q], st[4 * q + 1], st[4 * q + 2], st[4 * q + 3]);
-        if (P == 2) ((uint2*)binc)[tid] = make_uint2(st[0], st[1]);
-    }
-    lds_barrier();
-
-    // ---- 4. scatter the keys into their buckets; non-finite thresholds start past the top
-    for (int i = tid; i < A; i += kHistThreads) {
-        const uint32_t t = TH[i];
-        if (t < 0x7f800000u) {
-            const uint32_t old = atomicAdd(&binc[(t >> shift) - base], 0x10000u);
-            KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)t << 32) | (uint32_t)i;
-        } else {
-            TH[i] = Ap + 1u;
-        }
-    }
-    for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
-        const uint32_t v = ((lo >> 23) + 1u + e) << 23;
-        const uint32_t old = atomicAdd(&binc[(v >> shift) - base], 0x10000u);
-        KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)v << 32) | (uint32_t)(A + e);
-    }
-    lds_barrier();
-
-    // ---- 5. order inside each bucket by counting: position = first + #smaller keys
-    for (uint32_t k = tid; k < Ap; k += kHistThreads) {
-        const uint64_t key = KH[k];
-        const uint32_t v = (uint32_t)(key >> 32), id = (uint32_t)key;
-        const uint32_t bi = binc[(v >> shift) - base];
-        const uint32_t o = bi & 0xffffu, n = bi >> 16;
-        uint32_t pos = o;
-        for (uint32_t t = o; t < o + n; t++) pos += (KH[t] < key) ? 1u : 0u;
-        U[pos + 1] = v;
-        if (id < (uint32_t)A) TH[id] = pos + 1;      // atom where this cell starts
-    }
-    if (tid == 0) U[0] = 0u;
-    lds_barrier();
-
-    // ---- 5b. merge equal bounds: R[i] = number of distinct values among
-    //          U[1..i] (the atom whose lower bound is U[i]); the distinct values
-    //          move to U[1..Dp] in place.  R lives where the keys were.
-    uint32_t* R = (uint32_t*)KH;                     // [Ap + 1]
-    uint32_t Dp = 0;
-    {
-        constexpr int kPerMax = (kDdaMaxThresholds + kMaxSplits + kHistThreads - 1) / kHistThreads;
-        const int per = (int)((Ap + kHistThreads - 1) / kHistThreads);
-        uint32_t uv[kPerMax], nf[kPerMax];
-        uint32_t mine = 0;
-#pragma unroll
-        for (int e = 0; e < kPerMax; e++) {
-            const uint32_t i = 1u + (uint32_t)(tid * per + e);
-            uv[e] = 0u;
-            nf[e] = 0u;
-            if (e < per && i <= Ap) {
-                uv[e] = U[i];
-                nf[e] = uv[e] != U[i - 1] ? 1u : 0u;
-                mine += nf[e];
-            }
-        }
-        const uint32_t incl = wave_scan_add(mine);
-        if (lane == 63) s_u[3][wid] = incl;
-        lds_barrier();                               // every read of U above is done
-        uint32_t run = incl - mine;
-#pragma unroll
-        for (int v = 0; v < kHistThreads / 64; v++) {
-            if (v < wid) run += s_u[3][v];
-            Dp += s_u[3][v];
+        for (int q = 0; q < kU; q++) {
+            const uint32_t i = (uint32_t)(tid + q * kHistThreads);
+            if (i < Dp + 4u) U[i] = (i == 0u || uv[q] == 0xffffffffu) ? uv[q] : uv[q] + d;
         }
 #pragma unroll
-        for (int e = 0; e < kPerMax; e++) {
-            const uint32_t i = 1u + (uint32_t)(tid * per + e);
-            if (e < per && i <= Ap) {
-                run += nf[e];
-                R[i] = run;
-                if (nf[e]) U[run] = uv[e];
-            }
-        }
-        if (tid == 0) R[0] = 0u;
-        if (tid < 3) U[Dp + 1u + (uint32_t)tid] = 0xffffffffu;
-    }
-    lds_barrier();
-
-    // ---- 6. cell starts in distinct atoms; bin entries {first | flags, next
-    //         bound}; then KH becomes the histogram
-    for (int i = tid; i < A; i += kHistThreads) {
-        const uint32_t p = TH[i];
-        TH[i] = p <= Ap ? R[p] : Dp + 1u;
-    }
-    {
-        uint32_t ef[16], ey[16];
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-            ef[e] = 0u;
-            ey[e] = 0u;
-            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
-            if (e < P && b < nb) {
-                const uint32_t bv = binc[b];
-                const uint32_t o = bv & 0xffffu, n = bv >> 16;
-                const uint32_t f = R[o], nd = R[o + n] - f;   // distinct bounds inside
-                ef[e] = f | (nd >= 2u ? kFlagWalk : 0u) | (b == nb - 1u ? kFlagTop : 0u);
-                ey[e] = U[f + 1];
-            }
-        }
-        lds_barrier();   // the counts alias the entries; R aliases the histogram
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const uint32_t b = (uint32_t)(tid + e * kHistThreads);
-            if (e < P && b < nb) ENT[b] = make_uint2(ef[e], ey[e]);
+        for (int q = 0; q < kT; q++) {
+            const int i = tid + q * kHistThreads;
+            if (i < A) TH[i] = tv[q];
         }
         for (uint32_t i = tid; i < ((Dp + 1u) << lcop); i += kHistThreads) hist[i] = 0ull;
+        lds_barrier();
+    } else {
+        if (tid < M) s_mid[tid] = set_mid(tid + 1, a.k);
+        for (int b = tid; b < nbins; b += kHistThreads) binc[b] = 0u;
+        lds_barrier();
+
+        // ---- 1. thresholds, their finite range and count
+        {
+            uint32_t wlo = 0x7f800000u, whi = 0u, wn = 0u;
+    #pragma unroll
+            for (int r = 0; r < kMaxTpt; r++) {
+                const int i = tid + r * kHistThreads;
+                if (r * kHistThreads < A && i < A) {
+                    const int c = i - (i / M) * M;
+                    const bool ok = alpha_ok(al[r]);
+                    const uint32_t t = ok ? threshold_bits(al[r], s_mid[c]) : 0x7f800000u;
+                    TH[i] = t;
+                    if (t < 0x7f800000u) { wlo = min(wlo, t); whi = max(whi, t); wn++; }
+                    if (ok) {   // for a plan: the exponents a scaled grid must keep normal
+                        const uint32_t ec = __float_as_uint(al[r]) >> 23;
+                        ec_lo = min(ec_lo, ec);
+                        ec_hi = max(ec_hi, ec);
+                        if (ec == 0u || t < 0x00800000u) plan_bad |= 1u;   // subnormal
+                        if (t >= 0x7f800000u) plan_bad |= 2u;              // overflowed
+                    }
+                }
+            }
+            wlo = wave_scan_min(wlo);
+            whi = wave_scan_max(whi);
+            wn = wave_scan_add(wn);
+            if (lane == 63) { s_u[0][wid] = wlo; s_u[1][wid] = whi; s_u[2][wid] = wn; }
+        }
+        lds_barrier();
+        uint32_t nfin = 0u;
+        lo = 0x7f800000u;
+        hi = 0u;
+    #pragma unroll
+        for (int v = 0; v < kHistThreads / 64; v++) {
+            lo = min(lo, s_u[0][v]);
+            hi = max(hi, s_u[1][v]);
+            nfin += s_u[2][v];
+        }
+        if (nfin == 0) { lo = 0x7f800000u; hi = 0x7f800000u; }
+        shift = 0;
+        while (((hi >> shift) - (lo >> shift)) >= (uint32_t)(nbins - 1)) shift++;   // <= 21
+        base = lo >> shift;
+        nb = (hi >> shift) - base + 1u;
+        // binade starts strictly inside (lo, hi)
+        const uint32_t nsplit = (hi > lo) ? ((hi - 1u) >> 23) - (lo >> 23) : 0u;
+        const uint32_t Ap = nfin + nsplit;
+
+        // ---- 2. bounds per bin: finite thresholds and the powers of two in (lo, hi)
+        for (int i = tid; i < A; i += kHistThreads) {
+            const uint32_t t = TH[i];
+            if (t < 0x7f800000u) atomicAdd(&binc[(t >> shift) - base], 1u);
+        }
+        for (uint32_t e = tid; e < nsplit; e += kHistThreads)
+            atomicAdd(&binc[((((lo >> 23) + 1u + e) << 23) >> shift) - base], 1u);
+        lds_barrier();
+
+        // ---- 3. first atom of every bin: exclusive scan of the counts, P bins per thread
+        const int P = nbins / kHistThreads;   // 16, 8, 4 or 2 bins per thread
+        {
+            uint32_t cnt[16];
+            uint4* b4 = (uint4*)binc;
+    #pragma unroll
+            for (int q = 0; q < 4; q++) {
+                if (4 * q < P && P >= 4) {
+                    const uint4 u = b4[tid * (P / 4) + q];
+                    cnt[4 * q] = u.x; cnt[4 * q + 1] = u.y; cnt[4 * q + 2] = u.z; cnt[4 * q + 3] = u.w;
+                } else {
+                    cnt[4 * q] = cnt[4 * q + 1] = cnt[4 * q + 2] = cnt[4 * q + 3] = 0u;
+                }
+            }
+            if (P == 2) {
+                const uint2 u = ((const uint2*)binc)[tid];
+                cnt[0] = u.x; cnt[1] = u.y;
+            }
+            uint32_t mine = 0;
+    #pragma unroll
+            for (int e = 0; e < 16; e++) mine += cnt[e];
+            const uint32_t incl = wave_scan_add(mine);
+            if (lane == 63) s_u[3][wid] = incl;
+            lds_barrier();
+            uint32_t run = incl - mine;
+            for (int v = 0; v < wid; v++) run += s_u[3][v];
+            uint32_t st[16];                        // fill counter (high half) starts at 0
+    #pragma unroll
+            for (int e = 0; e < 16; e++) { st[e] = run; run += cnt[e]; }
+    #pragma unroll
+            for (int q = 0; q < 4; q++)
+                if (4 * q < P && P >= 4)
+                    b4[tid * (P / 4) + q] = make_uint4(st[4 * q], st[4 * q + 1], st[4 * q + 2], st[4 * q + 3]);
+            if (P == 2) ((uint2*)binc)[tid] = make_uint2(st[0], st[1]);
+        }
+        lds_barrier();
+
+        // ---- 4. scatter the keys into their buckets; non-finite thresholds start past the top
+        for (int i = tid; i < A; i += kHistThreads) {
+            const uint32_t t = TH[i];
+            if (t < 0x7f800000u) {
+                const uint32_t old = atomicAdd(&binc[(t >> shift) - base], 0x10000u);
+                KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)t << 32) | (uint32_t)i;
+            } else {
+                TH[i] = Ap + 1u;
+            }
+        }
+        for (uint32_t e = tid; e < nsplit; e += kHistThreads) {
+            const uint32_t v = ((lo >> 23) + 1u + e) << 23;
+            const uint32_t old = atomicAdd(&binc[(v >> shift) - base], 0x10000u);
+            KH[(old & 0xffffu) + (old >> 16)] = ((uint64_t)v << 32) | (uint32_t)(A + e);
+        }
+        lds_barrier();
+
+        // ---- 5. order inside each bucket by counting: position = first + #smaller keys
+        for (uint32_t k = tid; k < Ap; k += kHistThreads) {
+            const uint64_t key = KH[k];
+            const uint32_t v = (uint32_t)(key >> 32), id = (uint32_t)key;
+            const uint32_t bi = binc[(v >> shift) - base];
+            const uint32_t o = bi & 0xffffu, n = bi >> 16;
+            uint32_t pos = o;
+            for (uint32_t t = o; t < o + n; t++) pos += (KH[t] < key) ? 1u : 0u;
+            U[pos + 1] = v;
+            if (id < (uint32_t)A) TH[id] = pos + 1;      // atom where this cell starts
+        }
+        if (tid == 0) U[0] = 0u;
+        lds_barrier();
+
+        // ---- 5b. merge equal bounds: R[i] = number of distinct values among
+        //          U[1..i] (the atom whose lower bound is U[i]); the distinct values
+        //          move to U[1..Dp] in place.  R lives where the keys were.
+        uint32_t* R = (uint32_t*)KH;                     // [Ap + 1]
+        Dp = 0;
+        {
+            constexpr int kPerMax = (kDdaMaxThresholds + kMaxSplits + kHistThreads - 1) / kHistThreads;
+            const int per = (int)((Ap + kHistThreads - 1) / kHistThreads);
+            uint32_t uv[kPerMax], nf[kPerMax];
+            uint32_t mine = 0;
+    #pragma unroll
+            for (int e = 0; e < kPerMax; e++) {
+                const uint32_t i = 1u + (uint32_t)(tid * per + e);
+                uv[e] = 0u;
+                nf[e] = 0u;
+                if (e < per && i <= Ap) {
+                    uv[e] = U[i];
+                    nf[e] = uv[e] != U[i - 1] ? 1u : 0u;
+                    mine += nf[e];
+                }
+            }
+            const uint32_t incl = wave_scan_add(mine);
+            if (lane == 63) s_u[3][wid] = incl;
+            lds_barrier();                               // every read of U above is done
+            uint32_t run = incl - mine;
+    #pragma unroll
+            for (int v = 0; v < kHistThreads / 64; v++) {
+                if (v < wid) run += s_u[3][v];
+                Dp += s_u[3][v];
+            }
+    #pragma unroll
+            for (int e = 0; e < kPerMax; e++) {
+                const uint32_t i = 1u + (uint32_t)(tid * per + e);
+                if (e < per && i <= Ap) {
+                    run += nf[e];
+                    R[i] = run;
+                    if (nf[e]) U[run] = uv[e];
+                }
+            }
+            if (tid == 0) R[0] = 0u;
+            if (tid < 3) U[Dp + 1u + (uint32_t)tid] = 0xffffffffu;
+        }
+        lds_barrier();
+
+        // ---- 6. cell starts in distinct atoms; bin entries {first | flags, next
+        //         bound}; then KH becomes the histogram
+        for (int i = tid; i < A; i += kHistThreads) {
+            const uint32_t p = TH[i];
+            TH[i] = p <= Ap ? R[p] : Dp + 1u;
+        }
+        {
+            uint32_t ef[16], ey[16];
+    #pragma unroll
+            for (int e = 0; e < 16; e++) {
+                ef[e] = 0u;
+                ey[e] = 0u;
+                const uint32_t b = (uint32_t)(tid + e * kHistThreads);
+                if (e < P && b < nb) {
+                    const uint32_t bv = binc[b];
+                    const uint32_t o = bv & 0xffffu, n = bv >> 16;
+                    const uint32_t f = R[o], nd = R[o + n] - f;   // distinct bounds inside
+                    ef[e] = f | (nd >= 2u ? kFlagWalk : 0u) | (b == nb - 1u ? kFlagTop : 0u);
+                    ey[e] = U[f + 1];
+                }
+            }
+            lds_barrier();   // the counts alias the entries; R aliases the histogram
+    #pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const uint32_t b = (uint32_t)(tid + e * kHistThreads);
+                if (e < P && b < nb) ENT[b] = make_uint2(ef[e], ey[e]);
+            }
+            for (uint32_t i = tid; i < ((Dp + 1u) << lcop); i += kHistThreads) hist[i] = 0ull;
+        }
+        lds_barrier();
     }
-    lds_barrier();
+    if (plan_out) {   // dump the tables and the range of pe that keeps them exact
+        uint32_t m0 = wave_scan_min(ec_lo), m1 = wave_scan_max(ec_hi), m2 = wave_scan_or(plan_bad);
+        if (lane == 63) { s_u[0][wid] = m0; s_u[1][wid] = m1; s_u[2][wid] = m2; }
+        lds_barrier();
+        if (tid == 0) {
+            uint32_t elo = 255u, ehi = 0u, bad = 0u;
+            for (int v = 0; v < kHistThreads / 64; v++) {
+                elo = min(elo, s_u[0][v]); ehi = max(ehi, s_u[1][v]); bad |= s_u[2][v];
+            }
+            int emin = -1000, emax = 1000;
+            if (elo <= ehi) { emin = 1 - (int)elo; emax = 254 - (int)ehi; }
+            if (lo < 0x7f800000u) {
+                emin = max(emin, 1 - (int)(lo >> 23));
+                emax = min(emax, 254 - (int)(hi >> 23));
+            }
+            if (bad & 2u) emin = max(emin, 0);
+            if ((bad & 1u) || lo >= 0x7f800000u) { emin = 0; emax = 0; }   // nothing to shift
+            if (emin > emax) { emin = 1; emax = 0; }   // empty: never used
+            DdaPlanHead h;
+            h.magic = kPlanMagic; h.n = a.n; h.k = a.k; h.G = a.G; h.M = M; h.A = A;
+            h.lbins = a.lbins; h.shift = shift; h.base = base; h.nb = nb; h.hi = hi; h.Dp = Dp;
+            h.emin = emin; h.emax = emax;
+            *(DdaPlanHead*)plan_out = h;
+        }
+        float* pf = (float*)(plan_out + plan_factors_off());
+        for (int j = tid; j < a.G; j += kHistThreads) pf[j] = grid[j];
+        uint2* pe = (uint2*)(plan_out + plan_ent_off(a.G));
+        for (uint32_t b = tid; b < nb; b += kHistThreads) pe[b] = ENT[b];
+        uint32_t* pu = (uint32_t*)(plan_out + plan_u_off(a.G, a.lbins));
+        for (uint32_t i = tid; i < Dp + 4u; i += kHistThreads) pu[i] = U[i];
+        uint32_t* pt = (uint32_t*)(plan_out + plan_th_off(a.G, A, a.lbins));
+        for (int i = tid; i < A; i += kHistThreads) pt[i] = TH[i];
+        return;
+    }
 
     // ---- 7. the pass
     double ss0 = 0.0, ss1 = 0.0, top_s1 = 0.0;
@@ -717,7 +880,9 @@ struct DdaJob {
     const float* x;
     int64_t len;
     const float* grid;
-    const float* gscale;   // NULL, or a device scalar multiplying every candidate
+    const float* gscale;   // NULL, or a device scalar multiplying every candidate (planned:
+                           // its binary exponent E gives the candidates 2^E grid[j])
+    const uint8_t* plan;   // NULL, or the job's plan (grid points at its factors)
     float* alpha_out;
     double* D_out;
     double* part;       // block vectors
@@ -740,7 +905,14 @@ __device__ __forceinline__ int dda_job_of_block(const DdaBatch& B, int b) {
 __global__ __launch_bounds__(kHistThreads) void k_dda_hist(DdaBatch B) {
     const int j = dda_job_of_block(B, (int)blockIdx.x);
     const DdaJob& J = B.job[j];
-    dda_hist_block(J.x, J.len, J.grid, J.gscale, J.a, J.part, (int)blockIdx.x - J.blk0);
+    dda_hist_block(J.x, J.len, J.grid, J.gscale, J.a, J.part, (int)blockIdx.x - J.blk0, J.plan,
+                   nullptr);
+}
+
+// One block: the set-up for the candidates factors[j] (scale 1), dumped as a plan.
+__global__ __launch_bounds__(kHistThreads) void k_dda_plan(DdaArgs a, const float* factors,
+                                                           uint8_t* plan) {
+    dda_hist_block(nullptr, 0, factors, nullptr, a, nullptr, 0, nullptr, plan);
 }
 
 // --------------------------------------------------------------------- group
@@ -795,7 +967,17 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
     const int S = fin_split(G, nb);
     const int p = tid & (S - 1), j = tid / S;
     const bool live = j < G;
-    const float al = live ? (J.gscale ? *J.gscale * grid[j] : grid[j]) : 0.0f;
+    float al = 0.0f;
+    if (live) {
+        if (J.plan) {   // 2^E grid[j], E the binary exponent of |scale|
+            const float sc = *J.gscale;
+            int E = 0;
+            frexpf(fabsf(sc), &E);
+            al = __builtin_isfinite(sc) ? ldexpf(grid[j], E) : __builtin_nanf("");
+        } else {
+            al = J.gscale ? *J.gscale * grid[j] : grid[j];
+        }
+    }
     double A = 0.0, B = 0.0, S2 = 0.0;
     uint32_t fl = 0;
     if (live) {
@@ -859,9 +1041,9 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
     }
 }
 
-static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, int nhist, int ngroups,
-                              hipStream_t s) {
-    // set once per device; racing threads set the same attribute
+// The set-up kernels use up to 156 KB of dynamic LDS; set once per device
+// (racing threads set the same attributes).
+static hipError_t set_lds_attributes() {
     static std::atomic<bool> lds_attr_set[64];
     int dev = 0;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64 &&
@@ -869,8 +1051,18 @@ static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, in
         hipError_t e = hipFuncSetAttribute((const void*)k_dda_hist,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 156 * 1024);
         if (e != hipSuccess) return e;
+        e = hipFuncSetAttribute((const void*)k_dda_plan, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                156 * 1024);
+        if (e != hipSuccess) return e;
         lds_attr_set[dev].store(true, std::memory_order_release);
     }
+    return hipSuccess;
+}
+
+static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, int nhist, int ngroups,
+                              hipStream_t s) {
+    const hipError_t e = set_lds_attributes();
+    if (e != hipSuccess) return e;
     k_dda_hist<<<nhist, kHistThreads, max_lds, s>>>(B);
     if (ngroups > 0) k_dda_group<<<ngroups, 256, 0, s>>>(B);
     k_dda_finalize<<<B.count, max_fin_threads, 0, s>>>(B);
@@ -889,8 +1081,10 @@ hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
             a.G = d.G; a.M = d.L.M; a.A = d.L.A; a.Aa = d.L.A + kMaxSplits;
             a.n = d.f.n; a.k = d.f.k;
             dda_blocks(d.len, &a.nblk, &a.rows_pb);
-            a.lbins = hist_lbins(d.L.A, a.rows_pb >= 8);
+            a.lbins = d.plan ? plan_lbins(d.L.A) : hist_lbins(d.L.A, a.rows_pb >= 8);
             J.x = d.x; J.len = d.len; J.grid = d.grid; J.gscale = d.gscale;
+            J.plan = d.plan;
+            if (d.plan) J.grid = (const float*)(d.plan + plan_factors_off());
             J.alpha_out = d.alpha_out; J.D_out = d.D_out;
             J.part = (double*)((char*)d.ws + d.L.off_part);
             J.grp = (double*)((char*)d.ws + d.L.off_group);
@@ -913,8 +1107,30 @@ hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,
                       float* alpha_out, double* D_out, void* ws, const DdaLayout& L,
                       hipStream_t s) {
-    const DdaJobDesc d{x, len, f, grid, G, alpha_out, D_out, ws, L, nullptr};
+    const DdaJobDesc d{x, len, f, grid, G, alpha_out, D_out, ws, L, nullptr, nullptr};
     return launch_dda_batch(&d, 1, s);
+}
+
+size_t dda_plan_bytes(const Fmt& f, int G) {
+    const int A = G * ((1 << (f.n - 1)) - 1);
+    return plan_total(G, A, plan_lbins(A));
+}
+
+hipError_t launch_dda_plan(const Fmt& f, const float* factors, int G, void* plan, hipStream_t s) {
+    DdaArgs a{};
+    a.G = G;
+    a.M = (1 << (f.n - 1)) - 1;
+    a.A = G * a.M;
+    a.Aa = a.A + kMaxSplits;
+    a.n = f.n;
+    a.k = f.k;
+    a.lbins = plan_lbins(a.A);
+    a.nblk = 1;
+    a.rows_pb = 1;
+    const hipError_t e = set_lds_attributes();
+    if (e != hipSuccess) return e;
+    k_dda_plan<<<1, kHistThreads, (int)hist_lds(a.A, a.lbins).total, s>>>(a, factors, (uint8_t*)plan);
+    return hipGetLastError();
 }
 
 }  // namespace esb

@@ -188,6 +188,40 @@ int esb_dda_align_noalloc(const float* x, int64_t len, int n, int k_sig, const f
     return hip_status(launch_dda(x, len, f, grid, G, alpha_out, D_out, ws, L, (hipStream_t)stream));
 }
 
+size_t esb_dda_plan_size(int n, int k_sig, int G) {
+    if (!valid_fmt(n, k_sig)) return 0;
+    DdaLayout L;
+    if (!dda_layout(0, make_fmt(n, k_sig), G, &L)) return 0;
+    return dda_plan_bytes(make_fmt(n, k_sig), G);
+}
+
+int esb_dda_plan(int n, int k_sig, const float* factors, int G, void* plan, size_t plan_bytes,
+                 void* stream) {
+    if (!valid_fmt(n, k_sig) || !factors) return ESB_E_INVALID;
+    const Fmt f = make_fmt(n, k_sig);
+    DdaLayout L;
+    if (!dda_layout(0, f, G, &L)) return ESB_E_INVALID;
+    if (!plan || plan_bytes < dda_plan_bytes(f, G) || (uintptr_t)plan % 16) return ESB_E_WORKSPACE;
+    return hip_status(launch_dda_plan(f, factors, G, plan, (hipStream_t)stream));
+}
+
+int esb_dda_align_planned(const float* x, int64_t len, int n, int k_sig, const void* plan, int G,
+                          const float* scale, float* alpha_out, double* D_out, void* workspace,
+                          size_t ws_bytes, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !plan || !scale || !alpha_out) return ESB_E_INVALID;
+    if (len > 0 && !x) return ESB_E_INVALID;
+    if ((uintptr_t)plan % 16) return ESB_E_INVALID;
+    DdaJobDesc d{};
+    d.f = make_fmt(n, k_sig);
+    if (!dda_layout(len, d.f, G, &d.L)) return ESB_E_INVALID;
+    if (!workspace || ws_bytes < d.L.total) return ESB_E_WORKSPACE;
+    d.x = x; d.len = len; d.grid = nullptr; d.G = G;
+    d.alpha_out = alpha_out; d.D_out = D_out; d.ws = workspace;
+    d.gscale = scale;
+    d.plan = (const uint8_t*)plan;
+    return hip_status(launch_dda_batch(&d, 1, (hipStream_t)stream));
+}
+
 size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs) {
     if (count < 0 || (count > 0 && !jobs)) return 0;
     size_t total = 0;
@@ -217,6 +251,7 @@ int esb_dda_align_batch(int count, const esb_dda_job* jobs, void* workspace, siz
         e.x = j.x; e.len = j.len; e.grid = j.grid; e.G = j.G;
         e.alpha_out = j.alpha_out; e.D_out = j.D_out;
         e.gscale = j.grid_scale;
+        e.plan = nullptr;
         e.ws = (char*)workspace + off;
         off += (e.L.total + 255) & ~(size_t)255;
     }
@@ -477,6 +512,84 @@ int esb_conv2d_post(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig
                      stream, post);
 }
 
+
+// Pooled output size of the fused convolution + ReLU + max pool (0 on error).
+static int pool_dims(const ConvGeom& g, int pool_r, int pool_stride, int pool_pad, int* PP, int* QQ) {
+    if (pool_r < 1 || pool_stride < 1 || pool_pad < 0 || pool_pad >= pool_r) return 0;
+    if (g.P + 2 * pool_pad < pool_r || g.Q + 2 * pool_pad < pool_r) return 0;
+    *PP = (g.P + 2 * pool_pad - pool_r) / pool_stride + 1;
+    *QQ = (g.Q + 2 * pool_pad - pool_r) / pool_stride + 1;
+    return 1;
+}
+
+size_t esb_conv2d_relu_maxpool_workspace_size(const esb_conv_desc* d, int nX, int kX_sig, int nW,
+                                              int kW_sig, int pool_window, int pool_stride,
+                                              int pool_pad) {
+    if (!valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig)) return 0;
+    ConvGeom g;
+    int64_t Mrows = 0, kred = 0;
+    if (conv_geom(d, &g, &Mrows, &kred) != ESB_OK) return 0;
+    int PP = 0, QQ = 0;
+    if (!pool_dims(g, pool_window, pool_stride, pool_pad, &PP, &QQ)) return 0;
+    const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
+    // the fused kernel needs none (a 4-byte aligned input is assumed here)
+    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad, nullptr)) return 0;
+    const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    return al((size_t)Mrows * (size_t)d->K * sizeof(float)) +
+           al((size_t)d->N * PP * QQ * (size_t)d->K * sizeof(float));
+}
+
+int esb_conv2d_relu_maxpool(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_sig,
+                            const float* alphaX, const uint8_t* w, int nW, int kW_sig,
+                            const float* alphaW, const esb_post* post, int pool_window,
+                            int pool_stride, int pool_pad, float* y, void* workspace,
+                            size_t ws_bytes, void* stream) {
+    if (!d || !valid_fmt(nX, kX_sig) || !valid_fmt(nW, kW_sig) || !alphaX || !alphaW) return ESB_E_INVALID;
+    if (!post || !post->relu || post->residual) return ESB_E_INVALID;
+    if (!post_ok(post, alphaX, alphaW)) return ESB_E_INVALID;
+    if (!y && !post->codes && !post->absmax_out) return ESB_E_INVALID;
+    ConvGeom g;
+    int64_t Mrows = 0, kred = 0;
+    if (conv_geom(d, &g, &Mrows, &kred) != ESB_OK) return ESB_E_INVALID;
+    int PP = 0, QQ = 0;
+    if (!pool_dims(g, pool_window, pool_stride, pool_pad, &PP, &QQ)) return ESB_E_INVALID;
+    if (Mrows > 0 && (!x || !w)) return ESB_E_INVALID;
+    const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
+    const int st = contraction_contract(kred, fx, fw);
+    if (st) return st;
+    const hipStream_t s = (hipStream_t)stream;
+    const Post P = make_post(post);
+    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad, x)) {
+        if (Mrows == 0) return ESB_OK;
+        return hip_status(launch_stem(g, x, fx, alphaX, w, fw, alphaW, y, PP, QQ, P, s));
+    }
+    // elsewhere: the convolution with its post-processing into the workspace, the pool, then
+    // the codes and the maximum of the pooled values
+    const size_t need = esb_conv2d_relu_maxpool_workspace_size(d, nX, kX_sig, nW, kW_sig,
+                                                                pool_window, pool_stride, pool_pad);
+    if (!workspace || ws_bytes < need) return ESB_E_WORKSPACE;
+    if (Mrows == 0) return ESB_OK;
+    const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    float* conv_out = (float*)workspace;
+    float* pooled = y ? y : (float*)((char*)workspace + al((size_t)Mrows * (size_t)d->K * sizeof(float)));
+    esb_post inner = *post;
+    inner.codes = nullptr;
+    inner.alpha = nullptr;
+    inner.absmax_out = nullptr;
+    int rc = conv_impl(d, x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, nullptr, conv_out, nullptr, 0,
+                       stream, &inner);
+    if (rc) return rc;
+    PoolGeom pg;
+    pg.N = d->N; pg.H = g.P; pg.W = g.Q; pg.C = d->K; pg.R = pool_window; pg.S = pool_window;
+    pg.sh = pool_stride; pg.sw = pool_stride; pg.ph = pool_pad; pg.pw = pool_pad; pg.P = PP; pg.Q = QQ;
+    hipError_t e = launch_maxpool(conv_out, pg, pooled, s);
+    const int64_t npool = (int64_t)d->N * PP * QQ * d->K;
+    if (e == hipSuccess && post->codes)
+        e = launch_project(pooled, npool, post->alpha, make_fmt(post->n, post->k_sig), post->codes,
+                           nullptr, s);
+    if (e == hipSuccess && post->absmax_out) e = launch_absmax(pooled, npool, post->absmax_out, s);
+    return hip_status(e);
+}
 
 // ------------------------------------------------------------ packed codes
 static bool packable(const Fmt& f) { return f.ebits <= 2 && f.k <= 1; }   // inside OCP E2M1

@@ -306,8 +306,13 @@ struct DdaJobDesc {
     void* ws;
     DdaLayout L;
     const float* gscale;   // NULL, or a device scalar: candidate j is fl32(*gscale * grid[j])
+    const uint8_t* plan;   // NULL, or a plan (grid unused): candidate j is 2^E factor_j,
+                           // E the binary exponent of |*gscale|
 };
 hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s);
+// Plans: the grid-only set-up of the DDA for candidates factors[j], built once.
+size_t dda_plan_bytes(const Fmt& f, int G);
+hipError_t launch_dda_plan(const Fmt& f, const float* factors, int G, void* plan, hipStream_t s);
 
 // ---------------------------------------------------------------- contraction
 // Decoding of one operand's codes to exact integers.
@@ -388,6 +393,15 @@ hipError_t launch_maxpool(const float* x, const PoolGeom& g, float* out, hipStre
 hipError_t launch_avgpool(const float* x, int N, int HW, int C, float* out, float* absmax,
                           hipStream_t s);
 hipError_t launch_absmax(const float* x, int64_t len, float* absmax, hipStream_t s);
+
+// Stem: convolution (stride 2, C <= 3, 64 output channels, int8 integers), the
+// post-processing with a ReLU, and the 3x3 / stride-2 / pad-1 max pool, fused;
+// y (or post.codes) receives the pooled outputs [N, PP, QQ, 64].
+bool stem_fits(const ConvGeom& g, int K, int groups, const Fmt& fx, const Fmt& fw, int pool_r,
+               int pool_stride, int pool_pad, const uint8_t* x);
+hipError_t launch_stem(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
+                       const uint8_t* w, const Fmt& fw, const float* alphaW, float* y, int PP,
+                       int QQ, const Post& post, hipStream_t s);
 
 // Depthwise convolution (groups == C == K): VALU kernel, HBM bound.
 hipError_t launch_dwconv(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,

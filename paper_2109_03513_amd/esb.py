@@ -82,6 +82,9 @@ def lib():
             "esb_dda_workspace_size": (sz, [i64, i32, i32, i32]),
             "esb_dda_align": (i32, [P, i64, i32, i32, P, i32, P, P, P, sz, P]),
             "esb_dda_align_noalloc": (i32, [P, i64, i32, i32, P, i32, P, P, P]),
+            "esb_dda_plan_size": (sz, [i32, i32, i32]),
+            "esb_dda_plan": (i32, [i32, i32, P, i32, P, sz, P]),
+            "esb_dda_align_planned": (i32, [P, i64, i32, i32, P, i32, P, P, P, P, sz, P]),
             "esb_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32, P, P,
                                i64, P]),
             "esb_conv2d": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
@@ -103,6 +106,11 @@ def lib():
             "esb_dda_align_batch": (i32, [i32, ctypes.POINTER(DdaJob), P, sz, P]),
             "esb_project_batch": (i32, [i32, ctypes.POINTER(ProjectJob), P]),
             "esb_maxpool2d": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P]),
+            "esb_conv2d_relu_maxpool_workspace_size": (sz, [ctypes.POINTER(ConvDesc), i32, i32, i32,
+                                                             i32, i32, i32, i32]),
+            "esb_conv2d_relu_maxpool": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32,
+                                              P, ctypes.POINTER(PostDesc), i32, i32, i32, P, P, sz,
+                                              P]),
             "esb_avgpool_global": (i32, [P, i32, i32, i32, P, P, P]),
             "esb_absmax": (i32, [P, i64, P, P]),
             "esb_dn_workspace_size": (sz, [i64]),
@@ -227,6 +235,43 @@ def esb_dda_align_noalloc(x, n, k_sig, grid, alpha_out, D_out=None, stream=None)
     return alpha_out, D_out
 
 
+def esb_dda_plan(n, k_sig, factors, plan=None, stream=None):
+    """The grid-only set-up of the DDA for candidates factors[j] (device fp32), built on the
+    device; returns the plan (a uint8 device tensor)."""
+    import torch
+    _dev_tensor(factors, torch.float32, "factors")
+    G = factors.numel()
+    need = int(lib().esb_dda_plan_size(n, k_sig, G))
+    if need == 0:
+        raise EsbError("esb_dda_plan_size", ESB_E_INVALID)
+    if plan is None:
+        plan = torch.empty(need, dtype=torch.uint8, device=factors.device)
+    _check("esb_dda_plan", lib().esb_dda_plan(n, k_sig, _ptr(factors), G, _ptr(plan),
+                                              plan.numel(), _stream(stream)))
+    return plan
+
+
+def esb_dda_align_planned(x, n, k_sig, plan, G, scale, alpha_out=None, D_out=None, workspace=None,
+                          stream=None, want_D=True):
+    """DDA over the candidates 2^E factors[j] of a plan, E the binary exponent of |scale|
+    (device scalar).  Returns (alpha_out, D_out)."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(scale, torch.float32, "scale")
+    dev = x.device
+    if alpha_out is None:
+        alpha_out = torch.empty(1, dtype=torch.float32, device=dev)
+    if D_out is None and want_D:
+        D_out = torch.empty(G, dtype=torch.float64, device=dev)
+    if workspace is None:
+        need = esb_dda_workspace_size(x.numel(), n, k_sig, G)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("esb_dda_align_planned", lib().esb_dda_align_planned(
+        _ptr(x), x.numel(), n, k_sig, _ptr(plan), G, _ptr(scale), _ptr(alpha_out), _ptr(D_out),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return alpha_out, D_out
+
+
 def esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig):
     return int(lib().esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig))
 
@@ -340,6 +385,42 @@ def esb_conv2d_post(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha, out
                                                     _ptr(alphaW), _ptr(acc), _ptr(y),
                                                     ctypes.byref(pd), wp, wb, _stream(stream)))
     return acc, y, codes
+
+
+def esb_conv2d_relu_maxpool(x, nX, kX_sig, alphaX, w, nW, kW_sig, alphaW, out_alpha=None,
+                            out_n=5, out_k_sig=3, a=None, b=None, stride=(2, 2), pad=(3, 3),
+                            pool=(3, 2, 1), y=None, want_y=True, codes=None, want_codes=False,
+                            absmax=None, workspace=None, stream=None):
+    """Convolution, post-processing with a ReLU and max pooling (pool = (window, stride, pad));
+    returns (y, codes), each [N, PP, QQ, K] or None."""
+    import torch
+    _dev_tensor(x, torch.uint8, "x")
+    _dev_tensor(w, torch.uint8, "w")
+    Nb, H, W, C = x.shape
+    K, R, S, _ = w.shape
+    P, Q = conv_out_hw(H, W, R, S, stride, pad)
+    PP, QQ = conv_out_hw(P, Q, pool[0], pool[0], (pool[1], pool[1]), (pool[2], pool[2]))
+    dev = x.device
+    if y is None and want_y:
+        y = torch.empty((Nb, PP, QQ, K), dtype=torch.float32, device=dev)
+    if codes is None and want_codes:
+        codes = torch.empty((Nb, PP, QQ, K), dtype=torch.uint8, device=dev)
+    pd = post_desc(out_alpha, out_n, out_k_sig, codes, a, b, None, True, absmax)
+    d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], 1)
+    wp, wb = _ws(workspace)
+    _check("esb_conv2d_relu_maxpool", lib().esb_conv2d_relu_maxpool(
+        ctypes.byref(d), _ptr(x), nX, kX_sig, _ptr(alphaX), _ptr(w), nW, kW_sig, _ptr(alphaW),
+        ctypes.byref(pd), pool[0], pool[1], pool[2], _ptr(y), wp, wb, _stream(stream)))
+    return y, codes
+
+
+def esb_conv2d_relu_maxpool_workspace_size(x_shape, w_shape, nX, kX_sig, nW, kW_sig,
+                                           stride=(2, 2), pad=(3, 3), pool=(3, 2, 1)):
+    Nb, H, W, C = x_shape
+    K, R, S, _ = w_shape
+    d = ConvDesc(Nb, H, W, C, K, R, S, stride[0], stride[1], pad[0], pad[1], 1)
+    return int(lib().esb_conv2d_relu_maxpool_workspace_size(ctypes.byref(d), nX, kX_sig, nW,
+                                                             kW_sig, pool[0], pool[1], pool[2]))
 
 
 def dda_jobs(specs):

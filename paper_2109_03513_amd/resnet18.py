@@ -3,19 +3,25 @@
 Every convolution and the classifier are quantized layers of Sec. 5 (the paper
 quantizes all layers of ResNet18, including the first and the last): the
 layer input is scaled by DDA (eq. (13)) over the candidate grid
-alpha_j = fl32(max|x| * c_j), c_j = fl32((j+1) / (64 C)), j = 0..63 (C the
-largest set value, so the grid spans (0, max|x| / C]), projected to ESB codes
-(eq. (8)) and contracted with the pre-quantized weights (eq. (15)) into fp32
-outputs.  Weights are quantized once, the same way, when the model is built.
+alpha_j = 2^E c_j, c_j = fl32((j+1) / (64 C)), j = 0..63, with C the largest
+set value and E the binary exponent of max|x| (2^(E-1) <= max|x| < 2^E), so
+that the grid spans (0, 2^E / C], past max|x| / C by less than a factor of
+two; projected to ESB codes (eq. (8)) and contracted with the pre-quantized
+weights (eq. (15)) into fp32 outputs.  Scaling every candidate by a power of
+two scales its exact thresholds by the same power, so the DDA's grid-only
+set-up is built once (esb_dda_plan) and every call only shifts it
+(esb_dda_align_planned).  Weights are quantized once, the same way, when the
+model is built.
 
 Every step runs in the library's kernels; torch only holds the buffers (and
 clears the running maxima at the start of a pass).  The ReLUs and the residual
 additions run in the convolutions' epilogues (esb_conv2d_post: the same fp32
 operations), which also raise a device scalar to the max |x| of the next
 layer's input, so that its DDA grid (esb_dda_job.grid_scale) needs no separate
-reduction; the image's maximum comes from esb_absmax.  The 3x3 / stride-2 max
-pool after conv1 is esb_maxpool2d (it keeps the maximum: the ReLU'd values are
->= 0 and every element lies in some window) and the global average pool
+reduction; the image's maximum comes from esb_absmax.  conv1, its ReLU and the
+3x3 / stride-2 max pool are one call (esb_conv2d_relu_maxpool: only the pooled
+output is written; the pool keeps the maximum: the ReLU'd values are >= 0 and
+every element lies in some window) and the global average pool
 esb_avgpool_global (a float64 sum of the 7x7 positions in order, divided by 49
 and rounded to fp32 once), which raises the maximum of the pooled features.
 No batch normalization (the weights are He-initialized).
@@ -72,6 +78,7 @@ class ResNet18ESB:
         dev = "cuda"
         self.cmax = value_max(n, k_sig)
         self.cgrid = torch.from_numpy(workloads.maxabs_grid_factors(self.cmax, GRID_POINTS)).to(dev)
+        self.plan = esb.esb_dda_plan(n, k_sig, self.cgrid, stream=self.sh)
         self.layers = {}
         sizes = {}
         for name, cin, cout, k, st, pd in workloads.RESNET18_CONVS:
@@ -89,21 +96,25 @@ class ResNet18ESB:
                 (batch, side, side, L["cin"]), (L["cout"], L["k"], L["k"], L["cin"]), n, k_sig, n,
                 k_sig, stride=(L["stride"],) * 2, pad=(L["pad"],) * 2))
         self.cws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        L1 = self.layers["conv1"]
+        pneed = esb.esb_conv2d_relu_maxpool_workspace_size(
+            (batch, 224, 224, 3), (L1["cout"], L1["k"], L1["k"], 3), n, k_sig, n, k_sig,
+            stride=(L1["stride"],) * 2, pad=(L1["pad"],) * 2)
+        self.pool_ws = torch.empty(pneed, dtype=torch.uint8, device=dev) if pneed else None
         self.amax = torch.zeros(32, dtype=torch.float32, device=dev)   # max |x| per layer input
         self.spare = torch.zeros(1, dtype=torch.float32, device=dev)   # max |x| for _quantize(x)
         # weights, quantized once: every tensor's DDA and projection as one batch
         names = list(self.layers) + ["fc"]
         ws = [torch.from_numpy(np.ascontiguousarray(weights[nm])).to(dev) for nm in names]
         wmax = torch.zeros(len(ws), dtype=torch.float32, device=dev)
-        for i, w in enumerate(ws):
-            esb.esb_absmax(w, wmax[i:i + 1], stream=self.sh)
         alphas = [torch.empty(1, dtype=torch.float32, device=dev) for _ in ws]
         codes = [torch.empty(w.shape, dtype=torch.uint8, device=dev) for w in ws]
-        jobs = esb.dda_jobs([(w, n, k_sig, self.cgrid, a_, None, wmax[i:i + 1])
-                             for i, (w, a_) in enumerate(zip(ws, alphas))])
-        wsb = torch.empty(max(esb.esb_dda_batch_workspace_size(jobs), 1), dtype=torch.uint8,
-                          device=dev)
-        esb.esb_dda_align_batch(jobs, wsb, stream=self.sh)
+        wsw = torch.empty(max(max(esb.esb_dda_workspace_size(w.numel(), n, k_sig, GRID_POINTS)
+                                  for w in ws), 1), dtype=torch.uint8, device=dev)
+        for i, (w, a_) in enumerate(zip(ws, alphas)):
+            esb.esb_absmax(w, wmax[i:i + 1], stream=self.sh)
+            esb.esb_dda_align_planned(w, n, k_sig, self.plan, GRID_POINTS, wmax[i:i + 1],
+                                      alpha_out=a_, workspace=wsw, stream=self.sh, want_D=False)
         esb.esb_project_batch(esb.project_jobs([(w, a_, n, k_sig, c) for w, a_, c in
                                                 zip(ws, alphas, codes)]), stream=self.sh)
         for nm, a_, c in zip(names, alphas, codes):
@@ -132,9 +143,9 @@ class ResNet18ESB:
         return out
 
     def _quantize(self, x, ws, xmax=None, label=""):
-        """DDA over alpha_j = fl32(max|x| * c_j) (the DDA scales the factors c_j by the device
-        scalar xmax itself, one correctly rounded product each), then the projection.  xmax:
-        a device scalar already holding max|x| (from the producing epilogue), else esb_absmax."""
+        """DDA over alpha_j = 2^E c_j, E the binary exponent of the device scalar xmax (the
+        plan's tables shifted by E), then the projection.  xmax: a device scalar already
+        holding max|x| (from the producing epilogue), else esb_absmax."""
         torch = self.torch
         alpha = torch.empty(1, dtype=torch.float32, device=x.device)
         codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
@@ -143,8 +154,10 @@ class ResNet18ESB:
             xmax = self.spare
             xmax.zero_()
             self._call("absmax", label, lambda: esb.esb_absmax(x, xmax, stream=self.sh), 4 * nel)
-        jobs = esb.dda_jobs([(x, self.n, self.ks, self.cgrid, alpha, None, xmax)])
-        self._call("dda", label, lambda: esb.esb_dda_align_batch(jobs, ws, stream=self.sh),
+        self._call("dda", label,
+                   lambda: esb.esb_dda_align_planned(x, self.n, self.ks, self.plan, GRID_POINTS,
+                                                     xmax, alpha_out=alpha, workspace=ws,
+                                                     stream=self.sh, want_D=False),
                    4 * nel)
         self._call("project", label,
                    lambda: esb.esb_project(x, alpha, self.n, self.ks, codes=codes, stream=self.sh),
@@ -185,6 +198,46 @@ class ResNet18ESB:
         self.last_q = (ax, cx)
         return y
 
+    def stem(self, x, xmax, absmax, out_alpha=None):
+        """conv1 with its ReLU and the 3x3 / stride-2 / pad-1 max pool in one call
+        (esb_conv2d_relu_maxpool): only the pooled output is written (and raises absmax),
+        as fp32 and, with out_alpha, as the next layer's codes.  xmax: the input's max|x|
+        for its DDA, or None when calib["conv1"] already holds the input's scale."""
+        torch = self.torch
+        L = self.layers["conv1"]
+        if xmax is None:
+            ax = self.calib["conv1"]
+            cx = esb.esb_project(x, ax, self.n, self.ks, stream=self.sh)
+        else:
+            ax, cx = self._quantize(x, self.ws["conv1"], xmax, "conv1")
+        Nb, H, W, C = cx.shape
+        st, pd = (L["stride"],) * 2, (L["pad"],) * 2
+        P, Q = esb.conv_out_hw(H, W, L["k"], L["k"], st, pd)
+        PP, QQ = esb.conv_out_hw(P, Q, 3, 3, (2, 2), (1, 1))
+        pooled = torch.empty((Nb, PP, QQ, L["cout"]), dtype=torch.float32, device=cx.device)
+        codes = (torch.empty((Nb, PP, QQ, L["cout"]), dtype=torch.uint8, device=cx.device)
+                 if out_alpha is not None else None)
+        ops = 2.0 * Nb * P * Q * L["cout"] * L["k"] * L["k"] * C
+        nbytes = cx.numel() + L["codes"].numel() + 4 * pooled.numel() + (
+            codes.numel() if codes is not None else 0)
+        self._call("contraction", "conv1",
+                   lambda: esb.esb_conv2d_relu_maxpool(
+                       cx, self.n, self.ks, ax, L["codes"], self.n, self.ks, L["alpha"],
+                       out_alpha=out_alpha, out_n=self.n, out_k_sig=self.ks, stride=st, pad=pd,
+                       y=pooled, codes=codes, want_codes=codes is not None, absmax=absmax,
+                       workspace=self.pool_ws, stream=self.sh),
+                   nbytes, ops)
+        if self.record:   # the full-resolution output, for the layer-by-layer comparison
+            self.units = None
+            acc, y, _ = esb.esb_conv2d_post(cx, self.n, self.ks, ax, L["codes"], self.n, self.ks,
+                                            L["alpha"], None, self.n, self.ks, relu=True,
+                                            stride=st, pad=pd, want_codes=False, want_acc=True,
+                                            want_y=True, stream=self.sh, workspace=self.cws)
+            self.trace.append(dict(name="conv1", x=x, alpha=ax, codes=cx, acc=acc, y=y,
+                                   pooled=pooled))
+        self.calib["conv1"] = ax
+        return pooled if codes is None else (pooled, codes)
+
     def forward(self, x, units=None):
         """The forward pass with per-layer DDA; units: a list that receives every library call
         of the pass (see _call)."""
@@ -200,16 +253,8 @@ class ResNet18ESB:
         m0 = slot()
         self._call("absmax", "image", lambda: esb.esb_absmax(x, m0, stream=self.sh), 4 * x.numel())
         m = slot()
-        a = self.conv("conv1", x, xmax=m0, relu=True, absmax=m)
-        # 3x3 max pool, stride 2, pad 1 (padding never wins); max|a| is unchanged
-        Nb, H, W, C = a.shape
-        P = (H + 2 - 3) // 2 + 1
-        pooled = torch.empty((Nb, P, P, C), dtype=torch.float32, device=a.device)
-        a_in = a
-        self._call("maxpool", "stem",
-                   lambda: esb.esb_maxpool2d(a_in, 3, 2, 1, out=pooled, stream=self.sh),
-                   4 * (a_in.numel() + pooled.numel()))
-        a = pooled
+        a = self.stem(x, m0, m)
+        self.units = units
         for stage in (1, 2, 3, 4):
             for blk in (0, 1):
                 p = "l%d.%d." % (stage, blk)
@@ -258,10 +303,7 @@ class ResNet18ESB:
         A = self.calib
         if "fc" not in A:
             raise RuntimeError("forward_fused needs the scales of a forward() first")
-        cx = esb.esb_project(x, A["conv1"], self.n, self.ks, stream=self.sh)
-        a, _ = self.conv_post("conv1", cx, relu=True, want_y=True)
-        a = esb.esb_maxpool2d(a, 3, 2, 1, stream=self.sh)
-        ca = esb.esb_project(a, A["l1.0.c1"], self.n, self.ks, stream=self.sh)
+        a, ca = self.stem(x, None, None, out_alpha=A["l1.0.c1"])
         blocks = [(s, b) for s in (1, 2, 3, 4) for b in (0, 1)]
         for i, (stage, blk) in enumerate(blocks):
             p = "l%d.%d." % (stage, blk)

@@ -49,9 +49,9 @@ def scale_grid(s, points=GRID_POINTS):
 
 def maxabs_grid_factors(cmax, points=GRID_POINTS):
     """Factors c_j = fl32((j+1) / (points * cmax)), j = 0..points-1, for the data-driven grid
-    alpha_j = fl32(max|x| * c_j) of the ResNet18 stack (cmax: the largest set value, so the
-    grid spans (0, max|x| / cmax]).  One fp32 product per candidate: it is computed the same
-    way on any device."""
+    alpha_j = 2^E c_j of the ResNet18 stack, E the binary exponent of max|x|
+    (2^(E-1) <= max|x| < 2^E; cmax: the largest set value, so the grid spans (0, 2^E / cmax]).
+    Multiplying by a power of two is exact: the grid is the same on any device."""
     j = np.arange(1, points + 1, dtype=np.float64)
     return (j / (points * float(cmax))).astype(np.float32)
 

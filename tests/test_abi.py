@@ -86,6 +86,20 @@ def test_argument_validation_without_launch(L):
     assert L.esb_absmax(fake, 10, None, None) == -1
     assert L.esb_absmax(None, 10, fake, None) == -1
     assert L.esb_absmax(None, 0, fake, None) == 0
+    # DDA plans: sizes, too small or unaligned plan buffers, missing arguments
+    assert L.esb_dda_plan_size(5, 3, 64) > 64 * 15 * 4
+    assert L.esb_dda_plan_size(5, 3, 0) == 0 and L.esb_dda_plan_size(9, 3, 64) == 0
+    assert L.esb_dda_plan_size(8, 7, 65) == 0                            # 65 * 127 > 8192
+    psz = L.esb_dda_plan_size(5, 3, 64)
+    assert L.esb_dda_plan(5, 3, fake, 64, fake, psz - 1, None) == -6
+    assert L.esb_dda_plan(5, 3, fake, 64, ctypes.c_void_p(0x1008), psz, None) == -6
+    assert L.esb_dda_plan(5, 3, None, 64, fake, psz, None) == -1
+    pl = L.esb_dda_align_planned
+    wsz = L.esb_dda_workspace_size(100, 5, 3, 64)
+    assert pl(fake, 100, 5, 3, fake, 64, fake, fake, None, fake, wsz - 1, None) == -6
+    assert pl(fake, 100, 5, 3, None, 64, fake, fake, None, fake, wsz, None) == -1
+    assert pl(fake, 100, 5, 3, fake, 64, None, fake, None, fake, wsz, None) == -1
+    assert pl(fake, 100, 5, 3, ctypes.c_void_p(0x1004), 64, fake, fake, None, fake, wsz, None) == -1
     # DDA with the static scratch: the same checks, and inputs beyond the scratch refused
     na = L.esb_dda_align_noalloc
     assert na(fake, 100, 8, 7, fake, 65, fake, None, None) == -1

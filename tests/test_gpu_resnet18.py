@@ -3,7 +3,7 @@ per-layer DDA on the device) against the same stack computed by the oracle from
 the same input images.
 
 The oracle quantizes every weight tensor and every layer input itself (DDA over
-the grid fl32(max|x| * c_j), projection) and runs the direct
+the grid 2^E c_j, E the binary exponent of max|x|, projection) and runs the direct
 convolutions; the glue between layers (ReLU, max pool, residual sums, the
 float64 average pool) is written again here in NumPy.  Each layer must agree
 exactly: the chosen alpha, every code, every int32 accumulator; the fp32
@@ -21,7 +21,10 @@ N, KS = 5, 3
 
 
 def grid_np(x, cmax):
-    return (np.float32(np.max(np.abs(x))) * wl.maxabs_grid_factors(cmax)).astype(np.float32)
+    """2^E c_j with E the binary exponent of max|x| (the stack's grid rule)."""
+    m = np.float32(np.max(np.abs(x)))
+    e = int(np.frexp(m)[1]) if m != 0 else 0
+    return np.ldexp(wl.maxabs_grid_factors(cmax), e).astype(np.float32)
 
 
 def quantize_np(x, cmax):
@@ -100,6 +103,8 @@ def test_resnet18_stack_matches_oracle(batch, seed):
 
     a = conv("conv1", x, relu)
     a = maxpool_np(a)
+    # the fused conv1 + ReLU + pool call wrote exactly the pooled tensor
+    np.testing.assert_array_equal(host(gpu["conv1"]["pooled"]).view(np.uint32), a.view(np.uint32))
     for stage in (1, 2, 3, 4):
         for blk in (0, 1):
             p = "l%d.%d." % (stage, blk)
