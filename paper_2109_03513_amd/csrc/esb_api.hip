@@ -532,8 +532,8 @@ size_t esb_conv2d_relu_maxpool_workspace_size(const esb_conv_desc* d, int nX, in
     int PP = 0, QQ = 0;
     if (!pool_dims(g, pool_window, pool_stride, pool_pad, &PP, &QQ)) return 0;
     const Fmt fx = make_fmt(nX, kX_sig), fw = make_fmt(nW, kW_sig);
-    // the fused kernel needs none (a 4-byte aligned input is assumed here)
-    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad, nullptr)) return 0;
+    // the fused kernel needs none
+    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad)) return 0;
     const auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
     return al((size_t)Mrows * (size_t)d->K * sizeof(float)) +
            al((size_t)d->N * PP * QQ * (size_t)d->K * sizeof(float));
@@ -559,7 +559,7 @@ int esb_conv2d_relu_maxpool(const esb_conv_desc* d, const uint8_t* x, int nX, in
     if (st) return st;
     const hipStream_t s = (hipStream_t)stream;
     const Post P = make_post(post);
-    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad, x)) {
+    if (stem_fits(g, d->K, d->groups, fx, fw, pool_window, pool_stride, pool_pad)) {
         if (Mrows == 0) return ESB_OK;
         return hip_status(launch_stem(g, x, fx, alphaX, w, fw, alphaW, y, PP, QQ, P, s));
     }

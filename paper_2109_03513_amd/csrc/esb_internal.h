@@ -398,7 +398,7 @@ hipError_t launch_absmax(const float* x, int64_t len, float* absmax, hipStream_t
 // post-processing with a ReLU, and the 3x3 / stride-2 / pad-1 max pool, fused;
 // y (or post.codes) receives the pooled outputs [N, PP, QQ, 64].
 bool stem_fits(const ConvGeom& g, int K, int groups, const Fmt& fx, const Fmt& fw, int pool_r,
-               int pool_stride, int pool_pad, const uint8_t* x);
+               int pool_stride, int pool_pad);
 hipError_t launch_stem(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                        const uint8_t* w, const Fmt& fw, const float* alphaW, float* y, int PP,
                        int QQ, const Post& post, hipStream_t s);

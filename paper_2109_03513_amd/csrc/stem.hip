@@ -8,7 +8,8 @@
 // batch 64: 205 MB of fp32) that the pool reads back.  Here a workgroup owns
 // an 8 x 8 tile of pooled outputs and all 64 output channels:
 //   * the input patch under the tile's 17 x 17 convolution outputs (39 x 39
-//     pixels for a 7 x 7 filter) is loaded once, decoded to exact int8
+//     pixels for a 7 x 7 filter; fetched while the previous tile's MFMAs run,
+//     positions outside the image as the +0 code) is decoded to exact int8
 //     integers m = q 2^k and kept in LDS in eight copies shifted by 0, 2, ...,
 //     14 bytes, so that every 16-byte piece of a filter row, which starts at
 //     an even byte, is one aligned LDS read;
@@ -44,85 +45,79 @@ constexpr int KO = 64;                   // output channels
 constexpr int RMAX = 8;                  // filter rows
 constexpr int PROWS = 2 * (CR - 1) + RMAX;   // input rows of a patch (<= 40)
 constexpr int ROWB = 128;                // bytes of one stored patch row (one copy)
+constexpr int CSTR = ROWB + 16;          // LDS stride of the copies: 9 bank groups of 16 bytes,
+                                         // so that the lanes of an MFMA read (pixels at
+                                         // different copies) spread over the banks
 constexpr int NCOPY = 8;                 // copies shifted by 2 v bytes, v = 0..7
-constexpr int STAGE_DW = ROWB / 4 + 2;   // decoded row as fetched (dword aligned), + 2 spare
+constexpr int STAGE_DW = ROWB / 4 + 4;   // a decoded patch row (+ spare dwords, zero)
+constexpr int WST = RMAX * 32 + 16;      // LDS bytes per output channel of the filter: 68
+                                         // dwords, so that the 16 lanes of a 16-byte read
+                                         // (16 channels) take 16 different groups of 4 banks
+constexpr int CTS = 40;                  // fp32 stride of an output row in the LDS tile: the
+                                         // two lane halves of a write (rows 4 apart) are 160
+                                         // dwords = 32 banks apart
+constexpr int PATCH_BYTES = PROWS * NCOPY * CSTR;
+constexpr int CT_BYTES = 32 * MB * CTS * 4;
+constexpr int TILE_BYTES = PATCH_BYTES > CT_BYTES ? PATCH_BYTES : CT_BYTES;
+constexpr int kFetch = PROWS * ROWB / 512;   // patch bytes fetched per thread (10 at 512 threads)
 
 struct StemParams {
-    ConvGeom g;                // input N, H, W, C; filter R, S; stride 2; pads; P x Q outputs
-    int PP, QQ;                // pooled outputs
-    int tiles_p, tiles_q, ntiles;
-    const uint8_t* x;
-    const uint8_t* w;
-    DecodeInfo dx, dw;
+    const uint8_t* x;          // input codes [N, H, W, C]
+    const uint8_t* w;          // filter codes [64, R, S, C]
+    float* y;                  // pooled fp32 [N, PP, QQ, 64], or NULL
     const float* alphaX;
     const float* alphaW;
+    DecodeInfo dx, dw;
+    Post post;                 // a, b, codes / alpha / pp, absmax (ReLU always)
+    int N, H, W, R, S, ph, pw, P, Q, PP, QQ;
+    int tiles_p, tiles_q, ntiles;
     int kX, kW;
-    float* y;                  // pooled fp32 [N, PP, QQ, 64], or NULL
-    Post post;                 // a, b, relu (on), codes / alpha / pp, absmax
+    uint32_t zero_code;        // the +0 code of the input format (outside the image)
 };
 
-__device__ __forceinline__ uint32_t decode4x(uint32_t w, const DecodeInfo& d) {
-    if (d.mode == 0) {
-        uint32_t r = 0;
-#pragma unroll
-        for (int b = 0; b < 4; b++) {
-            uint32_t c = (w >> (8 * b)) & ((1u << d.n) - 1u);
-            const uint32_t s = (c >> (d.n - 1)) & 1u;
-            const uint32_t e = (c >> d.k) & (uint32_t)d.emax;
-            const uint32_t f = c & ((1u << d.k) - 1u);
-            const int m = (e == (uint32_t)d.emax) ? (int)f : (int)(((1u << d.k) | f) << e);
-            r |= ((uint32_t)(s ? -m : m) & 0xffu) << (8 * b);
-        }
-        return r;
-    }
-    const uint32_t sel = w & 0x07070707u;
-    const uint32_t r0 = __builtin_amdgcn_perm(d.lut[1], d.lut[0], sel);
-    if (d.mode == 3) return r0;
-    const uint32_t r1 = __builtin_amdgcn_perm(d.lut[3], d.lut[2], sel);
-    const uint32_t m3 = ((w >> 3) & 0x01010101u) * 0xffu;
-    const uint32_t r01 = (r1 & m3) | (r0 & ~m3);
-    if (d.mode == 4) return r01;
-    const uint32_t r2 = __builtin_amdgcn_perm(d.lut[5], d.lut[4], sel);
-    const uint32_t r3 = __builtin_amdgcn_perm(d.lut[7], d.lut[6], sel);
-    const uint32_t r23 = (r3 & m3) | (r2 & ~m3);
-    const uint32_t m4 = ((w >> 4) & 0x01010101u) * 0xffu;
-    return (r23 & m4) | (r01 & ~m4);
+__device__ __forceinline__ int decode_byte(uint32_t c, const DecodeInfo& d) {
+    c &= (1u << d.n) - 1u;
+    const uint32_t sg = (c >> (d.n - 1)) & 1u;
+    const uint32_t e = (c >> d.k) & (uint32_t)d.emax;
+    const uint32_t f = c & ((1u << d.k) - 1u);
+    const int m = (e == (uint32_t)d.emax) ? (int)f : (int)(((1u << d.k) | f) << e);
+    return sg ? -m : m;
 }
 
-__global__ __launch_bounds__(kThreads) void k_stem(StemParams p) {
-    // patch: [PROWS][NCOPY][ROWB] int8; after the MFMAs the same bytes hold the
-    // rectified outputs of one channel half, [NPIX][32] fp32
-    __shared__ __align__(16) uint8_t patch[PROWS * NCOPY * ROWB];
+// Four waves per SIMD: two workgroups share a CU (LDS and registers fit).
+template <int C>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void k_stem(StemParams p) {
+    // patch: [PROWS][NCOPY][CSTR] int8; after the MFMAs the same bytes hold the
+    // rectified outputs of one channel half, [32 MB][CTS] fp32
+    __shared__ __align__(16) uint8_t patch[TILE_BYTES];
     __shared__ __align__(16) uint32_t stage[PROWS * STAGE_DW];
-    __shared__ __align__(16) uint8_t wlds[KO * RMAX * 32];   // the decoded filter
-    const ConvGeom& g = p.g;
+    __shared__ __align__(16) uint8_t wlds[KO * WST];          // the decoded filter
+    __shared__ int8_t xlut[256];                             // code -> m of the input format
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = wave & 1;                 // output channels 32 half .. 32 half + 31
     const int mb0 = wave >> 1;                 // M blocks mb0, mb0 + WGR, ...
-    const int R = g.R, C = g.C, SC = g.S * g.C;
-    const int prow_n = 2 * (CR - 1) + R;       // patch rows used
-    const int pbytes = (2 * (CC - 1) + g.S) * C;   // bytes of a patch row used
+    const int R = p.R, SC = p.S * C;
 
-    // the filter, decoded once into LDS as 64 x R rows of 32 bytes (zero past
-    // S*C); lane l reads the B fragment of channel 32 half + l % 32, bytes
-    // 16 (l / 32) .. + 15 of the row of filter row r
-    for (int it = tid; it < KO * R * 8; it += kThreads) {
-        const int n = it / (R * 8), r = (it / 8) % R, t4 = it % 8;
-        uint32_t v = 0u;
-#pragma unroll
-        for (int b = 0; b < 4; b++) {
-            const int j = 4 * t4 + b;
-            if (j < SC) {
-                const uint32_t code = p.w[((int64_t)n * R + r) * SC + j];
-                v |= (decode4x(code, p.dw) & 0xffu) << (8 * b);
-            }
-        }
-        *(uint32_t*)&wlds[(n * R + r) * 32 + 4 * t4] = v;
+    // decode tables and the filter, once: the filter as 64 x RMAX rows of 32 bytes
+    // (zero past S*C and for rows past R); lane l later reads the B fragment of
+    // channel 32 half + l % 32, bytes 16 (l / 32) .. + 15 of the row of filter row r
+    if (tid < 256) xlut[tid] = (int8_t)decode_byte((uint32_t)tid, p.dx);
+    for (int it = tid; it < KO * RMAX * 32; it += kThreads) {
+        const int n = it / (RMAX * 32), r = (it / 32) % RMAX, j = it % 32;
+        int m = 0;
+        if (r < R && j < SC) m = decode_byte(p.w[((int64_t)n * R + r) * SC + j], p.dw);
+        wlds[n * WST + r * 32 + j] = (uint8_t)m;
     }
-    const int boff = ((32 * half + (lane & 31)) * R) * 32 + 16 * (lane >> 5);
+    const int boff = (32 * half + (lane & 31)) * WST + 16 * (lane >> 5);
+    for (int it = tid; it < PROWS * STAGE_DW; it += kThreads) stage[it] = 0u;
     const float s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kX + p.kW));
     const float qa = post_alpha(p.post);
+    const bool qok = alpha_valid(qa), qfast = fast_scale(qa);
+    const float qr = 1.0f / qa;
+    // 16-byte stores of y, 4-byte stores of the codes where the pointers allow
+    const bool vec_out = (uintptr_t)p.y % 16 == 0 && (uintptr_t)p.post.codes % 4 == 0;
     uint32_t amax = 0;
     const int lr = lane & 31, lg = lane >> 5;
 
@@ -136,152 +131,171 @@ __global__ __launch_bounds__(kThreads) void k_stem(StemParams p) {
         if (mb < MB && pix < NPIX) {
             const int tr = pix / CC, tc = pix - tr * CC;
             const int o = 2 * tc * C + 16 * lg;
-            off = (2 * tr * NCOPY + ((o & 15) >> 1)) * ROWB + (o & ~15);
+            off = (2 * tr * NCOPY + ((o & 15) >> 1)) * CSTR + (o & ~15);
         }
         aoff[i] = off;
     }
 
-    for (int tile = blockIdx.x; tile < p.ntiles; tile += gridDim.x) {
-        const int img = tile / (p.tiles_p * p.tiles_q);
-        const int rem = tile - img * p.tiles_p * p.tiles_q;
-        const int pp0 = (rem / p.tiles_q) * TP, qq0 = (rem % p.tiles_q) * TQ;
-        const int cr0 = 2 * pp0 - 1, cc0 = 2 * qq0 - 1;     // conv position of tile row 0
-        const int ih0 = 2 * cr0 - g.ph, iw0 = 2 * cc0 - g.pw;  // input position of patch (0, 0)
-
-        // ---- the patch: fetch whole dwords of each row, decode, zero what lies
-        //      outside the image; then the eight shifted copies.  Row pr of the
-        //      patch starts `lead` bytes into the dword it is fetched with.
-        const int64_t gb0 = ((int64_t)iw0) * C;                  // byte of column iw0 in a row
-        auto row_base = [&](int pr) {                            // byte of the input row
-            return ((int64_t)img * g.H + (ih0 + pr)) * g.W * C;
-        };
-        auto row_lead = [&](int pr) {
-            return (int)((((row_base(pr) + gb0) % 4) + 4) % 4);
-        };
-        const int ndw = (3 + pbytes + 3) / 4;                    // dwords fetched per row
-        for (int it = tid; it < prow_n * ndw; it += kThreads) {
-            const int pr = it / ndw, q = it - pr * ndw;
-            const int ih = ih0 + pr;
-            uint32_t v = 0u;
-            if ((unsigned)ih < (unsigned)g.H) {
-                const int64_t rowb = row_base(pr);
-                const int64_t rowe = rowb + (int64_t)g.W * C;
-                const int64_t a = rowb + gb0 - row_lead(pr) + 4 * q;   // first byte of the dword
-                uint32_t raw = 0u, keep = 0u;
-                if (a >= rowb && a + 4 <= rowe) {
-                    raw = *(const uint32_t*)(p.x + a);
-                    keep = 0xffffffffu;
-                } else {
+    // The patch of a tile: byte bb of row pr is input row ih0 + pr, column
+    // iw0 + bb / C, channel bb % C; bytes outside the image are the +0 code.
+    // Thread t fetches byte bb = t % 128 of rows t / 128 + 4 u (512 threads); the
+    // bytes of the next tile are in flight while the current tile's MFMAs run.
+    static_assert(kThreads == 4 * ROWB && PROWS % 4 == 0, "fetch layout");
+    const int tiles_img = p.tiles_p * p.tiles_q;
+    const int fbb = tid & (ROWB - 1), fpr = tid >> 7;
+    const int fcol = fbb / C, fch = fbb - fcol * C;
+    const int rowstride = 4 * p.W * C;          // bytes between rows fpr + 4 u and + 4 (u + 1)
+    const int imgbytes = p.H * p.W * C;         // < 2^31 (checked by the launcher)
+    uint32_t raw[kFetch];
+    auto fetch = [&](int tile) {
+        const int img = tile / tiles_img, rem = tile - img * tiles_img;
+        const int tp = rem / p.tiles_q, tq = rem - tp * p.tiles_q;
+        const int ih = 2 * (2 * tp * TP - 1) - p.ph + fpr;
+        const int iw = 2 * (2 * tq * TQ - 1) - p.pw + fcol;
+        const bool colin = (unsigned)iw < (unsigned)p.W;
+        const uint8_t* xi = p.x + (int64_t)img * imgbytes;
+        int off = (ih * p.W + (colin ? iw : 0)) * C + fch;
 #pragma unroll
-                    for (int b = 0; b < 4; b++)
-                        if (a + b >= rowb && a + b < rowe) {
-                            raw |= (uint32_t)p.x[a + b] << (8 * b);
-                            keep |= 0xffu << (8 * b);
-                        }
-                }
-                v = decode4x(raw, p.dx) & keep;
-            }
-            stage[pr * STAGE_DW + q] = v;
+        for (int u = 0; u < kFetch; u++) {
+            const bool in = colin && (unsigned)(ih + 4 * u) < (unsigned)p.H;
+            const uint32_t c = xi[in ? off : 0];
+            raw[u] = in ? c : p.zero_code;
+            off += rowstride;
         }
-        for (int it = tid; it < prow_n * STAGE_DW; it += kThreads) {   // dwords past ndw: zero
-            const int pr = it / STAGE_DW, q = it - pr * STAGE_DW;
-            if (q >= ndw) stage[it] = 0u;
-        }
-        __syncthreads();
-        // copy v, dword d: patch bytes 4 d + 2 v .. + 3, i.e. stage bytes from lead + 4 d + 2 v
-        for (int it = tid; it < prow_n * NCOPY * (ROWB / 4); it += kThreads) {
-            const int d = it % (ROWB / 4);
-            const int rv = it / (ROWB / 4);
-            const int v = rv % NCOPY, pr = rv / NCOPY;
-            const int sb = row_lead(pr) + 4 * d + 2 * v;          // stage byte
-            const int sq = sb >> 2, sh = sb & 3;
-            const uint32_t lo = sq < STAGE_DW ? stage[pr * STAGE_DW + sq] : 0u;
-            const uint32_t hi = sq + 1 < STAGE_DW ? stage[pr * STAGE_DW + sq + 1] : 0u;
-            const uint32_t val = sh ? __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)sh) : lo;
-            *(uint32_t*)&patch[(pr * NCOPY + v) * ROWB + 4 * d] = val;
-        }
-        __syncthreads();
+    };
+    if (blockIdx.x < p.ntiles) fetch(blockIdx.x);
+    __syncthreads();   // the decode table, filter and zeroed stage are in place
 
-        // ---- the contraction: one 32x32x32 int8 MFMA per filter row and block
+    for (int tile = blockIdx.x; tile < p.ntiles; tile += gridDim.x) {
+        const int img = tile / tiles_img, rem = tile - img * tiles_img;
+        const int tp = rem / p.tiles_q, tq = rem - tp * p.tiles_q;
+        const int pp0 = tp * TP, qq0 = tq * TQ;
+        const int cr0 = 2 * pp0 - 1, cc0 = 2 * qq0 - 1;     // conv position of tile row 0
+
+        // ---- decode into the stage, then the eight shifted copies
+        uint8_t* stage8 = (uint8_t*)stage;
+#pragma unroll
+        for (int u = 0; u < kFetch; u++)
+            stage8[(fpr + 4 * u) * (STAGE_DW * 4) + fbb] = (uint8_t)xlut[raw[u] & 0xffu];
+        __syncthreads();
+        // copy v, dword d: patch bytes 4 d + 2 v .. + 3 = stage dword d + v / 2,
+        // shifted by 2 bytes for odd v; one thread per (row, dword), all copies
+        for (int it = tid; it < PROWS * (ROWB / 4); it += kThreads) {
+            const int d = it % (ROWB / 4), pr = it / (ROWB / 4);
+            uint32_t sw[5];
+#pragma unroll
+            for (int u = 0; u < 5; u++) sw[u] = stage[pr * STAGE_DW + d + u];
+#pragma unroll
+            for (int v = 0; v < NCOPY; v++) {
+                const uint32_t val = (v & 1) ? __builtin_amdgcn_alignbyte(sw[(v >> 1) + 1], sw[v >> 1], 2u)
+                                             : sw[v >> 1];
+                *(uint32_t*)&patch[(pr * NCOPY + v) * CSTR + 4 * d] = val;
+            }
+        }
+        __syncthreads();
+        if (tile + (int)gridDim.x < p.ntiles) fetch(tile + gridDim.x);   // in flight below
+
+        // ---- the contraction: one 32x32x32 int8 MFMA per filter row and block;
+        //      the A fragments of filter row r + 1 are read while those of r run
         v16i acc[MBW];
 #pragma unroll
         for (int i = 0; i < MBW; i++)
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[i][r] = 0;
-        // A fragments of filter row r + 1 are read while the MFMAs of row r run
         v4i fa[2][MBW];
 #pragma unroll
         for (int i = 0; i < MBW; i++) fa[0][i] = *(const v4i*)&patch[aoff[i]];
+        // all RMAX filter rows: the rows past R are zero in the filter copy, and
+        // the patch rows they read (2 * 16 + 7 at most) are inside the patch
 #pragma unroll
         for (int r = 0; r < RMAX; r++) {
-            if (r < R) {
-                if (r + 1 < R) {
-#pragma unroll
-                    for (int i = 0; i < MBW; i++)
-                        fa[(r + 1) & 1][i] = *(const v4i*)&patch[aoff[i] + (r + 1) * NCOPY * ROWB];
-                }
-                const v4i bf = *(const v4i*)&wlds[boff + 32 * r];
+            if (r + 1 < RMAX) {
 #pragma unroll
                 for (int i = 0; i < MBW; i++)
-                    if (mb0 + WGR * i < MB)
-                        acc[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[r & 1][i], bf, acc[i], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
+                    fa[(r + 1) & 1][i] = *(const v4i*)&patch[aoff[i] + (r + 1) * NCOPY * CSTR];
             }
+            const v4i bf = *(const v4i*)&wlds[boff + 32 * r];
+#pragma unroll
+            for (int i = 0; i < MBW; i++)
+                if (mb0 + WGR * i < MB)
+                    acc[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[r & 1][i], bf, acc[i], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();   // every read of the patch is done
 
-        // ---- per channel half: the scaled sums into LDS, then the post-processing,
-        //      the ReLU and the pool (conv positions outside the output left out)
-        float* ct = (float*)patch;                  // [NPIX][32]
+        // ---- per channel half: the post-processed, rectified outputs into LDS,
+        //      then the pool (tiles at the image border leave out the conv
+        //      positions outside the output: every value is >= 0 and every window
+        //      holds a position inside)
+        const bool interior = cr0 >= 0 && cr0 + CR <= p.P && cc0 >= 0 && cc0 + CC <= p.Q;
+        float* ct = (float*)patch;                  // [32 MB][CTS]
 #pragma unroll 1
         for (int hh = 0; hh < 2; hh++) {
             if (half == hh) {
+                const int ch = 32 * hh + lr;
+                const float pa = p.post.a ? p.post.a[ch] : 1.0f;
+                const float pb = p.post.b ? p.post.b[ch] : 0.0f;
                 // register r of block mb is row 32 mb + 8 (r / 4) + 4 lg + r % 4: one base
                 // address per block, the rest immediate offsets
 #pragma unroll
                 for (int i = 0; i < MBW; i++) {
                     const int mb = mb0 + WGR * i;
-                    float* base = ct + (32 * mb + 4 * lg) * 32 + lr;
-                    if (32 * mb + 31 < NPIX) {
+                    float* base = ct + (32 * mb + 4 * lg) * CTS + lr;
+                    if (mb < MB) {
 #pragma unroll
-                        for (int r = 0; r < 16; r++)
-                            base[(8 * (r >> 2) + (r & 3)) * 32] = s * (float)acc[i][r];
-                    } else if (mb < MB) {
-#pragma unroll
-                        for (int r = 0; r < 16; r++)
-                            if (32 * mb + 8 * (r >> 2) + 4 * lg + (r & 3) < NPIX)
-                                base[(8 * (r >> 2) + (r & 3)) * 32] = s * (float)acc[i][r];
+                        for (int r = 0; r < 16; r++) {
+                            // rows NPIX .. 32 MB - 1 are written too and never read
+                            const float z = __builtin_fmaf(pa, s * (float)acc[i][r], pb);
+                            base[(8 * (r >> 2) + (r & 3)) * CTS] = z > 0.0f ? z : 0.0f;
+                        }
                     }
                 }
             }
             __syncthreads();
-            const int c = tid & 31, ch = 32 * hh + c;
-            const float pa = p.post.a ? p.post.a[ch] : 1.0f;
-            const float pb = p.post.b ? p.post.b[ch] : 0.0f;
-#pragma unroll 2
-            for (int k = 0; k < (TP * TQ * 32) / kThreads; k++) {
-                const int pi = (tid >> 5) + k * (kThreads / 32);
-                const int pr = pi / TQ, pc = pi - pr * TQ;
-                const int pp = pp0 + pr, qq = qq0 + pc;
-                float m = 0.0f;
+            // four channels of one pooled output per thread: lanes 8 apart take pooled
+            // columns 2 apart (conv outputs 4 apart, 160 dwords), so each 16-lane
+            // group of a 16-byte read covers the 64 banks once
+            {
+                const int quad = tid & 7, j = tid >> 3;
+                const int pr = j >> 3, pc = 2 * (j & 1) + ((j >> 1) & 1) + 4 * ((j >> 2) & 1);
+                const float* t = ct + ((2 * pr) * CC + 2 * pc) * CTS + 4 * quad;
+                // rectified values are >= 0 and never NaN: their bit patterns order
+                // as unsigned integers
+                uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
 #pragma unroll
                 for (int dr = 0; dr < 3; dr++) {
-                    const bool rin = (unsigned)(cr0 + 2 * pr + dr) < (unsigned)g.P;
+                    const bool rin = interior || (unsigned)(cr0 + 2 * pr + dr) < (unsigned)p.P;
 #pragma unroll
                     for (int dc = 0; dc < 3; dc++) {
-                        const bool in = rin && (unsigned)(cc0 + 2 * pc + dc) < (unsigned)g.Q;
-                        float z = __builtin_fmaf(pa, ct[((2 * pr + dr) * CC + 2 * pc + dc) * 32 + c], pb);
-                        z = z > 0.0f ? z : 0.0f;
-                        m = in ? fmaxf(m, z) : m;
+                        const bool in = rin && (interior || (unsigned)(cc0 + 2 * pc + dc) < (unsigned)p.Q);
+                        const f32x4 v = *(const f32x4*)(t + (dr * CC + dc) * CTS);
+                        if (in) {
+                            m0 = max(m0, __float_as_uint(v.x));
+                            m1 = max(m1, __float_as_uint(v.y));
+                            m2 = max(m2, __float_as_uint(v.z));
+                            m3 = max(m3, __float_as_uint(v.w));
+                        }
                     }
                 }
+                const int pp = pp0 + pr, qq = qq0 + pc;
                 if (pp < p.PP && qq < p.QQ) {
-                    const int64_t o = (((int64_t)img * p.PP + pp) * p.QQ + qq) * KO + ch;
-                    if (p.y) p.y[o] = m;
-                    if (p.post.codes)
-                        p.post.codes[o] = (uint8_t)(alpha_valid(qa) ? esb_code(m, qa, p.post.pp)
-                                                                    : p.post.pp.zero_code);
-                    amax = max(amax, __float_as_uint(m) & 0x7fffffffu);
+                    const int64_t o = (((int64_t)img * p.PP + pp) * p.QQ + qq) * KO + 32 * hh + 4 * quad;
+                    const f32x4 v = {__uint_as_float(m0), __uint_as_float(m1), __uint_as_float(m2),
+                                     __uint_as_float(m3)};
+                    const uint32_t c4 = p.post.codes == nullptr ? 0u
+                                        : qok ? code4(v, qa, qr, qfast, p.post.pp)
+                                              : p.post.pp.zero_code * 0x01010101u;
+                    if (vec_out) {
+                        if (p.y) *(f32x4*)(p.y + o) = v;
+                        if (p.post.codes) *(uint32_t*)(p.post.codes + o) = c4;
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < 4; c++) {
+                            if (p.y) p.y[o + c] = v[c];
+                            if (p.post.codes) p.post.codes[o + c] = (uint8_t)(c4 >> (8 * c));
+                        }
+                    }
+                    amax = max(amax, max(max(m0, m1), max(m2, m3)));
                 }
             }
             __syncthreads();
@@ -293,19 +307,20 @@ __global__ __launch_bounds__(kThreads) void k_stem(StemParams p) {
 }  // namespace
 
 bool stem_fits(const ConvGeom& g, int K, int groups, const Fmt& fx, const Fmt& fw, int pool_r,
-               int pool_stride, int pool_pad, const uint8_t* x) {
+               int pool_stride, int pool_pad) {
     return groups == 1 && K == KO && g.sh == 2 && g.sw == 2 && g.C >= 1 && g.C <= 3 &&
-           (uintptr_t)x % 4 == 0 &&
            g.S * g.C <= 32 && g.R >= 1 && g.R <= RMAX && g.S >= 1 && pool_r == 3 &&
            pool_stride == 2 && pool_pad == 1 && fx.max_int <= 127 && fw.max_int <= 127 &&
-           g.P >= 1 && g.Q >= 1 && (int64_t)g.R * g.S * g.C * fx.max_int * fw.max_int <= 0x7fffffff;
+           g.P >= 1 && g.Q >= 1 && (int64_t)g.H * g.W * g.C < ((int64_t)1 << 31) &&
+           (int64_t)g.R * g.S * g.C * fx.max_int * fw.max_int <= 0x7fffffff;
 }
 
 hipError_t launch_stem(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
                        const uint8_t* w, const Fmt& fw, const float* alphaW, float* y, int PP,
                        int QQ, const Post& post, hipStream_t s) {
     StemParams p;
-    p.g = g;
+    p.N = g.Nb; p.H = g.H; p.W = g.W; p.R = g.R; p.S = g.S; p.ph = g.ph; p.pw = g.pw;
+    p.P = g.P; p.Q = g.Q;
     p.PP = PP;
     p.QQ = QQ;
     p.tiles_p = (PP + TP - 1) / TP;
@@ -318,6 +333,7 @@ hipError_t launch_stem(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const
     p.w = w;
     p.dx = decode_info(fx);
     p.dw = decode_info(fw);
+    p.zero_code = fx.zero_code;
     p.alphaX = alphaX;
     p.alphaW = alphaW;
     p.kX = fx.k;
@@ -326,7 +342,9 @@ hipError_t launch_stem(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const
     p.post = post;
     int64_t blocks = (int64_t)num_cus() * 2;   // two workgroups fit a CU (LDS, registers)
     if (blocks > nt) blocks = nt;
-    k_stem<<<(unsigned)blocks, kThreads, 0, s>>>(p);
+    if (g.C == 1) k_stem<1><<<(unsigned)blocks, kThreads, 0, s>>>(p);
+    else if (g.C == 2) k_stem<2><<<(unsigned)blocks, kThreads, 0, s>>>(p);
+    else k_stem<3><<<(unsigned)blocks, kThreads, 0, s>>>(p);
     return hipGetLastError();
 }
 

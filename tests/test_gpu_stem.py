@@ -109,3 +109,31 @@ def test_fused_equals_conv_then_pool(esb):
                                   want_y=True)
     p = esb.esb_maxpool2d(z, 3, 2, 1)
     np.testing.assert_array_equal(host(y).view(np.uint32), host(p).view(np.uint32))
+
+
+@pytest.mark.parametrize("qa", [0.35, 1e-38])
+def test_stem_unaligned_outputs_and_scales(esb, qa):
+    """Outputs one element past a 16-byte boundary take the per-channel stores, and a
+    subnormal output scale takes the exact (division) code path: both bit-exact."""
+    torch = torch_cuda()
+    Nb, H, W, C, R = 2, 45, 38, 3, 7
+    x = wl.random_codes(95, (Nb, H, W, C), 8)
+    w = wl.random_codes(96, (64, R, R, C), 8)
+    qa = np.float32(qa)
+    pooled, codes = reference(x, w, (5, 3), (5, 3), (2, 2), (3, 3), None, None, qa, (5, 3),
+                              (3, 2, 1))
+    n = pooled.size
+    ybuf = torch.zeros(n + 1, dtype=torch.float32, device="cuda")
+    cbuf = torch.zeros(n + 1, dtype=torch.uint8, device="cuda")
+    y = ybuf[1:].view(pooled.shape)
+    c = cbuf[1:].view(pooled.shape)
+    assert y.data_ptr() % 16 != 0 and c.data_ptr() % 4 != 0
+    amax = scalar(0.0)
+    log("stem unaligned outputs qa=%g" % qa)
+    esb.esb_conv2d_relu_maxpool(dev(x), 5, 3, scalar(ALPHA_X), dev(w), 5, 3, scalar(ALPHA_W),
+                                out_alpha=scalar(qa), out_n=5, out_k_sig=3, stride=(2, 2),
+                                pad=(3, 3), y=y, codes=c, want_codes=True, absmax=amax)
+    np.testing.assert_array_equal(host(y).view(np.uint32), pooled.view(np.uint32))
+    np.testing.assert_array_equal(host(c), codes)
+    assert host(ybuf)[0] == 0 and host(cbuf)[0] == 0
+    assert host(amax)[0] == np.max(pooled)
