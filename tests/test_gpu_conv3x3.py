@@ -1,0 +1,98 @@
+"""The direct 3x3 / stride-1 / pad-1 convolution kernel (64 input and 64 output channels on
+the fp8 MFMA; tiles of 256 output pixels over the batch, crossing image boundaries) against
+the oracle's convolution and post-processing: bit-exact int32 sums, fp32 outputs and codes,
+equal running maximum; and bit for bit equal to the implicit-GEMM path, which an input one
+byte off a 16-byte boundary takes."""
+import numpy as np
+import pytest
+
+import oracle
+from gpuutil import dev, host, log, scalar, torch_cuda
+from paper_2109_03513_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+ALPHA_X, ALPHA_W = 0.43, 0.027
+C = K = 64
+
+
+@pytest.fixture(scope="module")
+def esb():
+    from paper_2109_03513_amd import esb as e
+    e.lib()
+    return e
+
+
+def unaligned(torch, a):
+    """A device copy of the uint8 array a whose data starts one byte past a 16-byte boundary."""
+    buf = torch.empty(a.size + 16, dtype=torch.uint8, device="cuda")
+    v = buf[1:1 + a.size].view(a.shape)
+    v.copy_(torch.from_numpy(np.ascontiguousarray(a)))
+    assert v.data_ptr() % 16 == 1
+    return v
+
+
+CASES = [
+    # N, H, W, fx, fw, variant
+    (2, 56, 56, (5, 3), (5, 3), "plain"),     # the ResNet18 l1 shape, batch 2
+    (3, 7, 7, (5, 3), (5, 3), "all"),         # 49-pixel images: a tile spans six of them
+    (1, 13, 5, (4, 2), (5, 3), "relu"),       # H != W, ragged last tile, mixed formats
+    (2, 9, 62, (5, 3), (4, 2), "residual"),   # widest rows taken (Q + 2 = 64)
+    (1, 1, 1, (5, 3), (5, 3), "affine"),      # one pixel
+    (4, 17, 23, (6, 3), (4, 1), "all"),       # ESB(6,3) x ESB(4,1)
+]
+
+
+def post_params(seed, y, variant):
+    r = np.random.default_rng(seed)
+    sd = float(np.std(y)) or 1.0
+    a = b = res = None
+    if variant in ("affine", "all"):
+        a = r.uniform(-0.5, 1.5, K).astype(np.float32)
+        b = (r.standard_normal(K) * 0.3 * sd).astype(np.float32)
+    if variant in ("residual", "all"):
+        res = (r.standard_normal(y.shape) * sd).astype(np.float32)
+    relu = variant in ("relu", "all")
+    return a, b, res, relu, np.float32(0.4 * sd)
+
+
+@pytest.mark.parametrize("Nb,H,W,fx,fw,variant", CASES)
+def test_conv3x3_direct(esb, Nb, H, W, fx, fw, variant):
+    torch = torch_cuda()
+    x = wl.random_codes(40 + H, (Nb, H, W, C), fx[0])
+    w = wl.random_codes(41 + W, (K, 3, 3, C), fw[0])
+    st, acc_o, y_o = oracle.conv2d(x, w, fx[0], fx[1], ALPHA_X, fw[0], fw[1], ALPHA_W,
+                                   stride=(1, 1), pad=(1, 1))
+    assert st == 0
+    log("conv3x3 direct %s %s" % ((Nb, H, W, fx, fw), variant))
+    if variant == "plain":
+        for want_acc in (True, False):
+            acc, y = esb.esb_conv2d(dev(x), fx[0], fx[1], scalar(ALPHA_X), dev(w), fw[0], fw[1],
+                                    scalar(ALPHA_W), stride=(1, 1), pad=(1, 1), want_acc=want_acc)
+            np.testing.assert_array_equal(host(y).view(np.uint32), y_o.view(np.uint32))
+            if want_acc:
+                np.testing.assert_array_equal(host(acc), acc_o)
+        acc_u, y_u = esb.esb_conv2d(unaligned(torch, x), fx[0], fx[1], scalar(ALPHA_X), dev(w),
+                                    fw[0], fw[1], scalar(ALPHA_W), stride=(1, 1), pad=(1, 1))
+        np.testing.assert_array_equal(host(acc_u), acc_o)
+        np.testing.assert_array_equal(host(y_u).view(np.uint32), y_o.view(np.uint32))
+        return
+    a, b, res, relu, qa = post_params(7, y_o, variant)
+    z_o, codes_o = oracle.post(y_o.reshape(-1, K), 5, 3, qa, a=a, bias=b,
+                               res=None if res is None else res.reshape(-1, K), relu=relu)
+    z_o = z_o.reshape(y_o.shape)
+    codes_o = codes_o.reshape(y_o.shape)
+    outs = []
+    for xin, want_acc in ((dev(x), True), (dev(x), False), (unaligned(torch, x), True)):
+        amax = scalar(0.0)
+        acc, y, codes = esb.esb_conv2d_post(
+            xin, fx[0], fx[1], scalar(ALPHA_X), dev(w), fw[0], fw[1], scalar(ALPHA_W),
+            scalar(qa), 5, 3, a=None if a is None else dev(a), b=None if b is None else dev(b),
+            residual=None if res is None else dev(res), relu=relu, stride=(1, 1), pad=(1, 1),
+            want_codes=True, want_acc=want_acc, want_y=True, absmax=amax)
+        np.testing.assert_array_equal(host(y).view(np.uint32), z_o.view(np.uint32))
+        np.testing.assert_array_equal(host(codes), codes_o)
+        assert host(amax)[0] == np.max(np.abs(z_o))
+        if want_acc:
+            np.testing.assert_array_equal(host(acc), acc_o)
+        outs.append(host(y))
+    np.testing.assert_array_equal(outs[0].view(np.uint32), outs[2].view(np.uint32))
