@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--cpu-images", type=int, default=32,
                    help="images of the oracle's forward for the CPU baseline")
     p.add_argument("--batch", type=int, default=64)
+    p.add_argument("--forward-once", action="store_true",
+                   help="build the ResNet18 model, run --warmup forwards, then one more eager "
+                        "forward (for counter runs: its kernels are the last dispatches)")
     p.add_argument("--reps", type=int, default=20)
     return p.parse_args()
 
@@ -87,6 +90,9 @@ def main():
         return
     if args.conv3x3:
         print(json.dumps(conv3x3_step(args)), flush=True)
+        return
+    if args.forward_once:
+        forward_once(args)
         return
     resnet18_headline(args)
 
@@ -592,6 +598,27 @@ def contraction_group(label):
     return label
 
 
+def forward_once(args):
+    """Model build, args.warmup forwards, then one eager forward, on one stream."""
+    import torch
+    from paper_2109_03513_amd import resnet18, workloads
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()
+    weights = workloads.resnet18_weights(0)
+    x = torch.from_numpy(workloads.resnet18_input(0, args.batch)).cuda()
+    with torch.cuda.stream(stream):
+        model = resnet18.ResNet18ESB(weights, args.batch, stream=stream)
+        for _ in range(args.warmup):
+            model.forward(x)
+        stream.synchronize()
+        print("last forward", flush=True)
+        model.forward(x)
+        stream.synchronize()
+    print(json.dumps({"forward_once": True, "batch": args.batch, "warmup": args.warmup}),
+          flush=True)
+
+
 def resnet18_headline(args):
     """The largest single-GPU workload: ResNet18 at batch 64, per-layer DDA on the device."""
     import numpy as np
@@ -737,8 +764,8 @@ def resnet18_headline(args):
                       "forwards queued behind a spin kernel (median of 3)" % graph_ok,
             "units_sum_ms": round(units_ms, 4),
             "groups": table,
-            "mfma_types": "E4M3 (fp8) MFMA on every contraction but conv1 (C = 3: int8 MFMA on "
-                          "the byte-gathering kernel); fp32 accumulation exact (integers < 2^24)",
+            "mfma_types": "E4M3 (fp8) MFMA on every contraction but conv1 (C = 3: int8 MFMA in "
+                          "the fused stem kernel); fp32 accumulation exact (integers < 2^24)",
             "fixed_scale_inference_images_per_s": round(B / (fused_ms * 1e-3), 1),
             "resnet18_conv3x3_b1_step": {k: step2[k] for k in ("value", "unit", "ms_per_step")},
         },
