@@ -1,27 +1,32 @@
-// Direct 3x3 / stride-1 / pad-1 convolution over ESB codes with 64 input and
-// 64 output channels, on the fp8 MFMA of gfx950 (Sec. 4.2: the convolution
-// stage; products of codes by eq. (15), exact as in the implicit-GEMM path).
+// Direct 3x3 / stride-1 / pad-1 convolution over ESB codes on the fp8 MFMA of
+// gfx950 (Sec. 4.2: the convolution stage; products of codes by eq. (15),
+// exact as in the implicit-GEMM path), for input and output channels that are
+// multiples of 64.
 //
 // The implicit-GEMM kernels fetch and decode every input element once per
-// filter tap it meets, nine times for a 3x3 filter.  Here a workgroup owns 256
-// consecutive output pixels (flattened over the batch) and all 64 channels:
-//  * the filter (64 x 9 x 64 codes) is decoded to E4M3 once per workgroup and
-//    stays in LDS (workgroups are persistent over the tiles);
-//  * the input rows under a tile are decoded to E4M3 once into an LDS patch,
-//    one 64-byte row per input pixel.  Every image is seen with a zero row
-//    above and below it and a zero column left and right (the padding), so a
-//    tile may cross images: output pixel (n, p, q) and tap (r, s) read patch
-//    pixel (n (P + 2) + p + r - R0, q + s), R0 the padded row of the tile's
-//    first pixel.  The four 16-byte chunks of a patch pixel are stored in the
-//    order chunk ^ ((pixel / 4) % 4), so that 16 consecutive pixels read at one
-//    chunk (a quarter-wave of a fragment load) hit 16 different bank groups;
-//  * per tap one v_mfma_scale_f32_32x32x64_f8f6f4 per 32 x 32 block; wave w
-//    takes output blocks 2w, 2w + 1 and both halves of the channels;
+// filter tap it meets, nine times for a 3x3 filter.  Here a workgroup owns TM
+// consecutive output pixels (flattened over the batch) and 64 output channels,
+// and runs over the input channels in chunks of 64:
+//  * per chunk, the input rows under the tile are decoded to E4M3 once into an
+//    LDS patch, one 64-byte row per input pixel.  Every image is seen with a
+//    zero row above and below it and a zero column left and right (the
+//    padding), so a tile may cross images: output pixel (n, p, q) and tap
+//    (r, s) read patch pixel (n (P + 2) + p + r - R0, q + s), R0 the padded row
+//    of the tile's first pixel.  The four 16-byte chunks of a patch pixel are
+//    stored in the order chunk ^ ((pixel / 4) % 4), so that 16 consecutive
+//    pixels read at one chunk (a quarter-wave of a fragment load) hit 16
+//    different bank groups;
+//  * per chunk the filter slice (64 outputs x 9 taps x 64 channels) is decoded
+//    into LDS; with one chunk (64 input channels) it is decoded once per
+//    workgroup and stays (workgroups are persistent over their tiles);
+//  * the codes of the next chunk (or tile) are loaded into registers while the
+//    current chunk's MFMAs run;
+//  * per tap one v_mfma_scale_f32_32x32x64_f8f6f4 per 32 x 32 block;
 //  * the epilogue is the contraction's: acc = the fp32 sum times 2^shift
 //    (an exact integer), y0 = fl32(s fl32(acc)) and the fused post-processing,
 //    four consecutive channels per lane after a round trip through LDS.
 // The fp32 sums are exact under the same admission rule as the implicit-GEMM
-// fp8 path (every product at most 2^12, 576 x the largest product < 2^24), so
+// fp8 path (every product at most 2^12, 9 C x the largest product < 2^24), so
 // the results equal that path's bit for bit.
 #include "esb_internal.h"
 
@@ -34,29 +39,33 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;           // four waves
-constexpr int TM = 256;                 // output pixels per tile (8 blocks of 32)
-constexpr int CH = 64;                  // input = output channels
+constexpr int NT = 64;                  // output channels per workgroup
+constexpr int CK = 64;                  // input channels per chunk
 constexpr int TAPS = 9;
-constexpr int WST = TAPS * CH + 16;     // LDS bytes per output channel of the filter: 148
-                                        // dwords, so the 16 lanes of a quarter-wave
+constexpr int WST = TAPS * CK + 16;     // LDS bytes per output channel of the filter slice:
+                                        // 148 dwords, so the 16 lanes of a quarter-wave
                                         // (16 channels) take 16 different bank groups
 constexpr int kPatchMax = 40 * 1024;    // bytes of the input patch
 constexpr int kMaxCols = kThreads / 4;  // Q + 2: one thread per 16-byte chunk of a patch row
 constexpr int SLAB = 72;                // fp32 row stride of the epilogue slabs
-constexpr int kMaxFill = 12;            // patch chunks per thread and tile
+constexpr int kMaxFill = 10;            // patch chunks per thread and chunk of channels
+constexpr int kWPer = NT * TAPS * 4 / kThreads;   // filter chunks per thread (9)
 static_assert(4 * 32 * SLAB * 4 <= kPatchMax, "epilogue slabs fit the patch");
+static_assert(kWPer * kThreads == NT * TAPS * 4, "whole filter chunks per thread");
+constexpr int64_t kMultiMaxPixels = 16384;   // several chunks: at most this many output pixels
 
 struct Conv3Params {
-    const uint8_t* x;          // [N, H, W, 64] codes (H = P, W = Q)
-    const uint8_t* w;          // [64, 3, 3, 64] codes
+    const uint8_t* x;          // [N, H, W, C] codes (H = P, W = Q)
+    const uint8_t* w;          // [K, 3, 3, C] codes
     const float* alphaX;
     const float* alphaW;
-    int32_t* acc;              // [M, 64] or NULL
-    float* y;                  // [M, 64] or NULL
+    int32_t* acc;              // [M, K] or NULL
+    float* y;                  // [M, K] or NULL
     MmaDecode dx, dw;
     Post post;
     int N, P, Q, M;            // M = N P Q output pixels
-    int ntiles;
+    int C, K;                  // channels in and out (multiples of 64)
+    int ntm, ntn;              // pixel tiles, channel tiles
     int out_shift;             // acc = fl32 sum * 2^out_shift
     int kX, kW;
 };
@@ -75,33 +84,33 @@ __device__ __forceinline__ int patch_off(int pix, int c) {
     return (pix << 6) | ((c ^ ((pix >> 2) & 3)) << 4);
 }
 
-// Two waves per SIMD: two workgroups share a CU (LDS 2 x 78 KB).  ACC: the
-// int32 sums are written too (a separate instance: keeping both outputs live
-// costs registers).
-template <bool ACC>
+// Two waves per SIMD: two workgroups share a CU (LDS 2 x 78 KB).  TMB: 32-pixel
+// blocks per tile (8, 4 or 2; four waves take TMB x 2 blocks of 32 x 32).
+// MULTI: more than one chunk of input channels (the filter slices then travel
+// per chunk; at most 4 blocks per tile, for the registers).  ACC: the int32
+// sums are written too (a separate instance: keeping both outputs live costs
+// registers).
+template <int TMB, bool MULTI, bool ACC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv3x3(Conv3Params p) {
-    __shared__ __align__(16) uint8_t wlds[CH * WST];
+    constexpr int TM = 32 * TMB;
+    constexpr int NMB = TMB >= 8 ? 2 : 1;    // output blocks of a wave: NMB x NNB
+    constexpr int NNB = TMB >= 4 ? 2 : 1;
+    static_assert(4 * NMB * NNB == 2 * TMB, "four waves cover the tile");
+    static_assert(!MULTI || TMB <= 4, "several chunks: at most 4 pixel blocks");
+    __shared__ __align__(16) uint8_t wlds[NT * WST];
     __shared__ __align__(16) uint8_t patch[kPatchMax];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane & 31, lg = lane >> 5;
+    // this wave's blocks: pixel blocks mbw + i (i < NMB), channel blocks nbw + j (j < NNB)
+    const int mbw = TMB == 8 ? 2 * wave : (TMB == 4 ? wave : wave >> 1);
+    const int nbw = TMB == 2 ? (wave & 1) : 0;
 
-    // ---- the filter, once: channel k, tap t, chunk c at k * WST + 64 t + 16 c;
-    //      the nine loads of a thread in flight together
-    {
-        constexpr int kPer = CH * TAPS * 4 / kThreads;
-        static_assert(kPer * kThreads == CH * TAPS * 4, "whole chunks per thread");
-        uint4 wv[kPer];
-#pragma unroll
-        for (int u = 0; u < kPer; u++) wv[u] = *(const uint4*)(p.w + 16 * (tid + u * kThreads));
-#pragma unroll
-        for (int u = 0; u < kPer; u++) {
-            const int it = tid + u * kThreads;
-            const int k = it / (TAPS * 4), rem = it - k * (TAPS * 4);
-            *(uint4*)&wlds[k * WST + 16 * rem] = dec16(wv[u], p.dw);
-        }
-    }
+    const int nt = (int)blockIdx.x % p.ntn;          // this workgroup's output channels
+    const int n0 = nt * NT;
+    const int wg = (int)blockIdx.x / p.ntn, nwg = (int)gridDim.x / p.ntn;
+    const int nchunks = MULTI ? p.C / CK : 1;
 
     const float s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kX + p.kW));
     const float qa = post_alpha(p.post);
@@ -114,127 +123,167 @@ void k_conv3x3(Conv3Params p) {
     const bool col_in = (unsigned)iw < (unsigned)p.Q;
     // B fragments: channel 32 j + lr, bytes 32 lg .. + 31 of tap t
     const int boff = lr * WST + 32 * lg;
+    const int64_t wrow = (int64_t)TAPS * p.C;        // filter bytes per output channel
 
     // The patch rows of a tile: padded rows R0 .. R0 + nrows - 1.
     auto rows_of = [&](int tile, int& R0, int& nrows) {
         const int m0 = tile * TM;
-        const int n0 = m0 / PQ, p0 = (m0 - n0 * PQ) / p.Q;
-        R0 = n0 * PP2 + p0;
+        const int i0 = m0 / PQ, p0 = (m0 - i0 * PQ) / p.Q;
+        R0 = i0 * PP2 + p0;
         const int m1 = min(m0 + TM, p.M) - 1;
-        const int n1 = m1 / PQ, p1 = (m1 - n1 * PQ) / p.Q;
-        nrows = n1 * PP2 + p1 + 3 - R0;
+        const int i1 = m1 / PQ, p1 = (m1 - i1 * PQ) / p.Q;
+        nrows = i1 * PP2 + p1 + 3 - R0;
     };
-    // This thread's chunks of a tile's patch, all loads in flight at once: chunk u
-    // is row fri + u rstep; bit u of vmask tells whether it lies inside the input.
-    uint4 raw[kMaxFill];
+    // The codes of one (tile, chunk): this thread's patch chunks (chunk u is row
+    // fri + u rstep; bit u of vmask: inside the input) and, with several chunks,
+    // its filter chunks; every load in flight at once.
+    uint4 raw[kMaxFill], wraw[kWPer];
     uint32_t vmask = 0;
-    auto fetch = [&](int tile) {
+    auto fetch = [&](int tile, int ch) {
         int R0, nrows;
         rows_of(tile, R0, nrows);
         const int pr = R0 + fri;
         int n = pr / PP2, hp = pr - n * PP2;             // padded row hp of image n
         vmask = 0;
+        const uint8_t* xc = p.x + CK * ch + 16 * fc;
 #pragma unroll
         for (int u = 0; u < kMaxFill; u++) {
             const int ih = hp - 1;
             const bool ok = fri < rstep && fri + u * rstep < nrows && col_in && n < p.N &&
                             (unsigned)ih < (unsigned)p.P;
             const int64_t pix = ok ? ((int64_t)n * p.P + ih) * p.Q + iw : 0;
-            raw[u] = *(const uint4*)(p.x + (pix << 6) + 16 * fc);
+            raw[u] = *(const uint4*)(xc + pix * p.C);
             vmask |= ok ? (1u << u) : 0u;
             hp += rstep;
             while (hp >= PP2) { hp -= PP2; n++; }
         }
+        if (MULTI) {
+#pragma unroll
+            for (int u = 0; u < kWPer; u++) {
+                const int it = tid + u * kThreads;
+                const int k = it / (TAPS * 4), rem = it - k * (TAPS * 4);
+                const int t = rem >> 2, c16 = rem & 3;
+                wraw[u] = *(const uint4*)(p.w + (n0 + k) * wrow + t * p.C + CK * ch + 16 * c16);
+            }
+        }
     };
-    if (blockIdx.x < p.ntiles) fetch(blockIdx.x);
+    auto store_filter = [&]() {
+#pragma unroll
+        for (int u = 0; u < kWPer; u++) {
+            const int it = tid + u * kThreads;
+            const int k = it / (TAPS * 4), rem = it - k * (TAPS * 4);
+            *(uint4*)&wlds[k * WST + 16 * rem] = dec16(wraw[u], p.dw);
+        }
+    };
 
-    for (int tile = blockIdx.x; tile < p.ntiles; tile += gridDim.x) {
+    // ---- one chunk of channels: the filter once per workgroup, already in LDS
+    if (!MULTI) {
+#pragma unroll
+        for (int u = 0; u < kWPer; u++) {
+            const int it = tid + u * kThreads;
+            const int k = it / (TAPS * 4), rem = it - k * (TAPS * 4);
+            wraw[u] = *(const uint4*)(p.w + (n0 + k) * wrow + 16 * rem);
+        }
+        store_filter();
+    }
+    if (wg < p.ntm) fetch(wg, 0);
+
+    for (int tile = wg; tile < p.ntm; tile += nwg) {
         const int m0 = tile * TM;
         int R0, nrows;
         rows_of(tile, R0, nrows);
 
-        __syncthreads();   // the previous tile's reads of the patch are done
-        if (fri < rstep) {
-#pragma unroll
-            for (int u = 0; u < kMaxFill; u++) {
-                const int i = fri + u * rstep;
-                if (i < nrows) {
-                    const uint4 v = ((vmask >> u) & 1u) ? dec16(raw[u], p.dx)
-                                                        : make_uint4(0u, 0u, 0u, 0u);   // E4M3 +0
-                    *(uint4*)&patch[patch_off(i * cols + fcol, fc)] = v;
-                }
-            }
-        }
-        __syncthreads();
-        if (tile + (int)gridDim.x < p.ntiles) fetch(tile + gridDim.x);   // in flight below
-
         // ---- per lane and output block: the patch pixel of tap (0, 0)
-        int pb[2];
+        int pb[NMB];
 #pragma unroll
-        for (int i = 0; i < 2; i++) {
-            const int m = min(m0 + 32 * (2 * wave + i) + lr, p.M - 1);   // rows past M: any pixel
+        for (int i = 0; i < NMB; i++) {
+            const int m = min(m0 + 32 * (mbw + i) + lr, p.M - 1);   // rows past M: any pixel
             const int n = m / PQ, rem = m - n * PQ;
             const int pp = rem / p.Q, q = rem - pp * p.Q;
             pb[i] = (n * PP2 + pp - R0) * cols + q;
         }
-        v16f acc[2][2];
+        v16f acc[NMB][NNB];
 #pragma unroll
-        for (int i = 0; i < 2; i++)
+        for (int i = 0; i < NMB; i++)
 #pragma unroll
-            for (int j = 0; j < 2; j++)
+            for (int j = 0; j < NNB; j++)
 #pragma unroll
                 for (int r = 0; r < 16; r++) acc[i][j][r] = 0.0f;
+
+        for (int ch = 0; ch < nchunks; ch++) {
+            __syncthreads();   // the previous chunk's (or tile's) reads of the LDS are done
+            if (fri < rstep) {
 #pragma unroll
-        for (int t = 0; t < TAPS; t++) {
-            const int tr = t / 3, ts = t - 3 * tr;
-            v8i fb[2], fa[2];
-#pragma unroll
-            for (int j = 0; j < 2; j++) {
-                const uint8_t* b = &wlds[boff + 32 * j * WST + 64 * t];
-                const v4i lo = *(const v4i*)b, hi = *(const v4i*)(b + 16);
-                fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                for (int u = 0; u < kMaxFill; u++) {
+                    const int i = fri + u * rstep;
+                    if (i < nrows) {
+                        const uint4 v = ((vmask >> u) & 1u) ? dec16(raw[u], p.dx)
+                                                            : make_uint4(0u, 0u, 0u, 0u);   // E4M3 +0
+                        *(uint4*)&patch[patch_off(i * cols + fcol, fc)] = v;
+                    }
+                }
             }
+            if (MULTI) store_filter();
+            __syncthreads();
+            // the next chunk's codes, in flight during this chunk's MFMAs
+            if (ch + 1 < nchunks) fetch(tile, ch + 1);
+            else if (tile + nwg < p.ntm) fetch(tile + nwg, 0);
+
 #pragma unroll
-            for (int i = 0; i < 2; i++) {
-                const int pix = pb[i] + tr * cols + ts;
-                const int a0 = patch_off(pix, 2 * lg);
-                const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
-                fa[i] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            for (int t = 0; t < TAPS; t++) {
+                const int tr = t / 3, ts = t - 3 * tr;
+                v8i fb[NNB], fa[NMB];
+#pragma unroll
+                for (int j = 0; j < NNB; j++) {
+                    const uint8_t* b = &wlds[boff + 32 * (nbw + j) * WST + 64 * t];
+                    const v4i lo = *(const v4i*)b, hi = *(const v4i*)(b + 16);
+                    fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+#pragma unroll
+                for (int i = 0; i < NMB; i++) {
+                    const int pix = pb[i] + tr * cols + ts;
+                    const int a0 = patch_off(pix, 2 * lg);
+                    const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
+                    fa[i] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+#pragma unroll
+                for (int i = 0; i < NMB; i++)
+#pragma unroll
+                    for (int j = 0; j < NNB; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            fa[i], fb[j], acc[i][j], 0, 0, 0, 127, 0, 127);
+                __builtin_amdgcn_sched_barrier(0);   // one tap's fragments live at a time
             }
-#pragma unroll
-            for (int i = 0; i < 2; i++)
-#pragma unroll
-                for (int j = 0; j < 2; j++)
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                        fa[i], fb[j], acc[i][j], 0, 0, 0, 127, 0, 127);
-            __builtin_amdgcn_sched_barrier(0);   // one tap's fragments live at a time
         }
 
-        // ---- epilogue, one output block of each wave at a time: register r of
-        //      block (i, j) is pixel m0 + 32 (2 wave + i) + 8 (r / 4) + 4 lg + r % 4,
-        //      channel 32 j + lr.  The scaled values go through the wave's LDS slab
-        //      (row stride 72 floats: the two lane halves of a write are 32 banks
-        //      apart) and come back as four consecutive channels per lane.
+        // ---- epilogue, one pixel block of each wave at a time: register r of
+        //      block (i, j) is pixel m0 + 32 (mbw + i) + 8 (r / 4) + 4 lg + r % 4,
+        //      channel n0 + 32 (nbw + j) + lr.  The scaled values go through the
+        //      wave's LDS slab (row stride 72 floats: the two lane halves of a
+        //      write are 32 banks apart) and come back as four consecutive
+        //      channels per lane.
         __syncthreads();   // every read of the patch is done: the slabs reuse it
         float* slab = (float*)patch + wave * (32 * SLAB);
+        constexpr int WCOLS = 32 * NNB;              // channels of a wave's blocks
+        const int c0 = 32 * nbw;                      // their first column in the tile
 #pragma unroll
-        for (int i = 0; i < 2; i++) {
-            const int mrow = m0 + 32 * (2 * wave + i);
+        for (int i = 0; i < NMB; i++) {
+            const int mrow = m0 + 32 * (mbw + i);
             if (ACC) {   // the exact integer sums, through the slab as well
 #pragma unroll
-                for (int j = 0; j < 2; j++)
+                for (int j = 0; j < NNB; j++)
 #pragma unroll
                     for (int r = 0; r < 16; r++)
                         ((int32_t*)slab)[(8 * (r >> 2) + 4 * lg + (r & 3)) * SLAB + 32 * j + lr] =
                             (int32_t)ldexpf(acc[i][j][r], p.out_shift);
                 __syncthreads();
 #pragma unroll 1
-                for (int e = 4 * lane; e < 32 * CH; e += 256) {
-                    const int row = e / CH, col = e - row * CH;
+                for (int e = 4 * lane; e < 32 * WCOLS; e += 256) {
+                    const int row = e / WCOLS, col = e - row * WCOLS;
                     const int m = mrow + row;
                     if (m < p.M) {
                         const int4 v = *(const int4*)((const int32_t*)slab + row * SLAB + col);
-                        int32_t* d = p.acc + (int64_t)m * CH + col;
+                        int32_t* d = p.acc + (int64_t)m * p.K + n0 + c0 + col;
                         if (((uintptr_t)d & 15) == 0) {
                             *(int4*)d = v;
                         } else {
@@ -245,21 +294,22 @@ void k_conv3x3(Conv3Params p) {
                 __syncthreads();
             }
 #pragma unroll
-            for (int j = 0; j < 2; j++)
+            for (int j = 0; j < NNB; j++)
 #pragma unroll
                 for (int r = 0; r < 16; r++)
                     slab[(8 * (r >> 2) + 4 * lg + (r & 3)) * SLAB + 32 * j + lr] =
                         s * ldexpf(acc[i][j][r], p.out_shift);
             __syncthreads();
 #pragma unroll 1
-            for (int e = 4 * lane; e < 32 * CH; e += 256) {
-                const int row = e / CH, col = e - row * CH;
+            for (int e = 4 * lane; e < 32 * WCOLS; e += 256) {
+                const int row = e / WCOLS, col = e - row * WCOLS;
                 const int m = mrow + row;
                 if (m < p.M) {
-                    const int64_t o = (int64_t)m * CH + col;
+                    const int ch = n0 + c0 + col;
+                    const int64_t o = (int64_t)m * p.K + ch;
                     const f32x4 v = *(const f32x4*)(slab + row * SLAB + col);
                     if (p.post.on) {
-                        amax = max(amax, post_store4(p.post, p.y, o, col, v, 4, qa));
+                        amax = max(amax, post_store4(p.post, p.y, o, ch, v, 4, qa));
                     } else if (p.y) {
                         if (((uintptr_t)(p.y + o) & 15) == 0) {
                             *(f32x4*)(p.y + o) = v;
@@ -276,35 +326,60 @@ void k_conv3x3(Conv3Params p) {
     post_absmax_flush(p.post, amax);
 }
 
-// Rows of the patch of a tile: the padded rows from the first pixel's to two
-// past the last pixel's, at most dg + 2 (images crossed) + 3 rows with dg the
-// output rows a tile spans beyond its first.
-int patch_rows_max(int P, int Q) {
+// Rows of the patch of a tile of TM pixels: the padded rows from the first
+// pixel's to two past the last pixel's, at most dg + 2 (images crossed) + 3
+// rows with dg the output rows a tile spans beyond its first.
+int patch_rows_max(int P, int Q, int TM) {
     const int dg = (Q - 1 + TM - 1) / Q;
     const int cross = (P - 1 + dg) / P;
     return dg + 2 * cross + 3;
+}
+
+bool tile_fits(int P, int Q, int TM) {
+    if (Q + 2 > kMaxCols) return false;
+    const int rstep = kThreads / (4 * (Q + 2));
+    const int rows = patch_rows_max(P, Q, TM);
+    return (rows + rstep - 1) / rstep <= kMaxFill && (int64_t)rows * (Q + 2) * 64 <= kPatchMax;
+}
+
+// 32-pixel blocks per tile: the largest of 8, 4, 2 (4, 2 with several chunks of
+// input channels) whose tiles fit the patch and give at least one workgroup per
+// CU, else the largest that fits.
+int choose_tmb(int64_t M, int ntn, int P, int Q, bool multi) {
+    const int cus = num_cus();
+    int fit = 0;
+    for (int tmb = multi ? 4 : 8; tmb >= 2; tmb >>= 1) {
+        if (!tile_fits(P, Q, 32 * tmb)) continue;
+        if (!fit) fit = tmb;
+        if ((M + 32 * tmb - 1) / (32 * tmb) * ntn >= cus) return tmb;
+    }
+    return fit;
 }
 
 }  // namespace
 
 bool conv3x3_fits(const ConvGeom& g, int K, int groups, int op, const uint8_t* x,
                   const uint8_t* w) {
-    if (!(groups == 1 && op == 1 && K == CH && g.C == CH && g.Cg == CH && g.pitch == CH &&
-          g.R == 3 && g.S == 3 && g.sh == 1 && g.sw == 1 && g.ph == 1 && g.pw == 1 &&
-          g.P == g.H && g.Q == g.W && g.P >= 1 && g.Q >= 1))
+    if (!(groups == 1 && op == 1 && K % NT == 0 && K >= NT && g.C % CK == 0 && g.C >= CK &&
+          g.Cg == g.C && g.pitch == g.C && g.R == 3 && g.S == 3 && g.sh == 1 && g.sw == 1 &&
+          g.ph == 1 && g.pw == 1 && g.P == g.H && g.Q == g.W && g.P >= 1 && g.Q >= 1))
         return false;
     if ((uintptr_t)x % 16 || (uintptr_t)w % 16) return false;
-    if (g.Q + 2 > kMaxCols) return false;
-    const int rstep = kThreads / (4 * (g.Q + 2));
-    if ((patch_rows_max(g.P, g.Q) + rstep - 1) / rstep > kMaxFill) return false;
     const int64_t M = (int64_t)g.Nb * g.P * g.Q;
-    if (M + TM >= ((int64_t)1 << 31) / CH) return false;
-    return (int64_t)patch_rows_max(g.P, g.Q) * (g.Q + 2) * 64 <= kPatchMax;
+    if ((M + 256) * K >= ((int64_t)1 << 31) || (int64_t)K * TAPS * g.C >= ((int64_t)1 << 31))
+        return false;
+    // With several chunks every workgroup decodes its 64 filter rows per chunk and tile:
+    // measured faster than the implicit-GEMM kernels only for few output pixels (ResNet18
+    // 3x3 at batch 64: 256 channels at 14 x 14 and 512 at 7 x 7 faster, 128 at 28 x 28
+    // with 50176 pixels slower).
+    if (g.C > CK && M > kMultiMaxPixels) return false;
+    return choose_tmb(M, K / NT, g.P, g.Q, g.C > CK) != 0;
 }
 
-hipError_t launch_conv3x3(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
-                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,
-                          float* y, hipStream_t s, const Post* post) {
+hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt& fx,
+                          const float* alphaX, const uint8_t* w, const Fmt& fw,
+                          const float* alphaW, int32_t* acc, float* y, hipStream_t s,
+                          const Post* post) {
     Conv3Params p{};
     p.x = x;
     p.w = w;
@@ -319,15 +394,33 @@ hipError_t launch_conv3x3(const ConvGeom& g, const uint8_t* x, const Fmt& fx, co
     p.P = g.P;
     p.Q = g.Q;
     p.M = g.Nb * g.P * g.Q;
+    p.C = g.C;
+    p.K = K;
     if (p.M == 0) return hipSuccess;
-    p.ntiles = (p.M + TM - 1) / TM;
+    p.ntn = K / NT;
+    const bool multi = g.C > CK;
+    const int tmb = choose_tmb(p.M, p.ntn, g.P, g.Q, multi);
+    if (tmb == 0) return hipErrorInvalidValue;
+    p.ntm = (p.M + 32 * tmb - 1) / (32 * tmb);
     p.out_shift = fx.k + fw.k + 12;
     p.kX = fx.k;
     p.kW = fw.k;
-    int blocks = num_cus() * 2;
-    if (blocks > p.ntiles) blocks = p.ntiles;
-    if (acc) k_conv3x3<true><<<blocks, kThreads, 0, s>>>(p);
-    else k_conv3x3<false><<<blocks, kThreads, 0, s>>>(p);
+    // persistent workgroups, a whole number per channel tile, two per CU
+    int per = (num_cus() * 2) / p.ntn;
+    if (per < 1) per = 1;
+    if (per > p.ntm) per = p.ntm;
+    const unsigned blocks = (unsigned)(per * p.ntn);
+#define ESB_CONV3_LAUNCH(TMB, MULTI)                                                 \
+    do {                                                                             \
+        if (acc) k_conv3x3<TMB, MULTI, true><<<blocks, kThreads, 0, s>>>(p);         \
+        else k_conv3x3<TMB, MULTI, false><<<blocks, kThreads, 0, s>>>(p);            \
+    } while (0)
+    if (!multi && tmb == 8) ESB_CONV3_LAUNCH(8, false);
+    else if (!multi && tmb == 4) ESB_CONV3_LAUNCH(4, false);
+    else if (!multi) ESB_CONV3_LAUNCH(2, false);
+    else if (tmb == 4) ESB_CONV3_LAUNCH(4, true);
+    else ESB_CONV3_LAUNCH(2, true);
+#undef ESB_CONV3_LAUNCH
     return hipGetLastError();
 }
 

@@ -457,7 +457,7 @@ static int conv_impl(const esb_conv_desc* d, const uint8_t* x, int nX, int kX_si
         return hip_status(launch_dwconv(g, x, fx, alphaX, w, fw, alphaW, acc, y, s, pp));
     const int op = mma_choose(fx, fw, kred);
     if (conv3x3_fits(g, d->K, d->groups, op, x, w))
-        return hip_status(launch_conv3x3(g, x, fx, alphaX, w, fw, alphaW, acc, y, s, pp));
+        return hip_status(launch_conv3x3(g, d->K, x, fx, alphaX, w, fw, alphaW, acc, y, s, pp));
     const bool f4 = mma_f4ok(fx, fw, kred) && g.Cg % 32 == 0;
     const bool f6 = !f4 && mma_f6ok(fx, fw, kred) && g.Cg % 64 == 0 && mma_f6_tiles(Mrows, Kg, d->groups);
     const bool fits = mma_fits(g, x, kred, d->groups, w, kred, ESB_B_NK);

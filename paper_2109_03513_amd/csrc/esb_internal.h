@@ -397,14 +397,16 @@ hipError_t launch_absmax(const float* x, int64_t len, float* absmax, hipStream_t
 // Stem: convolution (stride 2, C <= 3, 64 output channels, int8 integers), the
 // post-processing with a ReLU, and the 3x3 / stride-2 / pad-1 max pool, fused;
 // y (or post.codes) receives the pooled outputs [N, PP, QQ, 64].
-// Direct 3x3 / stride-1 / pad-1 convolution with 64 input and 64 output
-// channels on the fp8 MFMA (op 1 of mma_choose; dense NHWC input and KRSC
-// filter, both 16-byte aligned): results identical to the implicit-GEMM path.
+// Direct 3x3 / stride-1 / pad-1 convolution with input and output channels
+// that are multiples of 64, on the fp8 MFMA (op 1 of mma_choose; dense NHWC
+// input and KRSC filter, both 16-byte aligned): results identical to the
+// implicit-GEMM path.
 bool conv3x3_fits(const ConvGeom& g, int K, int groups, int op, const uint8_t* x,
                   const uint8_t* w);
-hipError_t launch_conv3x3(const ConvGeom& g, const uint8_t* x, const Fmt& fx, const float* alphaX,
-                          const uint8_t* w, const Fmt& fw, const float* alphaW, int32_t* acc,
-                          float* y, hipStream_t s, const Post* post);
+hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt& fx,
+                          const float* alphaX, const uint8_t* w, const Fmt& fw,
+                          const float* alphaW, int32_t* acc, float* y, hipStream_t s,
+                          const Post* post);
 
 bool stem_fits(const ConvGeom& g, int K, int groups, const Fmt& fx, const Fmt& fw, int pool_r,
                int pool_stride, int pool_pad);

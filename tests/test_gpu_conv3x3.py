@@ -1,8 +1,9 @@
-"""The direct 3x3 / stride-1 / pad-1 convolution kernel (64 input and 64 output channels on
-the fp8 MFMA; tiles of 256 output pixels over the batch, crossing image boundaries) against
-the oracle's convolution and post-processing: bit-exact int32 sums, fp32 outputs and codes,
-equal running maximum; and bit for bit equal to the implicit-GEMM path, which an input one
-byte off a 16-byte boundary takes."""
+"""The direct 3x3 / stride-1 / pad-1 convolution kernel (input and output channels in
+multiples of 64 on the fp8 MFMA; tiles of 256, 128 or 64 output pixels over the batch,
+crossing image boundaries; input channels in chunks of 64) against the oracle's convolution
+and post-processing: bit-exact int32 sums, fp32 outputs and codes, equal running maximum;
+and bit for bit equal to the implicit-GEMM path, which an input one byte off a 16-byte
+boundary takes."""
 import numpy as np
 import pytest
 
@@ -12,7 +13,6 @@ from paper_2109_03513_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
 ALPHA_X, ALPHA_W = 0.43, 0.027
-C = K = 64
 
 
 @pytest.fixture(scope="module")
@@ -32,17 +32,25 @@ def unaligned(torch, a):
 
 
 CASES = [
-    # N, H, W, fx, fw, variant
-    (2, 56, 56, (5, 3), (5, 3), "plain"),     # the ResNet18 l1 shape, batch 2
-    (3, 7, 7, (5, 3), (5, 3), "all"),         # 49-pixel images: a tile spans six of them
-    (1, 13, 5, (4, 2), (5, 3), "relu"),       # H != W, ragged last tile, mixed formats
-    (2, 9, 62, (5, 3), (4, 2), "residual"),   # widest rows taken (Q + 2 = 64)
-    (1, 1, 1, (5, 3), (5, 3), "affine"),      # one pixel
-    (4, 17, 23, (6, 3), (4, 1), "all"),       # ESB(6,3) x ESB(4,1)
+    # N, H, W, C, K, fx, fw, variant
+    (2, 56, 56, 64, 64, (5, 3), (5, 3), "plain"),     # the ResNet18 l1 shape, batch 2
+    (3, 7, 7, 64, 64, (5, 3), (5, 3), "all"),         # 49-pixel images: a tile spans six of them
+    (1, 13, 5, 64, 64, (4, 2), (5, 3), "relu"),       # H != W, ragged last tile, mixed formats
+    (2, 9, 62, 64, 64, (5, 3), (4, 2), "residual"),   # widest rows taken (Q + 2 = 64)
+    (1, 1, 1, 64, 64, (5, 3), (5, 3), "affine"),      # one pixel
+    (4, 17, 23, 64, 64, (6, 3), (4, 1), "all"),       # ESB(6,3) x ESB(4,1)
+    # several chunks of input channels and / or tiles of output channels
+    (2, 28, 28, 128, 128, (5, 3), (5, 3), "all"),     # the l2 shape, batch 2 (1568 pixels)
+    (3, 14, 14, 256, 192, (5, 3), (4, 2), "relu"),    # four chunks, three channel tiles
+    (1, 5, 9, 192, 64, (5, 3), (5, 3), "residual"),   # three chunks, ragged
+    (2, 7, 7, 512, 128, (5, 3), (5, 3), "plain"),     # eight chunks (the l4 reduction)
+    # 64-pixel tiles: taken on 256 CUs when tiles of 128 give fewer workgroups than CUs
+    (50, 7, 7, 128, 512, (5, 3), (5, 3), "plain"),    # several chunks
+    (16, 14, 14, 64, 512, (5, 3), (5, 3), "affine"),  # one chunk, eight channel tiles
 ]
 
 
-def post_params(seed, y, variant):
+def post_params(seed, y, K, variant):
     r = np.random.default_rng(seed)
     sd = float(np.std(y)) or 1.0
     a = b = res = None
@@ -55,15 +63,15 @@ def post_params(seed, y, variant):
     return a, b, res, relu, np.float32(0.4 * sd)
 
 
-@pytest.mark.parametrize("Nb,H,W,fx,fw,variant", CASES)
-def test_conv3x3_direct(esb, Nb, H, W, fx, fw, variant):
+@pytest.mark.parametrize("Nb,H,W,C,K,fx,fw,variant", CASES)
+def test_conv3x3_direct(esb, Nb, H, W, C, K, fx, fw, variant):
     torch = torch_cuda()
-    x = wl.random_codes(40 + H, (Nb, H, W, C), fx[0])
-    w = wl.random_codes(41 + W, (K, 3, 3, C), fw[0])
+    x = wl.random_codes(40 + H + C, (Nb, H, W, C), fx[0])
+    w = wl.random_codes(41 + W + K, (K, 3, 3, C), fw[0])
     st, acc_o, y_o = oracle.conv2d(x, w, fx[0], fx[1], ALPHA_X, fw[0], fw[1], ALPHA_W,
                                    stride=(1, 1), pad=(1, 1))
     assert st == 0
-    log("conv3x3 direct %s %s" % ((Nb, H, W, fx, fw), variant))
+    log("conv3x3 direct %s %s" % ((Nb, H, W, C, K, fx, fw), variant))
     if variant == "plain":
         for want_acc in (True, False):
             acc, y = esb.esb_conv2d(dev(x), fx[0], fx[1], scalar(ALPHA_X), dev(w), fw[0], fw[1],
@@ -76,7 +84,7 @@ def test_conv3x3_direct(esb, Nb, H, W, fx, fw, variant):
         np.testing.assert_array_equal(host(acc_u), acc_o)
         np.testing.assert_array_equal(host(y_u).view(np.uint32), y_o.view(np.uint32))
         return
-    a, b, res, relu, qa = post_params(7, y_o, variant)
+    a, b, res, relu, qa = post_params(7, y_o, K, variant)
     z_o, codes_o = oracle.post(y_o.reshape(-1, K), 5, 3, qa, a=a, bias=b,
                                res=None if res is None else res.reshape(-1, K), relu=relu)
     z_o = z_o.reshape(y_o.shape)
