@@ -84,6 +84,81 @@ __device__ __forceinline__ int patch_off(int pix, int c) {
     return (pix << 6) | ((c ^ ((pix >> 2) & 3)) << 4);
 }
 
+// The outputs of one 32-pixel block from a wave's slab (row stride sl floats,
+// WCOLS channels from channel c0): four consecutive channels per lane.  AHEAD:
+// the residual loads four at a time in flight before they are used (for kernels
+// with one block per wave: with two, the registers do not fit); else one output
+// group after the other.  Returns the lane's max |z| bit pattern.
+template <int WCOLS, bool AHEAD>
+__device__ __forceinline__ uint32_t store_block(const Conv3Params& p, const float* slab, int sl,
+                                                int mrow, int c0, int lane, float qa) {
+    constexpr int NIT = 32 * WCOLS / 256;
+    uint32_t amax = 0;
+    if (!AHEAD) {
+#pragma unroll 1
+        for (int e = 4 * lane; e < 32 * WCOLS; e += 256) {
+            const int row = e / WCOLS, col = e - row * WCOLS;
+            const int m = mrow + row;
+            if (m < p.M) {
+                const int ch = c0 + col;
+                const int64_t o = (int64_t)m * p.K + ch;
+                const f32x4 v = *(const f32x4*)(slab + row * sl + col);
+                if (p.post.on) {
+                    amax = max(amax, post_store4(p.post, p.y, o, ch, v, 4, qa));
+                } else if (p.y) {
+                    if (((uintptr_t)(p.y + o) & 15) == 0) {
+                        *(f32x4*)(p.y + o) = v;
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < 4; c++) p.y[o + c] = v[c];
+                    }
+                }
+            }
+        }
+        return amax;
+    }
+    if (p.post.on) {
+#pragma unroll
+        for (int k0 = 0; k0 < NIT; k0 += 4) {   // four residual loads in flight at a time
+            f32x4 rr[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int e = 4 * lane + 256 * (k0 + k), row = e / WCOLS, col = e - row * WCOLS;
+                const int m = mrow + row;
+                rr[k] = (k0 + k < NIT && m < p.M) ? post_res4(p.post, (int64_t)m * p.K + c0 + col)
+                                                  : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int e = 4 * lane + 256 * (k0 + k), row = e / WCOLS, col = e - row * WCOLS;
+                const int m = mrow + row;
+                if (k0 + k < NIT && m < p.M) {
+                    const int ch = c0 + col;
+                    const f32x4 v = *(const f32x4*)(slab + row * sl + col);
+                    amax = max(amax, post_apply4(p.post, p.y, (int64_t)m * p.K + ch, ch, v, rr[k], qa));
+                }
+            }
+        }
+    } else if (p.y) {
+#pragma unroll
+        for (int k = 0; k < NIT; k++) {
+            const int e = 4 * lane + 256 * k, row = e / WCOLS, col = e - row * WCOLS;
+            const int m = mrow + row;
+            if (m < p.M) {
+                const int64_t o = (int64_t)m * p.K + c0 + col;
+                const f32x4 v = *(const f32x4*)(slab + row * sl + col);
+                if (((uintptr_t)(p.y + o) & 15) == 0) {
+                    *(f32x4*)(p.y + o) = v;
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 4; c++) p.y[o + c] = v[c];
+                }
+            }
+        }
+    }
+    return amax;
+}
+
 // Two waves per SIMD: two workgroups share a CU (LDS 2 x 78 KB).  TMB: 32-pixel
 // blocks per tile (8, 4 or 2; four waves take TMB x 2 blocks of 32 x 32).
 // MULTI: more than one chunk of input channels (the filter slices then travel
@@ -300,30 +375,223 @@ void k_conv3x3(Conv3Params p) {
                     slab[(8 * (r >> 2) + 4 * lg + (r & 3)) * SLAB + 32 * j + lr] =
                         s * ldexpf(acc[i][j][r], p.out_shift);
             __syncthreads();
+            amax = max(amax, store_block<WCOLS, NMB == 1>(p, slab, SLAB, mrow, n0 + c0, lane, qa));
+            __syncthreads();
+        }
+    }
+    post_absmax_flush(p.post, amax);
+}
+
+// ---------------------------------------------------------------------------
+// Resident filter: for more than one chunk of input channels, one workgroup of
+// eight waves per CU keeps the filter rows of its output channels (NTR = 64 or
+// 32 of them, all 9 C bytes each) decoded in LDS for all of its tiles, so only
+// the patch rows travel per chunk.  Tiles of 256 pixels, one 32-pixel block per
+// wave; a row of the filter copy is 9 C + 16 bytes (an odd number of 16-byte
+// groups: the 16 lanes of a quarter-wave take 16 different bank groups).
+constexpr int kResThreads = 512;
+constexpr int kResFilterMax = 76 * 1024;   // bytes of the resident filter copy
+constexpr int kResFill = 10;               // filter chunks and patch chunks per thread
+
+template <int NNB, bool ACC>
+__global__ __launch_bounds__(kResThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_conv3x3_res(Conv3Params p) {
+    constexpr int NTR = 32 * NNB;              // output channels per workgroup
+    constexpr int TM = 256;                    // pixels per tile: block `wave` of 8
+    constexpr int SL = NTR + 8;                // slab row stride (floats): two lane halves
+                                               // 4 rows apart are 32 banks apart
+    static_assert(4 * 32 * SL * 4 <= kPatchMax, "epilogue slabs fit");
+    __shared__ __align__(16) uint8_t wres[kResFilterMax];
+    __shared__ __align__(16) uint8_t patch[kPatchMax];
+    __shared__ __align__(16) uint8_t spare[kPatchMax];   // the slabs of waves 4..7
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lr = lane & 31, lg = lane >> 5;
+
+    const int nt = (int)blockIdx.x % p.ntn;
+    const int n0 = nt * NTR;
+    const int wg = (int)blockIdx.x / p.ntn, nwg = (int)gridDim.x / p.ntn;
+    const int nchunks = p.C / CK;
+    const int wst = TAPS * p.C + 16;                      // LDS bytes per filter row
+    const int row16 = TAPS * p.C / 16;                    // 16-byte chunks of a filter row
+
+    // ---- the filter rows n0 .. n0 + NTR - 1, once, every load in flight
+    {
+        uint4 wv[kResFill];
+#pragma unroll
+        for (int u = 0; u < kResFill; u++) {
+            const int it = tid + u * kResThreads;
+            const int k = it / row16, rem = it - k * row16;
+            wv[u] = k < NTR ? *(const uint4*)(p.w + (int64_t)(n0 + k) * (TAPS * p.C) + 16 * rem)
+                            : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kResFill; u++) {
+            const int it = tid + u * kResThreads;
+            const int k = it / row16, rem = it - k * row16;
+            if (k < NTR) *(uint4*)&wres[k * wst + 16 * rem] = dec16(wv[u], p.dw);
+        }
+    }
+
+    const float s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kX + p.kW));
+    const float qa = post_alpha(p.post);
+    uint32_t amax = 0;
+    const int cols = p.Q + 2, PP2 = p.P + 2, PQ = p.P * p.Q;
+    const int cpr = 4 * cols;
+    const int fci = tid % cpr, fri = tid / cpr, rstep = kResThreads / cpr;
+    const int fcol = fci >> 2, fc = fci & 3, iw = fcol - 1;
+    const bool col_in = (unsigned)iw < (unsigned)p.Q;
+    // B fragments: output channel 32 j + lr, bytes 32 lg .. + 31 of (tap t, chunk ch)
+    const int boff = lr * wst + 32 * lg;
+
+    auto rows_of = [&](int tile, int& R0, int& nrows) {
+        const int m0 = tile * TM;
+        const int i0 = m0 / PQ, p0 = (m0 - i0 * PQ) / p.Q;
+        R0 = i0 * PP2 + p0;
+        const int m1 = min(m0 + TM, p.M) - 1;
+        const int i1 = m1 / PQ, p1 = (m1 - i1 * PQ) / p.Q;
+        nrows = i1 * PP2 + p1 + 3 - R0;
+    };
+    uint4 raw[kResFill];
+    uint32_t vmask = 0;
+    auto fetch = [&](int tile, int ch) {
+        int R0, nrows;
+        rows_of(tile, R0, nrows);
+        const int pr = R0 + fri;
+        int n = pr / PP2, hp = pr - n * PP2;
+        vmask = 0;
+        const uint8_t* xc = p.x + CK * ch + 16 * fc;
+#pragma unroll
+        for (int u = 0; u < kResFill; u++) {
+            const int ih = hp - 1;
+            const bool ok = fri < rstep && fri + u * rstep < nrows && col_in && n < p.N &&
+                            (unsigned)ih < (unsigned)p.P;
+            const int64_t pix = ok ? ((int64_t)n * p.P + ih) * p.Q + iw : 0;
+            raw[u] = *(const uint4*)(xc + pix * p.C);
+            vmask |= ok ? (1u << u) : 0u;
+            hp += rstep;
+            while (hp >= PP2) { hp -= PP2; n++; }
+        }
+    };
+    if (wg < p.ntm) fetch(wg, 0);
+
+    for (int tile = wg; tile < p.ntm; tile += nwg) {
+        const int m0 = tile * TM;
+        int R0, nrows;
+        rows_of(tile, R0, nrows);
+        int pb;
+        {
+            const int m = min(m0 + 32 * wave + lr, p.M - 1);   // rows past M: any pixel
+            const int n = m / PQ, rem = m - n * PQ;
+            const int pp = rem / p.Q, q = rem - pp * p.Q;
+            pb = (n * PP2 + pp - R0) * cols + q;
+        }
+        v16f acc[NNB];
+#pragma unroll
+        for (int j = 0; j < NNB; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[j][r] = 0.0f;
+
+        for (int ch = 0; ch < nchunks; ch++) {
+            __syncthreads();   // the previous chunk's (or tile's) reads of the patch are done
+            if (fri < rstep) {
+#pragma unroll
+                for (int u = 0; u < kResFill; u++) {
+                    const int i = fri + u * rstep;
+                    if (i < nrows) {
+                        const uint4 v = ((vmask >> u) & 1u) ? dec16(raw[u], p.dx)
+                                                            : make_uint4(0u, 0u, 0u, 0u);   // E4M3 +0
+                        *(uint4*)&patch[patch_off(i * cols + fcol, fc)] = v;
+                    }
+                }
+            }
+            __syncthreads();
+            if (ch + 1 < nchunks) fetch(tile, ch + 1);
+            else if (tile + nwg < p.ntm) fetch(tile + nwg, 0);
+
+            const uint8_t* wb = &wres[boff + CK * ch];
+#pragma unroll
+            for (int t = 0; t < TAPS; t++) {
+                const int tr = t / 3, ts = t - 3 * tr;
+                v8i fb[NNB], fa;
+#pragma unroll
+                for (int j = 0; j < NNB; j++) {
+                    const uint8_t* b = wb + 32 * j * wst + t * p.C;
+                    const v4i lo = *(const v4i*)b, hi = *(const v4i*)(b + 16);
+                    fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+                {
+                    const int pix = pb + tr * cols + ts;
+                    const int a0 = patch_off(pix, 2 * lg);
+                    const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
+                    fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+#pragma unroll
+                for (int j = 0; j < NNB; j++)
+                    acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        fa, fb[j], acc[j], 0, 0, 0, 127, 0, 127);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+
+        // ---- epilogue: block `wave` (pixels m0 + 32 wave ..), register r of
+        //      channel block j is pixel + 8 (r / 4) + 4 lg + r % 4, channel
+        //      n0 + 32 j + lr; through the wave's slab, four channels per lane
+        __syncthreads();   // every read of the patch is done: the slabs reuse it
+        float* slab = (float*)(wave < 4 ? patch : spare) + (wave & 3) * (32 * SL);
+        const int mrow = m0 + 32 * wave;
+        if (ACC) {
+#pragma unroll
+            for (int j = 0; j < NNB; j++)
+#pragma unroll
+                for (int r = 0; r < 16; r++)
+                    ((int32_t*)slab)[(8 * (r >> 2) + 4 * lg + (r & 3)) * SL + 32 * j + lr] =
+                        (int32_t)ldexpf(acc[j][r], p.out_shift);
+            __syncthreads();
 #pragma unroll 1
-            for (int e = 4 * lane; e < 32 * WCOLS; e += 256) {
-                const int row = e / WCOLS, col = e - row * WCOLS;
+            for (int e = 4 * lane; e < 32 * NTR; e += 256) {
+                const int row = e / NTR, col = e - row * NTR;
                 const int m = mrow + row;
                 if (m < p.M) {
-                    const int ch = n0 + c0 + col;
-                    const int64_t o = (int64_t)m * p.K + ch;
-                    const f32x4 v = *(const f32x4*)(slab + row * SLAB + col);
-                    if (p.post.on) {
-                        amax = max(amax, post_store4(p.post, p.y, o, ch, v, 4, qa));
-                    } else if (p.y) {
-                        if (((uintptr_t)(p.y + o) & 15) == 0) {
-                            *(f32x4*)(p.y + o) = v;
-                        } else {
-#pragma unroll
-                            for (int c = 0; c < 4; c++) p.y[o + c] = v[c];
-                        }
+                    const int4 v = *(const int4*)((const int32_t*)slab + row * SL + col);
+                    int32_t* d = p.acc + (int64_t)m * p.K + n0 + col;
+                    if (((uintptr_t)d & 15) == 0) {
+                        *(int4*)d = v;
+                    } else {
+                        d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
                     }
                 }
             }
             __syncthreads();
         }
+#pragma unroll
+        for (int j = 0; j < NNB; j++)
+#pragma unroll
+            for (int r = 0; r < 16; r++)
+                slab[(8 * (r >> 2) + 4 * lg + (r & 3)) * SL + 32 * j + lr] =
+                    s * ldexpf(acc[j][r], p.out_shift);
+        __syncthreads();
+        amax = max(amax, store_block<NTR, true>(p, slab, SL, mrow, n0, lane, qa));
     }
     post_absmax_flush(p.post, amax);
+}
+
+// Output channels per workgroup of the resident-filter kernel (64, else 32), 0
+// when neither copy fits.
+int res_ntr(int C, int K) {
+    for (int ntr = 64; ntr >= 32; ntr >>= 1)
+        if (K % ntr == 0 && (int64_t)ntr * (TAPS * C + 16) <= kResFilterMax &&
+            (int64_t)ntr * TAPS * C <= (int64_t)kResFill * 16 * kResThreads)
+            return ntr;
+    return 0;
+}
+
+bool res_tile_fits(int P, int Q) {
+    if (4 * (Q + 2) > kResThreads) return false;
+    const int rstep = kResThreads / (4 * (Q + 2));
+    const int dg = (Q - 1 + 256 - 1) / Q, cross = (P - 1 + dg) / P;
+    const int rows = dg + 2 * cross + 3;
+    return (rows + rstep - 1) / rstep <= kResFill && (int64_t)rows * (Q + 2) * 64 <= kPatchMax;
 }
 
 // Rows of the patch of a tile of TM pixels: the padded rows from the first
@@ -372,7 +640,8 @@ bool conv3x3_fits(const ConvGeom& g, int K, int groups, int op, const uint8_t* x
     // measured faster than the implicit-GEMM kernels only for few output pixels (ResNet18
     // 3x3 at batch 64: 256 channels at 14 x 14 and 512 at 7 x 7 faster, 128 at 28 x 28
     // with 50176 pixels slower).
-    if (g.C > CK && M > kMultiMaxPixels) return false;
+    if (g.C > CK && M > kMultiMaxPixels)   // several chunks and many pixels: resident filter
+        return res_ntr(g.C, K) != 0 && res_tile_fits(g.P, g.Q);
     return choose_tmb(M, K / NT, g.P, g.Q, g.C > CK) != 0;
 }
 
@@ -397,14 +666,32 @@ hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt&
     p.C = g.C;
     p.K = K;
     if (p.M == 0) return hipSuccess;
+    p.out_shift = fx.k + fw.k + 12;
+    p.kX = fx.k;
+    p.kW = fw.k;
+    if (g.C > CK && p.M > kMultiMaxPixels) {   // the resident-filter kernel, one workgroup per CU
+        const int ntr = res_ntr(g.C, K);
+        if (ntr == 0 || !res_tile_fits(g.P, g.Q)) return hipErrorInvalidValue;
+        p.ntn = K / ntr;
+        p.ntm = (p.M + 255) / 256;
+        int per = num_cus() / p.ntn;
+        if (per < 1) per = 1;
+        if (per > p.ntm) per = p.ntm;
+        const unsigned blocks = (unsigned)(per * p.ntn);
+        if (ntr == 64) {
+            if (acc) k_conv3x3_res<2, true><<<blocks, kResThreads, 0, s>>>(p);
+            else k_conv3x3_res<2, false><<<blocks, kResThreads, 0, s>>>(p);
+        } else {
+            if (acc) k_conv3x3_res<1, true><<<blocks, kResThreads, 0, s>>>(p);
+            else k_conv3x3_res<1, false><<<blocks, kResThreads, 0, s>>>(p);
+        }
+        return hipGetLastError();
+    }
     p.ntn = K / NT;
     const bool multi = g.C > CK;
     const int tmb = choose_tmb(p.M, p.ntn, g.P, g.Q, multi);
     if (tmb == 0) return hipErrorInvalidValue;
     p.ntm = (p.M + 32 * tmb - 1) / (32 * tmb);
-    p.out_shift = fx.k + fw.k + 12;
-    p.kX = fx.k;
-    p.kW = fw.k;
     // persistent workgroups, a whole number per channel tile, two per CU
     int per = (num_cus() * 2) / p.ntn;
     if (per < 1) per = 1;

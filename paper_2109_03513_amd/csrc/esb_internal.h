@@ -173,28 +173,32 @@ __device__ __forceinline__ uint32_t post_store(const Post& P, float* y, int64_t 
     return P.absmax ? (__float_as_uint(z) & 0x7fffffffu) : 0u;
 }
 
-// Four consecutive outputs o .. o+3 (channels ch .. ch+3; nv of them inside the
-// output) through the fused post-processing; 16-byte residual / y accesses and
-// one 4-byte code store where the addresses allow.
-__device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t o, int64_t ch,
-                                                f32x4 v, int nv, float qa) {
-    if (nv < 4) {
-        uint32_t m = 0;
-        for (int c = 0; c < nv; c++) m = max(m, post_store(P, y, o + c, ch + c, v[c], qa));
-        return m;
-    }
-    f32x4 z;
-#pragma unroll
-    for (int c = 0; c < 4; c++)
-        z[c] = __builtin_fmaf(P.a ? P.a[ch + c] : 1.0f, v[c], P.b ? P.b[ch + c] : 0.0f);
+// The residual of outputs o .. o+3 (16-byte load where the address allows), or
+// zeros without a residual: callers may load it ahead of post_apply4.
+__device__ __forceinline__ f32x4 post_res4(const Post& P, int64_t o) {
+    f32x4 r = {0.0f, 0.0f, 0.0f, 0.0f};
     if (P.res) {
-        f32x4 r;
         if (((uintptr_t)(P.res + o) & 15) == 0) {
             r = *(const f32x4*)(P.res + o);
         } else {
 #pragma unroll
             for (int c = 0; c < 4; c++) r[c] = P.res[o + c];
         }
+    }
+    return r;
+}
+
+// Four consecutive outputs o .. o+3 (channels ch .. ch+3, all inside the
+// output) through the fused post-processing, their residual r already loaded
+// (post_res4); 16-byte y stores and one 4-byte code store where the addresses
+// allow.
+__device__ __forceinline__ uint32_t post_apply4(const Post& P, float* y, int64_t o, int64_t ch,
+                                                f32x4 v, f32x4 r, float qa) {
+    f32x4 z;
+#pragma unroll
+    for (int c = 0; c < 4; c++)
+        z[c] = __builtin_fmaf(P.a ? P.a[ch + c] : 1.0f, v[c], P.b ? P.b[ch + c] : 0.0f);
+    if (P.res) {
 #pragma unroll
         for (int c = 0; c < 4; c++) z[c] = z[c] + r[c];
     }
@@ -227,6 +231,19 @@ __device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t
         for (int c = 0; c < 4; c++) m = max(m, __float_as_uint(z[c]) & 0x7fffffffu);
     }
     return m;
+}
+
+// Four consecutive outputs o .. o+3 (channels ch .. ch+3; nv of them inside the
+// output) through the fused post-processing; 16-byte residual / y accesses and
+// one 4-byte code store where the addresses allow.
+__device__ __forceinline__ uint32_t post_store4(const Post& P, float* y, int64_t o, int64_t ch,
+                                                f32x4 v, int nv, float qa) {
+    if (nv < 4) {
+        uint32_t m = 0;
+        for (int c = 0; c < nv; c++) m = max(m, post_store(P, y, o + c, ch + c, v[c], qa));
+        return m;
+    }
+    return post_apply4(P, y, o, ch, v, post_res4(P, o), qa);
 }
 
 // The running |z| maxima of a workgroup into *absmax.  Every thread of the

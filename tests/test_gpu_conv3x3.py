@@ -1,6 +1,7 @@
-"""The direct 3x3 / stride-1 / pad-1 convolution kernel (input and output channels in
+"""The direct 3x3 / stride-1 / pad-1 convolution kernels (input and output channels in
 multiples of 64 on the fp8 MFMA; tiles of 256, 128 or 64 output pixels over the batch,
-crossing image boundaries; input channels in chunks of 64) against the oracle's convolution
+crossing image boundaries; input channels in chunks of 64; the filter slice per chunk, or
+resident for the workgroup) against the oracle's convolution
 and post-processing: bit-exact int32 sums, fp32 outputs and codes, equal running maximum;
 and bit for bit equal to the implicit-GEMM path, which an input one byte off a 16-byte
 boundary takes."""
@@ -47,6 +48,10 @@ CASES = [
     # 64-pixel tiles: taken on 256 CUs when tiles of 128 give fewer workgroups than CUs
     (50, 7, 7, 128, 512, (5, 3), (5, 3), "plain"),    # several chunks
     (16, 14, 14, 64, 512, (5, 3), (5, 3), "affine"),  # one chunk, eight channel tiles
+    # several chunks and more than 16384 pixels: the resident-filter kernel (eight waves,
+    # one workgroup per CU, 64 or 32 output channels per workgroup)
+    (24, 28, 28, 128, 128, (5, 3), (5, 3), "all"),    # 64 channels per workgroup, ragged
+    (88, 14, 14, 256, 64, (5, 3), (4, 2), "plain"),   # 32 channels per workgroup
 ]
 
 
