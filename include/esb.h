@@ -195,8 +195,11 @@ int esb_pack(const uint8_t* codes, int rows, int K, int64_t ld, int n, int k_sig
  * GEMM with B given packed by esb_pack (N rows of K/2 bytes), A as codes (packed
  * per call into the workspace), results bit-identical to esb_gemm with
  * ESB_B_NK.  Both formats inside E2M1, K % 32 == 0, K * max|mA| * max|mB| < 2^24
- * (else ESB_E_UNSUPPORTED / ESB_E_OVERFLOW).  Skinny shapes split the reduction
- * over more workgroups, with exact int32 partial sums in the workspace.
+ * (else ESB_E_UNSUPPORTED / ESB_E_OVERFLOW).  Skinny shapes (fully connected
+ * layers at a small batch) split the reduction: over the four waves of one
+ * workgroup per 64 x 32 output tile, summed exactly in LDS, where such tiles give
+ * at least half the CUs a workgroup; otherwise over workgroups, with exact int32
+ * partial sums in the workspace.
  *   workspace  device, at least esb_gemm_packed_workspace_size() bytes
  *              (ESB_E_WORKSPACE otherwise); A 16-byte aligned, lda % 16 == 0.
  */

@@ -621,7 +621,9 @@ size_t esb_gemm_packed_workspace_size(int M, int N, int K, int nA, int kA_sig, i
     size_t need = al((size_t)M * (size_t)(K / 2));            // A, packed per call
     int kc = K;
     const int ks = mma_splitk(M, N, K, &kc);
-    if (ks > 1) need += (size_t)ks * (size_t)M * (size_t)N * sizeof(int32_t);
+    // skinny shapes: the reduction split over the waves of one workgroup (no
+    // partial sums in memory) when that fills the chip, else over workgroups
+    if (ks > 1 && !fc_f4_fits(M, N, K)) need += (size_t)ks * (size_t)M * (size_t)N * sizeof(int32_t);
     return need > 0 ? need : 1;
 }
 
@@ -647,6 +649,14 @@ int esb_gemm_packed(int M, int N, int K, const uint8_t* A, int64_t lda, int nA, 
     ConvGeom g;
     g.Nb = M; g.H = 1; g.W = 1; g.C = K; g.pitch = (int)lda;
     g.Cg = K; g.R = 1; g.S = 1; g.sh = 1; g.sw = 1; g.ph = 0; g.pw = 0; g.P = 1; g.Q = 1;
+    if (fc_f4_fits(M, N, K)) {
+        uint8_t* dA = (uint8_t*)workspace;   // A packed like B, rows of K/2 bytes
+        hipError_t e = launch_pack_fp4(A, M, K, lda, fa, dA, (hipStream_t)stream);
+        if (e == hipSuccess)
+            e = launch_fc_f4(M, N, K, dA, K / 2, B_packed, K / 2, fa.k, fb.k, alphaA, alphaB, acc, y,
+                             ldc, (hipStream_t)stream);
+        return hip_status(e);
+    }
     return hip_status(launch_mma_pre(M, N, K, 1, g, A, M, K, lda, fa, alphaA, nullptr, N, K / 2, fb,
                                      alphaB, acc, y, ldc, 1, workspace, B_packed, true,
                                      (hipStream_t)stream));

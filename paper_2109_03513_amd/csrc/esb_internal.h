@@ -401,6 +401,15 @@ hipError_t launch_mma_pre(int M, int N, int K, int groups, const ConvGeom& ga, c
 // sums after the decoded operands in ws (see esb_gemm_packed_workspace_size).
 hipError_t launch_pack_fp4(const uint8_t* codes, int64_t rows, int64_t K, int64_t ld, const Fmt& f,
                            uint8_t* packed, hipStream_t s);
+// Skinny GEMM over packed E2M1 rows (A and B, K/2 bytes per row): one workgroup
+// per 64 x 32 output tile, the reduction split over its four waves and summed
+// in LDS.  fc_f4_fits: the shapes it takes (where 128 x 128 tiles would split the
+// reduction over workgroups and 64 x 32 tiles give at least half the CUs one).
+bool fc_f4_fits(int64_t M, int64_t N, int64_t K);
+hipError_t launch_fc_f4(int M, int N, int K, const uint8_t* A_packed, int64_t lda_bytes,
+                        const uint8_t* B_packed, int64_t ldb_bytes, int kA, int kB,
+                        const float* alphaA, const float* alphaB, int32_t* acc, float* y,
+                        int64_t ldc, hipStream_t s);
 
 // Glue between layers: NHWC max pooling, the global average pool, max |x|.
 struct PoolGeom {

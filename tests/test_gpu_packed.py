@@ -61,10 +61,14 @@ def test_pack_layout_is_e2m1(esb, fmt):
 
 
 @pytest.mark.parametrize("M,N,K,fa,fb", [
-    (128, 4096, 9216, (3, 2), (3, 1)),     # AlexNet FC at batch 128: split reduction
+    (128, 4096, 9216, (3, 2), (3, 1)),     # AlexNet FC at batch 128: the reduction split over
+                                           # the waves of one workgroup per 64 x 32 tile
+    (100, 4001, 4160, (4, 2), (3, 1)),     # same kernel: ragged M and N (N % 4 != 0: unaligned
+                                           # rows), a partial last 128-byte line (32 bytes)
+    (200, 2600, 8256, (3, 2), (4, 2)),     # same kernel: four M tiles, the last of 8 rows
     (301, 1000, 2048, (4, 2), (4, 2)),     # ragged M, N; ESB(4,1) both
     (4097, 2050, 512, (2, 1), (3, 2)),     # many tiles: no split
-    (64, 3000, 8192, (3, 2), (4, 2)),      # 64 x 64 tiles, split
+    (64, 3000, 8192, (3, 2), (4, 2)),      # 64 x 64 tiles, split over workgroups
 ])
 def test_gemm_packed_vs_oracle(esb, M, N, K, fa, fb):
     (bA, ksA), (bB, ksB) = fa, fb
@@ -96,3 +100,40 @@ def test_gemm_packed_reused_workspace(esb):
                                      scalar(1.0), ws)
         acc0, _ = esb.esb_gemm(dev(A), 3, 2, scalar(1.0), dev(B), 3, 1, scalar(1.0))
         np.testing.assert_array_equal(host(acc), host(acc0))
+
+
+def extreme_codes(b, ks, shape, seed):
+    """Mostly the largest magnitude, else the smallest nonzero one, 30 % negative."""
+    v = oracle.valueset(b, ks)
+    top = oracle.encode(float(v[-1]), b, ks)
+    small = oracle.encode(float(v[v > 0][0]), b, ks)
+    r = np.random.default_rng(seed)
+    c = np.where(r.random(shape) < 0.8, top, small).astype(np.uint8)
+    neg = r.random(shape) < 0.3
+    return np.where(neg, c | (1 << (b - 1)), c).astype(np.uint8)
+
+
+def test_gemm_packed_wave_split_at_accumulator_bound(esb):
+    """The wave-split kernel with ESB(4,1) both: products m_A*m_B from 1 to 144 in one
+    reduction and K * 144 just below 2^24, where every per-wave partial and the total are
+    still exact in fp32; ragged M; accumulators only, then outputs only."""
+    M, N, K = 100, 2048, 116480
+    A = extreme_codes(4, 2, (M, K), 21)
+    B = extreme_codes(4, 2, (N, K), 22)
+    top = oracle.encode(6.0, 4, 2)
+    A[0, :] = top          # output (0, 0) = K * 144 = 16773120, the largest sum below 2^24
+    B[0, :] = top
+    need = esb.esb_gemm_packed_workspace_size(M, N, K, 4, 2, 4, 2)
+    log("gemm_packed bound M=%d N=%d K=%d ws=%d" % (M, N, K, need))
+    assert need < M * K   # A packed only: no partial sums in memory
+    Bp = esb.esb_pack(dev(B), 4, 2)
+    acc, _ = esb.esb_gemm_packed(dev(A), 4, 2, scalar(0.37), Bp, 4, 2, scalar(0.021),
+                                 workspace(need), want_y=False)
+    _, y = esb.esb_gemm_packed(dev(A), 4, 2, scalar(0.37), Bp, 4, 2, scalar(0.021),
+                               workspace(need), want_acc=False)
+    rows = np.array([0, 31, 32, 63, 64, M - 1], dtype=np.int64)
+    st, oacc, oy = oracle.gemm(np.ascontiguousarray(A[rows]), B, 4, 2, 0.37, 4, 2, 0.021)
+    assert st == 0
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    assert_rel(host(y)[rows], oy, YREL, "y")
+    assert oacc[0, 0] == K * 144
