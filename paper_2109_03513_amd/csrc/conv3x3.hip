@@ -94,6 +94,83 @@ __device__ __forceinline__ uint32_t store_block(const Conv3Params& p, const floa
                                                 int mrow, int c0, int lane, float qa) {
     constexpr int NIT = 32 * WCOLS / 256;
     uint32_t amax = 0;
+    // Post-processing without a per-channel affine and without codes (ReLU /
+    // residual / max|z| only) takes lean code instead of the general
+    // post-processing; the unrolled form also takes the plain output (the rolled
+    // form keeps its own plain loop, which issues no global load between the
+    // stores).  z = v + 0 is the affine step of the general path with a = 1, b = 0
+    // (one rounding: it turns -0 into +0), so both agree bit for bit.
+    const bool lean = p.post.on ? (!p.post.a && !p.post.b && !p.post.codes) : AHEAD;
+    const bool on = p.post.on != 0;
+    const float* res = on ? p.post.res : nullptr;
+    const bool relu = on && p.post.relu;
+    const bool am = on && p.post.absmax;
+    auto lean4 = [&](int64_t o, f32x4 z, f32x4 r) {
+        if (on) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) z[c] = z[c] + 0.0f;
+        }
+        if (res) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) z[c] = z[c] + r[c];
+        }
+        if (relu) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) z[c] = z[c] > 0.0f ? z[c] : 0.0f;
+        }
+        if (p.y) {
+            float* d = p.y + o;
+            if (((uintptr_t)d & 15) == 0) {
+                *(f32x4*)d = z;
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; c++) d[c] = z[c];
+            }
+        }
+        uint32_t mz = 0;
+        if (am) {
+#pragma unroll
+            for (int c = 0; c < 4; c++) mz = max(mz, __float_as_uint(z[c]) & 0x7fffffffu);
+        }
+        return mz;
+    };
+    auto res4 = [&](int64_t o) {
+        f32x4 r = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (res) {
+            const float* q = res + o;
+            if (((uintptr_t)q & 15) == 0) {
+                r = *(const f32x4*)q;
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; c++) r[c] = q[c];
+            }
+        }
+        return r;
+    };
+    if (AHEAD && lean) {   // unrolled, the residual loads four at a time ahead of use
+#pragma unroll
+        for (int k0 = 0; k0 < NIT; k0 += 4) {
+            f32x4 rr[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int e = 4 * lane + 256 * (k0 + k), row = e / WCOLS, col = e - row * WCOLS;
+                const int m = mrow + row;
+                rr[k] = (k0 + k < NIT && m < p.M) ? res4((int64_t)m * p.K + c0 + col)
+                                                  : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+#pragma unroll
+            for (int k = 0; k < 4; k++) {
+                const int e = 4 * lane + 256 * (k0 + k), row = e / WCOLS, col = e - row * WCOLS;
+                const int m = mrow + row;
+                if (k0 + k < NIT && m < p.M) {
+                    const int64_t o = (int64_t)m * p.K + c0 + col;
+                    const f32x4 v = *(const f32x4*)(slab + row * sl + col);
+                    amax = max(amax, lean4(o, v, rr[k]));
+                }
+            }
+        }
+        return amax;
+    }
     if (!AHEAD) {
 #pragma unroll 1
         for (int e = 4 * lane; e < 32 * WCOLS; e += 256) {
@@ -103,7 +180,9 @@ __device__ __forceinline__ uint32_t store_block(const Conv3Params& p, const floa
                 const int ch = c0 + col;
                 const int64_t o = (int64_t)m * p.K + ch;
                 const f32x4 v = *(const f32x4*)(slab + row * sl + col);
-                if (p.post.on) {
+                if (lean) {
+                    amax = max(amax, lean4(o, v, res4(o)));
+                } else if (p.post.on) {
                     amax = max(amax, post_store4(p.post, p.y, o, ch, v, 4, qa));
                 } else if (p.y) {
                     if (((uintptr_t)(p.y + o) & 15) == 0) {
