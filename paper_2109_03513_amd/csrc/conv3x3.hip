@@ -1,5 +1,5 @@
-// Direct 3x3 / stride-1 / pad-1 convolution over ESB codes on the fp8 MFMA of
-// gfx950 (Sec. 4.2: the convolution stage; products of codes by eq. (15),
+// Direct 3x3 / pad-1 convolution, stride 1 or 2, over ESB codes on the fp8 MFMA
+// of gfx950 (Sec. 4.2: the convolution stage; products of codes by eq. (15),
 // exact as in the implicit-GEMM path), for input and output channels that are
 // multiples of 64.
 //
@@ -11,8 +11,10 @@
 //    LDS patch, one 64-byte row per input pixel.  Every image is seen with a
 //    zero row above and below it and a zero column left and right (the
 //    padding), so a tile may cross images: output pixel (n, p, q) and tap
-//    (r, s) read patch pixel (n (P + 2) + p + r - R0, q + s), R0 the padded row
-//    of the tile's first pixel.  The four 16-byte chunks of a patch pixel are
+//    (r, s) read padded row n (H + 2) + st p + r - R0 (R0 the first padded row of
+//    the tile) and padded column st q + s.  With stride 2 a patch row holds the
+//    even padded columns first, then the odd ones, so that a tap over 32
+//    consecutive output pixels still reads consecutive patch pixels.  The four 16-byte chunks of a patch pixel are
 //    stored in the order chunk ^ ((pixel / 4) % 4), so that 16 consecutive
 //    pixels read at one chunk (a quarter-wave of a fragment load) hit 16
 //    different bank groups;
@@ -64,6 +66,8 @@ struct Conv3Params {
     MmaDecode dx, dw;
     Post post;
     int N, P, Q, M;            // M = N P Q output pixels
+    int H, W, st;              // input height and width, stride (1, or 2 in k_conv3x3)
+    int half;                  // stride 2: padded columns of even index, (W + 3) / 2
     int C, K;                  // channels in and out (multiples of 64)
     int ntm, ntn;              // pixel tiles, channel tiles
     int out_shift;             // acc = fl32 sum * 2^out_shift
@@ -269,12 +273,19 @@ void k_conv3x3(Conv3Params p) {
     const float s = ldexpf(p.alphaX[0] * p.alphaW[0], -(p.kX + p.kW));
     const float qa = post_alpha(p.post);
     uint32_t amax = 0;
-    const int cols = p.Q + 2, PP2 = p.P + 2, PQ = p.P * p.Q;
+    constexpr int FILL = kMaxFill;
+    const int st = p.st;
+    const int cols = p.W + 2, PP2 = p.H + 2, PQ = p.P * p.Q;
     // patch fill: thread t takes chunk t % (4 cols) of rows t / (4 cols), + rstep, ...
     const int cpr = 4 * cols;
     const int fci = tid % cpr, fri = tid / cpr, rstep = kThreads / cpr;
     const int fcol = fci >> 2, fc = fci & 3, iw = fcol - 1;
-    const bool col_in = (unsigned)iw < (unsigned)p.Q;
+    const bool col_in = (unsigned)iw < (unsigned)p.W;
+    // where padded column fcol sits in a patch row: stride 1 in order; stride 2 the
+    // even columns first, then the odd ones, so that the taps of consecutive output
+    // pixels (columns 2q + s) read consecutive patch pixels
+    const int dcol = st == 1 ? fcol : ((fcol & 1) ? p.half + (fcol >> 1) : (fcol >> 1));
+    const int tcol1 = st == 1 ? 1 : p.half, tcol2 = st == 1 ? 2 : 1;   // taps s = 1, 2
     // B fragments: channel 32 j + lr, bytes 32 lg .. + 31 of tap t
     const int boff = lr * WST + 32 * lg;
     const int64_t wrow = (int64_t)TAPS * p.C;        // filter bytes per output channel
@@ -283,15 +294,15 @@ void k_conv3x3(Conv3Params p) {
     auto rows_of = [&](int tile, int& R0, int& nrows) {
         const int m0 = tile * TM;
         const int i0 = m0 / PQ, p0 = (m0 - i0 * PQ) / p.Q;
-        R0 = i0 * PP2 + p0;
+        R0 = i0 * PP2 + st * p0;
         const int m1 = min(m0 + TM, p.M) - 1;
         const int i1 = m1 / PQ, p1 = (m1 - i1 * PQ) / p.Q;
-        nrows = i1 * PP2 + p1 + 3 - R0;
+        nrows = i1 * PP2 + st * p1 + 3 - R0;
     };
     // The codes of one (tile, chunk): this thread's patch chunks (chunk u is row
     // fri + u rstep; bit u of vmask: inside the input) and, with several chunks,
     // its filter chunks; every load in flight at once.
-    uint4 raw[kMaxFill], wraw[kWPer];
+    uint4 raw[FILL], wraw[kWPer];
     uint32_t vmask = 0;
     auto fetch = [&](int tile, int ch) {
         int R0, nrows;
@@ -301,11 +312,11 @@ void k_conv3x3(Conv3Params p) {
         vmask = 0;
         const uint8_t* xc = p.x + CK * ch + 16 * fc;
 #pragma unroll
-        for (int u = 0; u < kMaxFill; u++) {
+        for (int u = 0; u < FILL; u++) {
             const int ih = hp - 1;
             const bool ok = fri < rstep && fri + u * rstep < nrows && col_in && n < p.N &&
-                            (unsigned)ih < (unsigned)p.P;
-            const int64_t pix = ok ? ((int64_t)n * p.P + ih) * p.Q + iw : 0;
+                            (unsigned)ih < (unsigned)p.H;
+            const int64_t pix = ok ? ((int64_t)n * p.H + ih) * p.W + iw : 0;
             raw[u] = *(const uint4*)(xc + pix * p.C);
             vmask |= ok ? (1u << u) : 0u;
             hp += rstep;
@@ -354,7 +365,7 @@ void k_conv3x3(Conv3Params p) {
             const int m = min(m0 + 32 * (mbw + i) + lr, p.M - 1);   // rows past M: any pixel
             const int n = m / PQ, rem = m - n * PQ;
             const int pp = rem / p.Q, q = rem - pp * p.Q;
-            pb[i] = (n * PP2 + pp - R0) * cols + q;
+            pb[i] = (n * PP2 + st * pp - R0) * cols + q;
         }
         v16f acc[NMB][NNB];
 #pragma unroll
@@ -368,12 +379,12 @@ void k_conv3x3(Conv3Params p) {
             __syncthreads();   // the previous chunk's (or tile's) reads of the LDS are done
             if (fri < rstep) {
 #pragma unroll
-                for (int u = 0; u < kMaxFill; u++) {
+                for (int u = 0; u < FILL; u++) {
                     const int i = fri + u * rstep;
                     if (i < nrows) {
                         const uint4 v = ((vmask >> u) & 1u) ? dec16(raw[u], p.dx)
                                                             : make_uint4(0u, 0u, 0u, 0u);   // E4M3 +0
-                        *(uint4*)&patch[patch_off(i * cols + fcol, fc)] = v;
+                        *(uint4*)&patch[patch_off(i * cols + dcol, fc)] = v;
                     }
                 }
             }
@@ -395,7 +406,7 @@ void k_conv3x3(Conv3Params p) {
                 }
 #pragma unroll
                 for (int i = 0; i < NMB; i++) {
-                    const int pix = pb[i] + tr * cols + ts;
+                    const int pix = pb[i] + tr * cols + (ts == 0 ? 0 : (ts == 1 ? tcol1 : tcol2));
                     const int a0 = patch_off(pix, 2 * lg);
                     const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
                     fa[i] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -676,27 +687,29 @@ bool res_tile_fits(int P, int Q) {
 // Rows of the patch of a tile of TM pixels: the padded rows from the first
 // pixel's to two past the last pixel's, at most dg + 2 (images crossed) + 3
 // rows with dg the output rows a tile spans beyond its first.
-int patch_rows_max(int P, int Q, int TM) {
+// With stride st the tile's output rows span st dg + 3 padded input rows, and each
+// image boundary crossed adds the H + 2 - st P padded rows past the last output row's.
+int patch_rows_max(int P, int Q, int TM, int H, int st) {
     const int dg = (Q - 1 + TM - 1) / Q;
     const int cross = (P - 1 + dg) / P;
-    return dg + 2 * cross + 3;
+    return st * dg + cross * (H + 2 - st * P) + 3;
 }
 
-bool tile_fits(int P, int Q, int TM) {
-    if (Q + 2 > kMaxCols) return false;
-    const int rstep = kThreads / (4 * (Q + 2));
-    const int rows = patch_rows_max(P, Q, TM);
-    return (rows + rstep - 1) / rstep <= kMaxFill && (int64_t)rows * (Q + 2) * 64 <= kPatchMax;
+bool tile_fits(int P, int Q, int TM, int H, int W, int st) {
+    if (W + 2 > kMaxCols) return false;
+    const int rstep = kThreads / (4 * (W + 2));
+    const int rows = patch_rows_max(P, Q, TM, H, st);
+    return (rows + rstep - 1) / rstep <= kMaxFill && (int64_t)rows * (W + 2) * 64 <= kPatchMax;
 }
 
 // 32-pixel blocks per tile: the largest of 8, 4, 2 (4, 2 with several chunks of
 // input channels) whose tiles fit the patch and give at least one workgroup per
 // CU, else the largest that fits.
-int choose_tmb(int64_t M, int ntn, int P, int Q, bool multi) {
+int choose_tmb(int64_t M, int ntn, int P, int Q, int H, int W, int st, bool multi) {
     const int cus = num_cus();
     int fit = 0;
     for (int tmb = multi ? 4 : 8; tmb >= 2; tmb >>= 1) {
-        if (!tile_fits(P, Q, 32 * tmb)) continue;
+        if (!tile_fits(P, Q, 32 * tmb, H, W, st)) continue;
         if (!fit) fit = tmb;
         if ((M + 32 * tmb - 1) / (32 * tmb) * ntn >= cus) return tmb;
     }
@@ -708,9 +721,19 @@ int choose_tmb(int64_t M, int ntn, int P, int Q, bool multi) {
 bool conv3x3_fits(const ConvGeom& g, int K, int groups, int op, const uint8_t* x,
                   const uint8_t* w) {
     if (!(groups == 1 && op == 1 && K % NT == 0 && K >= NT && g.C % CK == 0 && g.C >= CK &&
-          g.Cg == g.C && g.pitch == g.C && g.R == 3 && g.S == 3 && g.sh == 1 && g.sw == 1 &&
-          g.ph == 1 && g.pw == 1 && g.P == g.H && g.Q == g.W && g.P >= 1 && g.Q >= 1))
+          g.Cg == g.C && g.pitch == g.C && g.R == 3 && g.S == 3 && g.ph == 1 && g.pw == 1 &&
+          g.P >= 1 && g.Q >= 1))
         return false;
+    const bool s1 = g.sh == 1 && g.sw == 1 && g.P == g.H && g.Q == g.W;
+    const bool s2 = g.sh == 2 && g.sw == 2 && g.P == (g.H - 1) / 2 + 1 && g.Q == (g.W - 1) / 2 + 1;
+    if (!s1 && !s2) return false;
+    // Stride 2 takes tiles of 64 output pixels (the patch holds four times the input
+    // of stride 1 per pixel), whose fill, repeated by every tile of 64 output channels,
+    // outweighs the MFMAs unless the input channels run to several chunks: measured
+    // at batch 64 against the implicit-GEMM path, 256 -> 512 at 14 x 14 24.1 against
+    // 28.4 us, but 64 -> 128 at 56 x 56 25.3 against 21.0 and 128 -> 256 at 28 x 28
+    // 28.5 against 19.6.
+    if (s2 && g.C < 4 * CK) return false;
     if ((uintptr_t)x % 16 || (uintptr_t)w % 16) return false;
     const int64_t M = (int64_t)g.Nb * g.P * g.Q;
     if ((M + 256) * K >= ((int64_t)1 << 31) || (int64_t)K * TAPS * g.C >= ((int64_t)1 << 31))
@@ -720,8 +743,8 @@ bool conv3x3_fits(const ConvGeom& g, int K, int groups, int op, const uint8_t* x
     // 3x3 at batch 64: 256 channels at 14 x 14 and 512 at 7 x 7 faster, 128 at 28 x 28
     // with 50176 pixels slower).
     if (g.C > CK && M > kMultiMaxPixels)   // several chunks and many pixels: resident filter
-        return res_ntr(g.C, K) != 0 && res_tile_fits(g.P, g.Q);
-    return choose_tmb(M, K / NT, g.P, g.Q, g.C > CK) != 0;
+        return s1 && res_ntr(g.C, K) != 0 && res_tile_fits(g.P, g.Q);
+    return choose_tmb(M, K / NT, g.P, g.Q, g.H, g.W, g.sh, g.C > CK) != 0;
 }
 
 hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt& fx,
@@ -741,6 +764,10 @@ hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt&
     p.N = g.Nb;
     p.P = g.P;
     p.Q = g.Q;
+    p.H = g.H;
+    p.W = g.W;
+    p.st = g.sh;
+    p.half = (g.W + 3) / 2;
     p.M = g.Nb * g.P * g.Q;
     p.C = g.C;
     p.K = K;
@@ -749,6 +776,7 @@ hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt&
     p.kX = fx.k;
     p.kW = fw.k;
     if (g.C > CK && p.M > kMultiMaxPixels) {   // the resident-filter kernel, one workgroup per CU
+        if (p.st != 1) return hipErrorInvalidValue;
         const int ntr = res_ntr(g.C, K);
         if (ntr == 0 || !res_tile_fits(g.P, g.Q)) return hipErrorInvalidValue;
         p.ntn = K / ntr;
@@ -768,7 +796,7 @@ hipError_t launch_conv3x3(const ConvGeom& g, int K, const uint8_t* x, const Fmt&
     }
     p.ntn = K / NT;
     const bool multi = g.C > CK;
-    const int tmb = choose_tmb(p.M, p.ntn, g.P, g.Q, multi);
+    const int tmb = choose_tmb(p.M, p.ntn, g.P, g.Q, g.H, g.W, p.st, multi);
     if (tmb == 0) return hipErrorInvalidValue;
     p.ntm = (p.M + 32 * tmb - 1) / (32 * tmb);
     // persistent workgroups, a whole number per channel tile, two per CU

@@ -1,7 +1,8 @@
-"""The direct 3x3 / stride-1 / pad-1 convolution kernels (input and output channels in
+"""The direct 3x3 / pad-1 convolution kernels, stride 1 and 2 (input and output channels in
 multiples of 64 on the fp8 MFMA; tiles of 256, 128 or 64 output pixels over the batch,
 crossing image boundaries; input channels in chunks of 64; the filter slice per chunk, or
-resident for the workgroup) against the oracle's convolution
+resident for the workgroup; with stride 2 the even padded columns of a patch row first)
+against the oracle's convolution
 and post-processing: bit-exact int32 sums, fp32 outputs and codes, equal running maximum;
 and bit for bit equal to the implicit-GEMM path, which an input one byte off a 16-byte
 boundary takes."""
@@ -53,6 +54,19 @@ CASES = [
     (24, 28, 28, 128, 128, (5, 3), (5, 3), "all"),    # 64 channels per workgroup, ragged
     (88, 14, 14, 256, 64, (5, 3), (4, 2), "plain"),   # 32 channels per workgroup
 ]
+# stride 2 (output (H - 1) / 2 + 1): N, H, W, C, K, fx, fw, variant.  The direct kernel
+# takes 256 or more input channels; the others check the implicit-GEMM path.
+CASES_S2 = [
+    (2, 14, 14, 256, 512, (5, 3), (4, 2), "plain"),   # l4.0.c1: four chunks, eight channel tiles
+    (3, 7, 7, 256, 64, (6, 3), (4, 1), "all"),        # 4 x 4 outputs per image
+    (2, 9, 11, 320, 128, (5, 3), (5, 3), "residual"), # five chunks, odd H and W
+    (4, 15, 17, 256, 64, (4, 2), (5, 3), "relu"),     # H != W, ragged last tile
+    (1, 1, 1, 256, 64, (5, 3), (5, 3), "affine"),     # one input pixel, one output
+    (2, 30, 62, 256, 64, (5, 3), (5, 3), "relu"),     # W + 2 = 64: 11 patch rows, implicit GEMM
+    (2, 56, 56, 64, 128, (5, 3), (5, 3), "all"),      # the ResNet18 l2.0.c1 shape, batch 2
+    (3, 28, 28, 128, 256, (5, 3), (5, 3), "relu"),    # l3.0.c1
+    (2, 13, 9, 64, 64, (5, 3), (5, 3), "residual"),   # odd H, W
+]
 
 
 def post_params(seed, y, K, variant):
@@ -68,24 +82,26 @@ def post_params(seed, y, K, variant):
     return a, b, res, relu, np.float32(0.4 * sd)
 
 
-@pytest.mark.parametrize("Nb,H,W,C,K,fx,fw,variant", CASES)
-def test_conv3x3_direct(esb, Nb, H, W, C, K, fx, fw, variant):
+@pytest.mark.parametrize("stride,Nb,H,W,C,K,fx,fw,variant",
+                         [(1,) + c for c in CASES] + [(2,) + c for c in CASES_S2])
+def test_conv3x3_direct(esb, stride, Nb, H, W, C, K, fx, fw, variant):
     torch = torch_cuda()
     x = wl.random_codes(40 + H + C, (Nb, H, W, C), fx[0])
     w = wl.random_codes(41 + W + K, (K, 3, 3, C), fw[0])
+    sd = (stride, stride)
     st, acc_o, y_o = oracle.conv2d(x, w, fx[0], fx[1], ALPHA_X, fw[0], fw[1], ALPHA_W,
-                                   stride=(1, 1), pad=(1, 1))
+                                   stride=sd, pad=(1, 1))
     assert st == 0
-    log("conv3x3 direct %s %s" % ((Nb, H, W, C, K, fx, fw), variant))
+    log("conv3x3 direct stride %d %s %s" % (stride, (Nb, H, W, C, K, fx, fw), variant))
     if variant == "plain":
         for want_acc in (True, False):
             acc, y = esb.esb_conv2d(dev(x), fx[0], fx[1], scalar(ALPHA_X), dev(w), fw[0], fw[1],
-                                    scalar(ALPHA_W), stride=(1, 1), pad=(1, 1), want_acc=want_acc)
+                                    scalar(ALPHA_W), stride=sd, pad=(1, 1), want_acc=want_acc)
             np.testing.assert_array_equal(host(y).view(np.uint32), y_o.view(np.uint32))
             if want_acc:
                 np.testing.assert_array_equal(host(acc), acc_o)
         acc_u, y_u = esb.esb_conv2d(unaligned(torch, x), fx[0], fx[1], scalar(ALPHA_X), dev(w),
-                                    fw[0], fw[1], scalar(ALPHA_W), stride=(1, 1), pad=(1, 1))
+                                    fw[0], fw[1], scalar(ALPHA_W), stride=sd, pad=(1, 1))
         np.testing.assert_array_equal(host(acc_u), acc_o)
         np.testing.assert_array_equal(host(y_u).view(np.uint32), y_o.view(np.uint32))
         return
@@ -100,7 +116,7 @@ def test_conv3x3_direct(esb, Nb, H, W, C, K, fx, fw, variant):
         acc, y, codes = esb.esb_conv2d_post(
             xin, fx[0], fx[1], scalar(ALPHA_X), dev(w), fw[0], fw[1], scalar(ALPHA_W),
             scalar(qa), 5, 3, a=None if a is None else dev(a), b=None if b is None else dev(b),
-            residual=None if res is None else dev(res), relu=relu, stride=(1, 1), pad=(1, 1),
+            residual=None if res is None else dev(res), relu=relu, stride=sd, pad=(1, 1),
             want_codes=True, want_acc=want_acc, want_y=True, absmax=amax)
         np.testing.assert_array_equal(host(y).view(np.uint32), z_o.view(np.uint32))
         np.testing.assert_array_equal(host(codes), codes_o)
