@@ -699,8 +699,8 @@ def resnet18_headline(args):
         gr["layers"].append(u["label"])
     units_ms = sum(gr["ms"] for gr in groups.values())
     kernels = {
-        "dda": "esb_dda_align_planned per layer input: k_dda_hist (+ k_dda_group) + k_dda_finalize",
-        "project": "esb_project per layer input: k_project_vec",
+        "quantize": "esb_quantize_planned per layer input: k_dda_hist (+ k_dda_group) + "
+                    "k_dda_project (the DDA's finishing step in every block of the projection)",
         "absmax": "esb_absmax: k_absmax",
         "maxpool": "esb_maxpool2d: k_maxpool",
         "avgpool": "esb_avgpool_global: k_avgpool",

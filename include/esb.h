@@ -245,6 +245,21 @@ int esb_dda_align_planned(const float* x, int64_t len, int n, int k_sig, const v
                           size_t ws_bytes, void* stream);
 
 /*
+ * Quantization of one tensor with a plan (eq. (9), (13), then eq. (6)-(8)): the
+ * planned aligner's alpha (and D_j), then the codes of x under that alpha, in
+ * one call.  Results are those of esb_dda_align_planned followed by esb_project
+ * with its alpha_out (identical alpha, D and codes).  For small tensors (at most
+ * 2048 * (CUs) elements, 16-byte aligned x, 4-byte aligned codes, the aligner's
+ * finishing step within one block of 256 threads) every block of the projection
+ * derives alpha itself instead of waiting for a separate finishing kernel.
+ *   arguments as esb_dda_align_planned; codes: device, len bytes (may be NULL
+ *   when len == 0); D_out may be NULL.
+ */
+int esb_quantize_planned(const float* x, int64_t len, int n, int k_sig, const void* plan, int G,
+                         const float* scale, float* alpha_out, double* D_out, uint8_t* codes,
+                         void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * esb_dda_align for callers that cannot allocate device memory: code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, search and results as esb_dda_align (alpha and D

@@ -956,11 +956,12 @@ __host__ __device__ inline int fin_split(int G, int nblk) {
 // and the argmin over (isnan(D), D, j), ties to the lowest index.
 // Block i of the grid finalizes job i (block vectors, or group vectors when
 // the job has groups).
-__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
-    const DdaJob& J = jobs.job[blockIdx.x];
+// The finishing step of job J inside one block (blockDim.x a multiple of 64 and at
+// least G * S): writes D_out[j] when D_out is given and *alpha_out from thread 0 when
+// alpha_out is given, and returns the chosen candidate to every thread.
+__device__ __forceinline__ float dda_finish(const DdaJob& J, float* __restrict__ alpha_out,
+                                            double* __restrict__ D_out) {
     const float* __restrict__ grid = J.grid;
-    float* __restrict__ alpha_out = J.alpha_out;
-    double* __restrict__ D_out = J.D_out;
     const double* __restrict__ part = J.ngrp > 0 ? J.grp : J.part;
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int G = J.a.G, nb = J.ngrp > 0 ? J.ngrp : J.a.nblk, ps = part_stride(G);
@@ -1013,6 +1014,8 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
         if (D_out) D_out[j] = D;
         bd = D; bj = j; ba = al;
     }
+    // (isnan(D), D, j) is a total order: the result does not depend on the order of
+    // the comparisons, and after the butterfly every lane of a wave holds its best
     auto pick = [](double& bd, int& bj, float& ba, double od, int oj, float oa) {
         const bool onan = od != od, mnan = bd != bd;
         const bool better = (oj != 0x7fffffff) &&
@@ -1027,17 +1030,71 @@ __global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
         pick(bd, bj, ba, od, oj, oa);
     }
     if (blockDim.x == 64) {
-        if (lane == 0) *alpha_out = ba;
-        return;
+        if (alpha_out && lane == 0) *alpha_out = ba;
+        return ba;
     }
     __shared__ double s_bd[kFinThreads / 64];
     __shared__ int s_bj[kFinThreads / 64];
     __shared__ float s_ba[kFinThreads / 64];
+    __shared__ float s_alpha;
     if (lane == 0) { s_bd[wid] = bd; s_bj[wid] = bj; s_ba[wid] = ba; }
     lds_barrier();
     if (tid == 0) {
         for (int v = 1; v < (int)(blockDim.x / 64); v++) pick(bd, bj, ba, s_bd[v], s_bj[v], s_ba[v]);
-        *alpha_out = ba;
+        if (alpha_out) *alpha_out = ba;
+        s_alpha = ba;
+    }
+    lds_barrier();
+    return s_alpha;
+}
+
+__global__ __launch_bounds__(kFinThreads) void k_dda_finalize(DdaBatch jobs) {
+    const DdaJob& J = jobs.job[blockIdx.x];
+    dda_finish(J, J.alpha_out, J.D_out);
+}
+
+// The finishing step fused with the projection onto the chosen scale (eq. (6)-(8)),
+// for one job: every block derives alpha itself with the finalize's arithmetic (the
+// same value everywhere), block 0 also writes alpha_out and D_out, and each block
+// then projects its tile of kQTile4 float4 of x (its loads issued before the
+// finishing sums); the last block also takes the len % 4 tail.  Results equal
+// k_dda_finalize followed by the projection.
+constexpr int kQTile4 = 4 * 256;
+__global__ __launch_bounds__(256) void k_dda_project(DdaBatch jobs, const float* __restrict__ x,
+                                                     int64_t len, ProjParams pp,
+                                                     uint8_t* __restrict__ codes) {
+    const DdaJob& J = jobs.job[0];
+    const int tid = threadIdx.x;
+    const int64_t n4 = len >> 2;
+    const f32x4* x4 = (const f32x4*)x;
+    uint32_t* out4 = (uint32_t*)codes;
+    const int64_t i0 = (int64_t)blockIdx.x * kQTile4 + tid;
+    const bool whole = i0 + 3 * 256 < n4;
+    f32x4 v[4];
+    if (whole) {
+#pragma unroll
+        for (int u = 0; u < 4; u++) v[u] = __builtin_nontemporal_load(&x4[i0 + u * 256]);
+    }
+    const bool first = blockIdx.x == 0;
+    const float alpha = dda_finish(J, first ? J.alpha_out : nullptr, first ? J.D_out : nullptr);
+    const bool ok = alpha_valid(alpha);
+    const bool fast = fast_scale(alpha);
+    const float r = 1.0f / alpha;
+    const uint32_t z4 = pp.zero_code * 0x01010101u;
+    if (whole) {
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+            __builtin_nontemporal_store(ok ? code4(v[u], alpha, r, fast, pp) : z4, &out4[i0 + u * 256]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int64_t i = i0 + u * 256;
+            if (i < n4) out4[i] = ok ? code4(x4[i], alpha, r, fast, pp) : z4;
+        }
+    }
+    if (blockIdx.x == gridDim.x - 1 && tid < (int)(len - 4 * n4)) {
+        const int64_t i = 4 * n4 + tid;
+        codes[i] = (uint8_t)(ok ? esb_code(x[i], alpha, pp) : pp.zero_code);
     }
 }
 
@@ -1069,39 +1126,75 @@ static hipError_t launch_batch(DdaBatch& B, int max_lds, int max_fin_threads, in
     return hipGetLastError();
 }
 
+// The launch set-up of up to kDdaMaxJobs jobs: their blocks, groups and LDS.
+static void build_batch(const DdaJobDesc* jobs, int count, DdaBatch& B, int& nhist, int& ngroups,
+                        int& max_lds, int& max_fin) {
+    B.count = count;
+    nhist = 0; ngroups = 0; max_lds = 0; max_fin = 64;
+    for (int i = 0; i < B.count; i++) {
+        const DdaJobDesc& d = jobs[i];
+        DdaJob& J = B.job[i];
+        DdaArgs& a = J.a;
+        a.G = d.G; a.M = d.L.M; a.A = d.L.A; a.Aa = d.L.A + kMaxSplits;
+        a.n = d.f.n; a.k = d.f.k;
+        dda_blocks(d.len, &a.nblk, &a.rows_pb);
+        a.lbins = d.plan ? plan_lbins(d.L.A) : hist_lbins(d.L.A, a.rows_pb >= 8);
+        J.x = d.x; J.len = d.len; J.grid = d.grid; J.gscale = d.gscale;
+        J.plan = d.plan;
+        if (d.plan) J.grid = (const float*)(d.plan + plan_factors_off());
+        J.alpha_out = d.alpha_out; J.D_out = d.D_out;
+        J.part = (double*)((char*)d.ws + d.L.off_part);
+        J.grp = (double*)((char*)d.ws + d.L.off_group);
+        J.blk0 = nhist;
+        nhist += a.nblk;
+        J.ngrp = dda_groups(a.nblk);
+        J.grp0 = ngroups;
+        ngroups += J.ngrp;
+        const int lds = (int)hist_lds(d.L.A, a.lbins).total;
+        if (lds > max_lds) max_lds = lds;
+        const int nt = (d.G * fin_split(d.G, J.ngrp > 0 ? J.ngrp : a.nblk) + 63) / 64 * 64;
+        if (nt > max_fin) max_fin = nt;   // <= kFinThreads
+    }
+}
+
 hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s) {
     for (int c0 = 0; c0 < count; c0 += kDdaMaxJobs) {
         DdaBatch B;
-        B.count = count - c0 < kDdaMaxJobs ? count - c0 : kDdaMaxJobs;
         int nhist = 0, ngroups = 0, max_lds = 0, max_fin = 64;
-        for (int i = 0; i < B.count; i++) {
-            const DdaJobDesc& d = jobs[c0 + i];
-            DdaJob& J = B.job[i];
-            DdaArgs& a = J.a;
-            a.G = d.G; a.M = d.L.M; a.A = d.L.A; a.Aa = d.L.A + kMaxSplits;
-            a.n = d.f.n; a.k = d.f.k;
-            dda_blocks(d.len, &a.nblk, &a.rows_pb);
-            a.lbins = d.plan ? plan_lbins(d.L.A) : hist_lbins(d.L.A, a.rows_pb >= 8);
-            J.x = d.x; J.len = d.len; J.grid = d.grid; J.gscale = d.gscale;
-            J.plan = d.plan;
-            if (d.plan) J.grid = (const float*)(d.plan + plan_factors_off());
-            J.alpha_out = d.alpha_out; J.D_out = d.D_out;
-            J.part = (double*)((char*)d.ws + d.L.off_part);
-            J.grp = (double*)((char*)d.ws + d.L.off_group);
-            J.blk0 = nhist;
-            nhist += a.nblk;
-            J.ngrp = dda_groups(a.nblk);
-            J.grp0 = ngroups;
-            ngroups += J.ngrp;
-            const int lds = (int)hist_lds(d.L.A, a.lbins).total;
-            if (lds > max_lds) max_lds = lds;
-            const int nt = (d.G * fin_split(d.G, J.ngrp > 0 ? J.ngrp : a.nblk) + 63) / 64 * 64;
-            if (nt > max_fin) max_fin = nt;   // <= kFinThreads
-        }
+        build_batch(jobs + c0, count - c0 < kDdaMaxJobs ? count - c0 : kDdaMaxJobs, B, nhist, ngroups,
+                    max_lds, max_fin);
         const hipError_t e = launch_batch(B, max_lds, max_fin, nhist, ngroups, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_dda_quantize(const DdaJobDesc& d, uint8_t* codes, hipStream_t s) {
+    DdaBatch B;
+    int nhist = 0, ngroups = 0, max_lds = 0, max_fin = 64;
+    build_batch(&d, 1, B, nhist, ngroups, max_lds, max_fin);
+    const DdaJob& J = B.job[0];
+    const int nb = J.ngrp > 0 ? J.ngrp : J.a.nblk;
+    // Fused when the finishing step's threads fit one block of 256, the vector path
+    // applies and the projection has at most two tiles per CU: every block reads all
+    // the group vectors, which for more blocks costs more than the finalize launch
+    // saves (ESB(5,2), 64 factors, against the two calls: 32768 elements 16.4 against
+    // 17.4 us, 1.6 M 22.9 against 24.1, 3.2 M equal, 12.8 M 52.0 against 43.2).
+    const int64_t tiles = ((d.len >> 2) + kQTile4 - 1) / kQTile4;
+    const bool fused = d.G * fin_split(d.G, nb) <= 256 && (uintptr_t)d.x % 16 == 0 &&
+                       (uintptr_t)codes % 4 == 0 && tiles <= 2 * (int64_t)num_cus();
+    if (!fused) {
+        const hipError_t e = launch_batch(B, max_lds, max_fin, nhist, ngroups, s);
+        if (e != hipSuccess) return e;
+        return launch_project(d.x, d.len, d.alpha_out, d.f, codes, nullptr, s);
+    }
+    hipError_t e = set_lds_attributes();
+    if (e != hipSuccess) return e;
+    k_dda_hist<<<nhist, kHistThreads, max_lds, s>>>(B);
+    if (ngroups > 0) k_dda_group<<<ngroups, 256, 0, s>>>(B);
+    k_dda_project<<<(unsigned)(tiles > 0 ? tiles : 1), 256, 0, s>>>(B, d.x, d.len, proj_params(d.f),
+                                                                    codes);
+    return hipGetLastError();
 }
 
 hipError_t launch_dda(const float* x, int64_t len, const Fmt& f, const float* grid, int G,

@@ -222,6 +222,23 @@ int esb_dda_align_planned(const float* x, int64_t len, int n, int k_sig, const v
     return hip_status(launch_dda_batch(&d, 1, (hipStream_t)stream));
 }
 
+int esb_quantize_planned(const float* x, int64_t len, int n, int k_sig, const void* plan, int G,
+                         const float* scale, float* alpha_out, double* D_out, uint8_t* codes,
+                         void* workspace, size_t ws_bytes, void* stream) {
+    if (!valid_fmt(n, k_sig) || len < 0 || !plan || !scale || !alpha_out) return ESB_E_INVALID;
+    if (len > 0 && (!x || !codes)) return ESB_E_INVALID;
+    if ((uintptr_t)plan % 16) return ESB_E_INVALID;
+    DdaJobDesc d{};
+    d.f = make_fmt(n, k_sig);
+    if (!dda_layout(len, d.f, G, &d.L)) return ESB_E_INVALID;
+    if (!workspace || ws_bytes < d.L.total) return ESB_E_WORKSPACE;
+    d.x = x; d.len = len; d.grid = nullptr; d.G = G;
+    d.alpha_out = alpha_out; d.D_out = D_out; d.ws = workspace;
+    d.gscale = scale;
+    d.plan = (const uint8_t*)plan;
+    return hip_status(launch_dda_quantize(d, codes, (hipStream_t)stream));
+}
+
 size_t esb_dda_batch_workspace_size(int count, const esb_dda_job* jobs) {
     if (count < 0 || (count > 0 && !jobs)) return 0;
     size_t total = 0;

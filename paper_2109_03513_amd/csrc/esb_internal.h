@@ -327,6 +327,9 @@ struct DdaJobDesc {
                            // E the binary exponent of |*gscale|
 };
 hipError_t launch_dda_batch(const DdaJobDesc* jobs, int count, hipStream_t s);
+// One job, then the projection of its tensor onto the chosen scale: the finishing
+// step fused into the projection where it fits one block (codes: len bytes).
+hipError_t launch_dda_quantize(const DdaJobDesc& d, uint8_t* codes, hipStream_t s);
 // Plans: the grid-only set-up of the DDA for candidates factors[j], built once.
 size_t dda_plan_bytes(const Fmt& f, int G);
 hipError_t launch_dda_plan(const Fmt& f, const float* factors, int G, void* plan, hipStream_t s);

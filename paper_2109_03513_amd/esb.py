@@ -85,6 +85,7 @@ def lib():
             "esb_dda_plan_size": (sz, [i32, i32, i32]),
             "esb_dda_plan": (i32, [i32, i32, P, i32, P, sz, P]),
             "esb_dda_align_planned": (i32, [P, i64, i32, i32, P, i32, P, P, P, P, sz, P]),
+            "esb_quantize_planned": (i32, [P, i64, i32, i32, P, i32, P, P, P, P, P, sz, P]),
             "esb_gemm": (i32, [i32, i32, i32, P, i64, i32, i32, P, P, i64, i32, i32, P, i32, P, P,
                                i64, P]),
             "esb_conv2d": (i32, [ctypes.POINTER(ConvDesc), P, i32, i32, P, P, i32, i32, P, P, P,
@@ -270,6 +271,30 @@ def esb_dda_align_planned(x, n, k_sig, plan, G, scale, alpha_out=None, D_out=Non
         _ptr(x), x.numel(), n, k_sig, _ptr(plan), G, _ptr(scale), _ptr(alpha_out), _ptr(D_out),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
     return alpha_out, D_out
+
+
+def esb_quantize_planned(x, n, k_sig, plan, G, scale, alpha_out=None, D_out=None, codes=None,
+                         workspace=None, stream=None, want_D=True):
+    """The planned DDA's alpha (and D), then the codes of x under it, in one call.
+    Returns (alpha_out, D_out, codes)."""
+    import torch
+    _dev_tensor(x, torch.float32, "x")
+    _dev_tensor(scale, torch.float32, "scale")
+    dev = x.device
+    if alpha_out is None:
+        alpha_out = torch.empty(1, dtype=torch.float32, device=dev)
+    if D_out is None and want_D:
+        D_out = torch.empty(G, dtype=torch.float64, device=dev)
+    if codes is None:
+        codes = torch.empty(x.shape, dtype=torch.uint8, device=dev)
+    if workspace is None:
+        need = esb_dda_workspace_size(x.numel(), n, k_sig, G)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check("esb_quantize_planned", lib().esb_quantize_planned(
+        _ptr(x), x.numel(), n, k_sig, _ptr(plan), G, _ptr(scale), _ptr(alpha_out), _ptr(D_out),
+        _ptr(codes), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(stream)))
+    return alpha_out, D_out, codes
 
 
 def esb_gemm_workspace_size(M, N, K, nA, kA_sig, nB, kB_sig):

@@ -10,8 +10,8 @@ two; projected to ESB codes (eq. (8)) and contracted with the pre-quantized
 weights (eq. (15)) into fp32 outputs.  Scaling every candidate by a power of
 two scales its exact thresholds by the same power, so the DDA's grid-only
 set-up is built once (esb_dda_plan) and every call only shifts it
-(esb_dda_align_planned).  Weights are quantized once, the same way, when the
-model is built.
+(esb_quantize_planned: the planned DDA and the projection in one call).  Weights
+are quantized once, the same way, when the model is built.
 
 Every step runs in the library's kernels; torch only holds the buffers (and
 clears the running maxima at the start of a pass).  The ReLUs and the residual
@@ -144,8 +144,9 @@ class ResNet18ESB:
 
     def _quantize(self, x, ws, xmax=None, label=""):
         """DDA over alpha_j = 2^E c_j, E the binary exponent of the device scalar xmax (the
-        plan's tables shifted by E), then the projection.  xmax: a device scalar already
-        holding max|x| (from the producing epilogue), else esb_absmax."""
+        plan's tables shifted by E), then the projection, in one call (esb_quantize_planned).
+        xmax: a device scalar already holding max|x| (from the producing epilogue), else
+        esb_absmax."""
         torch = self.torch
         alpha = torch.empty(1, dtype=torch.float32, device=x.device)
         codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
@@ -154,14 +155,13 @@ class ResNet18ESB:
             xmax = self.spare
             xmax.zero_()
             self._call("absmax", label, lambda: esb.esb_absmax(x, xmax, stream=self.sh), 4 * nel)
-        self._call("dda", label,
-                   lambda: esb.esb_dda_align_planned(x, self.n, self.ks, self.plan, GRID_POINTS,
-                                                     xmax, alpha_out=alpha, workspace=ws,
-                                                     stream=self.sh, want_D=False),
-                   4 * nel)
-        self._call("project", label,
-                   lambda: esb.esb_project(x, alpha, self.n, self.ks, codes=codes, stream=self.sh),
-                   5 * nel)
+        # one call: the DDA's pass (4 B per element read), then the projection (4 B read,
+        # 1 B written), its blocks choosing alpha themselves
+        self._call("quantize", label,
+                   lambda: esb.esb_quantize_planned(x, self.n, self.ks, self.plan, GRID_POINTS,
+                                                    xmax, alpha_out=alpha, codes=codes,
+                                                    workspace=ws, stream=self.sh, want_D=False),
+                   9 * nel)
         return alpha, codes
 
     def conv(self, name, x, quantized=None, xmax=None, residual=None, relu=False, absmax=None):
