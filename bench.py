@@ -244,15 +244,16 @@ def conv3x3_step(args, with_cpu=True):
 
 
 def measured_traffic(key):
-    """HBM bytes per launch of `key` from the committed counter runs, or None when the
+    """HBM bytes per launch of `key` from the committed counter runs, or None when a
     kernel source changed since they were taken (sha256 recorded with the figure)."""
     import hashlib
     try:
         table = json.load(open(os.path.join(ROOT, "profiles", "hbm_traffic.json")))
         ent = table[key]
-        src = open(os.path.join(ROOT, ent["source"]), "rb").read()
-        if hashlib.sha256(src).hexdigest() != ent["sha256"]:
-            return None
+        for path, digest in ent["sources"].items():   # every source of the group's kernels
+            src = open(os.path.join(ROOT, path), "rb").read()
+            if hashlib.sha256(src).hexdigest() != digest:
+                return None
         return ent["bytes"]
     except (OSError, KeyError, ValueError):
         return None
