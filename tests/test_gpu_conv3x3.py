@@ -46,9 +46,12 @@ CASES = [
     (3, 14, 14, 256, 192, (5, 3), (4, 2), "relu"),    # four chunks, three channel tiles
     (1, 5, 9, 192, 64, (5, 3), (5, 3), "residual"),   # three chunks, ragged
     (2, 7, 7, 512, 128, (5, 3), (5, 3), "plain"),     # eight chunks (the l4 reduction)
-    # 64-pixel tiles: taken on 256 CUs when tiles of 128 give fewer workgroups than CUs
-    (50, 7, 7, 128, 512, (5, 3), (5, 3), "plain"),    # several chunks
+    # one chunk: 64-pixel tiles when tiles of 128 give fewer workgroups than CUs; several
+    # chunks: 128-pixel tiles down to half a workgroup per CU
+    (50, 7, 7, 128, 512, (5, 3), (5, 3), "plain"),    # several chunks, 128-pixel tiles
     (16, 14, 14, 64, 512, (5, 3), (5, 3), "affine"),  # one chunk, eight channel tiles
+    (8, 1, 40, 128, 64, (5, 3), (5, 3), "all"),       # several chunks, 64-pixel tiles (one-row
+                                                      # images: 128 pixels need 15 patch rows)
     # several chunks and more than 16384 pixels: the resident-filter kernel (eight waves,
     # one workgroup per CU, 64 or 32 output channels per workgroup)
     (24, 28, 28, 128, 128, (5, 3), (5, 3), "all"),    # 64 channels per workgroup, ragged
