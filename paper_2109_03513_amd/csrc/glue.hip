@@ -68,6 +68,7 @@ __global__ __launch_bounds__(256) void k_maxpool(const float* __restrict__ x, Po
 // Bit pattern of |v| ordered as an unsigned integer (NaN above +Inf).
 __device__ __forceinline__ uint32_t abs_bits(float v) { return __float_as_uint(v) & 0x7fffffffu; }
 
+constexpr int kAvgAhead = 64;
 __global__ __launch_bounds__(256) void k_avgpool(const float* __restrict__ x, int N, int HW, int C,
                                                  float* __restrict__ out, uint32_t* absmax) {
     const int64_t total = (int64_t)N * C;
@@ -77,7 +78,16 @@ __global__ __launch_bounds__(256) void k_avgpool(const float* __restrict__ x, in
         const int64_t n = t / C, c = t - n * C;
         const float* p = x + n * HW * C + c;
         double sum = 0.0;
-        for (int i = 0; i < HW; i++) sum += (double)p[(int64_t)i * C];
+        // positions kAvgAhead at a time, every load in flight before the first add
+        // (indices clamped, so the loads carry no branch); the adds in position order
+        for (int i0 = 0; i0 < HW; i0 += kAvgAhead) {
+            float v[kAvgAhead];
+#pragma unroll
+            for (int u = 0; u < kAvgAhead; u++) v[u] = p[(int64_t)min(i0 + u, HW - 1) * C];
+#pragma unroll
+            for (int u = 0; u < kAvgAhead; u++)
+                if (i0 + u < HW) sum += (double)v[u];
+        }
         const float v = (float)(sum / (double)HW);
         out[t] = v;
         m = max(m, abs_bits(v));
