@@ -35,6 +35,17 @@ def run(esb, x, b, ks, grid):
 NEAR = 1e-10
 
 
+def chosen(Do, j, grid):
+    """The candidates the GPU may return: the oracle's choice, or, when another candidate's
+    D is within NEAR of the best without being equal to it, any of those near-equal ones."""
+    best = Do[j]
+    if np.isfinite(best) and best > 0:
+        near = np.flatnonzero(~np.isnan(Do) & (Do <= best * (1.0 + NEAR)))
+        if not np.all(Do[near] == best):
+            return grid[near]
+    return grid[j:j + 1]
+
+
 def check(esb, x, b, ks, grid, what):
     """D within REL of the oracle; alpha equal to the oracle's unless another candidate is
     within NEAR of the best without being exactly equal to it (then alpha is one of those
@@ -163,3 +174,42 @@ def test_dda_reused_workspace(esb):
         assert_rel(host(D), Do, REL, "reuse %d" % i)
         if n > 0:
             assert host(a)[0] == grid[j]
+
+
+def test_dda_groups_repeated(esb):
+    """Inputs of more than 32 histogram blocks (block vectors summed in groups before the
+    finishing step): twelve calls on one workspace alternate two inputs (4 and 13 groups),
+    so each call's vectors overwrite the previous call's at the same addresses; every
+    call's alpha and D against the oracle, then the planned quantize call of the forward
+    the same way (alpha, and the codes of the oracle's projection under it)."""
+    torch = pytest.importorskip("torch")
+    lengths = [400000, 1605632]
+    need = max(esb.esb_dda_workspace_size(n, 5, 3, 64) for n in lengths)
+    ws = torch.full((need,), 0x5A, dtype=torch.uint8, device="cuda")
+    grid = wl.scale_grid(1.0)
+    xs = [np.maximum(np.random.default_rng([91, i]).standard_normal(n), 0.0).astype(np.float32)
+          * np.float32(0.5 + i) for i, n in enumerate(lengths)]
+    ref = [oracle.dda(x, 5, 3, grid) for x in xs]
+    for it in range(12):
+        i = it % 2
+        log("dda groups repeated call %d len=%d" % (it, xs[i].size))
+        a, D = esb.esb_dda_align(dev(xs[i]), 5, 3, dev(grid), workspace=ws)
+        j, Do = ref[i]
+        assert_rel(host(D), Do, REL, "call %d" % it)
+        assert host(a)[0] in chosen(Do, j, grid), (it, host(a)[0], grid[j])
+    factors = wl.scale_grid(1.0).astype(np.float32)
+    plan = esb.esb_dda_plan(5, 3, dev(factors))
+    for it in range(6):
+        i = it % 2
+        x = xs[i]
+        scale = np.float32(np.abs(x).max())
+        log("quantize groups repeated call %d len=%d" % (it, x.size))
+        a, _, codes = esb.esb_quantize_planned(dev(x), 5, 3, plan, factors.size,
+                                               dev(np.array([scale], dtype=np.float32)),
+                                               workspace=ws)
+        _, e = np.frexp(scale)
+        cand = np.ldexp(factors.astype(np.float64), int(e)).astype(np.float32)
+        jq, Dq = oracle.dda(x, 5, 3, cand)
+        aq = host(a)[0]
+        assert aq in chosen(Dq, jq, cand), (it, aq, cand[jq])
+        np.testing.assert_array_equal(host(codes), oracle.project(x, aq, 5, 3))
