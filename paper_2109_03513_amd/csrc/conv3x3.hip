@@ -394,10 +394,9 @@ void k_conv3x3(Conv3Params p) {
             if (ch + 1 < nchunks) fetch(tile, ch + 1);
             else if (tile + nwg < p.ntm) fetch(tile + nwg, 0);
 
-#pragma unroll
-            for (int t = 0; t < TAPS; t++) {
+            // fragments of tap t (B: channel 32 j + lr; A: the patch pixel of tap t)
+            auto frags = [&](int t, v8i (&fa)[NMB], v8i (&fb)[NNB]) {
                 const int tr = t / 3, ts = t - 3 * tr;
-                v8i fb[NNB], fa[NMB];
 #pragma unroll
                 for (int j = 0; j < NNB; j++) {
                     const uint8_t* b = &wlds[boff + 32 * (nbw + j) * WST + 64 * t];
@@ -411,13 +410,28 @@ void k_conv3x3(Conv3Params p) {
                     const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
                     fa[i] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                 }
+            };
+            // the next tap's fragments are read before this tap's MFMAs are issued, so
+            // their LDS latency overlaps the MFMAs (two taps' fragments live at a time)
+            v8i fa[NMB], fb[NNB];
+            frags(0, fa, fb);
+#pragma unroll
+            for (int t = 0; t < TAPS; t++) {
+                v8i na[NMB], nb[NNB];
+                if (t + 1 < TAPS) frags(t + 1, na, nb);
 #pragma unroll
                 for (int i = 0; i < NMB; i++)
 #pragma unroll
                     for (int j = 0; j < NNB; j++)
                         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                             fa[i], fb[j], acc[i][j], 0, 0, 0, 127, 0, 127);
-                __builtin_amdgcn_sched_barrier(0);   // one tap's fragments live at a time
+                __builtin_amdgcn_sched_barrier(0);
+                if (t + 1 < TAPS) {
+#pragma unroll
+                    for (int i = 0; i < NMB; i++) fa[i] = na[i];
+#pragma unroll
+                    for (int j = 0; j < NNB; j++) fb[j] = nb[j];
+                }
             }
         }
 
@@ -600,27 +614,35 @@ void k_conv3x3_res(Conv3Params p) {
             else if (tile + nwg < p.ntm) fetch(tile + nwg, 0);
 
             const uint8_t* wb = &wres[boff + CK * ch];
-#pragma unroll
-            for (int t = 0; t < TAPS; t++) {
+            auto frags = [&](int t, v8i& fa, v8i (&fb)[NNB]) {
                 const int tr = t / 3, ts = t - 3 * tr;
-                v8i fb[NNB], fa;
 #pragma unroll
                 for (int j = 0; j < NNB; j++) {
                     const uint8_t* b = wb + 32 * j * wst + t * p.C;
                     const v4i lo = *(const v4i*)b, hi = *(const v4i*)(b + 16);
                     fb[j] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                 }
-                {
-                    const int pix = pb + tr * cols + ts;
-                    const int a0 = patch_off(pix, 2 * lg);
-                    const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
-                    fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                }
+                const int pix = pb + tr * cols + ts;
+                const int a0 = patch_off(pix, 2 * lg);
+                const v4i lo = *(const v4i*)&patch[a0], hi = *(const v4i*)&patch[a0 ^ 16];
+                fa = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            };
+            v8i fa, fb[NNB];   // the next tap's fragments read before this tap's MFMAs
+            frags(0, fa, fb);
+#pragma unroll
+            for (int t = 0; t < TAPS; t++) {
+                v8i na, nb[NNB];
+                if (t + 1 < TAPS) frags(t + 1, na, nb);
 #pragma unroll
                 for (int j = 0; j < NNB; j++)
                     acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                         fa, fb[j], acc[j], 0, 0, 0, 127, 0, 127);
                 __builtin_amdgcn_sched_barrier(0);
+                if (t + 1 < TAPS) {
+                    fa = na;
+#pragma unroll
+                    for (int j = 0; j < NNB; j++) fb[j] = nb[j];
+                }
             }
         }
 
