@@ -128,3 +128,38 @@ def test_conv3x3_direct(esb, stride, Nb, H, W, C, K, fx, fw, variant):
             np.testing.assert_array_equal(host(acc), acc_o)
         outs.append(host(y))
     np.testing.assert_array_equal(outs[0].view(np.uint32), outs[2].view(np.uint32))
+
+
+def random_shapes(count, seed=2109):
+    """Seeded shapes in the direct kernels' domain (channels in multiples of 64, stride 1
+    or 2), each at most about 1.5e8 multiply-adds so that the oracle finishes quickly."""
+    r = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        st = int(r.choice([1, 2]))
+        C = 64 * int(r.choice([1, 2, 3, 4, 5, 8]))
+        K = 64 * int(r.choice([1, 2, 3]))
+        H, W = int(r.integers(1, 41)), int(r.integers(1, 41))
+        Nb = int(r.integers(1, 5))
+        P, Q = (H - 1) // st + 1, (W - 1) // st + 1
+        if Nb * P * Q * K * 9 * C > 150_000_000:
+            continue
+        out.append((st, Nb, H, W, C, K))
+    return out
+
+
+@pytest.mark.parametrize("st,Nb,H,W,C,K", random_shapes(24))
+def test_conv3x3_direct_random_shapes(esb, st, Nb, H, W, C, K):
+    """Plain outputs and int32 sums against the oracle on seeded shapes: ragged tiles, tiles
+    across images, odd and even chunk counts, both strides (stride 2 below 256 channels and
+    shapes the direct kernels do not take run the implicit GEMM: the same results)."""
+    x = wl.random_codes(5000 + H * W + C, (Nb, H, W, C), 5)
+    w = wl.random_codes(6000 + K + C, (K, 3, 3, C), 5)
+    sd = (st, st)
+    status, acc_o, y_o = oracle.conv2d(x, w, 5, 3, ALPHA_X, 5, 3, ALPHA_W, stride=sd, pad=(1, 1))
+    assert status == 0
+    log("conv3x3 random stride %d %s" % (st, (Nb, H, W, C, K)))
+    acc, y = esb.esb_conv2d(dev(x), 5, 3, scalar(ALPHA_X), dev(w), 5, 3, scalar(ALPHA_W),
+                            stride=sd, pad=(1, 1), want_acc=True)
+    np.testing.assert_array_equal(host(acc), acc_o)
+    np.testing.assert_array_equal(host(y).view(np.uint32), y_o.view(np.uint32))
