@@ -331,6 +331,16 @@ def sweep(args):
                 ms = time_launches(lambda: esb.esb_dda_align(x, n, ks, grid, alpha_out=ao, D_out=Do,
                                                              workspace=ws, stream=sh), args.reps, stream)
                 emit("dda_n%d_k%d_G64_2^27" % (n, ks), ms, nbytes=4.0 * big)
+                # the same search with a plan (the grid-only set-up built once): candidates
+                # 2^E f_j with E the binary exponent of max|x|, the forward's form
+                fac = torch.from_numpy(workloads.scale_grid(1.0)).to(dev)
+                plan = esb.esb_dda_plan(n, ks, fac, stream=sh)
+                xmax = x.abs().max().reshape(1)
+                ms = time_launches(lambda: esb.esb_dda_align_planned(x, n, ks, plan, 64, xmax,
+                                                                     alpha_out=ao, D_out=Do,
+                                                                     workspace=ws, stream=sh),
+                                   args.reps, stream)
+                emit("dda_planned_n%d_k%d_G64_2^27" % (n, ks), ms, nbytes=4.0 * big)
         if want("dn"):
             # normalization statistics (two passes), projection of normalized data, and the
             # analytic aligner over 4096 candidates (Alg. 1: W_q = ESB(DN(W)))
