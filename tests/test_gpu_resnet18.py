@@ -120,7 +120,9 @@ def test_resnet18_stack_matches_oracle(batch, seed):
 def test_resnet18_fused_equals_dda_forward():
     """With the scales of a DDA forward fixed (calibration on the same batch), the fused
     forward (epilogues writing the next layer's codes) gives the same logits bit for bit:
-    the epilogue's residual sum and ReLU are the glue's own fp32 operations."""
+    the epilogue's residual sum and ReLU are the glue's own fp32 operations.  The DDA
+    forward on this input (seed 1) is itself compared with the oracle's stack in
+    test_resnet18_stack_matches_oracle, so the fused logits are pinned to the oracle too."""
     import torch
     from paper_2109_03513_amd import resnet18
     batch = 2
