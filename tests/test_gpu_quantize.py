@@ -86,3 +86,25 @@ def test_quantize_codes_match_oracle(esb):
     a, codes = compare(esb, dev(x), 5, 3, plan, factors.size,
                        scalar(float(np.abs(x).max())), "oracle")
     np.testing.assert_array_equal(codes, oracle.project(x, np.float32(a), 5, 3))
+
+
+def boundary_lengths():
+    """Lengths at the edges of the call's paths: the last block count without group sums
+    (32 blocks of 2 rows of 4096 elements), the last projection size that takes the
+    finishing step in every block (two tiles of 4096 elements per CU on a 256-CU part),
+    and the len % 4 tails around them."""
+    out = []
+    for base in (32 * 2 * 4096, 2 * 4096 * 256):
+        for d in (-4097, -5, -1, 0, 1, 3, 4096):
+            out.append(base + d)
+    return out
+
+
+@pytest.mark.parametrize("length", boundary_lengths())
+def test_quantize_path_boundaries(esb, length):
+    factors = wl.scale_grid(1.0).astype(np.float32)
+    plan = esb.esb_dda_plan(5, 3, dev(factors))
+    x = activations(length % 1000 + 31, length)
+    log("quantize boundary len=%d" % length)
+    compare(esb, dev(x), 5, 3, plan, factors.size, scalar(float(np.abs(x).max())),
+            "len %d" % length)
